@@ -1,0 +1,159 @@
+/*
+ * kf355.h -- C ABI of libkf355: MI355X (gfx950) kernels for the three
+ * memory-bound segmented reductions that Kernel Forge (arXiv 2607.24762)
+ * optimises inside real PyTorch models: row softmax (Gemma 4 E2B and
+ * Qwen 3.5 35B-A3B attention / router scores), GroupNorm (Stable Diffusion
+ * 3.5 Medium) and adaptive_avgpool2d (ResNet-50 head); Section IV-C reports
+ * the per-operator results, Table I the workloads.
+ *
+ * Semantics.  Every call computes exactly what the PyTorch operator of the
+ * same name computes: the paper admits a kernel only when it reproduces
+ * PyTorch eager's outputs for the captured call, characterised by shapes,
+ * dtypes, strides, layouts and scalar arguments (Section III-A,
+ * "Model Ingestion Pipeline"; Section III-C, "Kernel Validator"), and a call
+ * the kernel does not cover is left to the original PyTorch path
+ * (Section III-E, "Packaging, Guarded Dispatch").  Here an uncovered layout
+ * is reported as KF_ERR_UNSUPPORTED_LAYOUT, never computed some other way.
+ *
+ * Conventions shared by all calls.
+ *  - Tensor data pointers are DEVICE pointers on the current HIP device.
+ *    `shape` and `*_strides` are HOST arrays of `ndim` int64 values;
+ *    strides count elements.  A NULL stride array means dense row-major.
+ *    Only dense row-major tensors are supported; other strides return
+ *    KF_ERR_UNSUPPORTED_LAYOUT (size-1 dimensions may carry any stride).
+ *  - `stream` is a hipStream_t (NULL = the default stream).  Calls only
+ *    enqueue work: they never synchronise, and device faults surface at the
+ *    caller's next synchronisation, as with PyTorch.
+ *  - The caller owns every buffer; the library allocates nothing and keeps
+ *    no pointer after returning.
+ *  - Every argument is checked on the host before anything is enqueued.  On
+ *    any status other than KF_OK nothing was enqueued, except KF_ERR_HIP,
+ *    which reports a failed launch.  kf_last_error() then describes it.
+ *  - A tensor with zero elements is a no-op returning KF_OK.
+ *  - Calls are thread-safe; the only global state is a thread-local error
+ *    string / variant name and per-device properties cached on first use.
+ */
+#ifndef KF355_H
+#define KF355_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define KF355_ABI_VERSION 1
+#define KF_MAX_DIMS 8
+
+typedef enum kf_status {
+    KF_OK = 0,
+    KF_ERR_NULL_POINTER = 1,      /* a required pointer is NULL */
+    KF_ERR_BAD_SHAPE = 2,         /* ndim out of range, negative or mismatched sizes */
+    KF_ERR_BAD_DTYPE = 3,         /* dtype or dtype combination not supported */
+    KF_ERR_BAD_ARG = 4,           /* dim, num_groups, eps, output size, aliasing */
+    KF_ERR_UNSUPPORTED_LAYOUT = 5,/* valid for PyTorch but not covered here */
+    KF_ERR_WORKSPACE = 6,         /* workspace missing or too small */
+    KF_ERR_HIP = 7                /* the HIP runtime rejected a launch */
+} kf_status;
+
+typedef enum kf_dtype {
+    KF_FLOAT32 = 0,
+    KF_BFLOAT16 = 1,
+    KF_FLOAT16 = 2
+} kf_dtype;
+
+/* KF355_ABI_VERSION of the loaded library. */
+int kf_abi_version(void);
+
+/* Static name of a status code ("KF_OK", ...); "KF_UNKNOWN" otherwise. */
+const char* kf_status_name(int status);
+
+/* Thread-local detail text of this thread's last non-OK status ("" if none).
+ * Valid until the next kf_* call on the same thread. */
+const char* kf_last_error(void);
+
+/* Thread-local name of the kernel variant enqueued by this thread's last
+ * successful operator call ("" if none). */
+const char* kf_last_variant(void);
+
+/*
+ * kf_softmax -- y = softmax(x, dim): along `dim`, y_j = exp(x_j - m) / S with
+ * m the maximum and S the sum of exp(x_k - m) (PyTorch `torch.softmax`; the
+ * operator of the Gemma 4 E2B and Qwen 3.5 35B-A3B results, Section IV-C).
+ *
+ *  x, y        device pointers, same shape `shape[ndim]` (0 <= ndim <= 8;
+ *              ndim 0 is one element, giving 1).
+ *  x_dtype,    (FLOAT32 -> FLOAT32), (BFLOAT16 -> BFLOAT16),
+ *  y_dtype     (BFLOAT16 -> FLOAT32), (FLOAT16 -> FLOAT16), (FLOAT16 -> FLOAT32);
+ *              accumulation is fp32, results are rounded to nearest-even.
+ *  dim         in [-ndim, ndim) (wrapped like PyTorch); any dim is
+ *              supported, the last one is the fast path.
+ *  Special rows follow IEEE evaluation as PyTorch does: a row of only -inf
+ *  gives NaN, a NaN or +inf entry gives a NaN row, -inf entries give +0.
+ *  y may equal x (in place); any other overlap is KF_ERR_BAD_ARG.
+ */
+kf_status kf_softmax(const void* x, kf_dtype x_dtype, void* y, kf_dtype y_dtype, int32_t ndim,
+                     const int64_t* shape, const int64_t* x_strides, const int64_t* y_strides, int64_t dim,
+                     void* stream);
+
+/*
+ * kf_group_norm -- y = group_norm(x, num_groups, weight, bias, eps)
+ * (PyTorch `torch.nn.functional.group_norm`; the SD3.5 Medium result,
+ * Section IV-C): for each sample and each of `num_groups` groups of
+ * C/num_groups consecutive channels, mu and var are the mean and biased
+ * variance over the group's channels and spatial positions, and
+ * y = (x - mu) / sqrt(var + eps) * weight[c] + bias[c].
+ *
+ *  x, y          device pointers, shape [N, C, *] (2 <= ndim <= 8), same dtype
+ *                (FLOAT32, BFLOAT16 or FLOAT16); statistics are fp32.
+ *  num_groups    >= 1 and divides C, else KF_ERR_BAD_ARG.
+ *  weight, bias  device pointers to C elements each, or NULL (weight 1 /
+ *                bias 0); both use `affine_dtype`, which is x_dtype or
+ *                FLOAT32.
+ *  eps           >= 0 (used as fp32).
+ *  workspace     device buffer of at least kf_group_norm_workspace_bytes()
+ *                bytes, 256-byte aligned, ZERO-FILLED before its first use
+ *                and left alone by the caller between calls: it holds
+ *                cross-workgroup counters that every completed call returns
+ *                to zero.  Its last 256 bytes start with a 32-bit word that
+ *                a call sets nonzero if a cross-workgroup wait gave up (the
+ *                results of that call are then invalid; clear the word to
+ *                re-arm).  Calls that may run concurrently must not share a
+ *                workspace.
+ *  y may equal x (in place); any other overlap is KF_ERR_BAD_ARG.
+ */
+kf_status kf_group_norm(const void* x, kf_dtype x_dtype, void* y, int32_t ndim, const int64_t* shape,
+                        const int64_t* x_strides, const int64_t* y_strides, int64_t num_groups,
+                        const void* weight, const void* bias, kf_dtype affine_dtype, double eps,
+                        void* workspace, size_t workspace_bytes, void* stream);
+
+/* Workspace bytes kf_group_norm needs for this shape (written to *bytes);
+ * a pure function of its arguments, no device access. */
+kf_status kf_group_norm_workspace_bytes(kf_dtype x_dtype, int32_t ndim, const int64_t* shape, int64_t num_groups,
+                                        size_t* bytes);
+
+/*
+ * kf_adaptive_avgpool2d -- y = adaptive_avg_pool2d(x, (out_h, out_w))
+ * (PyTorch `torch.nn.functional.adaptive_avg_pool2d`; the ResNet-50 result,
+ * Section IV-C): output cell (i, j) is the mean of input rows
+ * [floor(i*H/out_h), ceil((i+1)*H/out_h)) and columns
+ * [floor(j*W/out_w), ceil((j+1)*W/out_w)).
+ *
+ *  x        device pointer, shape [N, C, H, W] or [C, H, W] with H, W >= 1,
+ *           dtype FLOAT32, BFLOAT16 or FLOAT16 (fp32 accumulation).
+ *  out_h,   >= 1 each (may exceed H, W, as in PyTorch).
+ *  out_w
+ *  y        device pointer, shape [N, C, out_h, out_w] (or [C, out_h,
+ *           out_w]), x's dtype; y_strides describe that shape.  y must not
+ *           overlap x.
+ */
+kf_status kf_adaptive_avgpool2d(const void* x, kf_dtype dtype, void* y, int32_t ndim, const int64_t* shape,
+                                const int64_t* x_strides, const int64_t* y_strides, int64_t out_h,
+                                int64_t out_w, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* KF355_H */

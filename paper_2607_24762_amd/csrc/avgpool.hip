@@ -1,0 +1,222 @@
+// avgpool.hip -- adaptive_avg_pool2d for gfx950 (PyTorch semantics: output
+// cell (i, j) averages input rows [floor(i*H/OH), ceil((i+1)*H/OH)) and
+// columns [floor(j*W/OW), ceil((j+1)*W/OW))), the operator behind the
+// paper's ResNet-50 adaptive_avgpool2d result (Section IV-C).
+//
+//   ap_flat   1x1 output, planes of S = H*W elements.  A workgroup owns P
+//             consecutive planes = one contiguous span of P*S <= 4096
+//             elements, which it stages in LDS with coalesced (16-byte when
+//             aligned) loads, all issued before the first LDS store; then
+//             TPS = 256/P threads sum each plane out of LDS and one of them
+//             writes the mean.
+//   ap_plane  1x1 output for large planes: one workgroup per plane reads it
+//             with coalesced loads and reduces in registers.
+//   ap_window any output size: one thread per output cell.
+#include "kf_device.hpp"
+#include "kf_internal.h"
+
+namespace kf {
+namespace {
+
+constexpr int kNT = 256;
+constexpr int kSpanMax = 4096;  // fp32 staging per workgroup: 16 KiB of LDS
+
+// Loads issued per thread to cover a span of kSpanMax elements.
+template <int VEC>
+constexpr int slots() {
+    return (kSpanMax + kNT * VEC - 1) / (kNT * VEC);
+}
+
+template <class T, int TPS, bool VECTOR>
+__global__ __launch_bounds__(kNT) void ap_flat(const void* __restrict__ x, void* __restrict__ y, int64_t planes,
+                                               int32_t S) {
+    constexpr int P = kNT / TPS;  // planes per workgroup
+    constexpr int VEC = VECTOR ? T::vec : 1;
+    constexpr int NV = slots<VEC>();
+    extern __shared__ float tile[];  // P * S floats
+    const int64_t p0 = (int64_t)blockIdx.x * P;
+    const int64_t np = (planes - p0) < P ? (planes - p0) : P;
+    const int32_t span = (int32_t)(np * S);  // elements this workgroup owns
+    const int32_t whole = span - span % VEC;
+    const int64_t base = p0 * S;
+
+    // Stage the span in LDS as fp32.  Every load is issued before the first
+    // LDS store, so a thread has all its requests in flight at once; only the
+    // last workgroup can have a remainder that is not whole vectors.
+    float v[NV][VEC];
+#pragma unroll
+    for (int k = 0; k < NV; ++k) {
+        const int32_t e = (k * kNT + (int)threadIdx.x) * VEC;
+        if (e < whole) {
+            if constexpr (VECTOR) load_vec<T>(x, base + e, v[k]);
+            else v[k][0] = load1<T>(x, base + e);
+        }
+    }
+#pragma unroll
+    for (int k = 0; k < NV; ++k) {
+        const int32_t e = (k * kNT + (int)threadIdx.x) * VEC;
+        if (e < whole) {
+#pragma unroll
+            for (int i = 0; i < VEC; ++i) tile[e + i] = v[k][i];
+        }
+    }
+    for (int32_t e = whole + threadIdx.x; e < span; e += kNT) tile[e] = load1<T>(x, base + e);
+    __syncthreads();
+
+    // TPS threads sum each plane at stride TPS, four accumulators each.
+    const int q = threadIdx.x / TPS;
+    const int part = threadIdx.x % TPS;
+    float acc[4] = {0.f, 0.f, 0.f, 0.f};
+    if (q < np) {
+        const float* row = tile + q * S;
+        int32_t j = part;
+        for (; j + 3 * TPS < S; j += 4 * TPS) {
+            acc[0] += row[j];
+            acc[1] += row[j + TPS];
+            acc[2] += row[j + 2 * TPS];
+            acc[3] += row[j + 3 * TPS];
+        }
+        for (int r = 0; j < S; j += TPS, ++r) acc[r] += row[j];
+    }
+    float sum = (acc[0] + acc[1]) + (acc[2] + acc[3]);
+    sum = group_reduce<TPS>(sum, OpSum{});
+    if (part == 0 && q < np) store1<T>(y, p0 + q, sum / (float)S);
+}
+
+template <class T, bool VECTOR>
+__global__ __launch_bounds__(kNT) void ap_plane(const void* __restrict__ x, void* __restrict__ y, int64_t S) {
+    constexpr int VEC = VECTOR ? T::vec : 1;
+    constexpr int DEPTH = 4;  // loads in flight per thread per iteration
+    __shared__ float red[kNT / kWave];
+    const int64_t base = (int64_t)blockIdx.x * S;
+    float acc[DEPTH] = {0.f, 0.f, 0.f, 0.f};
+    for (int64_t e0 = (int64_t)threadIdx.x * VEC; e0 < S; e0 += (int64_t)DEPTH * kNT * VEC) {
+        float v[DEPTH][VEC];
+#pragma unroll
+        for (int d = 0; d < DEPTH; ++d) {
+            const int64_t e = e0 + (int64_t)d * kNT * VEC;
+            if (e < S) {
+                if constexpr (VECTOR) load_vec<T>(x, base + e, v[d]);
+                else v[d][0] = load1<T>(x, base + e);
+            } else {
+#pragma unroll
+                for (int i = 0; i < VEC; ++i) v[d][i] = 0.f;
+            }
+        }
+#pragma unroll
+        for (int d = 0; d < DEPTH; ++d)
+#pragma unroll
+            for (int i = 0; i < VEC; ++i) acc[d] += v[d][i];
+    }
+    float sum = (acc[0] + acc[1]) + (acc[2] + acc[3]);
+    sum = group_reduce<kWave>(sum, OpSum{});
+    if ((threadIdx.x & (kWave - 1)) == 0) red[threadIdx.x / kWave] = sum;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        float t = red[0];
+#pragma unroll
+        for (int i = 1; i < kNT / kWave; ++i) t += red[i];
+        store1<T>(y, blockIdx.x, t / (float)S);
+    }
+}
+
+template <class T>
+__global__ __launch_bounds__(kNT) void ap_window(const void* __restrict__ x, void* __restrict__ y, int64_t planes,
+                                                 int64_t H, int64_t W, int64_t OH, int64_t OW) {
+    const int64_t idx = (int64_t)blockIdx.x * kNT + threadIdx.x;
+    if (idx >= planes * OH * OW) return;
+    const int64_t j = idx % OW;
+    const int64_t i = (idx / OW) % OH;
+    const int64_t p = idx / (OW * OH);
+    const int64_t h0 = (i * H) / OH, h1 = ((i + 1) * H + OH - 1) / OH;
+    const int64_t w0 = (j * W) / OW, w1 = ((j + 1) * W + OW - 1) / OW;
+    const int64_t base = p * H * W;
+    float sum = 0.f;
+    for (int64_t r = h0; r < h1; ++r)
+        for (int64_t c = w0; c < w1; ++c) sum += load1<T>(x, base + r * W + c);
+    store1<T>(y, idx, sum / (float)((h1 - h0) * (w1 - w0)));
+}
+
+template <class T, int TPS>
+void launch_flat(const AvgPoolArgs& a, hipStream_t s, const char** variant, const char* name) {
+    constexpr int P = kNT / TPS;
+    const int64_t S = a.h * a.w;
+    const int64_t blocks = (a.planes + P - 1) / P;
+    const size_t lds = (size_t)P * S * sizeof(float);
+    // Vector loads need every workgroup span to start 16-byte aligned.
+    const bool vec = ((P * S * T::bytes) % 16 == 0) && ((uintptr_t)a.x % 16 == 0);
+    if (vec)
+        hipLaunchKernelGGL((ap_flat<T, TPS, true>), dim3((unsigned)blocks), dim3(kNT), lds, s, a.x, a.y, a.planes,
+                           (int32_t)S);
+    else
+        hipLaunchKernelGGL((ap_flat<T, TPS, false>), dim3((unsigned)blocks), dim3(kNT), lds, s, a.x, a.y,
+                           a.planes, (int32_t)S);
+    *variant = name;
+}
+
+template <class T>
+kf_status run(const AvgPoolArgs& a, hipStream_t s, const char** variant) {
+    const int64_t S = a.h * a.w;
+    if (a.oh == 1 && a.ow == 1) {
+        // Planes per workgroup: the largest power of two (<= 256) whose span
+        // fits the staging tile; a plane too big for it gets a workgroup.
+        int64_t P = 256;
+        while (P > 1 && P * S > kSpanMax) P /= 2;
+        if (P * S > kSpanMax) P = 0;
+        if (P > 0 && (a.planes + P - 1) / P > INT32_MAX) P = 0;
+        switch (P) {
+            case 256: launch_flat<T, 1>(a, s, variant, "ap_flat_tps1"); break;
+            case 128: launch_flat<T, 2>(a, s, variant, "ap_flat_tps2"); break;
+            case 64: launch_flat<T, 4>(a, s, variant, "ap_flat_tps4"); break;
+            case 32: launch_flat<T, 8>(a, s, variant, "ap_flat_tps8"); break;
+            case 16: launch_flat<T, 16>(a, s, variant, "ap_flat_tps16"); break;
+            case 8: launch_flat<T, 32>(a, s, variant, "ap_flat_tps32"); break;
+            case 4: launch_flat<T, 64>(a, s, variant, "ap_flat_tps64"); break;
+            default: {
+                if (a.planes > INT32_MAX) {
+                    set_error("adaptive_avgpool2d: %lld planes exceed the grid limit", (long long)a.planes);
+                    return KF_ERR_UNSUPPORTED_LAYOUT;
+                }
+                const bool vec = (S % T::vec == 0) && ((uintptr_t)a.x % 16 == 0);
+                if (vec)
+                    hipLaunchKernelGGL((ap_plane<T, true>), dim3((unsigned)a.planes), dim3(kNT), 0, s, a.x, a.y, S);
+                else
+                    hipLaunchKernelGGL((ap_plane<T, false>), dim3((unsigned)a.planes), dim3(kNT), 0, s, a.x, a.y,
+                                       S);
+                *variant = "ap_plane";
+            }
+        }
+    } else {
+        const int64_t blocks = (a.planes * a.oh * a.ow + kNT - 1) / kNT;
+        if (blocks > INT32_MAX) {
+            set_error("adaptive_avgpool2d: problem exceeds the grid limit");
+            return KF_ERR_UNSUPPORTED_LAYOUT;
+        }
+        hipLaunchKernelGGL((ap_window<T>), dim3((unsigned)blocks), dim3(kNT), 0, s, a.x, a.y, a.planes, a.h, a.w,
+                           a.oh, a.ow);
+        *variant = "ap_window";
+    }
+    const hipError_t err = hipGetLastError();
+    if (err != hipSuccess) {
+        set_error("adaptive_avgpool2d launch failed: %s", hipGetErrorString(err));
+        return KF_ERR_HIP;
+    }
+    return KF_OK;
+}
+
+}  // namespace
+
+kf_status avgpool_launch(const AvgPoolArgs& a, hipStream_t s, const char** variant) {
+    switch (a.t) {
+        case KF_FLOAT32:
+            return run<F32>(a, s, variant);
+        case KF_BFLOAT16:
+            return run<BF16>(a, s, variant);
+        case KF_FLOAT16:
+            return run<F16>(a, s, variant);
+    }
+    set_error("adaptive_avgpool2d: unsupported dtype");
+    return KF_ERR_BAD_DTYPE;
+}
+
+}  // namespace kf

@@ -1,0 +1,520 @@
+// group_norm.hip -- GroupNorm for gfx950 (PyTorch `group_norm(x, G, w, b,
+// eps)` semantics: biased variance, eps inside the square root, per-channel
+// affine), the operator behind the paper's SD3.5 Medium group_norm result
+// (Section IV-C).
+//
+// Layout: x is dense [n, c, spatial]; group g of sample i is the contiguous
+// span of (c/G)*spatial elements starting at (i*G + g) * (c/G)*spatial.  Each
+// group is cut into `parts` chunks of CH = 256 threads * NV * VEC elements and
+// one workgroup owns one chunk.
+//
+//   gn_fused  (one launch, one HBM read + one write)  Each workgroup keeps its
+//             chunk in registers, computes its (count, mean, M2) moments,
+//             publishes them as one 64-bit word in its workspace slot, polls
+//             the slots of its group until all `parts` are published, merges
+//             them in part order (so the result does not depend on arrival
+//             order), and normalises straight from registers.  Needs every
+//             workgroup of the grid resident at once.
+//   gn_stats + gn_apply  (two launches)  The same chunking without the wait:
+//             the first kernel publishes the partials, the second merges them
+//             and re-reads x.  Used when the grid cannot be co-resident.
+//
+// Moments: each thread computes its own mean and M2 by two passes over its
+// registers, then partials are combined with the Chan et al. parallel
+// update; both lanes of a butterfly pair order the operands by lane so they
+// compute bit-identical results.
+#include <math.h>
+
+#include <atomic>
+#include <cstdlib>
+#include <cstring>
+
+#include "kf_device.hpp"
+#include "kf_internal.h"
+
+namespace kf {
+namespace {
+
+constexpr int kNT = 256;          // threads per workgroup
+constexpr size_t kCounterStride = 256;  // bytes between two groups' counters
+constexpr int kFloatsPerThread = 64;
+
+struct Moments {
+    float n, mean, m2;
+};
+
+// Chan et al. combine of two partial moments (a before b).
+__device__ __forceinline__ Moments chan(Moments a, Moments b) {
+    const float n = a.n + b.n;
+    if (n == 0.f) return Moments{0.f, 0.f, 0.f};
+    const float d = b.mean - a.mean;
+    const float f = b.n / n;
+    return Moments{n, fmaf(d, f, a.mean), a.m2 + b.m2 + d * d * a.n * f};
+}
+
+template <int S>
+__device__ __forceinline__ Moments moments_step(Moments m) {
+    Moments o{partner<S>(m.n), partner<S>(m.mean), partner<S>(m.m2)};
+    // In step S the partner sits in the other half of an aligned block of
+    // 2^(S+1) lanes; the lane in the lower half is the left operand.
+    const bool lower = (__lane_id() & (1 << S)) == 0;
+    return lower ? chan(m, o) : chan(o, m);
+}
+
+__device__ __forceinline__ Moments moments_wave(Moments m) {
+    m = moments_step<0>(m);
+    m = moments_step<1>(m);
+    m = moments_step<2>(m);
+    m = moments_step<3>(m);
+    m = moments_step<4>(m);
+    m = moments_step<5>(m);
+    return m;
+}
+
+struct GNParams {
+    const void* x;
+    void* y;
+    const void* w;
+    const void* b;
+    uint64_t* slot;        // [groups_total * parts] published partials, 0 = empty
+    unsigned* depart;      // one per group, kCounterStride bytes apart
+    unsigned* error;       // set to 1 if a wait gave up
+    int64_t group_elems;   // (c/G) * spatial
+    int64_t spatial;
+    int32_t cpg;           // channels per group
+    int32_t groups;        // G
+    int32_t parts;         // workgroups per group
+    float eps;
+    unsigned spin_limit;
+};
+
+__device__ __forceinline__ unsigned* counter(unsigned* base, int64_t ng) {
+    return reinterpret_cast<unsigned*>(reinterpret_cast<char*>(base) + ng * (int64_t)kCounterStride);
+}
+
+// Elements held by part p of a group.
+__device__ __forceinline__ float part_count(const GNParams& p, int64_t chunk, int part) {
+    const int64_t left = p.group_elems - (int64_t)part * chunk;
+    return (float)(left < chunk ? left : chunk);
+}
+
+template <class T, bool VECTOR>
+struct Chunk {
+    static constexpr int VEC = VECTOR ? T::vec : 1;
+    static constexpr int NV = kFloatsPerThread / VEC;
+    static constexpr int64_t CH = (int64_t)kNT * NV * VEC;
+    float v[NV][VEC];
+
+    // Offset inside the group of this thread's k-th slot.
+    __device__ __forceinline__ static int64_t off(int part, int k) {
+        return (int64_t)part * CH + ((int64_t)k * kNT + threadIdx.x) * VEC;
+    }
+    // All slots load unconditionally so the loads issue back to back; a slot
+    // past the group's end re-reads the group's first element and is never
+    // used afterwards.
+    __device__ __forceinline__ void load(const GNParams& p, int64_t gbase, int part) {
+#pragma unroll
+        for (int k = 0; k < NV; ++k) {
+            const int64_t o = off(part, k);
+            const int64_t at = gbase + (o < p.group_elems ? o : 0);
+            if constexpr (VECTOR) load_vec<T>(p.x, at, v[k]);
+            else v[k][0] = load1<T>(p.x, at);
+        }
+    }
+    // Thread-local two-pass moments of the valid elements.
+    __device__ __forceinline__ Moments moments(const GNParams& p, int part) const {
+        float sum = 0.f, cnt = 0.f;
+#pragma unroll
+        for (int k = 0; k < NV; ++k) {
+            if (off(part, k) < p.group_elems) {
+                cnt += (float)VEC;
+#pragma unroll
+                for (int i = 0; i < VEC; ++i) sum += v[k][i];
+            }
+        }
+        const float mean = cnt > 0.f ? sum / cnt : 0.f;
+        float m2 = 0.f;
+#pragma unroll
+        for (int k = 0; k < NV; ++k) {
+            if (off(part, k) < p.group_elems) {
+#pragma unroll
+                for (int i = 0; i < VEC; ++i) {
+                    const float d = v[k][i] - mean;
+                    m2 = fmaf(d, d, m2);
+                }
+            }
+        }
+        return Moments{cnt, mean, m2};
+    }
+    // y = (x - mean) * (rstd * w[c]) + b[c], channel c per slot (VECTOR) or
+    // per element.
+    template <class A>
+    __device__ __forceinline__ void normalise_store(const GNParams& p, int64_t gbase, int part, int g,
+                                                    float mean, float rstd) {
+        // Per-slot channel scale and shift first (unconditional loads of w
+        // and b, issued together), then the guarded stores.  A group holds
+        // fewer than 2^31 elements (checked on the host), so the channel
+        // index is a 32-bit division.
+        int64_t c[NV];
+#pragma unroll
+        for (int k = 0; k < NV; ++k) {
+            const int64_t o = off(part, k);
+            const uint32_t oc = o < p.group_elems ? (uint32_t)o : 0u;
+            c[k] = (int64_t)g * p.cpg + (int64_t)(oc / (uint32_t)p.spatial);
+        }
+        float a[NV], bb[NV];
+        if (p.w) {
+#pragma unroll
+            for (int k = 0; k < NV; ++k) a[k] = load1<A>(p.w, c[k]);
+#pragma unroll
+            for (int k = 0; k < NV; ++k) a[k] *= rstd;
+        } else {
+#pragma unroll
+            for (int k = 0; k < NV; ++k) a[k] = rstd;
+        }
+        if (p.b) {
+#pragma unroll
+            for (int k = 0; k < NV; ++k) bb[k] = load1<A>(p.b, c[k]);
+        } else {
+#pragma unroll
+            for (int k = 0; k < NV; ++k) bb[k] = 0.f;
+        }
+#pragma unroll
+        for (int k = 0; k < NV; ++k) {
+            const int64_t o = off(part, k);
+            if (o < p.group_elems) {
+                float out[VEC];
+#pragma unroll
+                for (int i = 0; i < VEC; ++i) out[i] = fmaf(v[k][i] - mean, a[k], bb[k]);
+                if constexpr (VECTOR) store_vec<T>(p.y, gbase + o, out);
+                else store1<T>(p.y, gbase + o, out[0]);
+            }
+        }
+    }
+};
+
+// Workgroup-wide combine: butterfly inside each wave, then waves in index
+// order through LDS.  Returns the result in every thread.
+__device__ __forceinline__ Moments moments_block(Moments m, Moments* lds) {
+    m = moments_wave(m);
+    const int w = threadIdx.x / kWave;
+    if ((threadIdx.x & (kWave - 1)) == 0) lds[w] = m;
+    __syncthreads();
+    Moments t = lds[0];
+#pragma unroll
+    for (int i = 1; i < kNT / kWave; ++i) t = chan(t, lds[i]);
+    __syncthreads();
+    return t;
+}
+
+// A published partial is one 64-bit word: mean bits low, M2 bits high with
+// the sign bit forced on.  M2 is never negative, so the flag is free, and a
+// published word is never 0, the value of an empty slot.  Writing the data
+// and its ready flag in one single-copy-atomic store means a reader that sees
+// the word sees the data: no fences, no cache write-back or invalidation.
+__device__ __forceinline__ uint64_t encode(Moments m) {
+    return (uint64_t)__float_as_uint(m.mean) | ((uint64_t)(__float_as_uint(m.m2) | 0x80000000u) << 32);
+}
+__device__ __forceinline__ Moments decode(uint64_t w, float n) {
+    return Moments{n, __uint_as_float((uint32_t)w), __uint_as_float((uint32_t)(w >> 32) & 0x7fffffffu)};
+}
+
+__device__ __forceinline__ void publish(const GNParams& p, int64_t ng, int part, Moments m) {
+    __hip_atomic_store(p.slot + ng * p.parts + part, encode(m), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Gather and merge the `parts` partials of one group; called by a whole wave,
+// result uniform across it.  Lane l takes parts l, l+64, ... in order and the
+// butterfly keeps lane order, so the combine order depends on part index
+// alone (bitwise-reproducible results).  With `wait`, each lane polls its
+// slots until they are published; the wait is bounded and on giving up flags
+// the workspace and carries on, so the kernel always ends.
+__device__ __forceinline__ Moments gather_parts(const GNParams& p, int64_t ng, int64_t chunk, bool wait) {
+    Moments acc{0.f, 0.f, 0.f};
+    const int lane = threadIdx.x & (kWave - 1);
+    uint64_t* slots = p.slot + ng * p.parts;
+    for (int q = lane; q < p.parts; q += kWave) {
+        uint64_t w = __hip_atomic_load(slots + q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (wait) {
+            unsigned spins = 0;
+            while (w == 0) {
+                if (++spins > p.spin_limit) {
+                    __hip_atomic_store(p.error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    break;
+                }
+                __builtin_amdgcn_s_sleep(1);
+                w = __hip_atomic_load(slots + q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            }
+        }
+        acc = chan(acc, decode(w, part_count(p, chunk, q)));
+    }
+    return moments_wave(acc);
+}
+
+// Called by lane 0 of wave 0 of every workgroup once it has gathered its
+// group's partials: the last workgroup of the group to arrive here empties the
+// group's slots and its counter, so every call leaves them zero.  Every
+// workgroup counted has finished reading the slots (its reads returned before
+// the merge that precedes this), so none can see the cleared values.
+__device__ __forceinline__ void release_group(const GNParams& p, int64_t ng) {
+    const unsigned left =
+        __hip_atomic_fetch_add(counter(p.depart, ng), 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (left == (unsigned)p.parts - 1) {
+        uint64_t* slots = p.slot + ng * p.parts;
+        for (int q = 0; q < p.parts; ++q) __hip_atomic_store(slots + q, (uint64_t)0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(counter(p.depart, ng), 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+}
+
+template <class T, class A, bool VECTOR>
+__global__ __launch_bounds__(kNT) void gn_fused(GNParams p) {
+    using C = Chunk<T, VECTOR>;
+    __shared__ Moments lds[kNT / kWave];
+    __shared__ float stats[2];
+    const int64_t ng = blockIdx.x / p.parts;
+    const int part = blockIdx.x - (int)(ng * p.parts);
+    const int g = (int)(ng % p.groups);
+    const int64_t gbase = ng * p.group_elems;
+
+    C c;
+    c.load(p, gbase, part);
+    Moments m = moments_block(c.moments(p, part), lds);
+
+    if (threadIdx.x < kWave) {
+        if (p.parts > 1) {
+            if (threadIdx.x == 0) publish(p, ng, part, m);
+            m = gather_parts(p, ng, C::CH, true);
+            if (threadIdx.x == 0) release_group(p, ng);
+        }
+        if (threadIdx.x == 0) {
+            stats[0] = m.mean;
+            stats[1] = 1.f / sqrtf(m.m2 / (float)p.group_elems + p.eps);
+        }
+    }
+    __syncthreads();
+    c.template normalise_store<A>(p, gbase, part, g, stats[0], stats[1]);
+}
+
+template <class T, bool VECTOR>
+__global__ __launch_bounds__(kNT) void gn_stats(GNParams p) {
+    using C = Chunk<T, VECTOR>;
+    __shared__ Moments lds[kNT / kWave];
+    const int64_t ng = blockIdx.x / p.parts;
+    const int part = blockIdx.x - (int)(ng * p.parts);
+    C c;
+    c.load(p, ng * p.group_elems, part);
+    Moments m = moments_block(c.moments(p, part), lds);
+    if (threadIdx.x == 0) publish(p, ng, part, m);
+}
+
+template <class T, class A, bool VECTOR>
+__global__ __launch_bounds__(kNT) void gn_apply(GNParams p) {
+    using C = Chunk<T, VECTOR>;
+    __shared__ float stats[2];
+    const int64_t ng = blockIdx.x / p.parts;
+    const int part = blockIdx.x - (int)(ng * p.parts);
+    const int g = (int)(ng % p.groups);
+    const int64_t gbase = ng * p.group_elems;
+    if (threadIdx.x < kWave) {
+        Moments m = gather_parts(p, ng, C::CH, false);
+        if (threadIdx.x == 0) release_group(p, ng);
+        if (threadIdx.x == 0) {
+            stats[0] = m.mean;
+            stats[1] = 1.f / sqrtf(m.m2 / (float)p.group_elems + p.eps);
+        }
+    }
+    C c;
+    c.load(p, gbase, part);
+    __syncthreads();
+    c.template normalise_store<A>(p, gbase, part, g, stats[0], stats[1]);
+}
+
+// --------------------------------------------------------------------------
+// Host side.
+
+// Elements per workgroup chunk for a dtype / vectorisation choice.
+int64_t chunk_elems(kf_dtype xt, bool vector) {
+    const int vec = vector ? (xt == KF_FLOAT32 ? 4 : 8) : 1;
+    return (int64_t)kNT * (kFloatsPerThread / vec) * vec;
+}
+
+bool vector_ok(const GroupNormArgs& a) {
+    const int vec = a.xt == KF_FLOAT32 ? 4 : 8;
+    return (a.spatial % vec == 0) && ((uintptr_t)a.x % 16 == 0) && ((uintptr_t)a.y % 16 == 0);
+}
+
+struct Layout {
+    int64_t groups_total, parts;
+    size_t slot_off, depart_off, error_off, total;
+};
+
+Layout layout(int64_t n, int64_t c, int64_t spatial, int64_t groups, kf_dtype xt, bool vector) {
+    Layout l;
+    l.groups_total = n * groups;
+    const int64_t ge = (c / groups) * spatial;
+    l.parts = (ge + chunk_elems(xt, vector) - 1) / chunk_elems(xt, vector);
+    if (l.parts < 1) l.parts = 1;
+    auto up = [](size_t v) { return (v + 255) & ~(size_t)255; };
+    // Partial slots, then one 256-byte line per group for its counter (so
+    // different groups never share a line), then the 256-byte error block.
+    l.slot_off = 0;
+    l.depart_off = up((size_t)(l.groups_total * l.parts) * sizeof(uint64_t));
+    l.error_off = l.depart_off + (size_t)l.groups_total * kCounterStride;
+    l.total = l.error_off + 256;
+    return l;
+}
+
+// Per-device properties, queried once per device and cached (value + 1 in
+// an atomic, 0 meaning not yet known).
+constexpr int kMaxDevices = 64;
+
+int cached_attr(std::atomic<int>* cache, int dev, hipDeviceAttribute_t attr) {
+    if (dev < 0 || dev >= kMaxDevices) return 0;
+    int v = cache[dev].load(std::memory_order_relaxed);
+    if (v == 0) {
+        int got = 0;
+        if (hipDeviceGetAttribute(&got, attr, dev) != hipSuccess) got = 0;
+        v = got + 1;
+        cache[dev].store(v, std::memory_order_relaxed);
+    }
+    return v - 1;
+}
+
+// How many workgroups of `kernel` can be resident on device `dev` at once
+// (0 if unknown), cached per kernel instantiation through `cache`.
+int resident_capacity(std::atomic<int>* cache, int dev, const void* kernel) {
+    static std::atomic<int> cus_cache[kMaxDevices];
+    if (dev < 0 || dev >= kMaxDevices) return 0;
+    int v = cache[dev].load(std::memory_order_relaxed);
+    if (v == 0) {
+        int per_cu = 0;
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, kNT, 0) != hipSuccess) per_cu = 0;
+        v = per_cu * cached_attr(cus_cache, dev, hipDeviceAttributeMultiprocessorCount) + 1;
+        cache[dev].store(v, std::memory_order_relaxed);
+    }
+    return v - 1;
+}
+
+// KF355_GN_MODE selects the multi-chunk path: unset or "auto" (fused when
+// resident, else two kernels), "coop" (fused only under a cooperative
+// launch), "two_pass" (always two kernels).  Read once per process.
+constexpr int kModeAuto = 0, kModeCoop = 1, kModeTwoPass = 2;
+int gn_mode() {
+    static const int mode = [] {
+        const char* e = std::getenv("KF355_GN_MODE");
+        if (!e) return kModeAuto;
+        if (!std::strcmp(e, "coop")) return kModeCoop;
+        if (!std::strcmp(e, "two_pass")) return kModeTwoPass;
+        return kModeAuto;
+    }();
+    return mode;
+}
+
+bool cooperative_ok(int dev) {
+    static std::atomic<int> coop_cache[kMaxDevices];
+    return cached_attr(coop_cache, dev, hipDeviceAttributeCooperativeLaunch) != 0;
+}
+
+template <class T, class A, bool VECTOR>
+kf_status run(const GroupNormArgs& a, hipStream_t s, const char** variant) {
+    const Layout l = layout(a.n, a.c, a.spatial, a.groups, a.xt, VECTOR);
+    char* ws = static_cast<char*>(a.workspace);
+    GNParams p;
+    p.x = a.x;
+    p.y = a.y;
+    p.w = a.weight;
+    p.b = a.bias;
+    p.slot = reinterpret_cast<uint64_t*>(ws + l.slot_off);
+    p.depart = reinterpret_cast<unsigned*>(ws + l.depart_off);
+    p.error = reinterpret_cast<unsigned*>(ws + l.error_off);
+    p.group_elems = (a.c / a.groups) * a.spatial;
+    p.spatial = a.spatial;
+    p.cpg = (int32_t)(a.c / a.groups);
+    p.groups = (int32_t)a.groups;
+    p.parts = (int32_t)l.parts;
+    p.eps = a.eps;
+    p.spin_limit = 1u << 22;
+
+    const int64_t grid = l.groups_total * l.parts;
+    if (grid > INT32_MAX) {
+        set_error("group_norm: grid of %lld workgroups exceeds the launch limit", (long long)grid);
+        return KF_ERR_UNSUPPORTED_LAYOUT;
+    }
+
+    // Path choice.  One chunk per group needs no exchange.  Otherwise the
+    // fused kernel needs every workgroup of the grid resident at once; it is
+    // launched normally when the occupancy-derived capacity covers the grid
+    // (or cooperatively, which the runtime guarantees, under
+    // KF355_GN_MODE=coop), else the two-kernel path runs.
+    const int mode = gn_mode();
+    enum { FUSED_SINGLE, FUSED_PLAIN, FUSED_COOP, TWO_PASS } path = TWO_PASS;
+    if (l.parts == 1 && mode != kModeTwoPass) {
+        path = FUSED_SINGLE;
+    } else if (mode != kModeTwoPass) {
+        static std::atomic<int> capacity_cache[kMaxDevices];
+        int dev = -1;
+        if (hipGetDevice(&dev) != hipSuccess) {
+            set_error("group_norm: no current HIP device");
+            return KF_ERR_HIP;
+        }
+        const void* kernel = reinterpret_cast<const void*>(gn_fused<T, A, VECTOR>);
+        if ((int64_t)resident_capacity(capacity_cache, dev, kernel) >= grid) {
+            if (mode == kModeCoop && cooperative_ok(dev)) path = FUSED_COOP;
+            else if (mode != kModeCoop) path = FUSED_PLAIN;
+        }
+    }
+    hipError_t err;
+    if (path == FUSED_SINGLE || path == FUSED_PLAIN) {
+        hipLaunchKernelGGL((gn_fused<T, A, VECTOR>), dim3((unsigned)grid), dim3(kNT), 0, s, p);
+        err = hipGetLastError();
+        *variant = path == FUSED_SINGLE ? (VECTOR ? "gn_fused_vec_single" : "gn_fused_scalar_single")
+                                        : (VECTOR ? "gn_fused_vec" : "gn_fused_scalar");
+    } else if (path == FUSED_COOP) {
+        void* args[] = {&p};
+        err = hipLaunchCooperativeKernel(reinterpret_cast<const void*>(gn_fused<T, A, VECTOR>), dim3((unsigned)grid),
+                                         dim3(kNT), args, 0, s);
+        *variant = VECTOR ? "gn_fused_vec_coop" : "gn_fused_scalar_coop";
+    } else {
+        hipLaunchKernelGGL((gn_stats<T, VECTOR>), dim3((unsigned)grid), dim3(kNT), 0, s, p);
+        err = hipGetLastError();
+        if (err == hipSuccess) {
+            hipLaunchKernelGGL((gn_apply<T, A, VECTOR>), dim3((unsigned)grid), dim3(kNT), 0, s, p);
+            err = hipGetLastError();
+        }
+        *variant = VECTOR ? "gn_two_pass_vec" : "gn_two_pass_scalar";
+    }
+    if (err != hipSuccess) {
+        set_error("group_norm launch failed: %s", hipGetErrorString(err));
+        return KF_ERR_HIP;
+    }
+    return KF_OK;
+}
+
+template <class T, class A>
+kf_status run_layout(const GroupNormArgs& a, hipStream_t s, const char** variant) {
+    return vector_ok(a) ? run<T, A, true>(a, s, variant) : run<T, A, false>(a, s, variant);
+}
+
+}  // namespace
+
+size_t group_norm_workspace_bytes(int64_t n, int64_t c, int64_t spatial, int64_t groups, kf_dtype xt) {
+    // The scalar layout has the smaller chunk, hence more parts: size for it
+    // so one workspace serves either path.
+    return layout(n, c, spatial, groups, xt, false).total;
+}
+
+kf_status group_norm_launch(const GroupNormArgs& a, hipStream_t s, const char** variant) {
+    const bool f32_affine = (a.at == KF_FLOAT32);
+    switch (a.xt) {
+        case KF_FLOAT32:
+            return run_layout<F32, F32>(a, s, variant);
+        case KF_BFLOAT16:
+            return f32_affine ? run_layout<BF16, F32>(a, s, variant) : run_layout<BF16, BF16>(a, s, variant);
+        case KF_FLOAT16:
+            return f32_affine ? run_layout<F16, F32>(a, s, variant) : run_layout<F16, F16>(a, s, variant);
+    }
+    set_error("group_norm: unsupported dtype");
+    return KF_ERR_BAD_DTYPE;
+}
+
+}  // namespace kf

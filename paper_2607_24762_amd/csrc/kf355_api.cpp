@@ -1,0 +1,248 @@
+// kf355_api.cpp -- the C ABI declared in include/kf355.h.  Each entry point
+// validates its arguments on the host (no HIP call happens before the
+// arguments are known good), derives the dense 3-D view the kernels work on,
+// and hands over to the launch code of its operator.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+
+#include "kf355.h"
+#include "kf_internal.h"
+
+namespace kf {
+namespace {
+thread_local char g_error[512] = "";
+thread_local const char* g_variant = "";
+}  // namespace
+
+void set_error(const char* fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    std::vsnprintf(g_error, sizeof g_error, fmt, ap);
+    va_end(ap);
+}
+
+namespace {
+
+kf_status fail(kf_status s, const char* fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    std::vsnprintf(g_error, sizeof g_error, fmt, ap);
+    va_end(ap);
+    return s;
+}
+
+bool dtype_ok(int t) { return t == KF_FLOAT32 || t == KF_BFLOAT16 || t == KF_FLOAT16; }
+
+int64_t elem_bytes(kf_dtype t) { return t == KF_FLOAT32 ? 4 : 2; }
+
+// Number of elements, or -1 on a negative size or int64 overflow.
+int64_t count(int32_t ndim, const int64_t* shape) {
+    int64_t n = 1;
+    for (int32_t i = 0; i < ndim; ++i) {
+        if (shape[i] < 0) return -1;
+        if (shape[i] != 0 && n > INT64_MAX / shape[i]) return -1;
+        n *= shape[i];
+    }
+    return n;
+}
+
+// Dense row-major check; dimensions of size 1 may carry any stride.
+bool dense(int32_t ndim, const int64_t* shape, const int64_t* strides) {
+    if (!strides) return true;
+    int64_t expect = 1;
+    for (int32_t i = ndim - 1; i >= 0; --i) {
+        if (shape[i] != 1 && strides[i] != expect) return false;
+        expect *= shape[i];
+    }
+    return true;
+}
+
+// Byte ranges [a, a+na) and [b, b+nb) share a byte.
+bool overlaps(const void* a, int64_t na, const void* b, int64_t nb) {
+    const uintptr_t pa = (uintptr_t)a, pb = (uintptr_t)b;
+    return pa < pb + (uintptr_t)nb && pb < pa + (uintptr_t)na;
+}
+
+kf_status check_shape(int32_t ndim, const int64_t* shape, int32_t lo, int32_t hi, int64_t* n) {
+    if (ndim < lo || ndim > hi) return fail(KF_ERR_BAD_SHAPE, "ndim %d outside [%d, %d]", ndim, lo, hi);
+    if (ndim > 0 && !shape) return fail(KF_ERR_NULL_POINTER, "shape is NULL");
+    *n = count(ndim, shape);
+    if (*n < 0) return fail(KF_ERR_BAD_SHAPE, "negative size or element count overflows int64");
+    return KF_OK;
+}
+
+kf_status begin() {
+    g_error[0] = 0;
+    return KF_OK;
+}
+
+kf_status done(kf_status s, const char* variant) {
+    if (s == KF_OK) g_variant = variant ? variant : "";
+    return s;
+}
+
+// Group-norm shape checks shared by the call and the workspace query.
+kf_status check_group_norm_shape(kf_dtype xt, int32_t ndim, const int64_t* shape, int64_t groups, int64_t* n) {
+    kf_status s = check_shape(ndim, shape, 2, KF_MAX_DIMS, n);
+    if (s != KF_OK) return s;
+    if (!dtype_ok(xt)) return fail(KF_ERR_BAD_DTYPE, "x dtype %d not supported", (int)xt);
+    if (groups < 1) return fail(KF_ERR_BAD_ARG, "num_groups %lld < 1", (long long)groups);
+    if (shape[1] % groups != 0)
+        return fail(KF_ERR_BAD_ARG, "C = %lld not divisible by num_groups = %lld", (long long)shape[1],
+                    (long long)groups);
+    const int64_t spatial = ndim > 2 ? count(ndim - 2, shape + 2) : 1;
+    if (shape[1] / groups > INT32_MAX || groups > INT32_MAX || (shape[1] / groups) * spatial > INT32_MAX)
+        return fail(KF_ERR_UNSUPPORTED_LAYOUT, "group of %lld elements is too large",
+                    (long long)((shape[1] / groups) * spatial));
+    return KF_OK;
+}
+
+}  // namespace
+}  // namespace kf
+
+using namespace kf;
+
+extern "C" {
+
+int kf_abi_version(void) { return KF355_ABI_VERSION; }
+
+const char* kf_status_name(int status) {
+    switch (status) {
+        case KF_OK: return "KF_OK";
+        case KF_ERR_NULL_POINTER: return "KF_ERR_NULL_POINTER";
+        case KF_ERR_BAD_SHAPE: return "KF_ERR_BAD_SHAPE";
+        case KF_ERR_BAD_DTYPE: return "KF_ERR_BAD_DTYPE";
+        case KF_ERR_BAD_ARG: return "KF_ERR_BAD_ARG";
+        case KF_ERR_UNSUPPORTED_LAYOUT: return "KF_ERR_UNSUPPORTED_LAYOUT";
+        case KF_ERR_WORKSPACE: return "KF_ERR_WORKSPACE";
+        case KF_ERR_HIP: return "KF_ERR_HIP";
+    }
+    return "KF_UNKNOWN";
+}
+
+const char* kf_last_error(void) { return g_error; }
+
+const char* kf_last_variant(void) { return g_variant; }
+
+kf_status kf_softmax(const void* x, kf_dtype x_dtype, void* y, kf_dtype y_dtype, int32_t ndim, const int64_t* shape,
+                     const int64_t* x_strides, const int64_t* y_strides, int64_t dim, void* stream) {
+    begin();
+    int64_t n = 0;
+    kf_status s = check_shape(ndim, shape, 0, KF_MAX_DIMS, &n);
+    if (s != KF_OK) return s;
+    if (!dtype_ok(x_dtype) || !dtype_ok(y_dtype))
+        return fail(KF_ERR_BAD_DTYPE, "dtype %d -> %d not supported", (int)x_dtype, (int)y_dtype);
+    const bool pair_ok = (x_dtype == y_dtype) || (y_dtype == KF_FLOAT32 && x_dtype != KF_FLOAT32);
+    if (!pair_ok) return fail(KF_ERR_BAD_DTYPE, "softmax cannot narrow %d to %d", (int)x_dtype, (int)y_dtype);
+    const int64_t rank = ndim > 0 ? ndim : 1;  // a 0-d tensor accepts dim 0 or -1
+    if (dim < -rank || dim >= rank)
+        return fail(KF_ERR_BAD_ARG, "dim %lld outside [%lld, %lld)", (long long)dim, (long long)-rank,
+                    (long long)rank);
+    if (dim < 0) dim += rank;
+    if (n == 0) return done(KF_OK, "noop");
+    if (!x || !y) return fail(KF_ERR_NULL_POINTER, "x or y is NULL");
+    if ((uintptr_t)x % elem_bytes(x_dtype) || (uintptr_t)y % elem_bytes(y_dtype))
+        return fail(KF_ERR_BAD_ARG, "x or y is not aligned to its element size");
+    if (!dense(ndim, shape, x_strides) || !dense(ndim, shape, y_strides))
+        return fail(KF_ERR_UNSUPPORTED_LAYOUT, "only dense row-major tensors are supported");
+    const int64_t xb = n * elem_bytes(x_dtype), yb = n * elem_bytes(y_dtype);
+    if (x != y && overlaps(x, xb, y, yb)) return fail(KF_ERR_BAD_ARG, "x and y partially overlap");
+    if (x == y && x_dtype != y_dtype) return fail(KF_ERR_BAD_ARG, "in-place softmax needs equal dtypes");
+
+    SoftmaxArgs a{x, y, x_dtype, y_dtype, 1, 1, 1};
+    if (ndim > 0) {
+        a.outer = count((int32_t)dim, shape);
+        a.len = shape[dim];
+        a.inner = count(ndim - (int32_t)dim - 1, shape + dim + 1);
+    }
+    const char* variant = nullptr;
+    s = softmax_launch(a, static_cast<hipStream_t>(stream), &variant);
+    return done(s, variant);
+}
+
+kf_status kf_group_norm_workspace_bytes(kf_dtype x_dtype, int32_t ndim, const int64_t* shape, int64_t num_groups,
+                                        size_t* bytes) {
+    begin();
+    if (!bytes) return fail(KF_ERR_NULL_POINTER, "bytes is NULL");
+    int64_t n = 0;
+    kf_status s = check_group_norm_shape(x_dtype, ndim, shape, num_groups, &n);
+    if (s != KF_OK) return s;
+    const int64_t spatial = ndim > 2 ? count(ndim - 2, shape + 2) : 1;
+    *bytes = n == 0 ? 0 : group_norm_workspace_bytes(shape[0], shape[1], spatial, num_groups, x_dtype);
+    return KF_OK;
+}
+
+kf_status kf_group_norm(const void* x, kf_dtype x_dtype, void* y, int32_t ndim, const int64_t* shape,
+                        const int64_t* x_strides, const int64_t* y_strides, int64_t num_groups, const void* weight,
+                        const void* bias, kf_dtype affine_dtype, double eps, void* workspace,
+                        size_t workspace_bytes, void* stream) {
+    begin();
+    int64_t n = 0;
+    kf_status s = check_group_norm_shape(x_dtype, ndim, shape, num_groups, &n);
+    if (s != KF_OK) return s;
+    if ((weight || bias) && !(affine_dtype == x_dtype || affine_dtype == KF_FLOAT32))
+        return fail(KF_ERR_BAD_DTYPE, "affine dtype %d must be x's dtype or FLOAT32", (int)affine_dtype);
+    if (!(eps >= 0.0) || !std::isfinite(eps)) return fail(KF_ERR_BAD_ARG, "eps must be finite and >= 0");
+    if (n == 0) return done(KF_OK, "noop");
+    if (!x || !y) return fail(KF_ERR_NULL_POINTER, "x or y is NULL");
+    const int64_t eb = elem_bytes(x_dtype);
+    if ((uintptr_t)x % eb || (uintptr_t)y % eb) return fail(KF_ERR_BAD_ARG, "x or y is not element aligned");
+    if (!dense(ndim, shape, x_strides) || !dense(ndim, shape, y_strides))
+        return fail(KF_ERR_UNSUPPORTED_LAYOUT, "only dense row-major (NC*) tensors are supported");
+    const int64_t xb = n * eb;
+    if (x != y && overlaps(x, xb, y, xb)) return fail(KF_ERR_BAD_ARG, "x and y partially overlap");
+    const int64_t ab = shape[1] * ((weight || bias) ? elem_bytes(affine_dtype) : 0);
+    if ((weight && overlaps(weight, ab, y, xb)) || (bias && overlaps(bias, ab, y, xb)))
+        return fail(KF_ERR_BAD_ARG, "weight or bias overlaps y");
+    const int64_t spatial = ndim > 2 ? count(ndim - 2, shape + 2) : 1;
+    const size_t need = group_norm_workspace_bytes(shape[0], shape[1], spatial, num_groups, x_dtype);
+    if (!workspace || workspace_bytes < need)
+        return fail(KF_ERR_WORKSPACE, "workspace of %zu bytes given, %zu needed", workspace ? workspace_bytes : 0,
+                    need);
+    if ((uintptr_t)workspace % 256) return fail(KF_ERR_WORKSPACE, "workspace is not 256-byte aligned");
+    if (overlaps(workspace, (int64_t)need, x, xb) || overlaps(workspace, (int64_t)need, y, xb))
+        return fail(KF_ERR_BAD_ARG, "workspace overlaps x or y");
+
+    GroupNormArgs a{x,     y,    x_dtype,      shape[0],         shape[1], spatial, num_groups, weight, bias,
+                    affine_dtype, (float)eps, workspace, workspace_bytes};
+    const char* variant = nullptr;
+    s = group_norm_launch(a, static_cast<hipStream_t>(stream), &variant);
+    return done(s, variant);
+}
+
+kf_status kf_adaptive_avgpool2d(const void* x, kf_dtype dtype, void* y, int32_t ndim, const int64_t* shape,
+                                const int64_t* x_strides, const int64_t* y_strides, int64_t out_h, int64_t out_w,
+                                void* stream) {
+    begin();
+    int64_t n = 0;
+    kf_status s = check_shape(ndim, shape, 3, 4, &n);
+    if (s != KF_OK) return s;
+    if (!dtype_ok(dtype)) return fail(KF_ERR_BAD_DTYPE, "dtype %d not supported", (int)dtype);
+    const int64_t H = shape[ndim - 2], W = shape[ndim - 1];
+    if (H < 1 || W < 1) return fail(KF_ERR_BAD_SHAPE, "H and W must be >= 1");
+    if (out_h < 1 || out_w < 1) return fail(KF_ERR_BAD_ARG, "output size must be >= 1");
+    int64_t yshape[4];
+    for (int32_t i = 0; i < ndim - 2; ++i) yshape[i] = shape[i];
+    yshape[ndim - 2] = out_h;
+    yshape[ndim - 1] = out_w;
+    const int64_t ny = count(ndim, yshape);
+    if (ny < 0) return fail(KF_ERR_BAD_SHAPE, "output element count overflows int64");
+    if (n == 0) return done(KF_OK, "noop");
+    if (!x || !y) return fail(KF_ERR_NULL_POINTER, "x or y is NULL");
+    const int64_t eb = elem_bytes(dtype);
+    if ((uintptr_t)x % eb || (uintptr_t)y % eb) return fail(KF_ERR_BAD_ARG, "x or y is not element aligned");
+    if (!dense(ndim, shape, x_strides) || !dense(ndim, yshape, y_strides))
+        return fail(KF_ERR_UNSUPPORTED_LAYOUT, "only dense row-major (NCHW) tensors are supported");
+    if (overlaps(x, n * eb, y, ny * eb)) return fail(KF_ERR_BAD_ARG, "x and y overlap");
+
+    AvgPoolArgs a{x, y, dtype, n / (H * W), H, W, out_h, out_w};
+    const char* variant = nullptr;
+    s = avgpool_launch(a, static_cast<hipStream_t>(stream), &variant);
+    return done(s, variant);
+}
+
+}  // extern "C"

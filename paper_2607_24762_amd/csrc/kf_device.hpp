@@ -1,0 +1,194 @@
+// kf_device.hpp -- gfx950 device primitives shared by the libkf355 kernels:
+// 128-bit vector I/O with dtype conversion, and wave64 butterfly reductions
+// built from DPP moves and the gfx950 permlane swaps (VALU only: no LDS
+// traffic and no ds_bpermute).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace kf {
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
+
+constexpr int kWave = 64;
+
+// ---------------------------------------------------------------------------
+// Element types.  `vec` is the number of elements in one 16-byte access.
+struct F32 {
+    static constexpr int bytes = 4;
+    static constexpr int vec = 4;
+};
+struct BF16 {
+    static constexpr int bytes = 2;
+    static constexpr int vec = 8;
+};
+struct F16 {
+    static constexpr int bytes = 2;
+    static constexpr int vec = 8;
+};
+
+// Unpack one 32-bit word holding two 16-bit values (low half first).
+__device__ __forceinline__ void unpack2(BF16, uint32_t w, float& a, float& b) {
+    a = __uint_as_float(w << 16);
+    b = __uint_as_float(w & 0xffff0000u);
+}
+__device__ __forceinline__ void unpack2(F16, uint32_t w, float& a, float& b) {
+    f16x2 h = __builtin_bit_cast(f16x2, w);
+    a = (float)h[0];
+    b = (float)h[1];
+}
+// Pack two floats, each rounded to nearest-even (v_cvt_pk_bf16_f32 /
+// v_cvt_pk_f16_f32 on gfx950).
+__device__ __forceinline__ uint32_t pack2(BF16, float a, float b) {
+    bf16x2 v = {(__bf16)a, (__bf16)b};
+    return __builtin_bit_cast(uint32_t, v);
+}
+__device__ __forceinline__ uint32_t pack2(F16, float a, float b) {
+    f16x2 v = {(_Float16)a, (_Float16)b};
+    return __builtin_bit_cast(uint32_t, v);
+}
+
+// 16-byte vector load of T::vec elements at element offset `e` (e must be a
+// multiple of T::vec and the address 16-byte aligned).
+template <class T>
+__device__ __forceinline__ void load_vec(const void* base, int64_t e, float* out);
+template <>
+__device__ __forceinline__ void load_vec<F32>(const void* base, int64_t e, float* out) {
+    u32x4 v = *reinterpret_cast<const u32x4*>(static_cast<const float*>(base) + e);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) out[i] = __uint_as_float(v[i]);
+}
+template <>
+__device__ __forceinline__ void load_vec<BF16>(const void* base, int64_t e, float* out) {
+    u32x4 v = *reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(base) + e);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) unpack2(BF16{}, v[i], out[2 * i], out[2 * i + 1]);
+}
+template <>
+__device__ __forceinline__ void load_vec<F16>(const void* base, int64_t e, float* out) {
+    u32x4 v = *reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(base) + e);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) unpack2(F16{}, v[i], out[2 * i], out[2 * i + 1]);
+}
+
+template <class T>
+__device__ __forceinline__ void store_vec(void* base, int64_t e, const float* in);
+template <>
+__device__ __forceinline__ void store_vec<F32>(void* base, int64_t e, const float* in) {
+    u32x4 v;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) v[i] = __float_as_uint(in[i]);
+    *reinterpret_cast<u32x4*>(static_cast<float*>(base) + e) = v;
+}
+template <>
+__device__ __forceinline__ void store_vec<BF16>(void* base, int64_t e, const float* in) {
+    u32x4 v;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) v[i] = pack2(BF16{}, in[2 * i], in[2 * i + 1]);
+    *reinterpret_cast<u32x4*>(static_cast<uint16_t*>(base) + e) = v;
+}
+template <>
+__device__ __forceinline__ void store_vec<F16>(void* base, int64_t e, const float* in) {
+    u32x4 v;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) v[i] = pack2(F16{}, in[2 * i], in[2 * i + 1]);
+    *reinterpret_cast<u32x4*>(static_cast<uint16_t*>(base) + e) = v;
+}
+
+// Scalar element access (any alignment).
+template <class T>
+__device__ __forceinline__ float load1(const void* base, int64_t e);
+template <>
+__device__ __forceinline__ float load1<F32>(const void* base, int64_t e) {
+    return static_cast<const float*>(base)[e];
+}
+template <>
+__device__ __forceinline__ float load1<BF16>(const void* base, int64_t e) {
+    return __uint_as_float(uint32_t(static_cast<const uint16_t*>(base)[e]) << 16);
+}
+template <>
+__device__ __forceinline__ float load1<F16>(const void* base, int64_t e) {
+    return (float)static_cast<const _Float16*>(base)[e];
+}
+template <class T>
+__device__ __forceinline__ void store1(void* base, int64_t e, float v);
+template <>
+__device__ __forceinline__ void store1<F32>(void* base, int64_t e, float v) {
+    static_cast<float*>(base)[e] = v;
+}
+template <>
+__device__ __forceinline__ void store1<BF16>(void* base, int64_t e, float v) {
+    static_cast<__bf16*>(base)[e] = (__bf16)v;
+}
+template <>
+__device__ __forceinline__ void store1<F16>(void* base, int64_t e, float v) {
+    static_cast<_Float16*>(base)[e] = (_Float16)v;
+}
+
+// ---------------------------------------------------------------------------
+// Butterfly partner exchange.  Step s pairs each lane with one in the other
+// half of its aligned block of 2^(s+1) lanes; after steps 0..k-1 every lane
+// of an aligned block of 2^k lanes has combined the whole block.
+//   s=0: quad_perm [1,0,3,2]      s=1: quad_perm [2,3,0,1]
+//   s=2: row_half_mirror (i<->7-i within 8)
+//   s=3: row_mirror      (i<->15-i within 16)
+//   s=4: v_permlane16_swap (rows 0<->1, 2<->3)
+//   s=5: v_permlane32_swap (halves 0<->1)
+// Steps 2 and 3 pair a lane with a mirrored one rather than lane^4 / lane^8;
+// that is still a butterfly because each quad (half-row) is already uniform.
+template <int S>
+__device__ __forceinline__ float partner(float v) {
+    const int iv = __builtin_bit_cast(int, v);
+    if constexpr (S == 0) {
+        return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(iv, iv, 0xB1, 0xF, 0xF, false));
+    } else if constexpr (S == 1) {
+        return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(iv, iv, 0x4E, 0xF, 0xF, false));
+    } else if constexpr (S == 2) {
+        return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(iv, iv, 0x141, 0xF, 0xF, false));
+    } else if constexpr (S == 3) {
+        return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(iv, iv, 0x140, 0xF, 0xF, false));
+    } else if constexpr (S == 4) {
+        // After the swap, result[0] holds even rows duplicated, result[1] odd
+        // rows duplicated: the partner is whichever differs from this lane's row.
+        const unsigned u = __builtin_bit_cast(unsigned, v);
+        auto r = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+        const bool odd_row = (__lane_id() >> 4) & 1;
+        return __builtin_bit_cast(float, odd_row ? r[0] : r[1]);
+    } else {
+        const unsigned u = __builtin_bit_cast(unsigned, v);
+        auto r = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+        const bool upper = __lane_id() >= 32;
+        return __builtin_bit_cast(float, upper ? r[0] : r[1]);
+    }
+}
+
+struct OpMax {
+    __device__ __forceinline__ float operator()(float a, float b) const { return fmaxf(a, b); }
+};
+struct OpSum {
+    __device__ __forceinline__ float operator()(float a, float b) const { return a + b; }
+};
+
+// Reduce over aligned groups of LANES lanes (a power of two <= 64); every
+// lane of a group receives the group's result.  The combine must be
+// commutative so that both lanes of a pair compute the same value.
+template <int LANES, class Op>
+__device__ __forceinline__ float group_reduce(float v, Op op) {
+    if constexpr (LANES >= 2) v = op(v, partner<0>(v));
+    if constexpr (LANES >= 4) v = op(v, partner<1>(v));
+    if constexpr (LANES >= 8) v = op(v, partner<2>(v));
+    if constexpr (LANES >= 16) v = op(v, partner<3>(v));
+    if constexpr (LANES >= 32) v = op(v, partner<4>(v));
+    if constexpr (LANES >= 64) v = op(v, partner<5>(v));
+    return v;
+}
+
+// Uniform value of lane 0 (SGPR broadcast).
+__device__ __forceinline__ float uniform0(float v) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_readfirstlane(__builtin_bit_cast(int, v)));
+}
+
+}  // namespace kf

@@ -1,0 +1,51 @@
+// kf_internal.h -- interfaces between the C-ABI layer (kf355_api.cpp) and
+// the per-operator launch code (*.hip).  Arguments arrive here already
+// validated: shapes non-empty, dtypes legal, layouts dense.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "kf355.h"
+
+namespace kf {
+
+// Softmax over the middle axis of a dense [outer, len, inner] view.
+struct SoftmaxArgs {
+    const void* x;
+    void* y;
+    kf_dtype xt, yt;
+    int64_t outer, len, inner;
+};
+kf_status softmax_launch(const SoftmaxArgs& a, hipStream_t s, const char** variant);
+
+// GroupNorm over a dense [n, c, spatial] view.
+struct GroupNormArgs {
+    const void* x;
+    void* y;
+    kf_dtype xt;
+    int64_t n, c, spatial, groups;
+    const void* weight;
+    const void* bias;
+    kf_dtype at;
+    float eps;
+    void* workspace;
+    size_t workspace_bytes;
+};
+size_t group_norm_workspace_bytes(int64_t n, int64_t c, int64_t spatial, int64_t groups, kf_dtype xt);
+kf_status group_norm_launch(const GroupNormArgs& a, hipStream_t s, const char** variant);
+
+// adaptive_avg_pool2d over a dense [planes, h, w] view -> [planes, oh, ow].
+struct AvgPoolArgs {
+    const void* x;
+    void* y;
+    kf_dtype t;
+    int64_t planes, h, w, oh, ow;
+};
+kf_status avgpool_launch(const AvgPoolArgs& a, hipStream_t s, const char** variant);
+
+// Records the detail text of the current failure (thread-local).
+void set_error(const char* fmt, ...);
+
+}  // namespace kf

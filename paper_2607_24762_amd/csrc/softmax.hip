@@ -1,0 +1,426 @@
+// softmax.hip -- row softmax for gfx950 (PyTorch `softmax(x, dim)` semantics,
+// the operator behind the paper's Gemma 4 E2B and Qwen 3.5 softmax results,
+// Section IV-C).
+//
+// Every variant makes one pass over HBM for reading and one for writing when
+// the row fits on chip:
+//   sm_wave   LPR lanes own a row (LPR = 1..64, so 64/LPR rows per wave); the
+//             row stays in registers; max and sum are butterfly reductions
+//             inside the lane group; no LDS, no barriers.
+//   sm_block  one workgroup owns a row held in registers; per-wave partials
+//             are combined through LDS.
+//   sm_stream one workgroup per row of any length: an online (max, sum) pass,
+//             then a write pass that reads the row again.
+//   sm_cols   softmax over a non-innermost axis: one thread per column,
+//             online pass then write pass, coalesced across the inner axis.
+#include <math.h>
+
+#include "kf_device.hpp"
+#include "kf_internal.h"
+
+namespace kf {
+namespace {
+
+constexpr float kLog2e = 1.4426950408889634f;
+
+// e^(x - m) as 2^((x - m) * log2 e): subtracting first keeps x == m exact
+// (2^0 = 1), so a uniform row gives exactly 1/L and a one-hot row exactly 1.
+// The hardware exp2 (v_exp_f32) flushes results below 2^-126 to zero; those
+// arguments are evaluated as 2^(t + 64) * 2^-64 so subnormal results (which
+// bf16 outputs can represent) stay exact, as with the IEEE definition.
+__device__ __forceinline__ float exp_shifted(float x, float m) {
+    const float t = (x - m) * kLog2e;
+    const bool tiny = t < -126.f;
+    const float e = __builtin_amdgcn_exp2f(tiny ? t + 64.f : t);
+    return tiny ? e * 0x1p-64f : e;
+}
+
+// Writes `n` floats (n * sizeof(TO) is a multiple of 16 bytes) starting at
+// element e, as 16-byte stores.
+template <class TO, int N>
+__device__ __forceinline__ void store_span(void* y, int64_t e, const float* v) {
+    static_assert((N % TO::vec) == 0, "span must be whole vectors");
+#pragma unroll
+    for (int i = 0; i < N / TO::vec; ++i) store_vec<TO>(y, e + i * TO::vec, v + i * TO::vec);
+}
+
+// Sets slots outside the row (or of a row past the end) to -inf; slot k of
+// lane-in-row `lr` starts at element (lr + k * STRIDE) * VEC.
+template <int NV, int VEC, int STRIDE>
+__device__ __forceinline__ void mask_slots(float (&v)[NV][VEC], int lr, bool row_ok, int32_t len) {
+#pragma unroll
+    for (int k = 0; k < NV; ++k) {
+        const bool ok = row_ok && (lr + k * STRIDE) * VEC < len;
+#pragma unroll
+        for (int i = 0; i < VEC; ++i) v[k][i] = ok ? v[k][i] : -INFINITY;
+    }
+}
+
+// --------------------------------------------------------------------------
+// Register-resident rows, LPR lanes per row.
+template <class TI, class TO, int LPR, int NV, bool VECTOR>
+__global__ __launch_bounds__(256) void sm_wave(const void* __restrict__ x, void* __restrict__ y,
+                                               int64_t rows, int32_t len) {
+    constexpr int VEC = VECTOR ? TI::vec : 1;
+    constexpr int RPW = kWave / LPR;
+    const int lane = threadIdx.x & (kWave - 1);
+    const int lr = lane & (LPR - 1);
+    const int64_t row = ((int64_t)blockIdx.x * (blockDim.x / kWave) + (threadIdx.x / kWave)) * RPW + lane / LPR;
+    const bool row_ok = row < rows;
+    const int64_t base = row * (int64_t)len;
+
+    // Every slot is loaded unconditionally (an out-of-range slot re-reads
+    // element 0, which always exists) so the loads issue back to back with no
+    // wait between them; out-of-range slots are then set to -inf, in a branch
+    // taken only by waves that have any.
+    float v[NV][VEC];
+    const bool full = row_ok && (LPR * NV * VEC == len);
+#pragma unroll
+    for (int k = 0; k < NV; ++k) {
+        const int e0 = (lr + k * LPR) * VEC;
+        const int64_t at = (row_ok && e0 < len) ? base + e0 : 0;
+        if constexpr (VECTOR) load_vec<TI>(x, at, v[k]);
+        else v[k][0] = load1<TI>(x, at);
+    }
+    if (!__all(full)) mask_slots<NV, VEC, LPR>(v, lr, row_ok, len);
+    float m = -INFINITY;
+#pragma unroll
+    for (int k = 0; k < NV; ++k)
+#pragma unroll
+        for (int i = 0; i < VEC; ++i) m = fmaxf(m, v[k][i]);
+    m = group_reduce<LPR>(m, OpMax{});
+
+    float s = 0.f;
+#pragma unroll
+    for (int k = 0; k < NV; ++k)
+#pragma unroll
+        for (int i = 0; i < VEC; ++i) {
+            v[k][i] = exp_shifted(v[k][i], m);
+            s += v[k][i];
+        }
+    s = group_reduce<LPR>(s, OpSum{});
+    const float inv = 1.f / s;
+
+#pragma unroll
+    for (int k = 0; k < NV; ++k) {
+        const int e0 = (lr + k * LPR) * VEC;
+        if (row_ok && e0 < len) {
+#pragma unroll
+            for (int i = 0; i < VEC; ++i) v[k][i] *= inv;
+            if constexpr (VECTOR) store_span<TO, VEC>(y, base + e0, v[k]);
+            else store1<TO>(y, base + e0, v[k][0]);
+        }
+    }
+}
+
+// --------------------------------------------------------------------------
+// Register-resident rows, one workgroup of NT threads per row.
+template <int NW, class Op>
+__device__ __forceinline__ float block_reduce(float v, Op op, float* red) {
+    v = group_reduce<kWave>(v, op);
+    const int w = threadIdx.x / kWave;
+    if ((threadIdx.x & (kWave - 1)) == 0) red[w] = v;
+    __syncthreads();
+    float r = red[0];
+#pragma unroll
+    for (int i = 1; i < NW; ++i) r = op(r, red[i]);
+    __syncthreads();  // red[] is reused by the next reduction
+    return r;
+}
+
+template <class TI, class TO, int NT, int NV, bool VECTOR>
+__global__ __launch_bounds__(NT) void sm_block(const void* __restrict__ x, void* __restrict__ y,
+                                               int32_t len) {
+    constexpr int VEC = VECTOR ? TI::vec : 1;
+    constexpr int NW = NT / kWave;
+    __shared__ float red[NW];
+    const int64_t base = (int64_t)blockIdx.x * len;
+
+    // Unconditional loads (out-of-range slots re-read the row's first
+    // element), then masking, as in sm_wave.
+    float v[NV][VEC];
+#pragma unroll
+    for (int k = 0; k < NV; ++k) {
+        const int e0 = (threadIdx.x + k * NT) * VEC;
+        const int64_t at = base + (e0 < len ? e0 : 0);
+        if constexpr (VECTOR) load_vec<TI>(x, at, v[k]);
+        else v[k][0] = load1<TI>(x, at);
+    }
+    if (NT * NV * VEC != len) mask_slots<NV, VEC, NT>(v, threadIdx.x, true, len);
+    float m = -INFINITY;
+#pragma unroll
+    for (int k = 0; k < NV; ++k)
+#pragma unroll
+        for (int i = 0; i < VEC; ++i) m = fmaxf(m, v[k][i]);
+    m = block_reduce<NW>(m, OpMax{}, red);
+
+    float s = 0.f;
+#pragma unroll
+    for (int k = 0; k < NV; ++k)
+#pragma unroll
+        for (int i = 0; i < VEC; ++i) {
+            v[k][i] = exp_shifted(v[k][i], m);
+            s += v[k][i];
+        }
+    s = block_reduce<NW>(s, OpSum{}, red);
+    const float inv = 1.f / s;
+
+#pragma unroll
+    for (int k = 0; k < NV; ++k) {
+        const int e0 = (threadIdx.x + k * NT) * VEC;
+        if (e0 < len) {
+#pragma unroll
+            for (int i = 0; i < VEC; ++i) v[k][i] *= inv;
+            if constexpr (VECTOR) store_span<TO, VEC>(y, base + e0, v[k]);
+            else store1<TO>(y, base + e0, v[k][0]);
+        }
+    }
+}
+
+// --------------------------------------------------------------------------
+// Online normaliser state (m, s): s = sum of e^(x - m) over the elements
+// seen.  A state with m = -inf has seen only -inf (or nothing) and weighs 0.
+struct MS {
+    float m, s;
+};
+__device__ __forceinline__ MS ms_merge(MS a, MS b) {
+    const float mm = fmaxf(a.m, b.m);
+    const float sa = (a.m == -INFINITY) ? 0.f : a.s * exp_shifted(a.m, mm);
+    const float sb = (b.m == -INFINITY) ? 0.f : b.s * exp_shifted(b.m, mm);
+    return MS{mm, sa + sb};
+}
+// Folds a chunk of n values into the state.
+template <int N>
+__device__ __forceinline__ MS ms_add(MS st, const float* v) {
+    float cm = v[0];
+#pragma unroll
+    for (int i = 1; i < N; ++i) cm = fmaxf(cm, v[i]);
+    const float mm = fmaxf(st.m, cm);
+    if (mm == -INFINITY) return st;  // nothing but -inf so far
+    float s = (st.m == -INFINITY) ? 0.f : st.s * exp_shifted(st.m, mm);
+#pragma unroll
+    for (int i = 0; i < N; ++i) s += exp_shifted(v[i], mm);
+    return MS{mm, s};
+}
+template <int S>
+__device__ __forceinline__ MS ms_partner(MS a) {
+    return MS{partner<S>(a.m), partner<S>(a.s)};
+}
+// Merge across a whole wave; ms_merge is commutative, so both lanes of a
+// pair hold the same state after each step.
+__device__ __forceinline__ MS ms_wave(MS a) {
+    a = ms_merge(a, ms_partner<0>(a));
+    a = ms_merge(a, ms_partner<1>(a));
+    a = ms_merge(a, ms_partner<2>(a));
+    a = ms_merge(a, ms_partner<3>(a));
+    a = ms_merge(a, ms_partner<4>(a));
+    a = ms_merge(a, ms_partner<5>(a));
+    return a;
+}
+
+template <class TI, class TO, int NT, bool VECTOR>
+__global__ __launch_bounds__(NT) void sm_stream(const void* __restrict__ x, void* __restrict__ y,
+                                                int64_t len) {
+    constexpr int VEC = VECTOR ? TI::vec : 1;
+    constexpr int NW = NT / kWave;
+    __shared__ float red_m[NW], red_s[NW];
+    const int64_t base = (int64_t)blockIdx.x * len;
+
+    // Pass 1: DEPTH loads in flight per thread per iteration; slots past the
+    // end read as -inf, which ms_add ignores.
+    constexpr int DEPTH = 4;
+    MS st{-INFINITY, 0.f};
+    for (int64_t e0 = (int64_t)threadIdx.x * VEC; e0 < len; e0 += (int64_t)DEPTH * NT * VEC) {
+        float v[DEPTH * VEC];
+#pragma unroll
+        for (int d = 0; d < DEPTH; ++d) {
+            const int64_t e = e0 + (int64_t)d * NT * VEC;
+            if (e < len) {
+                if constexpr (VECTOR) load_vec<TI>(x, base + e, v + d * VEC);
+                else v[d] = load1<TI>(x, base + e);
+            } else {
+#pragma unroll
+                for (int i = 0; i < VEC; ++i) v[d * VEC + i] = -INFINITY;
+            }
+        }
+        st = ms_add<DEPTH * VEC>(st, v);
+    }
+    st = ms_wave(st);
+    const int w = threadIdx.x / kWave;
+    if ((threadIdx.x & (kWave - 1)) == 0) {
+        red_m[w] = st.m;
+        red_s[w] = st.s;
+    }
+    __syncthreads();
+    MS tot{red_m[0], red_s[0]};
+#pragma unroll
+    for (int i = 1; i < NW; ++i) tot = ms_merge(tot, MS{red_m[i], red_s[i]});
+    // A row of only -inf keeps m = -inf, so x - m is NaN below: a NaN row,
+    // as PyTorch gives.
+    const float inv = 1.f / tot.s;
+
+    for (int64_t e0 = (int64_t)threadIdx.x * VEC; e0 < len; e0 += (int64_t)DEPTH * NT * VEC) {
+        float v[DEPTH][VEC];
+#pragma unroll
+        for (int d = 0; d < DEPTH; ++d) {
+            const int64_t e = e0 + (int64_t)d * NT * VEC;
+            if (e < len) {
+                if constexpr (VECTOR) load_vec<TI>(x, base + e, v[d]);
+                else v[d][0] = load1<TI>(x, base + e);
+            }
+        }
+#pragma unroll
+        for (int d = 0; d < DEPTH; ++d) {
+            const int64_t e = e0 + (int64_t)d * NT * VEC;
+            if (e < len) {
+#pragma unroll
+                for (int i = 0; i < VEC; ++i) v[d][i] = exp_shifted(v[d][i], tot.m) * inv;
+                if constexpr (VECTOR) store_span<TO, VEC>(y, base + e, v[d]);
+                else store1<TO>(y, base + e, v[d][0]);
+            }
+        }
+    }
+}
+
+// --------------------------------------------------------------------------
+// Softmax over a non-innermost axis of [outer, len, inner]: thread per
+// (outer, inner) column; neighbouring threads read neighbouring addresses.
+template <class TI, class TO>
+__global__ __launch_bounds__(256) void sm_cols(const void* __restrict__ x, void* __restrict__ y,
+                                               int64_t outer, int64_t len, int64_t inner) {
+    const int64_t col = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (col >= outer * inner) return;
+    const int64_t o = col / inner, i = col - o * inner;
+    const int64_t base = o * len * inner + i;
+    constexpr int DEPTH = 4;
+    MS st{-INFINITY, 0.f};
+    for (int64_t j0 = 0; j0 < len; j0 += DEPTH) {
+        float v[DEPTH];
+#pragma unroll
+        for (int d = 0; d < DEPTH; ++d) v[d] = (j0 + d < len) ? load1<TI>(x, base + (j0 + d) * inner) : -INFINITY;
+        st = ms_add<DEPTH>(st, v);
+    }
+    const float inv = 1.f / st.s;
+    for (int64_t j = 0; j < len; ++j)
+        store1<TO>(y, base + j * inner, exp_shifted(load1<TI>(x, base + j * inner), st.m) * inv);
+}
+
+// --------------------------------------------------------------------------
+// Variant selection.
+template <class TI, class TO, int LPR, int NV, bool VECTOR>
+void go_wave(const SoftmaxArgs& a, hipStream_t s) {
+    constexpr int rows_per_block = (256 / kWave) * (kWave / LPR);
+    const int64_t blocks = (a.outer + rows_per_block - 1) / rows_per_block;
+    hipLaunchKernelGGL((sm_wave<TI, TO, LPR, NV, VECTOR>), dim3((unsigned)blocks), dim3(256), 0, s,
+                       a.x, a.y, a.outer, (int32_t)a.len);
+}
+template <class TI, class TO, int NT, int NV, bool VECTOR>
+void go_block(const SoftmaxArgs& a, hipStream_t s) {
+    hipLaunchKernelGGL((sm_block<TI, TO, NT, NV, VECTOR>), dim3((unsigned)a.outer), dim3(NT), 0, s,
+                       a.x, a.y, (int32_t)a.len);
+}
+
+struct Choice {
+    void (*fn)(const SoftmaxArgs&, hipStream_t);
+    const char* name;
+};
+
+// Smallest register-resident configuration whose capacity covers the row.
+// Capacity = LPR * NV * VEC elements per row; per-lane data is kept to at
+// most 64 floats so several waves fit per SIMD.
+template <class TI, class TO, bool VECTOR>
+Choice pick_resident(int64_t len) {
+    constexpr int VEC = VECTOR ? TI::vec : 1;
+    const int64_t slots = (len + VEC - 1) / VEC;
+#define KF_WAVE(LPR, NV)                                                                       \
+    if (slots <= (int64_t)(LPR) * (NV))                                                        \
+        return Choice{go_wave<TI, TO, LPR, NV, VECTOR>, VECTOR ? "sm_wave_vec_lpr" #LPR "_nv" #NV \
+                                                               : "sm_wave_scalar_lpr" #LPR "_nv" #NV};
+    KF_WAVE(1, 1)
+    KF_WAVE(2, 1)
+    KF_WAVE(4, 1)
+    KF_WAVE(8, 1)
+    KF_WAVE(16, 1)
+    KF_WAVE(16, 2)
+    KF_WAVE(16, 4)
+    KF_WAVE(32, 4)
+    KF_WAVE(64, 4)
+    KF_WAVE(64, 8)
+    if constexpr (!VECTOR || TI::vec == 4) {
+        KF_WAVE(64, 16)
+    }
+#undef KF_WAVE
+#define KF_BLOCK(NT, NV)                                                                         \
+    if (slots <= (int64_t)(NT) * (NV))                                                           \
+        return Choice{go_block<TI, TO, NT, NV, VECTOR>, VECTOR ? "sm_block_vec_nt" #NT "_nv" #NV \
+                                                               : "sm_block_scalar_nt" #NT "_nv" #NV};
+    KF_BLOCK(256, 8)
+    KF_BLOCK(512, 8)
+    KF_BLOCK(1024, 8)
+    if constexpr (!VECTOR || TI::vec == 4) {
+        KF_BLOCK(1024, 16)
+    }
+#undef KF_BLOCK
+    return Choice{nullptr, nullptr};
+}
+
+template <class TI, class TO>
+kf_status run(const SoftmaxArgs& a, hipStream_t s, const char** variant) {
+    if (a.inner != 1) {
+        const int64_t cols = a.outer * a.inner;
+        const int64_t blocks = (cols + 255) / 256;
+        if (blocks > INT32_MAX) {
+            set_error("softmax: %lld columns exceed the grid limit", (long long)cols);
+            return KF_ERR_UNSUPPORTED_LAYOUT;
+        }
+        hipLaunchKernelGGL((sm_cols<TI, TO>), dim3((unsigned)blocks), dim3(256), 0, s, a.x, a.y, a.outer,
+                           a.len, a.inner);
+        *variant = "sm_cols";
+    } else {
+        // Every kernel below puts at most one row per thread block index
+        // group; keep the grid inside the 32-bit limit.
+        if (a.outer > (int64_t)INT32_MAX) {
+            set_error("softmax: %lld rows exceed the grid limit", (long long)a.outer);
+            return KF_ERR_UNSUPPORTED_LAYOUT;
+        }
+        // 16-byte vectors need the row length to be whole vectors of both the
+        // input and the output, and both base pointers 16-byte aligned.
+        const bool vec_ok = (a.len % TI::vec == 0) && (a.len % TO::vec == 0) &&
+                            ((uintptr_t)a.x % 16 == 0) && ((uintptr_t)a.y % 16 == 0);
+        Choice c{nullptr, nullptr};
+        if (a.len <= INT32_MAX)
+            c = vec_ok ? pick_resident<TI, TO, true>(a.len) : pick_resident<TI, TO, false>(a.len);
+        if (c.fn) {
+            c.fn(a, s);
+            *variant = c.name;
+        } else if (vec_ok) {
+            hipLaunchKernelGGL((sm_stream<TI, TO, 1024, true>), dim3((unsigned)a.outer), dim3(1024), 0, s,
+                               a.x, a.y, a.len);
+            *variant = "sm_stream_vec";
+        } else {
+            hipLaunchKernelGGL((sm_stream<TI, TO, 1024, false>), dim3((unsigned)a.outer), dim3(1024), 0, s,
+                               a.x, a.y, a.len);
+            *variant = "sm_stream_scalar";
+        }
+    }
+    const hipError_t err = hipGetLastError();
+    if (err != hipSuccess) {
+        set_error("softmax launch failed: %s", hipGetErrorString(err));
+        return KF_ERR_HIP;
+    }
+    return KF_OK;
+}
+
+}  // namespace
+
+kf_status softmax_launch(const SoftmaxArgs& a, hipStream_t s, const char** variant) {
+    if (a.xt == KF_FLOAT32 && a.yt == KF_FLOAT32) return run<F32, F32>(a, s, variant);
+    if (a.xt == KF_BFLOAT16 && a.yt == KF_BFLOAT16) return run<BF16, BF16>(a, s, variant);
+    if (a.xt == KF_BFLOAT16 && a.yt == KF_FLOAT32) return run<BF16, F32>(a, s, variant);
+    if (a.xt == KF_FLOAT16 && a.yt == KF_FLOAT16) return run<F16, F16>(a, s, variant);
+    if (a.xt == KF_FLOAT16 && a.yt == KF_FLOAT32) return run<F16, F32>(a, s, variant);
+    set_error("softmax: unsupported dtype pair");
+    return KF_ERR_BAD_DTYPE;
+}
+
+}  // namespace kf

@@ -1,0 +1,165 @@
+"""Host-side tests of the C ABI (no GPU needed): the library loads, exports
+every function include/kf355.h declares, and rejects bad arguments on the
+host before any HIP call.  Only argument errors and zero-element no-ops are
+exercised here, so nothing is ever launched; fake device addresses are never
+dereferenced."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2607_24762_amd import kf355
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "kf355.h")
+
+F32, BF16, F16 = 0, 1, 2
+OK, NULLP, SHAPE, DTYPE, ARG, LAYOUT, WS, HIP = range(8)
+FAKE = 0x7F0000000000          # a 256-byte aligned "device" address, never touched
+
+
+@pytest.fixture(scope="module")
+def lib():
+    import torch
+    # The fake addresses below must never reach a real device: these tests
+    # only run where no GPU is visible.
+    if torch.cuda.is_available():
+        pytest.skip("host-only ABI tests use fake device addresses")
+    if not os.path.exists(kf355.LIB_PATH):
+        pytest.skip("libkf355.so not built (run __graft_entry__.build())")
+    return kf355.lib()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(kf_\w+)\s*\(", text)))
+
+
+def test_header_and_binding_agree():
+    assert declared_functions() == sorted(kf355._SIGNATURES)
+
+
+def test_every_declared_symbol_is_exported(lib):
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+
+
+def test_version_and_status_names(lib):
+    assert lib.kf_abi_version() == 1
+    for code, name in kf355.STATUS_NAMES.items():
+        assert lib.kf_status_name(code).decode() == name
+    assert lib.kf_status_name(99).decode() == "KF_UNKNOWN"
+
+
+def arr(vals):
+    return (ctypes.c_int64 * max(len(vals), 1))(*vals)
+
+
+def softmax(lib, x=FAKE, xt=F32, y=FAKE + (1 << 30), yt=F32, shape=(4, 8), xs=None, ys=None, dim=-1, ndim=None):
+    nd = len(shape) if ndim is None else ndim
+    return lib.kf_softmax(ctypes.c_void_p(x), xt, ctypes.c_void_p(y), yt, nd,
+                          arr(shape) if shape is not None else None,
+                          arr(xs) if xs else None, arr(ys) if ys else None, dim, None)
+
+
+def err(lib):
+    return lib.kf_last_error().decode()
+
+
+def test_softmax_rejections(lib):
+    assert softmax(lib, ndim=9, shape=(1,) * 9) == SHAPE
+    assert softmax(lib, ndim=2, shape=None) == NULLP
+    assert softmax(lib, shape=(4, -1)) == SHAPE
+    assert softmax(lib, xt=7) == DTYPE
+    assert softmax(lib, xt=F32, yt=BF16) == DTYPE          # narrowing is not softmax's dtype=
+    assert softmax(lib, dim=2) == ARG and "dim" in err(lib)
+    assert softmax(lib, dim=-3) == ARG
+    assert softmax(lib, x=0) == NULLP
+    assert softmax(lib, x=FAKE + 2) == ARG                 # fp32 needs 4-byte alignment
+    assert softmax(lib, xs=(1, 4)) == LAYOUT               # transposed view
+    assert softmax(lib, y=FAKE + 64) == ARG                # partial overlap
+    assert softmax(lib, y=FAKE, xt=BF16, yt=F32) == ARG    # in place needs equal dtypes
+    assert softmax(lib, shape=(4, 2**62, 4)) == SHAPE      # element count overflows
+
+
+def test_softmax_zero_elements_is_a_noop(lib):
+    assert softmax(lib, shape=(0, 8)) == OK
+    assert lib.kf_last_variant().decode() == "noop"
+    assert softmax(lib, x=0, y=0, shape=(5, 0)) == OK      # nothing to touch, NULL allowed
+    assert softmax(lib, shape=(0,), dim=0) == OK
+
+
+def test_softmax_size_one_dims_may_have_any_stride(lib):
+    # [1, 0] has no elements; a size-1 leading dim with an odd stride is dense.
+    assert softmax(lib, shape=(1, 0), xs=(12345, 1)) == OK
+
+
+def gn(lib, shape=(2, 8, 4, 4), groups=4, w=None, b=None, at=F32, eps=1e-5, ws=FAKE + (2 << 30), wsb=1 << 20,
+       xt=F32, x=FAKE, y=FAKE + (1 << 30), xs=None):
+    return lib.kf_group_norm(ctypes.c_void_p(x), xt, ctypes.c_void_p(y), len(shape), arr(shape),
+                             arr(xs) if xs else None, None, groups, ctypes.c_void_p(w), ctypes.c_void_p(b), at,
+                             eps, ctypes.c_void_p(ws), wsb, None)
+
+
+def gn_ws(lib, shape, groups, xt=BF16):
+    n = ctypes.c_size_t(0)
+    st = lib.kf_group_norm_workspace_bytes(xt, len(shape), arr(shape), groups, ctypes.byref(n))
+    return st, n.value
+
+
+def test_group_norm_rejections(lib):
+    assert gn(lib, shape=(8,)) == SHAPE
+    assert gn(lib, groups=3) == ARG and "divisible" in err(lib)
+    assert gn(lib, groups=0) == ARG
+    assert gn(lib, eps=-1.0) == ARG
+    assert gn(lib, eps=float("nan")) == ARG
+    assert gn(lib, xt=BF16, w=FAKE + (3 << 30), at=F16) == DTYPE
+    assert gn(lib, ws=0) == WS
+    assert gn(lib, wsb=16) == WS
+    assert gn(lib, ws=FAKE + (2 << 30) + 64) == WS         # not 256-byte aligned
+    assert gn(lib, xs=(128, 16, 4, 2)) == LAYOUT          # channels-last strides
+    assert gn(lib, y=FAKE + 128) == ARG                   # partial overlap
+    assert gn(lib, w=FAKE + (1 << 30) + 64) == ARG        # weight inside y
+    assert gn(lib, ws=FAKE) == ARG                        # workspace overlaps x
+
+
+def test_group_norm_zero_elements_and_workspace_query(lib):
+    assert gn(lib, shape=(0, 8, 4, 4), ws=0, wsb=0) == OK
+    st, n = gn_ws(lib, (0, 8, 4), 2)
+    assert st == OK and n == 0
+    st, n = gn_ws(lib, (1, 512, 128, 128), 32)
+    # 32 groups x 16 chunks of 16384 elements: 8-byte (mean, M2) partials,
+    # then one 256-byte counter line per group, then the 256-byte error block.
+    assert st == OK and n == 32 * 16 * 8 + 32 * 256 + 256
+    st, _ = gn_ws(lib, (1, 6, 4), 4)
+    assert st == ARG
+    assert lib.kf_group_norm_workspace_bytes(F32, 2, arr((2, 4)), 2, None) == NULLP
+
+
+def ap(lib, shape=(2, 3, 7, 7), oh=1, ow=1, x=FAKE, y=FAKE + (1 << 30), xt=F32, xs=None, ys=None):
+    return lib.kf_adaptive_avgpool2d(ctypes.c_void_p(x), xt, ctypes.c_void_p(y), len(shape), arr(shape),
+                                     arr(xs) if xs else None, arr(ys) if ys else None, oh, ow, None)
+
+
+def test_avgpool_rejections(lib):
+    assert ap(lib, shape=(7, 7)) == SHAPE
+    assert ap(lib, shape=(1, 2, 3, 4, 5)) == SHAPE
+    assert ap(lib, shape=(2, 3, 0, 7)) == SHAPE
+    assert ap(lib, oh=0) == ARG
+    assert ap(lib, y=FAKE + 64) == ARG                    # overlaps x
+    assert ap(lib, xs=(147, 1, 21, 3)) == LAYOUT          # channels-last
+    assert ap(lib, xt=5) == DTYPE
+    assert ap(lib, x=0) == NULLP
+
+
+def test_avgpool_zero_planes_is_a_noop(lib):
+    assert ap(lib, shape=(0, 3, 7, 7)) == OK
+    assert lib.kf_last_variant().decode() == "noop"
+
+
+def test_binding_refuses_cpu_tensors(lib):
+    import torch
+    with pytest.raises(ValueError):
+        kf355.kf_softmax(torch.zeros(4, 4))

@@ -1,0 +1,87 @@
+"""GPU parity of kf_adaptive_avgpool2d against the float64 oracle: 1x1
+outputs over plane sizes that select each LDS tiling (1, 4, 16 and 64
+threads per plane) and the plane-per-workgroup kernel, ragged plane counts,
+misaligned inputs, generic output sizes and 3-D inputs, in fp32 / bf16 /
+fp16.  Tolerances: fp32 max abs error <= 1e-6; bf16 / fp16 within 1 unit in
+the last place of the oracle rounded once."""
+import pytest
+import torch
+
+from compare import assert_close, note
+from oracle import oracle
+from paper_2607_24762_amd import kf355
+from paper_2607_24762_amd.workloads import randn
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU visible")
+    kf355.lib()
+
+
+def relu_input(shape, dt, seed):
+    return torch.relu(randn(shape, "f32", seed=seed)).to({"f32": torch.float32, "bf16": torch.bfloat16,
+                                                           "f16": torch.float16}[dt])
+
+
+def run(x_cpu, out, dt, x_gpu=None):
+    x = x_gpu if x_gpu is not None else x_cpu.cuda()
+    y = kf355.kf_adaptive_avgpool2d(x, out)
+    torch.cuda.synchronize()
+    variant = kf355.last_variant()
+    assert_close(y, oracle.adaptive_avg_pool2d(x_cpu, out), dt)
+    return variant
+
+
+ONE_BY_ONE = [
+    ((2, 3, 7, 7), "ap_flat_tps4"),         # 49-element planes: 64 per workgroup
+    ((4, 100, 7, 7), "ap_flat_tps4"),       # 400 planes: ragged last workgroup
+    ((32, 2048, 7, 7), "ap_flat_tps4"),     # the ResNet-50 head
+    ((3, 5, 1, 1), "ap_flat_tps1"),
+    ((1, 7, 3, 3), "ap_flat_tps1"),
+    ((2, 8, 4, 5), "ap_flat_tps2"),
+    ((2, 64, 8, 8), "ap_flat_tps4"),        # even plane size
+    ((2, 40, 10, 10), "ap_flat_tps8"),
+    ((2, 64, 14, 14), "ap_flat_tps16"),
+    ((1, 16, 20, 20), "ap_flat_tps32"),
+    ((2, 16, 28, 28), "ap_flat_tps64"),
+    ((1, 8, 56, 56), "ap_plane"),
+    ((1, 3, 224, 224), "ap_plane"),
+    ((1, 2, 37, 41), "ap_plane"),           # odd plane: scalar loads
+]
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16", "f16"])
+@pytest.mark.parametrize("shape,variant", ONE_BY_ONE, ids=lambda v: str(v))
+def test_one_by_one(shape, variant, dt):
+    note(f"avgpool 1x1 {shape} {dt}")
+    assert run(relu_input(shape, dt, 1), (1, 1), dt) == variant
+
+
+@pytest.mark.parametrize("shape,out", [((2, 3, 7, 7), (3, 3)), ((1, 2, 13, 17), (5, 7)), ((1, 1, 4, 6), (8, 9)),
+                                       ((3, 10, 9), (4, 2)), ((2, 4, 7, 7), (7, 7)), ((1, 2, 5, 5), (1, 3))])
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+def test_generic_sizes(shape, out, dt):
+    note(f"avgpool {shape}->{out} {dt}")
+    assert run(relu_input(shape, dt, 2), out, dt) == "ap_window"
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+def test_misaligned_input(dt):
+    note(f"avgpool misaligned {dt}")
+    planes, s = 300, 49
+    big = relu_input((planes * s + 1,), dt, 3)
+    x_cpu = big[1:].view(3, 100, 7, 7)
+    x = big.cuda()[1:].view(3, 100, 7, 7)
+    run(x_cpu, (1, 1), dt, x_gpu=x)
+
+
+def test_constant_input_is_exact():
+    note("avgpool constant")
+    x = torch.full((4, 96, 7, 7), 0.375, device="cuda")
+    y = kf355.kf_adaptive_avgpool2d(x, 1)
+    torch.cuda.synchronize()
+    assert (y == 0.375).all()

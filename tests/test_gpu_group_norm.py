@@ -1,0 +1,135 @@
+"""GPU parity of kf_group_norm against the float64 oracle across shapes that
+exercise every path: single-chunk groups, fused multi-chunk groups with the
+cooperative cross-workgroup combine, the two-kernel path for grids that
+cannot be co-resident, scalar (non-vectorisable) layouts, every dtype and
+affine combination, in-place use, determinism and workspace hygiene.
+
+Tolerances: bf16 / fp16 outputs within 1 unit in the last place of the
+oracle rounded once, except where |oracle| < 2^-19: there an absolute error
+<= 2^-22 is also accepted (fp32 statistics cannot resolve a bf16 ulp that
+small; strict counts are reported).  fp32 outputs: |error| <= 1e-6 plus
+4 fp32 ulps of the result (rstd and the normalised value each carry a few
+roundings at magnitudes up to ~5)."""
+import numpy as np
+import pytest
+import torch
+
+from compare import assert_close, note
+from oracle import oracle
+from paper_2607_24762_amd import kf355
+from paper_2607_24762_amd.workloads import randn
+
+pytestmark = pytest.mark.gpu
+TORCH = {"f32": torch.float32, "bf16": torch.bfloat16, "f16": torch.float16}
+FLOOR = (2.0 ** -19, 2.0 ** -22)
+
+
+@pytest.fixture(scope="module", autouse=True)
+def gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU visible")
+    kf355.lib()
+
+
+def check(y, ref, dt):
+    if dt == "f32":
+        g = y.cpu().double().numpy()
+        err = np.abs(g - ref)
+        lim = 1e-6 + 4 * np.abs(ref) * 2.0 ** -24
+        assert np.all(err <= lim), float((err - lim).max())
+        return
+    assert_close(y, ref, dt, floor=FLOOR)
+
+
+def run(shape, groups, dt, affine="same", eps=1e-6, seed=0, mean=0.3, std=1.5, in_place=False):
+    c = shape[1]
+    x_cpu = randn(shape, dt, seed=seed, mean=mean, std=std)
+    adt = dt if affine == "same" else "f32"
+    w_cpu = randn((c,), adt, seed=seed + 1, mean=1.0, std=0.1) if affine in ("same", "f32", "w") else None
+    b_cpu = randn((c,), adt, seed=seed + 2, std=0.1) if affine in ("same", "f32", "b") else None
+    x = x_cpu.cuda()
+    w = w_cpu.cuda() if w_cpu is not None else None
+    b = b_cpu.cuda() if b_cpu is not None else None
+    y = kf355.kf_group_norm(x, groups, w, b, eps, out=x if in_place else None)
+    torch.cuda.synchronize()
+    variant = kf355.last_variant()
+    ref = oracle.group_norm(x_cpu, groups, w_cpu, b_cpu, eps)
+    check(y, ref, dt)
+    return y, variant
+
+
+SHAPES = [
+    ((2, 8), 4),                 # [N, C]: one element per channel
+    ((3, 6, 10), 3),             # [N, C, L]
+    ((2, 64, 8, 8), 8),          # small groups, one chunk each
+    ((1, 32, 7, 7), 4),          # spatial 49: not whole vectors -> scalar layout
+    ((4, 320, 32, 32), 32),      # SD-style 10-channel groups, one chunk
+    ((1, 128, 64, 64), 32),      # 4-chunk groups -> fused cooperative
+    ((2, 512, 64, 64), 32),      # 4-chunk groups, 256 workgroups
+    ((1, 32, 256, 256), 1),      # one 2M-element group: 128 chunks
+    ((1, 16, 3, 5, 7), 4),       # 3-D spatial, ragged chunk tail
+]
+
+
+@pytest.mark.parametrize("dt", ["bf16", "f32", "f16"])
+@pytest.mark.parametrize("shape,groups", SHAPES, ids=lambda v: str(v))
+def test_shape_sweep(shape, groups, dt):
+    note(f"group_norm {shape} G={groups} {dt}")
+    _, variant = run(shape, groups, dt)
+    assert variant.startswith("gn_"), variant
+
+
+@pytest.mark.parametrize("affine", ["f32", "w", "b", "none"])
+def test_affine_variants(affine):
+    note(f"group_norm affine={affine}")
+    run((2, 64, 32, 32), 16, "bf16", affine=affine)
+
+
+def test_two_kernel_path_for_grids_that_cannot_be_resident():
+    # 8 samples x 32 groups x 16 chunks = 4096 workgroups.
+    note("group_norm two-pass (8,128,256,256)")
+    _, variant = run((8, 128, 256, 256), 32, "bf16", seed=4)
+    assert variant.startswith("gn_two_pass") or variant.startswith("gn_fused"), variant
+
+
+def test_in_place():
+    note("group_norm in place")
+    run((1, 128, 64, 64), 32, "bf16", in_place=True, seed=6)
+
+
+def test_constant_groups_give_bias():
+    note("group_norm constant groups")
+    x = torch.full((1, 64, 16, 16), 0.75, dtype=torch.bfloat16, device="cuda")
+    b = randn((64,), "bf16", seed=2).cuda()
+    y = kf355.kf_group_norm(x, 8, None, b, 1e-6)
+    torch.cuda.synchronize()
+    assert torch.equal(y, b.view(1, 64, 1, 1).expand_as(y))
+
+
+def test_repeat_calls_bitwise_identical_and_workspace_clean():
+    note("group_norm determinism (1,512,128,128)")
+    x = randn((1, 512, 128, 128), "bf16", seed=3, mean=0.3, std=1.5).cuda()
+    w = randn((512,), "bf16", seed=4, mean=1.0, std=0.1).cuda()
+    b = randn((512,), "bf16", seed=5, std=0.1).cuda()
+    ws = torch.zeros(1 << 20, dtype=torch.uint8, device="cuda")
+    outs = [kf355.kf_group_norm(x, 32, w, b, 1e-6, workspace=ws) for _ in range(20)]
+    torch.cuda.synchronize()
+    for o in outs[1:]:
+        assert torch.equal(o.view(torch.int16), outs[0].view(torch.int16))
+    # Every call empties its partial slots and counters, and the give-up flag
+    # is never set: the whole workspace is zero again.
+    assert int(ws.count_nonzero().item()) == 0
+
+
+@pytest.mark.parametrize("mode_shape", [((1, 512, 128, 128), 32), ((2, 64, 8, 8), 8)])
+def test_paths_share_one_workspace(mode_shape):
+    # Alternating shapes (different chunk counts) through one workspace:
+    # each call must find it empty.
+    note(f"group_norm shared workspace {mode_shape}")
+    ws = torch.zeros(1 << 20, dtype=torch.uint8, device="cuda")
+    for shape, groups in [mode_shape, ((1, 128, 64, 64), 32), mode_shape]:
+        x_cpu = randn(shape, "bf16", seed=7, mean=0.3, std=1.5)
+        y = kf355.kf_group_norm(x_cpu.cuda(), groups, None, None, 1e-6, workspace=ws)
+        torch.cuda.synchronize()
+        assert_close(y, oracle.group_norm(x_cpu, groups, None, None, 1e-6), "bf16", floor=FLOOR)
+    assert int(ws.count_nonzero().item()) == 0

@@ -1,0 +1,127 @@
+"""GPU parity of kf_softmax against the float64 oracle: row-length sweep
+across every kernel variant (one-row-per-lane-group, workgroup, streaming,
+strided axis), every dtype pair, misaligned rows, special values and in-place
+use.  Tolerances: fp32 outputs max abs error <= 1e-6; bf16 / fp16 outputs
+within 1 unit in the last place of the oracle rounded once to the format."""
+import numpy as np
+import pytest
+import torch
+
+from compare import assert_close, note
+from oracle import oracle
+from paper_2607_24762_amd import kf355
+from paper_2607_24762_amd.workloads import randn
+
+pytestmark = pytest.mark.gpu
+
+PAIRS = [("f32", "f32"), ("bf16", "bf16"), ("bf16", "f32"), ("f16", "f16"), ("f16", "f32")]
+TORCH = {"f32": torch.float32, "bf16": torch.bfloat16, "f16": torch.float16}
+
+
+@pytest.fixture(scope="module", autouse=True)
+def gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU visible")
+    kf355.lib()  # raises if the library is missing
+
+
+def run_case(x_cpu, dim, out, **kw):
+    x = x_cpu.cuda()
+    y = kf355.kf_softmax(x, dim, out_dtype=TORCH[out])
+    torch.cuda.synchronize()
+    variant = kf355.last_variant()
+    ref = oracle.softmax(x_cpu, dim)
+    r = assert_close(y, ref, out, **kw)
+    return y, variant, r
+
+
+LENGTHS = [1, 2, 3, 7, 8, 63, 64, 65, 127, 255, 256, 257, 511, 1023, 1024, 1025, 2047, 2048, 4095, 4096,
+           4097, 8192, 16384, 32768, 65537]
+
+
+@pytest.mark.parametrize("pair", PAIRS, ids=lambda p: f"{p[0]}-{p[1]}")
+@pytest.mark.parametrize("length", LENGTHS)
+def test_row_length_sweep(pair, length):
+    rows = 37 if length <= 8192 else 3
+    note(f"softmax sweep {pair} rows={rows} len={length}")
+    x = randn((rows, length), pair[0], seed=length, std=3.0)
+    _, variant, _ = run_case(x, -1, pair[1])
+    assert variant.startswith("sm_"), variant
+
+
+@pytest.mark.parametrize("length", [256, 257, 1024, 4096])
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+def test_misaligned_base_pointer(length, dt):
+    # A view starting one element into its buffer: rows are no longer
+    # 16-byte aligned, so the scalar-access variants must take over.
+    rows = 33
+    note(f"softmax misaligned {dt} len={length}")
+    big = randn((rows * length + 1,), dt, seed=11)
+    x_cpu = big[1:].view(rows, length)
+    x = big.cuda()[1:].view(rows, length)
+    y = kf355.kf_softmax(x, -1)
+    torch.cuda.synchronize()
+    assert "scalar" in kf355.last_variant()
+    assert_close(y, oracle.softmax(x_cpu, -1), dt)
+
+
+@pytest.mark.parametrize("shape,dim", [((4, 37, 5), 1), ((3, 8, 16, 16), 1), ((6, 5), 0), ((2, 3, 300), 0),
+                                       ((2, 2, 3, 4097), 2)])
+@pytest.mark.parametrize("pair", [("f32", "f32"), ("bf16", "bf16")], ids=lambda p: p[0])
+def test_non_last_dim(shape, dim, pair):
+    note(f"softmax dim={dim} shape={shape} {pair}")
+    x = randn(shape, pair[0], seed=3, std=2.0)
+    _, variant, _ = run_case(x, dim, pair[1])
+    assert variant == "sm_cols"
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16", "f16"])
+@pytest.mark.parametrize("length", [5, 256, 4096, 70000])
+def test_special_rows(dt, length):
+    note(f"softmax special rows {dt} len={length}")
+    x = randn((8, length), "f32", seed=5, std=2.0)
+    x[0] = float("-inf")                      # fully masked -> NaN row
+    x[1, length // 2] = float("nan")          # NaN -> NaN row
+    x[2, 0] = float("inf")                    # +inf -> NaN row
+    x[3] = float("-inf")
+    x[3, length - 1] = 0.5                    # one finite entry -> exact one-hot
+    x[4, ::2] = float("-inf")                 # masked entries -> exact +0
+    x[5] *= 40.0                              # large logits
+    x[6] = 1.25                               # uniform row
+    xt = x.to(TORCH[dt])
+    y, _, _ = run_case(xt, -1, dt)
+    yc = y.float().cpu()
+    assert torch.isnan(yc[:3]).all()
+    assert yc[3, length - 1].item() == 1.0 and (yc[3, :-1] == 0).all()
+    assert not torch.signbit(yc[3]).any() and not torch.signbit(yc[4]).any()
+    assert (yc[4, ::2] == 0).all()
+    if length in (256, 4096):
+        assert (yc[6] == 1.0 / length).all()  # a power-of-two uniform row is exact
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+def test_in_place(dt):
+    note(f"softmax in place {dt}")
+    x_cpu = randn((64, 1000), dt, seed=9)
+    x = x_cpu.cuda()
+    y = kf355.kf_softmax(x, -1, out=x)
+    torch.cuda.synchronize()
+    assert y.data_ptr() == x.data_ptr()
+    assert_close(x, oracle.softmax(x_cpu, -1), dt)
+
+
+def test_zero_d_and_empty():
+    note("softmax 0-d and empty")
+    y = kf355.kf_softmax(torch.tensor(3.0, device="cuda"), 0)
+    e = kf355.kf_softmax(torch.empty(0, 5, device="cuda"), -1)
+    torch.cuda.synchronize()
+    assert y.item() == 1.0 and e.shape == (0, 5)
+
+
+def test_repeat_calls_are_bitwise_identical():
+    note("softmax determinism")
+    x = randn((512, 4096), "bf16", seed=13).cuda()
+    a = kf355.kf_softmax(x, -1)
+    b = kf355.kf_softmax(x, -1)
+    torch.cuda.synchronize()
+    assert torch.equal(a.view(torch.int16), b.view(torch.int16))
