@@ -186,7 +186,7 @@ struct Chunk {
                 float out[VEC];
 #pragma unroll
                 for (int i = 0; i < VEC; ++i) out[i] = fmaf(v[k][i] - mean, a[k], bb[k]);
-                if constexpr (VECTOR) store_vec<T>(p.y, gbase + o, out);
+                if constexpr (VECTOR) store_vec<T, true>(p.y, gbase + o, out);
                 else store1<T>(p.y, gbase + o, out[0]);
             }
         }

@@ -36,12 +36,13 @@ __device__ __forceinline__ float exp_shifted(float x, float m) {
 }
 
 // Writes `n` floats (n * sizeof(TO) is a multiple of 16 bytes) starting at
-// element e, as 16-byte stores.
+// element e, as non-temporal 16-byte stores: softmax output is written once
+// and not re-read by this kernel.
 template <class TO, int N>
 __device__ __forceinline__ void store_span(void* y, int64_t e, const float* v) {
     static_assert((N % TO::vec) == 0, "span must be whole vectors");
 #pragma unroll
-    for (int i = 0; i < N / TO::vec; ++i) store_vec<TO>(y, e + i * TO::vec, v + i * TO::vec);
+    for (int i = 0; i < N / TO::vec; ++i) store_vec<TO, true>(y, e + i * TO::vec, v + i * TO::vec);
 }
 
 // Sets slots outside the row (or of a row past the end) to -inf; slot k of
