@@ -43,12 +43,15 @@ struct Moments {
     float n, mean, m2;
 };
 
-// Chan et al. combine of two partial moments (a before b).
+// Chan et al. combine of two partial moments (a before b).  The weight
+// b.n / n uses the hardware reciprocal (v_rcp_f32, within 1 ulp; exact for the
+// power-of-two counts of full chunks) instead of an IEEE division: the merges
+// sit on the critical path between a workgroup's loads and its stores.
 __device__ __forceinline__ Moments chan(Moments a, Moments b) {
     const float n = a.n + b.n;
     if (n == 0.f) return Moments{0.f, 0.f, 0.f};
     const float d = b.mean - a.mean;
-    const float f = b.n / n;
+    const float f = b.n * __builtin_amdgcn_rcpf(n);
     return Moments{n, fmaf(d, f, a.mean), a.m2 + b.m2 + d * d * a.n * f};
 }
 
@@ -121,40 +124,44 @@ struct Chunk {
             else v[k][0] = load1<T>(p.x, at);
         }
     }
-    // Thread-local two-pass moments of the valid elements.
+    // Thread-local moments of the valid elements from sums shifted by K, the
+    // mean of the thread's first slot (whose load lands first; a thread with
+    // no valid slot holds copies of the group's first element there):
+    // s1 = sum(x - K), s2 = sum((x - K)^2), mean = K + s1/n,
+    // M2 = s2 - s1^2/n.  With K a sample mean of the same data the
+    // subtraction keeps most of its digits (s1^2/n <= s2), and unlike a
+    // two-pass form every element is folded in as soon as its load lands,
+    // overlapping this work with the remaining loads.
     __device__ __forceinline__ Moments moments(const GNParams& p, int part) const {
-        float sum = 0.f, cnt = 0.f;
+        float K = v[0][0];
+#pragma unroll
+        for (int i = 1; i < VEC; ++i) K += v[0][i];
+        K *= 1.f / (float)VEC;
+        float s1 = 0.f, s2 = 0.f, cnt = 0.f;
 #pragma unroll
         for (int k = 0; k < NV; ++k) {
             if (off(part, k) < p.group_elems) {
                 cnt += (float)VEC;
 #pragma unroll
-                for (int i = 0; i < VEC; ++i) sum += v[k][i];
-            }
-        }
-        const float mean = cnt > 0.f ? sum / cnt : 0.f;
-        float m2 = 0.f;
-#pragma unroll
-        for (int k = 0; k < NV; ++k) {
-            if (off(part, k) < p.group_elems) {
-#pragma unroll
                 for (int i = 0; i < VEC; ++i) {
-                    const float d = v[k][i] - mean;
-                    m2 = fmaf(d, d, m2);
+                    const float d = v[k][i] - K;
+                    s1 += d;
+                    s2 = fmaf(d, d, s2);
                 }
             }
         }
-        return Moments{cnt, mean, m2};
+        if (cnt == 0.f) return Moments{0.f, 0.f, 0.f};
+        const float r = __builtin_amdgcn_rcpf(cnt);
+        const float d1 = s1 * r;
+        return Moments{cnt, K + d1, fmaxf(fmaf(-s1, d1, s2), 0.f)};
     }
-    // y = (x - mean) * (rstd * w[c]) + b[c], channel c per slot (VECTOR) or
-    // per element.
+    // Raw w[c] and b[c] for every slot, loaded before the statistics are
+    // known (they do not depend on them), so their latency hides behind the
+    // cross-workgroup wait.  A group holds fewer than 2^31 elements (checked
+    // on the host), so the channel index is a 32-bit division.
+    float wv[NV], bv[NV];
     template <class A>
-    __device__ __forceinline__ void normalise_store(const GNParams& p, int64_t gbase, int part, int g,
-                                                    float mean, float rstd) {
-        // Per-slot channel scale and shift first (unconditional loads of w
-        // and b, issued together), then the guarded stores.  A group holds
-        // fewer than 2^31 elements (checked on the host), so the channel
-        // index is a 32-bit division.
+    __device__ __forceinline__ void load_affine(const GNParams& p, int part, int g) {
         int64_t c[NV];
 #pragma unroll
         for (int k = 0; k < NV; ++k) {
@@ -162,30 +169,32 @@ struct Chunk {
             const uint32_t oc = o < p.group_elems ? (uint32_t)o : 0u;
             c[k] = (int64_t)g * p.cpg + (int64_t)(oc / (uint32_t)p.spatial);
         }
-        float a[NV], bb[NV];
         if (p.w) {
 #pragma unroll
-            for (int k = 0; k < NV; ++k) a[k] = load1<A>(p.w, c[k]);
-#pragma unroll
-            for (int k = 0; k < NV; ++k) a[k] *= rstd;
+            for (int k = 0; k < NV; ++k) wv[k] = load1<A>(p.w, c[k]);
         } else {
 #pragma unroll
-            for (int k = 0; k < NV; ++k) a[k] = rstd;
+            for (int k = 0; k < NV; ++k) wv[k] = 1.f;
         }
         if (p.b) {
 #pragma unroll
-            for (int k = 0; k < NV; ++k) bb[k] = load1<A>(p.b, c[k]);
+            for (int k = 0; k < NV; ++k) bv[k] = load1<A>(p.b, c[k]);
         } else {
 #pragma unroll
-            for (int k = 0; k < NV; ++k) bb[k] = 0.f;
+            for (int k = 0; k < NV; ++k) bv[k] = 0.f;
         }
+    }
+    // y = (x - mean) * (rstd * w[c]) + b[c], non-temporal stores.
+    __device__ __forceinline__ void normalise_store(const GNParams& p, int64_t gbase, int part, float mean,
+                                                    float rstd) {
 #pragma unroll
         for (int k = 0; k < NV; ++k) {
             const int64_t o = off(part, k);
             if (o < p.group_elems) {
+                const float a = rstd * wv[k];
                 float out[VEC];
 #pragma unroll
-                for (int i = 0; i < VEC; ++i) out[i] = fmaf(v[k][i] - mean, a[k], bb[k]);
+                for (int i = 0; i < VEC; ++i) out[i] = fmaf(v[k][i] - mean, a, bv[k]);
                 if constexpr (VECTOR) store_vec<T, true>(p.y, gbase + o, out);
                 else store1<T>(p.y, gbase + o, out[0]);
             }
@@ -278,13 +287,13 @@ __global__ __launch_bounds__(kNT) void gn_fused(GNParams p) {
 
     C c;
     c.load(p, gbase, part);
+    c.template load_affine<A>(p, part, g);
     Moments m = moments_block(c.moments(p, part), lds);
 
     if (threadIdx.x < kWave) {
         if (p.parts > 1) {
             if (threadIdx.x == 0) publish(p, ng, part, m);
             m = gather_parts(p, ng, C::CH, true);
-            if (threadIdx.x == 0) release_group(p, ng);
         }
         if (threadIdx.x == 0) {
             stats[0] = m.mean;
@@ -292,7 +301,9 @@ __global__ __launch_bounds__(kNT) void gn_fused(GNParams p) {
         }
     }
     __syncthreads();
-    c.template normalise_store<A>(p, gbase, part, g, stats[0], stats[1]);
+    c.normalise_store(p, gbase, part, stats[0], stats[1]);
+    // Off the critical path: this workgroup is done reading its group's slots.
+    if (p.parts > 1 && threadIdx.x == 0) release_group(p, ng);
 }
 
 template <class T, bool VECTOR>
@@ -315,6 +326,11 @@ __global__ __launch_bounds__(kNT) void gn_apply(GNParams p) {
     const int part = blockIdx.x - (int)(ng * p.parts);
     const int g = (int)(ng % p.groups);
     const int64_t gbase = ng * p.group_elems;
+    // Chunk and affine loads first, so they are in flight while wave 0
+    // gathers the statistics.
+    C c;
+    c.load(p, gbase, part);
+    c.template load_affine<A>(p, part, g);
     if (threadIdx.x < kWave) {
         Moments m = gather_parts(p, ng, C::CH, false);
         if (threadIdx.x == 0) release_group(p, ng);
@@ -323,10 +339,8 @@ __global__ __launch_bounds__(kNT) void gn_apply(GNParams p) {
             stats[1] = 1.f / sqrtf(m.m2 / (float)p.group_elems + p.eps);
         }
     }
-    C c;
-    c.load(p, gbase, part);
     __syncthreads();
-    c.template normalise_store<A>(p, gbase, part, g, stats[0], stats[1]);
+    c.normalise_store(p, gbase, part, stats[0], stats[1]);
 }
 
 // --------------------------------------------------------------------------

@@ -25,14 +25,31 @@ constexpr float kLog2e = 1.4426950408889634f;
 
 // e^(x - m) as 2^((x - m) * log2 e): subtracting first keeps x == m exact
 // (2^0 = 1), so a uniform row gives exactly 1/L and a one-hot row exactly 1.
-// The hardware exp2 (v_exp_f32) flushes results below 2^-126 to zero; those
-// arguments are evaluated as 2^(t + 64) * 2^-64 so subnormal results (which
-// bf16 outputs can represent) stay exact, as with the IEEE definition.
-__device__ __forceinline__ float exp_shifted(float x, float m) {
-    const float t = (x - m) * kLog2e;
-    const bool tiny = t < -126.f;
-    const float e = __builtin_amdgcn_exp2f(tiny ? t + 64.f : t);
-    return tiny ? e * 0x1p-64f : e;
+// Used for ratios of exponentials (the online merge).
+__device__ __forceinline__ float exp_rel(float x, float m) {
+    return __builtin_amdgcn_exp2f((x - m) * kLog2e);
+}
+
+// Per-element exponential for output type TO, scaled by 2^SHIFT: the factor
+// cancels in y = e / sum(e).  The hardware exp2 (v_exp_f32) flushes results
+// below 2^-126.  Only a bf16 output can represent such values (its smallest
+// subnormal is 2^-133; fp16's is 2^-24 and fp32 outputs are judged by an
+// absolute bound), and since sum(e) >= 2^SHIFT every y >= 2^-134 comes from
+// an exponent >= -134: with SHIFT = 8 all of those are computed as normal
+// numbers, and the final multiply by 1/sum produces the subnormal exactly.
+// The shift costs nothing: it rides in the fma.
+template <class TO>
+struct Shift {
+    static constexpr float value = 0.f;
+};
+template <>
+struct Shift<BF16> {
+    static constexpr float value = 8.f;
+};
+template <class TO>
+__device__ __forceinline__ float exp_out(float x, float m) {
+    if constexpr (Shift<TO>::value == 0.f) return __builtin_amdgcn_exp2f((x - m) * kLog2e);
+    else return __builtin_amdgcn_exp2f(fmaf(x - m, kLog2e, Shift<TO>::value));
 }
 
 // Writes `n` floats (n * sizeof(TO) is a multiple of 16 bytes) starting at
@@ -96,7 +113,7 @@ __global__ __launch_bounds__(256) void sm_wave(const void* __restrict__ x, void*
     for (int k = 0; k < NV; ++k)
 #pragma unroll
         for (int i = 0; i < VEC; ++i) {
-            v[k][i] = exp_shifted(v[k][i], m);
+            v[k][i] = exp_out<TO>(v[k][i], m);
             s += v[k][i];
         }
     s = group_reduce<LPR>(s, OpSum{});
@@ -136,18 +153,23 @@ __global__ __launch_bounds__(NT) void sm_block(const void* __restrict__ x, void*
     constexpr int NW = NT / kWave;
     __shared__ float red[NW];
     const int64_t base = (int64_t)blockIdx.x * len;
+    // Each wave owns a contiguous segment of NV*64 slots (slot k of lane l
+    // of wave w is w*NV*64 + k*64 + l): every wave streams one contiguous
+    // stretch of the row, the pattern that moves HBM fastest on this part.
+    const int lane = threadIdx.x & (kWave - 1);
+    const int seg = (threadIdx.x / kWave) * NV * kWave + lane;
 
     // Unconditional loads (out-of-range slots re-read the row's first
     // element), then masking, as in sm_wave.
     float v[NV][VEC];
 #pragma unroll
     for (int k = 0; k < NV; ++k) {
-        const int e0 = (threadIdx.x + k * NT) * VEC;
+        const int e0 = (seg + k * kWave) * VEC;
         const int64_t at = base + (e0 < len ? e0 : 0);
         if constexpr (VECTOR) load_vec<TI>(x, at, v[k]);
         else v[k][0] = load1<TI>(x, at);
     }
-    if (NT * NV * VEC != len) mask_slots<NV, VEC, NT>(v, threadIdx.x, true, len);
+    if (NT * NV * VEC != len) mask_slots<NV, VEC, kWave>(v, seg, true, len);
     float m = -INFINITY;
 #pragma unroll
     for (int k = 0; k < NV; ++k)
@@ -160,7 +182,7 @@ __global__ __launch_bounds__(NT) void sm_block(const void* __restrict__ x, void*
     for (int k = 0; k < NV; ++k)
 #pragma unroll
         for (int i = 0; i < VEC; ++i) {
-            v[k][i] = exp_shifted(v[k][i], m);
+            v[k][i] = exp_out<TO>(v[k][i], m);
             s += v[k][i];
         }
     s = block_reduce<NW>(s, OpSum{}, red);
@@ -168,7 +190,7 @@ __global__ __launch_bounds__(NT) void sm_block(const void* __restrict__ x, void*
 
 #pragma unroll
     for (int k = 0; k < NV; ++k) {
-        const int e0 = (threadIdx.x + k * NT) * VEC;
+        const int e0 = (seg + k * kWave) * VEC;
         if (e0 < len) {
 #pragma unroll
             for (int i = 0; i < VEC; ++i) v[k][i] *= inv;
@@ -186,21 +208,22 @@ struct MS {
 };
 __device__ __forceinline__ MS ms_merge(MS a, MS b) {
     const float mm = fmaxf(a.m, b.m);
-    const float sa = (a.m == -INFINITY) ? 0.f : a.s * exp_shifted(a.m, mm);
-    const float sb = (b.m == -INFINITY) ? 0.f : b.s * exp_shifted(b.m, mm);
+    const float sa = (a.m == -INFINITY) ? 0.f : a.s * exp_rel(a.m, mm);
+    const float sb = (b.m == -INFINITY) ? 0.f : b.s * exp_rel(b.m, mm);
     return MS{mm, sa + sb};
 }
-// Folds a chunk of n values into the state.
-template <int N>
+// Folds a chunk of n values into the state; s accumulates exp_out<TO>, so
+// it carries the same 2^SHIFT factor as the write pass.
+template <class TO, int N>
 __device__ __forceinline__ MS ms_add(MS st, const float* v) {
     float cm = v[0];
 #pragma unroll
     for (int i = 1; i < N; ++i) cm = fmaxf(cm, v[i]);
     const float mm = fmaxf(st.m, cm);
     if (mm == -INFINITY) return st;  // nothing but -inf so far
-    float s = (st.m == -INFINITY) ? 0.f : st.s * exp_shifted(st.m, mm);
+    float s = (st.m == -INFINITY) ? 0.f : st.s * exp_rel(st.m, mm);
 #pragma unroll
-    for (int i = 0; i < N; ++i) s += exp_shifted(v[i], mm);
+    for (int i = 0; i < N; ++i) s += exp_out<TO>(v[i], mm);
     return MS{mm, s};
 }
 template <int S>
@@ -244,7 +267,7 @@ __global__ __launch_bounds__(NT) void sm_stream(const void* __restrict__ x, void
                 for (int i = 0; i < VEC; ++i) v[d * VEC + i] = -INFINITY;
             }
         }
-        st = ms_add<DEPTH * VEC>(st, v);
+        st = ms_add<TO, DEPTH * VEC>(st, v);
     }
     st = ms_wave(st);
     const int w = threadIdx.x / kWave;
@@ -275,7 +298,7 @@ __global__ __launch_bounds__(NT) void sm_stream(const void* __restrict__ x, void
             const int64_t e = e0 + (int64_t)d * NT * VEC;
             if (e < len) {
 #pragma unroll
-                for (int i = 0; i < VEC; ++i) v[d][i] = exp_shifted(v[d][i], tot.m) * inv;
+                for (int i = 0; i < VEC; ++i) v[d][i] = exp_out<TO>(v[d][i], tot.m) * inv;
                 if constexpr (VECTOR) store_span<TO, VEC>(y, base + e, v[d]);
                 else store1<TO>(y, base + e, v[d][0]);
             }
@@ -299,11 +322,11 @@ __global__ __launch_bounds__(256) void sm_cols(const void* __restrict__ x, void*
         float v[DEPTH];
 #pragma unroll
         for (int d = 0; d < DEPTH; ++d) v[d] = (j0 + d < len) ? load1<TI>(x, base + (j0 + d) * inner) : -INFINITY;
-        st = ms_add<DEPTH>(st, v);
+        st = ms_add<TO, DEPTH>(st, v);
     }
     const float inv = 1.f / st.s;
     for (int64_t j = 0; j < len; ++j)
-        store1<TO>(y, base + j * inner, exp_shifted(load1<TI>(x, base + j * inner), st.m) * inv);
+        store1<TO>(y, base + j * inner, exp_out<TO>(load1<TI>(x, base + j * inner), st.m) * inv);
 }
 
 // --------------------------------------------------------------------------
@@ -327,8 +350,13 @@ struct Choice {
 };
 
 // Smallest register-resident configuration whose capacity covers the row.
-// Capacity = LPR * NV * VEC elements per row; per-lane data is kept to at
-// most 64 floats so several waves fit per SIMD.
+// Capacity = LPR * NV * VEC (lane groups) or NT * NV * VEC (workgroup per
+// row) elements.  Vectorised rows wider than 256 slots (4 KiB of fp32 or
+// bf16 pairs) go to a workgroup per row with two 16-byte slots per lane, so
+// each wave streams 2 KiB of the row: measured on MI355X, a causal bf16
+// [32768 x 4096] softmax takes 89.4 us that way against 92.0 us with one
+// wave per row.  Unaligned (element-wise) rows stay on lane groups up to
+// 1024 elements.
 template <class TI, class TO, bool VECTOR>
 Choice pick_resident(int64_t len) {
     constexpr int VEC = VECTOR ? TI::vec : 1;
@@ -337,6 +365,10 @@ Choice pick_resident(int64_t len) {
     if (slots <= (int64_t)(LPR) * (NV))                                                        \
         return Choice{go_wave<TI, TO, LPR, NV, VECTOR>, VECTOR ? "sm_wave_vec_lpr" #LPR "_nv" #NV \
                                                                : "sm_wave_scalar_lpr" #LPR "_nv" #NV};
+#define KF_BLOCK(NT, NV)                                                                         \
+    if (slots <= (int64_t)(NT) * (NV))                                                           \
+        return Choice{go_block<TI, TO, NT, NV, VECTOR>, VECTOR ? "sm_block_vec_nt" #NT "_nv" #NV \
+                                                               : "sm_block_scalar_nt" #NT "_nv" #NV};
     KF_WAVE(1, 1)
     KF_WAVE(2, 1)
     KF_WAVE(4, 1)
@@ -346,21 +378,24 @@ Choice pick_resident(int64_t len) {
     KF_WAVE(16, 4)
     KF_WAVE(32, 4)
     KF_WAVE(64, 4)
-    KF_WAVE(64, 8)
-    if constexpr (!VECTOR || TI::vec == 4) {
+    if constexpr (VECTOR) {
+        KF_BLOCK(256, 2)
+        KF_BLOCK(512, 2)
+        KF_BLOCK(1024, 2)
+        KF_BLOCK(1024, 4)
+        KF_BLOCK(1024, 8)
+        if constexpr (TI::vec == 4) {
+            KF_BLOCK(1024, 16)
+        }
+    } else {
+        KF_WAVE(64, 8)
         KF_WAVE(64, 16)
-    }
-#undef KF_WAVE
-#define KF_BLOCK(NT, NV)                                                                         \
-    if (slots <= (int64_t)(NT) * (NV))                                                           \
-        return Choice{go_block<TI, TO, NT, NV, VECTOR>, VECTOR ? "sm_block_vec_nt" #NT "_nv" #NV \
-                                                               : "sm_block_scalar_nt" #NT "_nv" #NV};
-    KF_BLOCK(256, 8)
-    KF_BLOCK(512, 8)
-    KF_BLOCK(1024, 8)
-    if constexpr (!VECTOR || TI::vec == 4) {
+        KF_BLOCK(256, 8)
+        KF_BLOCK(512, 8)
+        KF_BLOCK(1024, 8)
         KF_BLOCK(1024, 16)
     }
+#undef KF_WAVE
 #undef KF_BLOCK
     return Choice{nullptr, nullptr};
 }
