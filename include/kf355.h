@@ -114,13 +114,14 @@ kf_status kf_softmax(const void* x, kf_dtype x_dtype, void* y, kf_dtype y_dtype,
  *  eps           >= 0 (used as fp32).
  *  workspace     device buffer of at least kf_group_norm_workspace_bytes()
  *                bytes, 256-byte aligned, ZERO-FILLED before its first use
- *                and left alone by the caller between calls: it holds
- *                cross-workgroup counters that every completed call returns
- *                to zero.  Its last 256 bytes start with a 32-bit word that
- *                a call sets nonzero if a cross-workgroup wait gave up (the
- *                results of that call are then invalid; clear the word to
- *                re-arm).  Calls that may run concurrently must not share a
- *                workspace.
+ *                and left alone by the caller between calls: it carries the
+ *                cross-workgroup exchange, which every completed call returns
+ *                to zero.  Its last 256 bytes start with a 32-bit word that a
+ *                call sets to 1 when a workgroup stopped waiting for the rest
+ *                of its group (e.g. because other kernels held the compute
+ *                units) and recomputed the group's statistics itself; the
+ *                results are identical either way, the word is informational.
+ *                Calls that may run concurrently must not share a workspace.
  *  y may equal x (in place); any other overlap is KF_ERR_BAD_ARG.
  */
 kf_status kf_group_norm(const void* x, kf_dtype x_dtype, void* y, int32_t ndim, const int64_t* shape,

@@ -81,14 +81,14 @@ struct GNParams {
     const void* b;
     uint64_t* slot;        // [groups_total * parts] published partials, 0 = empty
     unsigned* depart;      // one per group, kCounterStride bytes apart
-    unsigned* error;       // set to 1 if a wait gave up
+    unsigned* error;       // set to 1 when a wait gave up (results stay valid)
     int64_t group_elems;   // (c/G) * spatial
     int64_t spatial;
     int32_t cpg;           // channels per group
     int32_t groups;        // G
     int32_t parts;         // workgroups per group
     float eps;
-    unsigned spin_limit;
+    uint32_t wait_ticks;   // give up waiting after this many 100 MHz ticks
 };
 
 __device__ __forceinline__ unsigned* counter(unsigned* base, int64_t ng) {
@@ -236,27 +236,28 @@ __device__ __forceinline__ void publish(const GNParams& p, int64_t ng, int part,
 // result uniform across it.  Lane l takes parts l, l+64, ... in order and the
 // butterfly keeps lane order, so the combine order depends on part index
 // alone (bitwise-reproducible results).  With `wait`, each lane polls its
-// slots until they are published; the wait is bounded and on giving up flags
-// the workspace and carries on, so the kernel always ends.
-__device__ __forceinline__ Moments gather_parts(const GNParams& p, int64_t ng, int64_t chunk, bool wait) {
+// slots until they are published or until p.wait_ticks of the 100 MHz real
+// time clock have passed; *ok reports (uniformly) whether every slot arrived.
+__device__ __forceinline__ Moments gather_parts(const GNParams& p, int64_t ng, int64_t chunk, bool wait,
+                                                bool* ok) {
     Moments acc{0.f, 0.f, 0.f};
     const int lane = threadIdx.x & (kWave - 1);
     uint64_t* slots = p.slot + ng * p.parts;
+    const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
+    bool all = true;
     for (int q = lane; q < p.parts; q += kWave) {
         uint64_t w = __hip_atomic_load(slots + q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         if (wait) {
-            unsigned spins = 0;
             while (w == 0) {
-                if (++spins > p.spin_limit) {
-                    __hip_atomic_store(p.error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                    break;
-                }
+                if (__builtin_amdgcn_s_memrealtime() - t0 > p.wait_ticks) break;
                 __builtin_amdgcn_s_sleep(1);
                 w = __hip_atomic_load(slots + q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             }
         }
+        all = all && (w != 0);
         acc = chan(acc, decode(w, part_count(p, chunk, q)));
     }
+    *ok = __all(all);
     return moments_wave(acc);
 }
 
@@ -280,6 +281,7 @@ __global__ __launch_bounds__(kNT) void gn_fused(GNParams p) {
     using C = Chunk<T, VECTOR>;
     __shared__ Moments lds[kNT / kWave];
     __shared__ float stats[2];
+    __shared__ int gathered;
     const int64_t ng = blockIdx.x / p.parts;
     const int part = blockIdx.x - (int)(ng * p.parts);
     const int g = (int)(ng % p.groups);
@@ -291,16 +293,45 @@ __global__ __launch_bounds__(kNT) void gn_fused(GNParams p) {
     Moments m = moments_block(c.moments(p, part), lds);
 
     if (threadIdx.x < kWave) {
+        bool ok = true;
         if (p.parts > 1) {
             if (threadIdx.x == 0) publish(p, ng, part, m);
-            m = gather_parts(p, ng, C::CH, true);
+            m = gather_parts(p, ng, C::CH, true, &ok);
         }
         if (threadIdx.x == 0) {
+            gathered = ok;
             stats[0] = m.mean;
             stats[1] = 1.f / sqrtf(m.m2 / (float)p.group_elems + p.eps);
         }
     }
     __syncthreads();
+    if (!gathered) {
+        // Some workgroup of this group has not published in time (it is not
+        // resident yet, e.g. while other kernels hold the CUs).  Recompute
+        // every part's moments here with the same loads, thread mapping and
+        // arithmetic its owner uses, and merge them in the same order: the
+        // statistics come out bit-identical, and the kernel never depends on
+        // co-residency.  (In-place calls never take this path: they are
+        // routed to the two-kernel form, since a chunk already normalised in
+        // place could not be re-read.)
+        Moments acc{0.f, 0.f, 0.f};
+        const int lane = threadIdx.x & (kWave - 1);
+        for (int q = 0; q < p.parts; ++q) {
+            c.load(p, gbase, q);
+            const Moments mq = moments_block(c.moments(p, q), lds);
+            if ((q & (kWave - 1)) == lane) acc = chan(acc, mq);
+        }
+        if (threadIdx.x < kWave) {
+            acc = moments_wave(acc);
+            if (threadIdx.x == 0) {
+                stats[0] = acc.mean;
+                stats[1] = 1.f / sqrtf(acc.m2 / (float)p.group_elems + p.eps);
+                __hip_atomic_store(p.error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            }
+        }
+        c.load(p, gbase, part);
+        __syncthreads();
+    }
     c.normalise_store(p, gbase, part, stats[0], stats[1]);
     // Off the critical path: this workgroup is done reading its group's slots.
     if (p.parts > 1 && threadIdx.x == 0) release_group(p, ng);
@@ -332,7 +363,8 @@ __global__ __launch_bounds__(kNT) void gn_apply(GNParams p) {
     c.load(p, gbase, part);
     c.template load_affine<A>(p, part, g);
     if (threadIdx.x < kWave) {
-        Moments m = gather_parts(p, ng, C::CH, false);
+        bool ok;
+        Moments m = gather_parts(p, ng, C::CH, false, &ok);
         if (threadIdx.x == 0) release_group(p, ng);
         if (threadIdx.x == 0) {
             stats[0] = m.mean;
@@ -424,6 +456,18 @@ int gn_mode() {
     return mode;
 }
 
+// How long (100 MHz ticks of s_memrealtime) a fused workgroup waits for the
+// rest of its group before recomputing the statistics itself: 100 us by
+// default; KF355_GN_WAIT_TICKS overrides it (tests set 0 to force the
+// recompute path).  Read once per process.
+uint32_t gn_wait_ticks() {
+    static const uint32_t ticks = [] {
+        const char* e = std::getenv("KF355_GN_WAIT_TICKS");
+        return e ? (uint32_t)std::strtoul(e, nullptr, 10) : 10000u;
+    }();
+    return ticks;
+}
+
 bool cooperative_ok(int dev) {
     static std::atomic<int> coop_cache[kMaxDevices];
     return cached_attr(coop_cache, dev, hipDeviceAttributeCooperativeLaunch) != 0;
@@ -447,7 +491,7 @@ kf_status run(const GroupNormArgs& a, hipStream_t s, const char** variant) {
     p.groups = (int32_t)a.groups;
     p.parts = (int32_t)l.parts;
     p.eps = a.eps;
-    p.spin_limit = 1u << 22;
+    p.wait_ticks = gn_wait_ticks();
 
     const int64_t grid = l.groups_total * l.parts;
     if (grid > INT32_MAX) {
@@ -456,15 +500,17 @@ kf_status run(const GroupNormArgs& a, hipStream_t s, const char** variant) {
     }
 
     // Path choice.  One chunk per group needs no exchange.  Otherwise the
-    // fused kernel needs every workgroup of the grid resident at once; it is
-    // launched normally when the occupancy-derived capacity covers the grid
-    // (or cooperatively, which the runtime guarantees, under
-    // KF355_GN_MODE=coop), else the two-kernel path runs.
+    // fused kernel is used when the occupancy-derived capacity covers the
+    // grid (so normally every workgroup is resident and the exchange
+    // completes; when it is not, the waiting workgroups recompute the
+    // statistics themselves), launched normally, or cooperatively under
+    // KF355_GN_MODE=coop.  In-place calls and grids larger than the
+    // capacity take the two-kernel path.
     const int mode = gn_mode();
     enum { FUSED_SINGLE, FUSED_PLAIN, FUSED_COOP, TWO_PASS } path = TWO_PASS;
     if (l.parts == 1 && mode != kModeTwoPass) {
         path = FUSED_SINGLE;
-    } else if (mode != kModeTwoPass) {
+    } else if (mode != kModeTwoPass && a.x != a.y) {
         static std::atomic<int> capacity_cache[kMaxDevices];
         int dev = -1;
         if (hipGetDevice(&dev) != hipSuccess) {

@@ -1,7 +1,7 @@
 """GPU parity of kf_group_norm against the float64 oracle across shapes that
 exercise every path: single-chunk groups, fused multi-chunk groups with the
-cooperative cross-workgroup combine, the two-kernel path for grids that
-cannot be co-resident, scalar (non-vectorisable) layouts, every dtype and
+cross-workgroup exchange (and its recompute fallback), the two-kernel path
+for grids that cannot be co-resident and for in-place calls, scalar (non-vectorisable) layouts, every dtype and
 affine combination, in-place use, determinism and workspace hygiene.
 
 Tolerances: bf16 / fp16 outputs within 1 unit in the last place of the
@@ -17,6 +17,7 @@ import torch
 from compare import assert_close, note
 from oracle import oracle
 from paper_2607_24762_amd import kf355
+from paper_2607_24762_amd import workloads as W
 from paper_2607_24762_amd.workloads import randn
 
 pytestmark = pytest.mark.gpu
@@ -64,7 +65,7 @@ SHAPES = [
     ((2, 64, 8, 8), 8),          # small groups, one chunk each
     ((1, 32, 7, 7), 4),          # spatial 49: not whole vectors -> scalar layout
     ((4, 320, 32, 32), 32),      # SD-style 10-channel groups, one chunk
-    ((1, 128, 64, 64), 32),      # 4-chunk groups -> fused cooperative
+    ((1, 128, 64, 64), 32),      # exactly one full chunk per group
     ((2, 512, 64, 64), 32),      # 4-chunk groups, 256 workgroups
     ((1, 32, 256, 256), 1),      # one 2M-element group: 128 chunks
     ((1, 16, 3, 5, 7), 4),       # 3-D spatial, ragged chunk tail
@@ -93,8 +94,13 @@ def test_two_kernel_path_for_grids_that_cannot_be_resident():
 
 
 def test_in_place():
+    # In place, chunks of a group are overwritten while others may still be
+    # read, so multi-chunk groups take the two-kernel path.
     note("group_norm in place")
-    run((1, 128, 64, 64), 32, "bf16", in_place=True, seed=6)
+    _, variant = run((1, 512, 64, 64), 32, "bf16", in_place=True, seed=6)   # 4 chunks per group
+    assert variant.startswith("gn_two_pass"), variant
+    _, variant = run((2, 64, 8, 8), 8, "bf16", in_place=True, seed=8)
+    assert variant.startswith("gn_fused"), variant  # one chunk per group: no exchange
 
 
 def test_constant_groups_give_bias():
@@ -107,18 +113,65 @@ def test_constant_groups_give_bias():
 
 
 def test_repeat_calls_bitwise_identical_and_workspace_clean():
-    note("group_norm determinism (1,512,128,128)")
+    note("group_norm determinism x1000 (1,512,128,128)")
     x = randn((1, 512, 128, 128), "bf16", seed=3, mean=0.3, std=1.5).cuda()
     w = randn((512,), "bf16", seed=4, mean=1.0, std=0.1).cuda()
     b = randn((512,), "bf16", seed=5, std=0.1).cuda()
     ws = torch.zeros(1 << 20, dtype=torch.uint8, device="cuda")
-    outs = [kf355.kf_group_norm(x, 32, w, b, 1e-6, workspace=ws) for _ in range(20)]
+    ref = kf355.kf_group_norm(x, 32, w, b, 1e-6, workspace=ws)
+    y = torch.empty_like(ref)
+    bad = torch.zeros((), dtype=torch.int64, device="cuda")
+    for _ in range(1000):
+        kf355.kf_group_norm(x, 32, w, b, 1e-6, out=y, workspace=ws)
+        bad += (y.view(torch.int16) != ref.view(torch.int16)).sum()
     torch.cuda.synchronize()
-    for o in outs[1:]:
-        assert torch.equal(o.view(torch.int16), outs[0].view(torch.int16))
-    # Every call empties its partial slots and counters, and the give-up flag
-    # is never set: the whole workspace is zero again.
+    assert int(bad.item()) == 0
+    # Every call empties its partial slots and counters, and no wait gave
+    # up: the whole workspace is zero again.
     assert int(ws.count_nonzero().item()) == 0
+
+
+def test_wait_timeout_recompute_is_bitwise_identical(tmp_path):
+    # A child process with KF355_GN_WAIT_TICKS=0 makes every workgroup that
+    # does not find its whole group published on the first poll recompute the
+    # group's statistics itself; the output must equal the normal path's bit
+    # for bit, the give-up word must be set and everything else left zero.
+    import subprocess
+    import sys
+    import os
+    note("group_norm forced-timeout recompute")
+    w = W.groupnorm_vae_bf16()
+    y = kf355.kf_group_norm(w["x"].cuda(), 32, w["weight"].cuda(), w["bias"].cuda(), w["eps"])
+    torch.cuda.synchronize()
+    child = os.path.join(os.path.dirname(os.path.abspath(__file__)), "gn_child.py")
+    out = str(tmp_path / "child.npz")
+    env = dict(os.environ, KF355_GN_WAIT_TICKS="0")
+    r = subprocess.run([sys.executable, "-u", child, out], env=env, timeout=300, capture_output=True, text=True)
+    print(r.stdout, r.stderr[-2000:])
+    assert r.returncode == 0
+    got = np.load(out)
+    assert str(got["variant"]) == "gn_fused_vec"
+    assert int(got["flag"]) == 1
+    assert int(got["rest"]) == 0
+    assert np.array_equal(got["bits"], y.view(torch.int16).cpu().numpy())
+
+
+def test_concurrent_calls_on_two_streams():
+    note("group_norm two streams")
+    w = W.groupnorm_vae_bf16()
+    x, g, b = w["x"].cuda(), w["weight"].cuda(), w["bias"].cuda()
+    ref = kf355.kf_group_norm(x, 32, g, b, w["eps"])
+    torch.cuda.synchronize()
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    outs = []
+    for _ in range(20):
+        with torch.cuda.stream(s1):
+            outs.append(kf355.kf_group_norm(x, 32, g, b, w["eps"]))
+        with torch.cuda.stream(s2):
+            outs.append(kf355.kf_group_norm(x, 32, g, b, w["eps"]))
+    torch.cuda.synchronize()
+    for o in outs:
+        assert torch.equal(o.view(torch.int16), ref.view(torch.int16))
 
 
 @pytest.mark.parametrize("mode_shape", [((1, 512, 128, 128), 32), ((2, 64, 8, 8), 8)])
