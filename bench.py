@@ -117,6 +117,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-eager", action="store_true")
+    ap.add_argument("--no-next", action="store_true", help="skip the fused causal softmax measurement")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: the operators shard by rows / groups / planes with no exchange, "
@@ -224,6 +225,40 @@ def main():
             us = e0.elapsed_time(e1) * 1e3 / n
             eager[name] = {"us_per_call": round(us, 3), "kf355_speedup": round(us / per_op[name]["us_per_call"], 3)}
 
+    next_rows = None
+    if not args.no_next:
+        # Fused scale + causal mask + softmax on the raw scores of the same
+        # attention shape: reads only the visible triangle, writes every
+        # entry.  Reported beside the step, not part of it.
+        del calls["softmax"]
+        torch.cuda.empty_cache()
+        raw = W.attn_scores_raw_bf16()
+        q = raw["x"].shape[-2]
+        heads = raw["x"].numel() // (q * q)
+        live = heads * q * (q + 1) // 2
+        cbytes = live * 2 + raw["x"].numel() * 2
+        src = raw["x"].to(dev)
+        cs = [kf355.prepare_softmax_causal(src.clone(), torch.empty_like(src), raw["scale"]) for _ in range(2)]
+        del src
+        cs[0]()
+        cvar = kf355.last_variant()
+        for i in range(args.warmup):
+            cs[i % 2]()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for i in range(args.steps):
+            cs[i % 2]()
+        e1.record()
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) * 1e3 / args.steps
+        gbs = cbytes / (us * 1e-6) / 1e9
+        next_rows = {"softmax_causal_fused": {
+            "workload": "bf16 [1,8,4096,4096] raw scores, scale 1/16, causal; same output as the step's softmax",
+            "us_per_call": round(us, 3), "gbps": round(gbs, 1), "frac_of_peak": round(gbs / PEAK_HBM_GBS, 4),
+            "algorithmic_bytes": cbytes, "variant": cvar,
+            "vs_unfused_softmax": round(per_op["softmax"]["us_per_call"] / us, 3)}}
+        del cs
+
     calib = copy_calibration(torch, dev, nbytes["softmax"])
     sm = per_op["softmax"]
     traffic = measured_traffic()
@@ -244,7 +279,7 @@ def main():
         "data": "synthetic (seeded, shapes and distributions of the paper's workloads)",
         "config": {"workload": WORKLOAD, "step_algorithmic_bytes": step_bytes},
         "per_op": per_op, "roofline": roofline, "cpu_baseline": base, "torch_eager": eager,
-        "calibration": calib,
+        "calibration": calib, "next_rows": next_rows,
     }
     print(json.dumps(out), flush=True)
 

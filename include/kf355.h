@@ -98,6 +98,26 @@ kf_status kf_softmax(const void* x, kf_dtype x_dtype, void* y, kf_dtype y_dtype,
                      void* stream);
 
 /*
+ * kf_softmax_causal -- the attention-score softmax of eager attention fused
+ * into one pass: y = softmax(scale * x + M, -1) over the last axis of x
+ * viewed as [..., q, k], where M is the causal mask aligned to the end of
+ * the key axis (query i sees keys j <= i + k - q, as with a key/value cache;
+ * M is 0 there and -inf elsewhere).  The paper's LLM workloads run eager
+ * attention (Table I), whose softmax calls (Section IV-C) follow exactly this
+ * scale-mask-softmax sequence.
+ *
+ *  Masked inputs are never used (their values may be anything, NaN
+ *  included) and the masked triangle is not read from memory; masked
+ *  outputs are +0.  A row with no visible key (q > k) is NaN, as the masked
+ *  softmax gives.  Arguments are as for kf_softmax, with ndim >= 2 and
+ *  `scale` any finite value; rows longer than 65536 bf16 / 32768 fp32
+ *  elements return KF_ERR_UNSUPPORTED_LAYOUT.  y may equal x (in place).
+ */
+kf_status kf_softmax_causal(const void* x, kf_dtype x_dtype, void* y, kf_dtype y_dtype, int32_t ndim,
+                            const int64_t* shape, const int64_t* x_strides, const int64_t* y_strides, double scale,
+                            void* stream);
+
+/*
  * kf_group_norm -- y = group_norm(x, num_groups, weight, bias, eps)
  * (PyTorch `torch.nn.functional.group_norm`; the SD3.5 Medium result,
  * Section IV-C): for each sample and each of `num_groups` groups of

@@ -33,6 +33,32 @@ void oracle_softmax_rows(const double* x, int64_t rows, int64_t len, double* y) 
     }
 }
 
+/* Scaled causal softmax: the masked score row z (scale * x where visible,
+ * -inf where masked) put through the softmax steps above, in the same
+ * order.  Only visible entries of x are read. */
+void oracle_softmax_causal(const double* x, int64_t batch, int64_t q, int64_t k, double scale, double* y) {
+    for (int64_t b = 0; b < batch; ++b) {
+        for (int64_t i = 0; i < q; ++i) {
+            const double* xr = x + (b * q + i) * k;
+            double* yr = y + (b * q + i) * k;
+            const int64_t last = i + (k - q);  /* highest visible key index */
+            double m = -INFINITY;
+            for (int64_t j = 0; j < k; ++j) {
+                const double z = (j <= last) ? scale * xr[j] : -INFINITY;
+                if (z > m) m = z;
+            }
+            double total = 0.0;
+            for (int64_t j = 0; j < k; ++j) {
+                const double z = (j <= last) ? scale * xr[j] : -INFINITY;
+                const double e = exp(z - m);
+                yr[j] = e;
+                total += e;
+            }
+            for (int64_t j = 0; j < k; ++j) yr[j] = yr[j] / total;
+        }
+    }
+}
+
 /* GroupNorm (PyTorch `group_norm(x, groups, w, b, eps)` definition): biased
  * variance from a second pass over the group, eps inside the square root,
  * per-channel affine after normalisation. */

@@ -36,6 +36,14 @@ extern "C" {
  * NaN row. */
 void oracle_softmax_rows(const double* x, int64_t rows, int64_t len, double* y);
 
+/* Scaled causal softmax over the last axis of x viewed as [batch, q, k]:
+ * query row i sees keys j <= i + (k - q) (the causal mask aligned to the
+ * end of the key axis, as with a key/value cache); every other key is
+ * masked.  z_j = scale * x_j for visible keys and -inf for masked ones, then
+ * the softmax definition above: masked outputs are +0, a row with no visible
+ * key is NaN, and masked inputs are never read. */
+void oracle_softmax_causal(const double* x, int64_t batch, int64_t q, int64_t k, double scale, double* y);
+
 /* GroupNorm over x viewed as [n, c, s] (s = product of spatial dims),
  * with c divisible by groups.  For every (sample, group) the set holds the
  * (c/groups)*s elements of that group's channels:

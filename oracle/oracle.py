@@ -51,11 +51,12 @@ def _load():
         dp = ctypes.POINTER(ctypes.c_double)
         i64 = ctypes.c_int64
         lib.oracle_softmax_rows.argtypes = [dp, i64, i64, dp]
+        lib.oracle_softmax_causal.argtypes = [dp, i64, i64, i64, ctypes.c_double, dp]
         lib.oracle_group_norm.argtypes = [dp, i64, i64, i64, i64, dp, dp, ctypes.c_double, dp]
         lib.oracle_adaptive_avgpool2d.argtypes = [dp, i64, i64, i64, i64, i64, dp]
         lib.oracle_round_to_format.argtypes = [dp, i64, ctypes.c_int, ctypes.c_int,
                                                ctypes.POINTER(ctypes.c_uint32)]
-        for f in (lib.oracle_softmax_rows, lib.oracle_group_norm,
+        for f in (lib.oracle_softmax_rows, lib.oracle_softmax_causal, lib.oracle_group_norm,
                   lib.oracle_adaptive_avgpool2d, lib.oracle_round_to_format):
             f.restype = None
         _lib = lib
@@ -104,6 +105,20 @@ def softmax(x, dim: int = -1) -> np.ndarray:
         _load().oracle_softmax_rows(_dptr(xm), rows, length, _dptr(ym))
     y = np.moveaxis(ym, -1, dim)
     return np.ascontiguousarray(y.reshape(()) if squeeze else y)
+
+
+def softmax_causal(x, scale: float = 1.0) -> np.ndarray:
+    """Scaled causal softmax over the last axis of x [..., q, k] in float64:
+    query i sees keys j <= i + (k - q); masked outputs are +0."""
+    x = _f64(x)
+    if x.ndim < 2:
+        raise ValueError("softmax_causal expects [..., q, k]")
+    q, k = x.shape[-2], x.shape[-1]
+    batch = x.size // (q * k) if q * k else 0
+    y = np.empty_like(x)
+    if x.size:
+        _load().oracle_softmax_causal(_dptr(x), batch, q, k, float(scale), _dptr(y))
+    return y
 
 
 def group_norm(x, num_groups: int, weight=None, bias=None, eps: float = 1e-5) -> np.ndarray:

@@ -164,6 +164,35 @@ kf_status kf_softmax(const void* x, kf_dtype x_dtype, void* y, kf_dtype y_dtype,
     return done(s, variant);
 }
 
+kf_status kf_softmax_causal(const void* x, kf_dtype x_dtype, void* y, kf_dtype y_dtype, int32_t ndim,
+                            const int64_t* shape, const int64_t* x_strides, const int64_t* y_strides, double scale,
+                            void* stream) {
+    begin();
+    int64_t n = 0;
+    kf_status s = check_shape(ndim, shape, 2, KF_MAX_DIMS, &n);
+    if (s != KF_OK) return s;
+    if (!dtype_ok(x_dtype) || !dtype_ok(y_dtype))
+        return fail(KF_ERR_BAD_DTYPE, "dtype %d -> %d not supported", (int)x_dtype, (int)y_dtype);
+    const bool pair_ok = (x_dtype == y_dtype) || (y_dtype == KF_FLOAT32 && x_dtype != KF_FLOAT32);
+    if (!pair_ok) return fail(KF_ERR_BAD_DTYPE, "softmax cannot narrow %d to %d", (int)x_dtype, (int)y_dtype);
+    if (!std::isfinite(scale)) return fail(KF_ERR_BAD_ARG, "scale must be finite");
+    if (n == 0) return done(KF_OK, "noop");
+    if (!x || !y) return fail(KF_ERR_NULL_POINTER, "x or y is NULL");
+    if ((uintptr_t)x % elem_bytes(x_dtype) || (uintptr_t)y % elem_bytes(y_dtype))
+        return fail(KF_ERR_BAD_ARG, "x or y is not aligned to its element size");
+    if (!dense(ndim, shape, x_strides) || !dense(ndim, shape, y_strides))
+        return fail(KF_ERR_UNSUPPORTED_LAYOUT, "only dense row-major tensors are supported");
+    const int64_t xb = n * elem_bytes(x_dtype), yb = n * elem_bytes(y_dtype);
+    if (x != y && overlaps(x, xb, y, yb)) return fail(KF_ERR_BAD_ARG, "x and y partially overlap");
+    if (x == y && x_dtype != y_dtype) return fail(KF_ERR_BAD_ARG, "in-place softmax needs equal dtypes");
+
+    const int64_t q = shape[ndim - 2], k = shape[ndim - 1];
+    CausalSoftmaxArgs a{x, y, x_dtype, y_dtype, n / (q * k), q, k, (float)scale};
+    const char* variant = nullptr;
+    s = softmax_causal_launch(a, static_cast<hipStream_t>(stream), &variant);
+    return done(s, variant);
+}
+
 kf_status kf_group_norm_workspace_bytes(kf_dtype x_dtype, int32_t ndim, const int64_t* shape, int64_t num_groups,
                                         size_t* bytes) {
     begin();

@@ -20,6 +20,16 @@ struct SoftmaxArgs {
 };
 kf_status softmax_launch(const SoftmaxArgs& a, hipStream_t s, const char** variant);
 
+// Scaled causal softmax over the last axis of a dense [batch, q, k] view.
+struct CausalSoftmaxArgs {
+    const void* x;
+    void* y;
+    kf_dtype xt, yt;
+    int64_t batch, q, k;
+    float scale;
+};
+kf_status softmax_causal_launch(const CausalSoftmaxArgs& a, hipStream_t s, const char** variant);
+
 // GroupNorm over a dense [n, c, spatial] view.
 struct GroupNormArgs {
     const void* x;

@@ -201,6 +201,78 @@ __global__ __launch_bounds__(NT) void sm_block(const void* __restrict__ x, void*
 }
 
 // --------------------------------------------------------------------------
+// Scaled causal softmax over rows of [batch * q, k]: query i = row % q sees
+// keys j < live = clamp(i + k - q + 1, 0, k).  One workgroup per row with
+// wave-contiguous segments as in sm_block; a wave whose whole segment is
+// masked issues no loads, so the masked triangle is never read, and every
+// slot is written (masked keys give exp(-inf) = +0).  A row with no visible
+// key has max -inf and comes out NaN, as the masked softmax definition does.
+template <class TI, class TO, int NT, int NV, bool VECTOR>
+__global__ __launch_bounds__(NT) void sm_causal(const void* __restrict__ x, void* __restrict__ y, int32_t q,
+                                                int32_t k, float scale) {
+    constexpr int VEC = VECTOR ? TI::vec : 1;
+    constexpr int NW = NT / kWave;
+    __shared__ float red[NW];
+    const int64_t row = blockIdx.x;
+    const int32_t i = (int32_t)(row % q);
+    const int32_t live = max(0, min(k, i + (k - q) + 1));
+    const int64_t base = row * k;
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = threadIdx.x / kWave;
+    const int seg = wave * NV * kWave + lane;
+
+    float v[NV][VEC];
+    if (wave * NV * kWave * VEC < live) {  // uniform per wave
+#pragma unroll
+        for (int kk = 0; kk < NV; ++kk) {
+            const int e0 = (seg + kk * kWave) * VEC;
+            const int64_t at = base + (e0 < live ? e0 : 0);
+            if constexpr (VECTOR) load_vec<TI>(x, at, v[kk]);
+            else v[kk][0] = load1<TI>(x, at);
+        }
+#pragma unroll
+        for (int kk = 0; kk < NV; ++kk) {
+            const int e0 = (seg + kk * kWave) * VEC;
+#pragma unroll
+            for (int ii = 0; ii < VEC; ++ii) v[kk][ii] = (e0 + ii < live) ? v[kk][ii] * scale : -INFINITY;
+        }
+    } else {
+#pragma unroll
+        for (int kk = 0; kk < NV; ++kk)
+#pragma unroll
+            for (int ii = 0; ii < VEC; ++ii) v[kk][ii] = -INFINITY;
+    }
+    float m = -INFINITY;
+#pragma unroll
+    for (int kk = 0; kk < NV; ++kk)
+#pragma unroll
+        for (int ii = 0; ii < VEC; ++ii) m = fmaxf(m, v[kk][ii]);
+    m = block_reduce<NW>(m, OpMax{}, red);
+
+    float s = 0.f;
+#pragma unroll
+    for (int kk = 0; kk < NV; ++kk)
+#pragma unroll
+        for (int ii = 0; ii < VEC; ++ii) {
+            v[kk][ii] = exp_out<TO>(v[kk][ii], m);
+            s += v[kk][ii];
+        }
+    s = block_reduce<NW>(s, OpSum{}, red);
+    const float inv = 1.f / s;
+
+#pragma unroll
+    for (int kk = 0; kk < NV; ++kk) {
+        const int e0 = (seg + kk * kWave) * VEC;
+        if (e0 < k) {
+#pragma unroll
+            for (int ii = 0; ii < VEC; ++ii) v[kk][ii] *= inv;
+            if constexpr (VECTOR) store_span<TO, VEC>(y, base + e0, v[kk]);
+            else store1<TO>(y, base + e0, v[kk][0]);
+        }
+    }
+}
+
+// --------------------------------------------------------------------------
 // Online normaliser state (m, s): s = sum of e^(x - m) over the elements
 // seen.  A state with m = -inf has seen only -inf (or nothing) and weighs 0.
 struct MS {
@@ -447,6 +519,51 @@ kf_status run(const SoftmaxArgs& a, hipStream_t s, const char** variant) {
     return KF_OK;
 }
 
+template <class TI, class TO, int NT, int NV, bool VECTOR>
+void go_causal(const CausalSoftmaxArgs& a, hipStream_t s) {
+    hipLaunchKernelGGL((sm_causal<TI, TO, NT, NV, VECTOR>), dim3((unsigned)(a.batch * a.q)), dim3(NT), 0, s, a.x,
+                       a.y, (int32_t)a.q, (int32_t)a.k, a.scale);
+}
+
+template <class TI, class TO>
+kf_status run_causal(const CausalSoftmaxArgs& a, hipStream_t s, const char** variant) {
+    if (a.batch * a.q > (int64_t)INT32_MAX || a.k > (int64_t)INT32_MAX || a.q > (int64_t)INT32_MAX) {
+        set_error("softmax_causal: %lld rows of %lld exceed the grid limit", (long long)(a.batch * a.q),
+                  (long long)a.k);
+        return KF_ERR_UNSUPPORTED_LAYOUT;
+    }
+    const bool vec = (a.k % TI::vec == 0) && (a.k % TO::vec == 0) && ((uintptr_t)a.x % 16 == 0) &&
+                     ((uintptr_t)a.y % 16 == 0);
+    const int64_t slots = vec ? a.k / TI::vec : a.k;
+    bool done = false;
+#define KF_CAUSAL(NT, NV)                                                                                    \
+    if (!done && slots <= (int64_t)(NT) * (NV)) {                                                            \
+        if (vec) go_causal<TI, TO, NT, NV, true>(a, s);                                                      \
+        else go_causal<TI, TO, NT, NV, false>(a, s);                                                         \
+        *variant = vec ? "sm_causal_vec_nt" #NT "_nv" #NV : "sm_causal_scalar_nt" #NT "_nv" #NV;             \
+        done = true;                                                                                         \
+    }
+    KF_CAUSAL(64, 1)
+    KF_CAUSAL(64, 2)
+    KF_CAUSAL(128, 2)
+    KF_CAUSAL(256, 2)
+    KF_CAUSAL(512, 2)
+    KF_CAUSAL(1024, 2)
+    KF_CAUSAL(1024, 4)
+    KF_CAUSAL(1024, 8)
+#undef KF_CAUSAL
+    if (!done) {
+        set_error("softmax_causal: rows of %lld elements exceed the register-resident kernels", (long long)a.k);
+        return KF_ERR_UNSUPPORTED_LAYOUT;
+    }
+    const hipError_t err = hipGetLastError();
+    if (err != hipSuccess) {
+        set_error("softmax_causal launch failed: %s", hipGetErrorString(err));
+        return KF_ERR_HIP;
+    }
+    return KF_OK;
+}
+
 }  // namespace
 
 kf_status softmax_launch(const SoftmaxArgs& a, hipStream_t s, const char** variant) {
@@ -459,4 +576,16 @@ kf_status softmax_launch(const SoftmaxArgs& a, hipStream_t s, const char** varia
     return KF_ERR_BAD_DTYPE;
 }
 
+}  // namespace kf
+
+namespace kf {
+kf_status softmax_causal_launch(const CausalSoftmaxArgs& a, hipStream_t s, const char** variant) {
+    if (a.xt == KF_FLOAT32 && a.yt == KF_FLOAT32) return run_causal<F32, F32>(a, s, variant);
+    if (a.xt == KF_BFLOAT16 && a.yt == KF_BFLOAT16) return run_causal<BF16, BF16>(a, s, variant);
+    if (a.xt == KF_BFLOAT16 && a.yt == KF_FLOAT32) return run_causal<BF16, F32>(a, s, variant);
+    if (a.xt == KF_FLOAT16 && a.yt == KF_FLOAT16) return run_causal<F16, F16>(a, s, variant);
+    if (a.xt == KF_FLOAT16 && a.yt == KF_FLOAT32) return run_causal<F16, F32>(a, s, variant);
+    set_error("softmax_causal: unsupported dtype pair");
+    return KF_ERR_BAD_DTYPE;
+}
 }  // namespace kf

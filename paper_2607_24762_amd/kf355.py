@@ -34,6 +34,8 @@ _SIGNATURES = {
     "kf_last_variant": (ctypes.c_char_p, []),
     "kf_softmax": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p, ctypes.c_int, ctypes.c_int32,
                                   _i64p, _i64p, _i64p, ctypes.c_int64, ctypes.c_void_p]),
+    "kf_softmax_causal": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p, ctypes.c_int,
+                                         ctypes.c_int32, _i64p, _i64p, _i64p, ctypes.c_double, ctypes.c_void_p]),
     "kf_group_norm": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p, ctypes.c_int32, _i64p, _i64p,
                                      _i64p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int,
                                      ctypes.c_double, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]),
@@ -117,6 +119,21 @@ def kf_softmax(x: torch.Tensor, dim: int = -1, out_dtype: torch.dtype | None = N
     return y
 
 
+def kf_softmax_causal(x: torch.Tensor, scale: float = 1.0, out_dtype: torch.dtype | None = None,
+                      out: torch.Tensor | None = None) -> torch.Tensor:
+    """softmax(scale * x + causal mask, -1) over x [..., q, k] through
+    kf_softmax_causal (query i sees keys j <= i + k - q)."""
+    _need_cuda(x)
+    y = out if out is not None else torch.empty(x.shape, dtype=out_dtype or x.dtype, device=x.device)
+    shape, _s = _arr(list(x.shape))
+    xs, _a = _arr(list(x.stride()))
+    ys, _b = _arr(list(y.stride()))
+    with torch.cuda.device(x.device):
+        _check(lib().kf_softmax_causal(ctypes.c_void_p(x.data_ptr()), _dtype(x), ctypes.c_void_p(y.data_ptr()),
+                                       _dtype(y), x.dim(), shape, xs, ys, float(scale), _stream(x)))
+    return y
+
+
 _ws_cache: dict = {}
 
 
@@ -176,6 +193,7 @@ def kf_adaptive_avgpool2d(x: torch.Tensor, output_size, out: torch.Tensor | None
 
 
 softmax = kf_softmax
+softmax_causal = kf_softmax_causal
 group_norm = kf_group_norm
 adaptive_avg_pool2d = kf_adaptive_avgpool2d
 
@@ -203,6 +221,16 @@ def prepare_softmax(x: torch.Tensor, y: torch.Tensor, dim: int = -1) -> Prepared
     args = (ctypes.c_void_p(x.data_ptr()), _dtype(x), ctypes.c_void_p(y.data_ptr()), _dtype(y), x.dim(), shape, xs,
             ys, dim, _stream(x))
     return Prepared(lib().kf_softmax, args, (x, y, a0, a1, a2))
+
+
+def prepare_softmax_causal(x: torch.Tensor, y: torch.Tensor, scale: float = 1.0) -> Prepared:
+    _need_cuda(x, y)
+    shape, a0 = _arr(list(x.shape))
+    xs, a1 = _arr(list(x.stride()))
+    ys, a2 = _arr(list(y.stride()))
+    args = (ctypes.c_void_p(x.data_ptr()), _dtype(x), ctypes.c_void_p(y.data_ptr()), _dtype(y), x.dim(), shape, xs,
+            ys, float(scale), _stream(x))
+    return Prepared(lib().kf_softmax_causal, args, (x, y, a0, a1, a2))
 
 
 def prepare_group_norm(x: torch.Tensor, y: torch.Tensor, num_groups: int, weight=None, bias=None,

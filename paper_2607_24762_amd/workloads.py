@@ -80,6 +80,15 @@ def attn_softmax_causal_bf16(seed: int = 4, heads: int = 8, seq: int = 4096) -> 
     return {"op": "softmax", "x": s, "dim": -1, "out_dtype": "bf16"}
 
 
+def attn_scores_raw_bf16(seed: int = 4, heads: int = 8, seq: int = 4096) -> dict:
+    """The same score draws as attn_softmax_causal_bf16 before scaling and
+    masking: bf16 [1, heads, seq, seq] = bf16(3 z), for the fused scaled
+    causal softmax with scale 1/16 (= 1/sqrt(256))."""
+    rng = np.random.default_rng(seed)
+    s = cast(3.0 * rng.standard_normal((1, heads, seq, seq)), "bf16")
+    return {"op": "softmax_causal", "x": s, "scale": 1.0 / 16.0, "out_dtype": "bf16"}
+
+
 def router_softmax_f32(seed: int = 5, experts: int = 256, tokens: int = 16384) -> dict:
     """MoE router logits: fp32 [tokens, experts], z ~ N(0, 1) plus +4 on an
     i.i.d. 5% of entries (u ~ U[0, 1) drawn after z, outlier where u < 0.05)."""

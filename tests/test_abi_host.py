@@ -96,6 +96,22 @@ def test_softmax_size_one_dims_may_have_any_stride(lib):
     assert softmax(lib, shape=(1, 0), xs=(12345, 1)) == OK
 
 
+def causal(lib, shape=(2, 4, 8), scale=0.5, x=FAKE, y=FAKE + (1 << 30), xt=F32, yt=F32, xs=None):
+    return lib.kf_softmax_causal(ctypes.c_void_p(x), xt, ctypes.c_void_p(y), yt, len(shape), arr(shape),
+                                 arr(xs) if xs else None, None, scale, None)
+
+
+def test_softmax_causal_rejections(lib):
+    assert causal(lib, shape=(8,)) == SHAPE               # needs [..., q, k]
+    assert causal(lib, scale=float("nan")) == ARG
+    assert causal(lib, scale=float("inf")) == ARG
+    assert causal(lib, xt=F32, yt=F16) == DTYPE
+    assert causal(lib, x=0) == NULLP
+    assert causal(lib, xs=(32, 1, 4)) == LAYOUT
+    assert causal(lib, y=FAKE + 4) == ARG
+    assert causal(lib, shape=(2, 0, 8)) == OK and lib.kf_last_variant().decode() == "noop"
+
+
 def gn(lib, shape=(2, 8, 4, 4), groups=4, w=None, b=None, at=F32, eps=1e-5, ws=FAKE + (2 << 30), wsb=1 << 20,
        xt=F32, x=FAKE, y=FAKE + (1 << 30), xs=None):
     return lib.kf_group_norm(ctypes.c_void_p(x), xt, ctypes.c_void_p(y), len(shape), arr(shape),

@@ -1,0 +1,113 @@
+"""GPU parity of kf_softmax_causal (scale + causal mask + softmax in one
+pass) against the float64 oracle: the attention workload shape, query /
+key lengths that differ (mask aligned to the end of the key axis), every
+dtype pair, row lengths across the kernel table, unaligned rows, garbage in
+the masked triangle, rows with no visible key, and in-place use.
+Tolerances as for kf_softmax: fp32 max abs error <= 1e-6, bf16 / fp16
+within 1 unit in the last place of the oracle rounded once."""
+import numpy as np
+import pytest
+import torch
+
+from compare import assert_close, compare, note
+from oracle import oracle
+from paper_2607_24762_amd import kf355
+from paper_2607_24762_amd import workloads as W
+from paper_2607_24762_amd.workloads import randn
+
+pytestmark = pytest.mark.gpu
+TORCH = {"f32": torch.float32, "bf16": torch.bfloat16, "f16": torch.float16}
+
+
+@pytest.fixture(scope="module", autouse=True)
+def gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU visible")
+    kf355.lib()
+
+
+def run(x_cpu, scale, out):
+    y = kf355.kf_softmax_causal(x_cpu.cuda(), scale, out_dtype=TORCH[out])
+    torch.cuda.synchronize()
+    variant = kf355.last_variant()
+    assert_close(y, oracle.softmax_causal(x_cpu, scale), out)
+    return y, variant
+
+
+def test_attention_workload_matches_oracle_and_unfused_path():
+    note("softmax_causal attention workload [1,8,4096,4096] bf16, scale 1/16")
+    w = W.attn_scores_raw_bf16()
+    x = w["x"].cuda()
+    y = kf355.kf_softmax_causal(x, w["scale"])
+    torch.cuda.synchronize()
+    assert kf355.last_variant() == "sm_causal_vec_nt256_nv2"
+    r = compare(y.cpu(), oracle.softmax_causal(w["x"], w["scale"]), "bf16")
+    print("[parity] softmax_causal attention:", r, flush=True)
+    assert r["ok"], r
+    # Scaling by 1/16 is exact, so the fused result must equal the unfused
+    # softmax of the pre-scaled, pre-masked scores bit for bit.
+    ref = kf355.kf_softmax(W.attn_softmax_causal_bf16()["x"].cuda(), -1)
+    torch.cuda.synchronize()
+    assert torch.equal(y.view(torch.int16), ref.view(torch.int16))
+
+
+@pytest.mark.parametrize("pair", [("f32", "f32"), ("bf16", "bf16"), ("bf16", "f32"), ("f16", "f16"), ("f16", "f32")],
+                         ids=lambda p: f"{p[0]}-{p[1]}")
+@pytest.mark.parametrize("qk", [(1, 1), (4, 4), (7, 7), (16, 64), (64, 64), (33, 257), (128, 1024), (5, 2048),
+                                (300, 4096), (64, 8192), (2, 16384), (1, 65536)])
+def test_lengths_and_dtypes(pair, qk):
+    q, k = qk
+    if pair[0] == "f32" and k > 32768:
+        pytest.skip("fp32 rows above 32768 are outside the register-resident table")
+    note(f"softmax_causal {pair} q={q} k={k}")
+    x = randn((2, q, k), pair[0], seed=q + k, std=3.0)
+    _, variant = run(x, 0.125, pair[1])
+    assert variant.startswith("sm_causal_"), variant
+
+
+@pytest.mark.parametrize("scale", [1.0, 0.0625, 0.37, -0.5])
+def test_scales(scale):
+    note(f"softmax_causal scale {scale}")
+    run(randn((3, 40, 40), "f32", seed=3, std=2.0), scale, "f32")
+
+
+def test_unaligned_rows_use_element_access():
+    note("softmax_causal unaligned")
+    q, k = 9, 257
+    big = randn((2 * q * k + 1,), "bf16", seed=5, std=2.0)
+    x_cpu = big[1:].view(2, q, k)
+    y = kf355.kf_softmax_causal(big.cuda()[1:].view(2, q, k), 0.5)
+    torch.cuda.synchronize()
+    assert "scalar" in kf355.last_variant()
+    assert_close(y, oracle.softmax_causal(x_cpu, 0.5), "bf16")
+
+
+def test_masked_triangle_is_never_used():
+    note("softmax_causal NaN in the masked triangle")
+    q = k = 512
+    x = randn((2, q, k), "bf16", seed=8, std=2.0)
+    poisoned = x.clone()
+    poisoned[:, torch.ones(q, k, dtype=torch.bool).triu(1)] = float("nan")
+    a = kf355.kf_softmax_causal(x.cuda(), 0.25)
+    b = kf355.kf_softmax_causal(poisoned.cuda(), 0.25)
+    torch.cuda.synchronize()
+    assert torch.equal(a.view(torch.int16), b.view(torch.int16))
+    masked = b.cpu()[:, torch.ones(q, k, dtype=torch.bool).triu(1)]
+    assert (masked.view(torch.int16) == 0).all()   # exact +0
+
+
+def test_rows_without_visible_keys_are_nan():
+    note("softmax_causal q > k")
+    x = randn((1, 6, 4), "f32", seed=1)
+    y, _ = run(x, 1.0, "f32")
+    yc = y.cpu()
+    assert torch.isnan(yc[0, :2]).all() and torch.isfinite(yc[0, 2:]).all()
+
+
+def test_in_place():
+    note("softmax_causal in place")
+    x_cpu = randn((2, 64, 1000), "bf16", seed=9)
+    x = x_cpu.cuda()
+    kf355.kf_softmax_causal(x, 0.3, out=x)
+    torch.cuda.synchronize()
+    assert_close(x, oracle.softmax_causal(x_cpu, 0.3), "bf16")
