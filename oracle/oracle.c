@@ -96,6 +96,29 @@ void oracle_group_norm(const double* x, int64_t n, int64_t c, int64_t s,
     }
 }
 
+/* LayerNorm (PyTorch `layer_norm(x, normalized_shape, w, b, eps)`
+ * definition): per row, biased variance from a second pass, eps inside the
+ * square root, elementwise affine after normalisation. */
+void oracle_layer_norm(const double* x, int64_t rows, int64_t d, const double* w, const double* b, double eps,
+                       double* y) {
+    for (int64_t r = 0; r < rows; ++r) {
+        const double* xr = x + r * d;
+        double* yr = y + r * d;
+        if (d == 0) continue;
+        double sum = 0.0;
+        for (int64_t j = 0; j < d; ++j) sum += xr[j];
+        const double mu = sum / (double)d;
+        double sq = 0.0;
+        for (int64_t j = 0; j < d; ++j) {
+            const double dv = xr[j] - mu;
+            sq += dv * dv;
+        }
+        const double inv_std = 1.0 / sqrt(sq / (double)d + eps);
+        for (int64_t j = 0; j < d; ++j)
+            yr[j] = (xr[j] - mu) * inv_std * (w ? w[j] : 1.0) + (b ? b[j] : 0.0);
+    }
+}
+
 /* adaptive_avg_pool2d (PyTorch definition): output cell (i, j) is the mean
  * of the input window [floor(i*h/oh), ceil((i+1)*h/oh)) x
  * [floor(j*w/ow), ceil((j+1)*w/ow)), computed with integer arithmetic. */

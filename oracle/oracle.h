@@ -54,6 +54,14 @@ void oracle_group_norm(const double* x, int64_t n, int64_t c, int64_t s,
                        int64_t groups, const double* w, const double* b,
                        double eps, double* y);
 
+/* LayerNorm over the last axis of x viewed as [rows, d] (d = product of the
+ * normalised trailing dims):
+ *   mu = sum x / d ; var = sum (x - mu)^2 / d   (biased, two-pass)
+ *   y  = (x - mu) / sqrt(var + eps) * w[j] + b[j]
+ * w == NULL means w = 1, b == NULL means b = 0. */
+void oracle_layer_norm(const double* x, int64_t rows, int64_t d, const double* w, const double* b, double eps,
+                       double* y);
+
 /* adaptive_avg_pool2d over x viewed as [planes, h, w] -> [planes, oh, ow].
  * Output cell (i, j) averages rows [floor(i*h/oh), ceil((i+1)*h/oh)) and
  * columns [floor(j*w/ow), ceil((j+1)*w/ow)). */

@@ -54,10 +54,11 @@ def _load():
         lib.oracle_softmax_causal.argtypes = [dp, i64, i64, i64, ctypes.c_double, dp]
         lib.oracle_group_norm.argtypes = [dp, i64, i64, i64, i64, dp, dp, ctypes.c_double, dp]
         lib.oracle_adaptive_avgpool2d.argtypes = [dp, i64, i64, i64, i64, i64, dp]
+        lib.oracle_layer_norm.argtypes = [dp, i64, i64, dp, dp, ctypes.c_double, dp]
         lib.oracle_round_to_format.argtypes = [dp, i64, ctypes.c_int, ctypes.c_int,
                                                ctypes.POINTER(ctypes.c_uint32)]
         for f in (lib.oracle_softmax_rows, lib.oracle_softmax_causal, lib.oracle_group_norm,
-                  lib.oracle_adaptive_avgpool2d, lib.oracle_round_to_format):
+                  lib.oracle_adaptive_avgpool2d, lib.oracle_layer_norm, lib.oracle_round_to_format):
             f.restype = None
         _lib = lib
     return _lib
@@ -144,6 +145,27 @@ def group_norm(x, num_groups: int, weight=None, bias=None, eps: float = 1e-5) ->
                               _dptr(w) if w is not None else null,
                               _dptr(b) if b is not None else null,
                               float(eps), _dptr(y))
+    return y
+
+
+def layer_norm(x, normalized_ndim: int = 1, weight=None, bias=None, eps: float = 1e-5) -> np.ndarray:
+    """PyTorch layer_norm(x, x.shape[-normalized_ndim:], weight, bias, eps)
+    in float64; weight / bias have the normalised shape (or are None)."""
+    x = _f64(x)
+    if not 1 <= normalized_ndim <= x.ndim:
+        raise ValueError("normalized_ndim must be in [1, x.ndim]")
+    d = int(np.prod(x.shape[x.ndim - normalized_ndim:], dtype=np.int64))
+    rows = x.size // d if d else 0
+    w = _f64(weight).reshape(-1) if weight is not None else None
+    b = _f64(bias).reshape(-1) if bias is not None else None
+    for v in (w, b):
+        if v is not None and v.size != d:
+            raise ValueError("affine parameters must have the normalised shape")
+    y = np.empty_like(x)
+    if x.size:
+        null = ctypes.POINTER(ctypes.c_double)()
+        _load().oracle_layer_norm(_dptr(x), rows, d, _dptr(w) if w is not None else null,
+                                  _dptr(b) if b is not None else null, float(eps), _dptr(y))
     return y
 
 
