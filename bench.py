@@ -259,6 +259,39 @@ def main():
             "vs_unfused_softmax": round(per_op["softmax"]["us_per_call"] / us, 3)}}
         del cs
 
+        # LayerNorm of the SD3.5 transformer blocks, rotating buffer sets.
+        lnw = W.layernorm_sd35_bf16()
+        lbytes = lnw["x"].numel() * 2 * 2
+        src = lnw["x"].to(dev)
+        cs = [kf355.prepare_layer_norm(src.clone(), torch.empty_like(src), 1, None, None, lnw["eps"])
+              for _ in range(sets_for(lbytes))]
+        del src
+        cs[0]()
+        lvar = kf355.last_variant()
+        for i in range(args.warmup):
+            cs[i % len(cs)]()
+        e0.record()
+        for i in range(args.steps):
+            cs[i % len(cs)]()
+        e1.record()
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) * 1e3 / args.steps
+        gbs = lbytes / (us * 1e-6) / 1e9
+        lx = cs[0]._keep[0]
+        n_eager = min(args.steps, 50)
+        e0.record()
+        for i in range(n_eager):
+            F.layer_norm(cs[i % len(cs)]._keep[0], lnw["normalized_shape"], None, None, lnw["eps"])
+        e1.record()
+        torch.cuda.synchronize()
+        eager_us = e0.elapsed_time(e1) * 1e3 / n_eager
+        next_rows["layer_norm"] = {
+            "workload": "bf16 [2,4096,1536], no affine, eps 1e-6 (SD3.5 Medium transformer)",
+            "us_per_call": round(us, 3), "gbps": round(gbs, 1), "frac_of_peak": round(gbs / PEAK_HBM_GBS, 4),
+            "algorithmic_bytes": lbytes, "variant": lvar, "buffer_sets": len(cs),
+            "torch_eager_us": round(eager_us, 3), "kf355_speedup": round(eager_us / us, 3)}
+        del cs, lx
+
     calib = copy_calibration(torch, dev, nbytes["softmax"])
     sm = per_op["softmax"]
     traffic = measured_traffic()

@@ -155,6 +155,26 @@ kf_status kf_group_norm_workspace_bytes(kf_dtype x_dtype, int32_t ndim, const in
                                         size_t* bytes);
 
 /*
+ * kf_layer_norm -- y = layer_norm(x, x.shape[-normalized_ndim:], weight,
+ * bias, eps) (PyTorch `torch.nn.functional.layer_norm`; the SD3.5 Medium
+ * layer_norm result, Section IV-C): for each row of the d = product of the
+ * last `normalized_ndim` sizes, mu and var are the mean and biased variance
+ * of the row and y = (x - mu) / sqrt(var + eps) * weight[j] + bias[j].
+ *
+ *  x, y             device pointers, same shape (1 <= ndim <= 8), same dtype
+ *                   (FLOAT32, BFLOAT16 or FLOAT16); statistics are fp32.
+ *  normalized_ndim  in [1, ndim].
+ *  weight, bias     device pointers to d elements each (the normalised
+ *                   shape, dense), or NULL (weight 1 / bias 0); both use
+ *                   `affine_dtype`, which is x_dtype or FLOAT32.
+ *  eps              >= 0 (used as fp32).
+ *  y may equal x (in place); any other overlap is KF_ERR_BAD_ARG.
+ */
+kf_status kf_layer_norm(const void* x, kf_dtype x_dtype, void* y, int32_t ndim, const int64_t* shape,
+                        const int64_t* x_strides, const int64_t* y_strides, int32_t normalized_ndim,
+                        const void* weight, const void* bias, kf_dtype affine_dtype, double eps, void* stream);
+
+/*
  * kf_adaptive_avgpool2d -- y = adaptive_avg_pool2d(x, (out_h, out_w))
  * (PyTorch `torch.nn.functional.adaptive_avg_pool2d`; the ResNet-50 result,
  * Section IV-C): output cell (i, j) is the mean of input rows

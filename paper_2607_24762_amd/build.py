@@ -16,7 +16,7 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libkf355.so")
 
-SOURCES = ["kf355_api.cpp", "softmax.hip", "group_norm.hip", "avgpool.hip"]
+SOURCES = ["kf355_api.cpp", "softmax.hip", "group_norm.hip", "layer_norm.hip", "avgpool.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
@@ -40,7 +40,7 @@ def _compile(src: str) -> str:
     return obj
 
 
-def build_library(jobs: int = 4) -> str:
+def build_library(jobs: int = 5) -> str:
     """Compile every source and link libkf355.so (always rebuilds)."""
     os.makedirs(BUILD, exist_ok=True)
     with cf.ThreadPoolExecutor(max_workers=jobs) as ex:

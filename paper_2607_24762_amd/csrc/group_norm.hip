@@ -39,41 +39,6 @@ constexpr int kNT = 256;          // threads per workgroup
 constexpr size_t kCounterStride = 256;  // bytes between two groups' counters
 constexpr int kFloatsPerThread = 64;
 
-struct Moments {
-    float n, mean, m2;
-};
-
-// Chan et al. combine of two partial moments (a before b).  The weight
-// b.n / n uses the hardware reciprocal (v_rcp_f32, within 1 ulp; exact for the
-// power-of-two counts of full chunks) instead of an IEEE division: the merges
-// sit on the critical path between a workgroup's loads and its stores.
-__device__ __forceinline__ Moments chan(Moments a, Moments b) {
-    const float n = a.n + b.n;
-    if (n == 0.f) return Moments{0.f, 0.f, 0.f};
-    const float d = b.mean - a.mean;
-    const float f = b.n * __builtin_amdgcn_rcpf(n);
-    return Moments{n, fmaf(d, f, a.mean), a.m2 + b.m2 + d * d * a.n * f};
-}
-
-template <int S>
-__device__ __forceinline__ Moments moments_step(Moments m) {
-    Moments o{partner<S>(m.n), partner<S>(m.mean), partner<S>(m.m2)};
-    // In step S the partner sits in the other half of an aligned block of
-    // 2^(S+1) lanes; the lane in the lower half is the left operand.
-    const bool lower = (__lane_id() & (1 << S)) == 0;
-    return lower ? chan(m, o) : chan(o, m);
-}
-
-__device__ __forceinline__ Moments moments_wave(Moments m) {
-    m = moments_step<0>(m);
-    m = moments_step<1>(m);
-    m = moments_step<2>(m);
-    m = moments_step<3>(m);
-    m = moments_step<4>(m);
-    m = moments_step<5>(m);
-    return m;
-}
-
 struct GNParams {
     const void* x;
     void* y;
@@ -202,20 +167,6 @@ struct Chunk {
     }
 };
 
-// Workgroup-wide combine: butterfly inside each wave, then waves in index
-// order through LDS.  Returns the result in every thread.
-__device__ __forceinline__ Moments moments_block(Moments m, Moments* lds) {
-    m = moments_wave(m);
-    const int w = threadIdx.x / kWave;
-    if ((threadIdx.x & (kWave - 1)) == 0) lds[w] = m;
-    __syncthreads();
-    Moments t = lds[0];
-#pragma unroll
-    for (int i = 1; i < kNT / kWave; ++i) t = chan(t, lds[i]);
-    __syncthreads();
-    return t;
-}
-
 // A published partial is one 64-bit word: mean bits low, M2 bits high with
 // the sign bit forced on.  M2 is never negative, so the flag is free, and a
 // published word is never 0, the value of an empty slot.  Writing the data
@@ -290,7 +241,7 @@ __global__ __launch_bounds__(kNT) void gn_fused(GNParams p) {
     C c;
     c.load(p, gbase, part);
     c.template load_affine<A>(p, part, g);
-    Moments m = moments_block(c.moments(p, part), lds);
+    Moments m = moments_block<kNT / kWave>(c.moments(p, part), lds);
 
     if (threadIdx.x < kWave) {
         bool ok = true;
@@ -318,7 +269,7 @@ __global__ __launch_bounds__(kNT) void gn_fused(GNParams p) {
         const int lane = threadIdx.x & (kWave - 1);
         for (int q = 0; q < p.parts; ++q) {
             c.load(p, gbase, q);
-            const Moments mq = moments_block(c.moments(p, q), lds);
+            const Moments mq = moments_block<kNT / kWave>(c.moments(p, q), lds);
             if ((q & (kWave - 1)) == lane) acc = chan(acc, mq);
         }
         if (threadIdx.x < kWave) {
@@ -345,7 +296,7 @@ __global__ __launch_bounds__(kNT) void gn_stats(GNParams p) {
     const int part = blockIdx.x - (int)(ng * p.parts);
     C c;
     c.load(p, ng * p.group_elems, part);
-    Moments m = moments_block(c.moments(p, part), lds);
+    Moments m = moments_block<kNT / kWave>(c.moments(p, part), lds);
     if (threadIdx.x == 0) publish(p, ng, part, m);
 }
 

@@ -243,6 +243,40 @@ kf_status kf_group_norm(const void* x, kf_dtype x_dtype, void* y, int32_t ndim, 
     return done(s, variant);
 }
 
+kf_status kf_layer_norm(const void* x, kf_dtype x_dtype, void* y, int32_t ndim, const int64_t* shape,
+                        const int64_t* x_strides, const int64_t* y_strides, int32_t normalized_ndim,
+                        const void* weight, const void* bias, kf_dtype affine_dtype, double eps, void* stream) {
+    begin();
+    int64_t n = 0;
+    kf_status s = check_shape(ndim, shape, 1, KF_MAX_DIMS, &n);
+    if (s != KF_OK) return s;
+    if (!dtype_ok(x_dtype)) return fail(KF_ERR_BAD_DTYPE, "x dtype %d not supported", (int)x_dtype);
+    if (normalized_ndim < 1 || normalized_ndim > ndim)
+        return fail(KF_ERR_BAD_ARG, "normalized_ndim %d outside [1, %d]", normalized_ndim, ndim);
+    if ((weight || bias) && !(affine_dtype == x_dtype || affine_dtype == KF_FLOAT32))
+        return fail(KF_ERR_BAD_DTYPE, "affine dtype %d must be x's dtype or FLOAT32", (int)affine_dtype);
+    if (!(eps >= 0.0) || !std::isfinite(eps)) return fail(KF_ERR_BAD_ARG, "eps must be finite and >= 0");
+    const int64_t d = count(normalized_ndim, shape + (ndim - normalized_ndim));
+    if (n == 0 || d == 0) return done(KF_OK, "noop");
+    if (!x || !y) return fail(KF_ERR_NULL_POINTER, "x or y is NULL");
+    const int64_t eb = elem_bytes(x_dtype);
+    if ((uintptr_t)x % eb || (uintptr_t)y % eb) return fail(KF_ERR_BAD_ARG, "x or y is not element aligned");
+    const int64_t ab = (weight || bias) ? elem_bytes(affine_dtype) : 1;
+    if ((uintptr_t)weight % ab || (uintptr_t)bias % ab)
+        return fail(KF_ERR_BAD_ARG, "weight or bias is not element aligned");
+    if (!dense(ndim, shape, x_strides) || !dense(ndim, shape, y_strides))
+        return fail(KF_ERR_UNSUPPORTED_LAYOUT, "only dense row-major tensors are supported");
+    const int64_t xb = n * eb;
+    if (x != y && overlaps(x, xb, y, xb)) return fail(KF_ERR_BAD_ARG, "x and y partially overlap");
+    if ((weight && overlaps(weight, d * ab, y, xb)) || (bias && overlaps(bias, d * ab, y, xb)))
+        return fail(KF_ERR_BAD_ARG, "weight or bias overlaps y");
+
+    LayerNormArgs a{x, y, x_dtype, n / d, d, weight, bias, affine_dtype, (float)eps};
+    const char* variant = nullptr;
+    s = layer_norm_launch(a, static_cast<hipStream_t>(stream), &variant);
+    return done(s, variant);
+}
+
 kf_status kf_adaptive_avgpool2d(const void* x, kf_dtype dtype, void* y, int32_t ndim, const int64_t* shape,
                                 const int64_t* x_strides, const int64_t* y_strides, int64_t out_h, int64_t out_w,
                                 void* stream) {

@@ -220,4 +220,64 @@ __device__ __forceinline__ float uniform0(float v) {
     return __builtin_bit_cast(float, __builtin_amdgcn_readfirstlane(__builtin_bit_cast(int, v)));
 }
 
+// ---------------------------------------------------------------------------
+// Moments (count, mean, M2) and their Chan et al. parallel combine, shared by
+// GroupNorm and LayerNorm.
+struct Moments {
+    float n, mean, m2;
+};
+
+// Chan et al. combine of two partial moments (a before b).  The weight
+// b.n / n uses the hardware reciprocal (v_rcp_f32, within 1 ulp; exact for
+// power-of-two counts) instead of an IEEE division: the merges sit on the
+// critical path between a workgroup's loads and its stores.
+__device__ __forceinline__ Moments chan(Moments a, Moments b) {
+    const float n = a.n + b.n;
+    if (n == 0.f) return Moments{0.f, 0.f, 0.f};
+    const float d = b.mean - a.mean;
+    const float f = b.n * __builtin_amdgcn_rcpf(n);
+    return Moments{n, fmaf(d, f, a.mean), a.m2 + b.m2 + d * d * a.n * f};
+}
+
+// Butterfly step S: the lane in the lower half of its aligned block of
+// 2^(S+1) lanes is the left operand, so both lanes of a pair compute
+// bit-identical results.
+template <int S>
+__device__ __forceinline__ Moments moments_step(Moments m) {
+    Moments o{partner<S>(m.n), partner<S>(m.mean), partner<S>(m.m2)};
+    const bool lower = (__lane_id() & (1 << S)) == 0;
+    return lower ? chan(m, o) : chan(o, m);
+}
+
+// Combine over aligned groups of LANES lanes (a power of two <= 64); every
+// lane of a group ends with the group's moments.
+template <int LANES>
+__device__ __forceinline__ Moments moments_group(Moments m) {
+    if constexpr (LANES >= 2) m = moments_step<0>(m);
+    if constexpr (LANES >= 4) m = moments_step<1>(m);
+    if constexpr (LANES >= 8) m = moments_step<2>(m);
+    if constexpr (LANES >= 16) m = moments_step<3>(m);
+    if constexpr (LANES >= 32) m = moments_step<4>(m);
+    if constexpr (LANES >= 64) m = moments_step<5>(m);
+    return m;
+}
+
+__device__ __forceinline__ Moments moments_wave(Moments m) { return moments_group<kWave>(m); }
+
+// Workgroup-wide combine of NW waves: butterfly inside each wave, then the
+// waves in index order through LDS (`lds` holds NW entries).  Every thread
+// gets the result.
+template <int NW>
+__device__ __forceinline__ Moments moments_block(Moments m, Moments* lds) {
+    m = moments_wave(m);
+    const int w = threadIdx.x / kWave;
+    if ((threadIdx.x & (kWave - 1)) == 0) lds[w] = m;
+    __syncthreads();
+    Moments t = lds[0];
+#pragma unroll
+    for (int i = 1; i < NW; ++i) t = chan(t, lds[i]);
+    __syncthreads();
+    return t;
+}
+
 }  // namespace kf

@@ -46,6 +46,19 @@ struct GroupNormArgs {
 size_t group_norm_workspace_bytes(int64_t n, int64_t c, int64_t spatial, int64_t groups, kf_dtype xt);
 kf_status group_norm_launch(const GroupNormArgs& a, hipStream_t s, const char** variant);
 
+// LayerNorm over the last d elements of a dense [rows, d] view.
+struct LayerNormArgs {
+    const void* x;
+    void* y;
+    kf_dtype xt;
+    int64_t rows, d;
+    const void* weight;
+    const void* bias;
+    kf_dtype at;
+    float eps;
+};
+kf_status layer_norm_launch(const LayerNormArgs& a, hipStream_t s, const char** variant);
+
 // adaptive_avg_pool2d over a dense [planes, h, w] view -> [planes, oh, ow].
 struct AvgPoolArgs {
     const void* x;

@@ -41,6 +41,9 @@ _SIGNATURES = {
                                      ctypes.c_double, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]),
     "kf_group_norm_workspace_bytes": (ctypes.c_int, [ctypes.c_int, ctypes.c_int32, _i64p, ctypes.c_int64,
                                                      ctypes.POINTER(ctypes.c_size_t)]),
+    "kf_layer_norm": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p, ctypes.c_int32, _i64p, _i64p,
+                                     _i64p, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int,
+                                     ctypes.c_double, ctypes.c_void_p]),
     "kf_adaptive_avgpool2d": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p, ctypes.c_int32, _i64p,
                                              _i64p, _i64p, ctypes.c_int64, ctypes.c_int64, ctypes.c_void_p]),
 }
@@ -178,6 +181,36 @@ def kf_group_norm(x: torch.Tensor, num_groups: int, weight: torch.Tensor | None 
     return y
 
 
+def _affine_dtype(x, weight, bias) -> int:
+    affine = weight if weight is not None else bias
+    if weight is not None and bias is not None and weight.dtype != bias.dtype:
+        raise KfError(3, "weight and bias must share a dtype")
+    return _dtype(affine) if affine is not None else _dtype(x)
+
+
+def kf_layer_norm(x: torch.Tensor, normalized_shape, weight: torch.Tensor | None = None,
+                  bias: torch.Tensor | None = None, eps: float = 1e-5, out: torch.Tensor | None = None) -> torch.Tensor:
+    """layer_norm(x, normalized_shape, weight, bias, eps) through kf_layer_norm."""
+    _need_cuda(x, weight, bias)
+    nshape = (normalized_shape,) if isinstance(normalized_shape, int) else tuple(normalized_shape)
+    if tuple(x.shape[x.dim() - len(nshape):]) != nshape:
+        raise KfError(2, f"normalized_shape {nshape} does not match the trailing sizes of {tuple(x.shape)}")
+    for p in (weight, bias):
+        if p is not None and (tuple(p.shape) != nshape or not p.is_contiguous()):
+            raise KfError(5, "weight and bias must be contiguous with the normalised shape")
+    y = out if out is not None else torch.empty_like(x, memory_format=torch.contiguous_format)
+    shape, _s = _arr(list(x.shape))
+    xs, _a = _arr(list(x.stride()))
+    ys, _b = _arr(list(y.stride()))
+    with torch.cuda.device(x.device):
+        _check(lib().kf_layer_norm(
+            ctypes.c_void_p(x.data_ptr()), _dtype(x), ctypes.c_void_p(y.data_ptr()), x.dim(), shape, xs, ys,
+            len(nshape), ctypes.c_void_p(weight.data_ptr() if weight is not None else None),
+            ctypes.c_void_p(bias.data_ptr() if bias is not None else None), _affine_dtype(x, weight, bias),
+            float(eps), _stream(x)))
+    return y
+
+
 def kf_adaptive_avgpool2d(x: torch.Tensor, output_size, out: torch.Tensor | None = None) -> torch.Tensor:
     """adaptive_avg_pool2d(x, output_size) through kf_adaptive_avgpool2d."""
     _need_cuda(x)
@@ -194,6 +227,7 @@ def kf_adaptive_avgpool2d(x: torch.Tensor, output_size, out: torch.Tensor | None
 
 softmax = kf_softmax
 softmax_causal = kf_softmax_causal
+layer_norm = kf_layer_norm
 group_norm = kf_group_norm
 adaptive_avg_pool2d = kf_adaptive_avgpool2d
 
@@ -247,6 +281,19 @@ def prepare_group_norm(x: torch.Tensor, y: torch.Tensor, num_groups: int, weight
             ctypes.c_void_p(bias.data_ptr() if bias is not None else None), at, float(eps),
             ctypes.c_void_p(ws.data_ptr()), ws.numel(), _stream(x))
     return Prepared(lib().kf_group_norm, args, (x, y, weight, bias, ws, a0, a1, a2))
+
+
+def prepare_layer_norm(x: torch.Tensor, y: torch.Tensor, normalized_ndim: int, weight=None, bias=None,
+                       eps: float = 1e-5) -> Prepared:
+    _need_cuda(x, y, weight, bias)
+    shape, a0 = _arr(list(x.shape))
+    xs, a1 = _arr(list(x.stride()))
+    ys, a2 = _arr(list(y.stride()))
+    args = (ctypes.c_void_p(x.data_ptr()), _dtype(x), ctypes.c_void_p(y.data_ptr()), x.dim(), shape, xs, ys,
+            normalized_ndim, ctypes.c_void_p(weight.data_ptr() if weight is not None else None),
+            ctypes.c_void_p(bias.data_ptr() if bias is not None else None), _affine_dtype(x, weight, bias),
+            float(eps), _stream(x))
+    return Prepared(lib().kf_layer_norm, args, (x, y, weight, bias, a0, a1, a2))
 
 
 def prepare_adaptive_avgpool2d(x: torch.Tensor, y: torch.Tensor) -> Prepared:

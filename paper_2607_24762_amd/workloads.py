@@ -89,6 +89,16 @@ def attn_scores_raw_bf16(seed: int = 4, heads: int = 8, seq: int = 4096) -> dict
     return {"op": "softmax_causal", "x": s, "scale": 1.0 / 16.0, "out_dtype": "bf16"}
 
 
+def layernorm_sd35_bf16(seed: int = 7, tokens: int = 4096, hidden: int = 1536) -> dict:
+    """SD3.5 Medium transformer LayerNorm: bf16 [2, tokens, hidden] (the two
+    classifier-free-guidance branches of a 1024x1024 image: 4096 patch
+    tokens of width 1536), x ~ N(0, 1), no affine (the adaptive-norm blocks
+    apply their own modulation), eps 1e-6."""
+    rng = np.random.default_rng(seed)
+    x = cast(rng.standard_normal((2, tokens, hidden)), "bf16")
+    return {"op": "layer_norm", "x": x, "normalized_shape": (hidden,), "weight": None, "bias": None, "eps": 1e-6}
+
+
 def router_softmax_f32(seed: int = 5, experts: int = 256, tokens: int = 16384) -> dict:
     """MoE router logits: fp32 [tokens, experts], z ~ N(0, 1) plus +4 on an
     i.i.d. 5% of entries (u ~ U[0, 1) drawn after z, outlier where u < 0.05)."""

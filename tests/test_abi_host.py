@@ -112,6 +112,24 @@ def test_softmax_causal_rejections(lib):
     assert causal(lib, shape=(2, 0, 8)) == OK and lib.kf_last_variant().decode() == "noop"
 
 
+def ln(lib, shape=(4, 64), nd=1, w=None, b=None, at=F32, eps=1e-5, x=FAKE, y=FAKE + (1 << 30), xt=F32, xs=None):
+    return lib.kf_layer_norm(ctypes.c_void_p(x), xt, ctypes.c_void_p(y), len(shape), arr(shape),
+                             arr(xs) if xs else None, None, nd, ctypes.c_void_p(w), ctypes.c_void_p(b), at, eps, None)
+
+
+def test_layer_norm_rejections(lib):
+    assert ln(lib, nd=0) == ARG
+    assert ln(lib, nd=3) == ARG
+    assert ln(lib, eps=-1.0) == ARG
+    assert ln(lib, xt=BF16, w=FAKE + (3 << 30), at=F16) == DTYPE
+    assert ln(lib, x=0) == NULLP
+    assert ln(lib, xs=(1, 4)) == LAYOUT
+    assert ln(lib, y=FAKE + 8) == ARG
+    assert ln(lib, w=FAKE + (1 << 30) + 4) == ARG          # weight inside y
+    assert ln(lib, w=FAKE + (3 << 30) + 2) == ARG          # fp32 weight not 4-byte aligned
+    assert ln(lib, shape=(0, 64)) == OK and lib.kf_last_variant().decode() == "noop"
+
+
 def gn(lib, shape=(2, 8, 4, 4), groups=4, w=None, b=None, at=F32, eps=1e-5, ws=FAKE + (2 << 30), wsb=1 << 20,
        xt=F32, x=FAKE, y=FAKE + (1 << 30), xs=None):
     return lib.kf_group_norm(ctypes.c_void_p(x), xt, ctypes.c_void_p(y), len(shape), arr(shape),
