@@ -1,0 +1,120 @@
+"""Guarded dispatch on the GPU: with the PyTorch entry points routed through
+a dispatcher, a small network (GroupNorm -> avgpool head, LayerNorm ->
+attention softmax) gives the eager outputs within the dispatch tolerance,
+every variant gets an audit label, the VAE-sized GroupNorm variant is
+measured faster and routed to libkf355, an unsupported layout stays on eager
+with its reason, autograd inputs bypass the dispatcher, and a saved package
+is reused without re-measuring."""
+import os
+
+import pytest
+import torch
+import torch.nn.functional as F
+
+from paper_2607_24762_amd import dispatch, kf355
+from paper_2607_24762_amd.workloads import randn
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU visible")
+    kf355.lib()
+
+
+def net(x, t, gw, gb):
+    """Each routed op reads an input that no other routed op produced, except
+    the pool, which reads the GroupNorm output: a one-ulp bf16 difference
+    upstream would otherwise be amplified past the fp32 tolerance."""
+    h = F.group_norm(x, 8, gw, gb, 1e-6)
+    pooled = F.adaptive_avg_pool2d(h, 1)
+    u = F.layer_norm(t, (t.shape[-1],), None, None, 1e-6)
+    tf = t.float()
+    s = torch.matmul(tf, tf.transpose(-1, -2).contiguous()) / 8.0
+    p = torch.softmax(s, dim=-1)
+    q = s.softmax(-1)
+    r = F.softmax(s.bfloat16(), dim=-1, dtype=torch.float32)
+    return h, pooled, u, p, q, r
+
+
+def inputs():
+    dev = "cuda"
+    x = randn((2, 64, 16, 16), "bf16", seed=11).to(dev)
+    t = randn((2, 48, 64), "bf16", seed=12).to(dev)
+    gw = randn((64,), "f32", seed=13, mean=1.0, std=0.1).to(dev)
+    gb = randn((64,), "f32", seed=14, std=0.1).to(dev)
+    return x, t, gw.bfloat16(), gb.bfloat16()
+
+
+def check_close(a, b):
+    ok, diff = dispatch.agree(a, b)
+    assert ok, (a.dtype, tuple(a.shape), diff)
+
+
+@pytest.mark.parametrize("measure", [False, True])
+def test_network_matches_eager_and_labels_every_variant(measure):
+    args = inputs()
+    ref = net(*args)
+    with dispatch.installed(dispatch.GuardedDispatcher(measure=measure)) as d:
+        first = net(*args)
+        second = net(*args)       # decided variants take their recorded path
+    for a, b, c in zip(first, second, ref):
+        check_close(a, c)
+        check_close(b, c)
+    ops = sorted(r["op"] for r in d.report())
+    assert ops == ["adaptive_avg_pool2d", "group_norm", "layer_norm", "softmax", "softmax"], ops
+    for r in d.report():
+        assert r["backend"] in ("kf355", "eager") and r["label"].startswith(r["backend"])
+        assert not r["reason"].startswith(("invalid", "unsupported")), r
+        if not measure:
+            assert r["backend"] == "kf355" and r["kernel"], r
+
+
+def test_vae_group_norm_is_routed_to_kf355():
+    x = randn((1, 512, 128, 128), "bf16", seed=3).cuda()
+    with dispatch.installed() as d:
+        y = F.group_norm(x, 32, None, None, 1e-6)
+    (r,) = d.report()
+    assert r["backend"] == "kf355" and r["kf_us"] < r["eager_us"], r
+    check_close(y, F.group_norm(x, 32, None, None, 1e-6))
+
+
+def test_unsupported_layout_stays_on_eager():
+    s = randn((64, 256), "f32", seed=5).cuda()
+    view = s[:, ::2]                                  # not dense: the library refuses it
+    with dispatch.installed() as d:
+        y = torch.softmax(view, -1)
+    (r,) = d.report()
+    assert r["backend"] == "eager" and r["reason"].startswith("unsupported"), r
+    assert torch.equal(y, torch.softmax(view, -1))
+
+
+def test_autograd_inputs_bypass_the_dispatcher():
+    s = randn((8, 32), "f32", seed=6).cuda().requires_grad_()
+    with dispatch.installed() as d:
+        y = torch.softmax(s, -1)
+        y.sum().backward()
+        with torch.no_grad():
+            torch.softmax(s, -1)
+    assert s.grad is not None
+    assert [r["op"] for r in d.report()] == ["softmax"]   # only the no-grad call was dispatched
+
+
+def test_saved_package_is_reused_without_measuring(tmp_path):
+    args = inputs()
+    with dispatch.installed() as d:
+        net(*args)
+    path = os.path.join(tmp_path, "kf355_dispatch.json")
+    d.save(path)
+
+    def no_timing(fn, reps):
+        raise AssertionError("a packaged variant was measured again")
+    e = dispatch.GuardedDispatcher(timer=no_timing)
+    e.load(path)
+    with dispatch.installed(e):
+        out = net(*args)
+    assert e.report() == d.report()
+    for a, b in zip(out, net(*args)):
+        check_close(a, b)
