@@ -98,6 +98,40 @@ kf_status kf_softmax(const void* x, kf_dtype x_dtype, void* y, kf_dtype y_dtype,
                      void* stream);
 
 /*
+ * kf_softmax_split -- kf_softmax (same arguments, semantics, dtype pairs and
+ * results to within rounding) for inputs of few long rows, such as the
+ * attention scores of one decode step [batch, heads, 1, kv] in eager
+ * attention (the paper's LLM workloads decode greedily with a KV cache,
+ * Section IV-B): when the rows alone would leave most of the GPU idle, each
+ * row is split over several workgroups that exchange their partial
+ * (max, sum of exponentials) states through `workspace` and merge them in a
+ * fixed order, so results are deterministic.  Views it does not split (rows
+ * many or short, dim not last, x == y, x or y off a 16-byte boundary) run as
+ * kf_softmax does.
+ *
+ *  workspace, workspace_bytes
+ *              device memory of at least kf_softmax_split_workspace_bytes()
+ *              bytes, 256-byte aligned, owned by the caller, ZERO-FILLED before
+ *              its first use; every call returns it to all-zero, so it can be
+ *              reused by later calls in stream order.  Calls that may run
+ *              concurrently need separate workspaces.  May be NULL when the
+ *              required size is 0.  Too small: KF_ERR_WORKSPACE.  The last 256
+ *              bytes of the required size start with a 32-bit word the kernel
+ *              sets to 1 when a workgroup gave up waiting for the rest of its
+ *              row and recomputed the row's state itself (results are the same
+ *              either way; informational).
+ */
+kf_status kf_softmax_split(const void* x, kf_dtype x_dtype, void* y, kf_dtype y_dtype, int32_t ndim,
+                           const int64_t* shape, const int64_t* x_strides, const int64_t* y_strides, int64_t dim,
+                           void* workspace, size_t workspace_bytes, void* stream);
+
+/* Workspace bytes kf_softmax_split needs for this input dtype, shape and dim
+ * (written to *bytes; 0 when such a view is never split).  Does not depend on
+ * the output dtype. */
+kf_status kf_softmax_split_workspace_bytes(kf_dtype x_dtype, int32_t ndim, const int64_t* shape, int64_t dim,
+                                           size_t* bytes);
+
+/*
  * kf_softmax_causal -- the attention-score softmax of eager attention fused
  * into one pass: y = softmax(scale * x + M, -1) over the last axis of x
  * viewed as [..., q, k], where M is the causal mask aligned to the end of

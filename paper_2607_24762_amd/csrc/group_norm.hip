@@ -25,18 +25,17 @@
 // compute bit-identical results.
 #include <math.h>
 
-#include <atomic>
 #include <cstdlib>
 #include <cstring>
 
 #include "kf_device.hpp"
+#include "kf_exchange.hpp"
 #include "kf_internal.h"
 
 namespace kf {
 namespace {
 
 constexpr int kNT = 256;          // threads per workgroup
-constexpr size_t kCounterStride = 256;  // bytes between two groups' counters
 constexpr int kFloatsPerThread = 64;
 
 struct GNParams {
@@ -44,21 +43,13 @@ struct GNParams {
     void* y;
     const void* w;
     const void* b;
-    uint64_t* slot;        // [groups_total * parts] published partials, 0 = empty
-    unsigned* depart;      // one per group, kCounterStride bytes apart
-    unsigned* error;       // set to 1 when a wait gave up (results stay valid)
+    Exchange ex;           // one unit per (sample, group), ex.parts chunks each
     int64_t group_elems;   // (c/G) * spatial
     int64_t spatial;
     int32_t cpg;           // channels per group
     int32_t groups;        // G
-    int32_t parts;         // workgroups per group
     float eps;
-    uint32_t wait_ticks;   // give up waiting after this many 100 MHz ticks
 };
-
-__device__ __forceinline__ unsigned* counter(unsigned* base, int64_t ng) {
-    return reinterpret_cast<unsigned*>(reinterpret_cast<char*>(base) + ng * (int64_t)kCounterStride);
-}
 
 // Elements held by part p of a group.
 __device__ __forceinline__ float part_count(const GNParams& p, int64_t chunk, int part) {
@@ -179,52 +170,25 @@ __device__ __forceinline__ Moments decode(uint64_t w, float n) {
     return Moments{n, __uint_as_float((uint32_t)w), __uint_as_float((uint32_t)(w >> 32) & 0x7fffffffu)};
 }
 
-__device__ __forceinline__ void publish(const GNParams& p, int64_t ng, int part, Moments m) {
-    __hip_atomic_store(p.slot + ng * p.parts + part, encode(m), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-
-// Gather and merge the `parts` partials of one group; called by a whole wave,
+// Gather and merge the partials of one group; called by a whole wave,
 // result uniform across it.  Lane l takes parts l, l+64, ... in order and the
 // butterfly keeps lane order, so the combine order depends on part index
 // alone (bitwise-reproducible results).  With `wait`, each lane polls its
-// slots until they are published or until p.wait_ticks of the 100 MHz real
-// time clock have passed; *ok reports (uniformly) whether every slot arrived.
+// slots until they are published or the exchange's wait bound has passed;
+// *ok reports (uniformly) whether every slot arrived.
 __device__ __forceinline__ Moments gather_parts(const GNParams& p, int64_t ng, int64_t chunk, bool wait,
                                                 bool* ok) {
     Moments acc{0.f, 0.f, 0.f};
     const int lane = threadIdx.x & (kWave - 1);
-    uint64_t* slots = p.slot + ng * p.parts;
     const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
     bool all = true;
-    for (int q = lane; q < p.parts; q += kWave) {
-        uint64_t w = __hip_atomic_load(slots + q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        if (wait) {
-            while (w == 0) {
-                if (__builtin_amdgcn_s_memrealtime() - t0 > p.wait_ticks) break;
-                __builtin_amdgcn_s_sleep(1);
-                w = __hip_atomic_load(slots + q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            }
-        }
+    for (int q = lane; q < p.ex.parts; q += kWave) {
+        const uint64_t w = ex_poll(p.ex, ng, q, t0, wait);
         all = all && (w != 0);
         acc = chan(acc, decode(w, part_count(p, chunk, q)));
     }
     *ok = __all(all);
     return moments_wave(acc);
-}
-
-// Called by lane 0 of wave 0 of every workgroup once it has gathered its
-// group's partials: the last workgroup of the group to arrive here empties the
-// group's slots and its counter, so every call leaves them zero.  Every
-// workgroup counted has finished reading the slots (its reads returned before
-// the merge that precedes this), so none can see the cleared values.
-__device__ __forceinline__ void release_group(const GNParams& p, int64_t ng) {
-    const unsigned left =
-        __hip_atomic_fetch_add(counter(p.depart, ng), 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    if (left == (unsigned)p.parts - 1) {
-        uint64_t* slots = p.slot + ng * p.parts;
-        for (int q = 0; q < p.parts; ++q) __hip_atomic_store(slots + q, (uint64_t)0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        __hip_atomic_store(counter(p.depart, ng), 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    }
 }
 
 template <class T, class A, bool VECTOR>
@@ -233,8 +197,8 @@ __global__ __launch_bounds__(kNT) void gn_fused(GNParams p) {
     __shared__ Moments lds[kNT / kWave];
     __shared__ float stats[2];
     __shared__ int gathered;
-    const int64_t ng = blockIdx.x / p.parts;
-    const int part = blockIdx.x - (int)(ng * p.parts);
+    const int64_t ng = blockIdx.x / p.ex.parts;
+    const int part = blockIdx.x - (int)(ng * p.ex.parts);
     const int g = (int)(ng % p.groups);
     const int64_t gbase = ng * p.group_elems;
 
@@ -245,8 +209,8 @@ __global__ __launch_bounds__(kNT) void gn_fused(GNParams p) {
 
     if (threadIdx.x < kWave) {
         bool ok = true;
-        if (p.parts > 1) {
-            if (threadIdx.x == 0) publish(p, ng, part, m);
+        if (p.ex.parts > 1) {
+            if (threadIdx.x == 0) ex_publish(p.ex, ng, part, encode(m));
             m = gather_parts(p, ng, C::CH, true, &ok);
         }
         if (threadIdx.x == 0) {
@@ -267,7 +231,7 @@ __global__ __launch_bounds__(kNT) void gn_fused(GNParams p) {
         // place could not be re-read.)
         Moments acc{0.f, 0.f, 0.f};
         const int lane = threadIdx.x & (kWave - 1);
-        for (int q = 0; q < p.parts; ++q) {
+        for (int q = 0; q < p.ex.parts; ++q) {
             c.load(p, gbase, q);
             const Moments mq = moments_block<kNT / kWave>(c.moments(p, q), lds);
             if ((q & (kWave - 1)) == lane) acc = chan(acc, mq);
@@ -277,7 +241,7 @@ __global__ __launch_bounds__(kNT) void gn_fused(GNParams p) {
             if (threadIdx.x == 0) {
                 stats[0] = acc.mean;
                 stats[1] = 1.f / sqrtf(acc.m2 / (float)p.group_elems + p.eps);
-                __hip_atomic_store(p.error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                ex_flag_timeout(p.ex);
             }
         }
         c.load(p, gbase, part);
@@ -285,27 +249,27 @@ __global__ __launch_bounds__(kNT) void gn_fused(GNParams p) {
     }
     c.normalise_store(p, gbase, part, stats[0], stats[1]);
     // Off the critical path: this workgroup is done reading its group's slots.
-    if (p.parts > 1 && threadIdx.x == 0) release_group(p, ng);
+    if (p.ex.parts > 1 && threadIdx.x == 0) ex_release(p.ex, ng);
 }
 
 template <class T, bool VECTOR>
 __global__ __launch_bounds__(kNT) void gn_stats(GNParams p) {
     using C = Chunk<T, VECTOR>;
     __shared__ Moments lds[kNT / kWave];
-    const int64_t ng = blockIdx.x / p.parts;
-    const int part = blockIdx.x - (int)(ng * p.parts);
+    const int64_t ng = blockIdx.x / p.ex.parts;
+    const int part = blockIdx.x - (int)(ng * p.ex.parts);
     C c;
     c.load(p, ng * p.group_elems, part);
     Moments m = moments_block<kNT / kWave>(c.moments(p, part), lds);
-    if (threadIdx.x == 0) publish(p, ng, part, m);
+    if (threadIdx.x == 0) ex_publish(p.ex, ng, part, encode(m));
 }
 
 template <class T, class A, bool VECTOR>
 __global__ __launch_bounds__(kNT) void gn_apply(GNParams p) {
     using C = Chunk<T, VECTOR>;
     __shared__ float stats[2];
-    const int64_t ng = blockIdx.x / p.parts;
-    const int part = blockIdx.x - (int)(ng * p.parts);
+    const int64_t ng = blockIdx.x / p.ex.parts;
+    const int part = blockIdx.x - (int)(ng * p.ex.parts);
     const int g = (int)(ng % p.groups);
     const int64_t gbase = ng * p.group_elems;
     // Chunk and affine loads first, so they are in flight while wave 0
@@ -316,7 +280,7 @@ __global__ __launch_bounds__(kNT) void gn_apply(GNParams p) {
     if (threadIdx.x < kWave) {
         bool ok;
         Moments m = gather_parts(p, ng, C::CH, false, &ok);
-        if (threadIdx.x == 0) release_group(p, ng);
+        if (threadIdx.x == 0) ex_release(p.ex, ng);
         if (threadIdx.x == 0) {
             stats[0] = m.mean;
             stats[1] = 1.f / sqrtf(m.m2 / (float)p.group_elems + p.eps);
@@ -342,7 +306,7 @@ bool vector_ok(const GroupNormArgs& a) {
 
 struct Layout {
     int64_t groups_total, parts;
-    size_t slot_off, depart_off, error_off, total;
+    ExchangeLayout ex;
 };
 
 Layout layout(int64_t n, int64_t c, int64_t spatial, int64_t groups, kf_dtype xt, bool vector) {
@@ -351,45 +315,8 @@ Layout layout(int64_t n, int64_t c, int64_t spatial, int64_t groups, kf_dtype xt
     const int64_t ge = (c / groups) * spatial;
     l.parts = (ge + chunk_elems(xt, vector) - 1) / chunk_elems(xt, vector);
     if (l.parts < 1) l.parts = 1;
-    auto up = [](size_t v) { return (v + 255) & ~(size_t)255; };
-    // Partial slots, then one 256-byte line per group for its counter (so
-    // different groups never share a line), then the 256-byte error block.
-    l.slot_off = 0;
-    l.depart_off = up((size_t)(l.groups_total * l.parts) * sizeof(uint64_t));
-    l.error_off = l.depart_off + (size_t)l.groups_total * kCounterStride;
-    l.total = l.error_off + 256;
+    l.ex = exchange_layout(l.groups_total, l.parts);
     return l;
-}
-
-// Per-device properties, queried once per device and cached (value + 1 in
-// an atomic, 0 meaning not yet known).
-constexpr int kMaxDevices = 64;
-
-int cached_attr(std::atomic<int>* cache, int dev, hipDeviceAttribute_t attr) {
-    if (dev < 0 || dev >= kMaxDevices) return 0;
-    int v = cache[dev].load(std::memory_order_relaxed);
-    if (v == 0) {
-        int got = 0;
-        if (hipDeviceGetAttribute(&got, attr, dev) != hipSuccess) got = 0;
-        v = got + 1;
-        cache[dev].store(v, std::memory_order_relaxed);
-    }
-    return v - 1;
-}
-
-// How many workgroups of `kernel` can be resident on device `dev` at once
-// (0 if unknown), cached per kernel instantiation through `cache`.
-int resident_capacity(std::atomic<int>* cache, int dev, const void* kernel) {
-    static std::atomic<int> cus_cache[kMaxDevices];
-    if (dev < 0 || dev >= kMaxDevices) return 0;
-    int v = cache[dev].load(std::memory_order_relaxed);
-    if (v == 0) {
-        int per_cu = 0;
-        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, kNT, 0) != hipSuccess) per_cu = 0;
-        v = per_cu * cached_attr(cus_cache, dev, hipDeviceAttributeMultiprocessorCount) + 1;
-        cache[dev].store(v, std::memory_order_relaxed);
-    }
-    return v - 1;
 }
 
 // KF355_GN_MODE selects the multi-chunk path: unset or "auto" (fused when
@@ -412,37 +339,24 @@ int gn_mode() {
 // default; KF355_GN_WAIT_TICKS overrides it (tests set 0 to force the
 // recompute path).  Read once per process.
 uint32_t gn_wait_ticks() {
-    static const uint32_t ticks = [] {
-        const char* e = std::getenv("KF355_GN_WAIT_TICKS");
-        return e ? (uint32_t)std::strtoul(e, nullptr, 10) : 10000u;
-    }();
+    static const uint32_t ticks = env_u32("KF355_GN_WAIT_TICKS", 10000u);
     return ticks;
-}
-
-bool cooperative_ok(int dev) {
-    static std::atomic<int> coop_cache[kMaxDevices];
-    return cached_attr(coop_cache, dev, hipDeviceAttributeCooperativeLaunch) != 0;
 }
 
 template <class T, class A, bool VECTOR>
 kf_status run(const GroupNormArgs& a, hipStream_t s, const char** variant) {
     const Layout l = layout(a.n, a.c, a.spatial, a.groups, a.xt, VECTOR);
-    char* ws = static_cast<char*>(a.workspace);
     GNParams p;
     p.x = a.x;
     p.y = a.y;
     p.w = a.weight;
     p.b = a.bias;
-    p.slot = reinterpret_cast<uint64_t*>(ws + l.slot_off);
-    p.depart = reinterpret_cast<unsigned*>(ws + l.depart_off);
-    p.error = reinterpret_cast<unsigned*>(ws + l.error_off);
+    p.ex = exchange_view(a.workspace, l.ex, l.parts, gn_wait_ticks());
     p.group_elems = (a.c / a.groups) * a.spatial;
     p.spatial = a.spatial;
     p.cpg = (int32_t)(a.c / a.groups);
     p.groups = (int32_t)a.groups;
-    p.parts = (int32_t)l.parts;
     p.eps = a.eps;
-    p.wait_ticks = gn_wait_ticks();
 
     const int64_t grid = l.groups_total * l.parts;
     if (grid > INT32_MAX) {
@@ -462,15 +376,15 @@ kf_status run(const GroupNormArgs& a, hipStream_t s, const char** variant) {
     if (l.parts == 1 && mode != kModeTwoPass) {
         path = FUSED_SINGLE;
     } else if (mode != kModeTwoPass && a.x != a.y) {
-        static std::atomic<int> capacity_cache[kMaxDevices];
+        static ResidencyCache capacity_cache;
         int dev = -1;
         if (hipGetDevice(&dev) != hipSuccess) {
             set_error("group_norm: no current HIP device");
             return KF_ERR_HIP;
         }
         const void* kernel = reinterpret_cast<const void*>(gn_fused<T, A, VECTOR>);
-        if ((int64_t)resident_capacity(capacity_cache, dev, kernel) >= grid) {
-            if (mode == kModeCoop && cooperative_ok(dev)) path = FUSED_COOP;
+        if ((int64_t)resident_capacity(capacity_cache, dev, kernel, kNT) >= grid) {
+            if (mode == kModeCoop && device_cooperative(dev)) path = FUSED_COOP;
             else if (mode != kModeCoop) path = FUSED_PLAIN;
         }
     }
@@ -511,7 +425,7 @@ kf_status run_layout(const GroupNormArgs& a, hipStream_t s, const char** variant
 size_t group_norm_workspace_bytes(int64_t n, int64_t c, int64_t spatial, int64_t groups, kf_dtype xt) {
     // The scalar layout has the smaller chunk, hence more parts: size for it
     // so one workspace serves either path.
-    return layout(n, c, spatial, groups, xt, false).total;
+    return layout(n, c, spatial, groups, xt, false).ex.total;
 }
 
 kf_status group_norm_launch(const GroupNormArgs& a, hipStream_t s, const char** variant) {

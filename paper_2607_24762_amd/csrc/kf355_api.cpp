@@ -75,6 +75,54 @@ kf_status check_shape(int32_t ndim, const int64_t* shape, int32_t lo, int32_t hi
     return KF_OK;
 }
 
+// The dense [outer, len, inner] view of a softmax over `dim` (wrapped), and
+// the element count; validates the shape and dim only.
+kf_status softmax_view(int32_t ndim, const int64_t* shape, int64_t dim, SoftmaxArgs* a, int64_t* n) {
+    kf_status s = check_shape(ndim, shape, 0, KF_MAX_DIMS, n);
+    if (s != KF_OK) return s;
+    const int64_t rank = ndim > 0 ? ndim : 1;  // a 0-d tensor accepts dim 0 or -1
+    if (dim < -rank || dim >= rank)
+        return fail(KF_ERR_BAD_ARG, "dim %lld outside [%lld, %lld)", (long long)dim, (long long)-rank,
+                    (long long)rank);
+    if (dim < 0) dim += rank;
+    *a = SoftmaxArgs{nullptr, nullptr, KF_FLOAT32, KF_FLOAT32, 1, 1, 1};
+    if (ndim > 0) {
+        a->outer = count((int32_t)dim, shape);
+        a->len = shape[dim];
+        a->inner = count(ndim - (int32_t)dim - 1, shape + dim + 1);
+    }
+    return KF_OK;
+}
+
+// Every check kf_softmax makes before launching; on KF_OK with *n == 0 the
+// call is a no-op.
+kf_status check_softmax(const void* x, kf_dtype x_dtype, void* y, kf_dtype y_dtype, int32_t ndim,
+                        const int64_t* shape, const int64_t* x_strides, const int64_t* y_strides, int64_t dim,
+                        SoftmaxArgs* a, int64_t* n) {
+    kf_status s = check_shape(ndim, shape, 0, KF_MAX_DIMS, n);
+    if (s != KF_OK) return s;
+    if (!dtype_ok(x_dtype) || !dtype_ok(y_dtype))
+        return fail(KF_ERR_BAD_DTYPE, "dtype %d -> %d not supported", (int)x_dtype, (int)y_dtype);
+    const bool pair_ok = (x_dtype == y_dtype) || (y_dtype == KF_FLOAT32 && x_dtype != KF_FLOAT32);
+    if (!pair_ok) return fail(KF_ERR_BAD_DTYPE, "softmax cannot narrow %d to %d", (int)x_dtype, (int)y_dtype);
+    s = softmax_view(ndim, shape, dim, a, n);
+    if (s != KF_OK) return s;
+    a->x = x;
+    a->y = y;
+    a->xt = x_dtype;
+    a->yt = y_dtype;
+    if (*n == 0) return KF_OK;
+    if (!x || !y) return fail(KF_ERR_NULL_POINTER, "x or y is NULL");
+    if ((uintptr_t)x % elem_bytes(x_dtype) || (uintptr_t)y % elem_bytes(y_dtype))
+        return fail(KF_ERR_BAD_ARG, "x or y is not aligned to its element size");
+    if (!dense(ndim, shape, x_strides) || !dense(ndim, shape, y_strides))
+        return fail(KF_ERR_UNSUPPORTED_LAYOUT, "only dense row-major tensors are supported");
+    const int64_t xb = *n * elem_bytes(x_dtype), yb = *n * elem_bytes(y_dtype);
+    if (x != y && overlaps(x, xb, y, yb)) return fail(KF_ERR_BAD_ARG, "x and y partially overlap");
+    if (x == y && x_dtype != y_dtype) return fail(KF_ERR_BAD_ARG, "in-place softmax needs equal dtypes");
+    return KF_OK;
+}
+
 kf_status begin() {
     g_error[0] = 0;
     return KF_OK;
@@ -131,36 +179,51 @@ const char* kf_last_variant(void) { return g_variant; }
 kf_status kf_softmax(const void* x, kf_dtype x_dtype, void* y, kf_dtype y_dtype, int32_t ndim, const int64_t* shape,
                      const int64_t* x_strides, const int64_t* y_strides, int64_t dim, void* stream) {
     begin();
+    kf::SoftmaxArgs a;
     int64_t n = 0;
-    kf_status s = check_shape(ndim, shape, 0, KF_MAX_DIMS, &n);
+    kf_status s = kf::check_softmax(x, x_dtype, y, y_dtype, ndim, shape, x_strides, y_strides, dim, &a, &n);
     if (s != KF_OK) return s;
-    if (!dtype_ok(x_dtype) || !dtype_ok(y_dtype))
-        return fail(KF_ERR_BAD_DTYPE, "dtype %d -> %d not supported", (int)x_dtype, (int)y_dtype);
-    const bool pair_ok = (x_dtype == y_dtype) || (y_dtype == KF_FLOAT32 && x_dtype != KF_FLOAT32);
-    if (!pair_ok) return fail(KF_ERR_BAD_DTYPE, "softmax cannot narrow %d to %d", (int)x_dtype, (int)y_dtype);
-    const int64_t rank = ndim > 0 ? ndim : 1;  // a 0-d tensor accepts dim 0 or -1
-    if (dim < -rank || dim >= rank)
-        return fail(KF_ERR_BAD_ARG, "dim %lld outside [%lld, %lld)", (long long)dim, (long long)-rank,
-                    (long long)rank);
-    if (dim < 0) dim += rank;
     if (n == 0) return done(KF_OK, "noop");
-    if (!x || !y) return fail(KF_ERR_NULL_POINTER, "x or y is NULL");
-    if ((uintptr_t)x % elem_bytes(x_dtype) || (uintptr_t)y % elem_bytes(y_dtype))
-        return fail(KF_ERR_BAD_ARG, "x or y is not aligned to its element size");
-    if (!dense(ndim, shape, x_strides) || !dense(ndim, shape, y_strides))
-        return fail(KF_ERR_UNSUPPORTED_LAYOUT, "only dense row-major tensors are supported");
-    const int64_t xb = n * elem_bytes(x_dtype), yb = n * elem_bytes(y_dtype);
-    if (x != y && overlaps(x, xb, y, yb)) return fail(KF_ERR_BAD_ARG, "x and y partially overlap");
-    if (x == y && x_dtype != y_dtype) return fail(KF_ERR_BAD_ARG, "in-place softmax needs equal dtypes");
-
-    SoftmaxArgs a{x, y, x_dtype, y_dtype, 1, 1, 1};
-    if (ndim > 0) {
-        a.outer = count((int32_t)dim, shape);
-        a.len = shape[dim];
-        a.inner = count(ndim - (int32_t)dim - 1, shape + dim + 1);
-    }
     const char* variant = nullptr;
     s = softmax_launch(a, static_cast<hipStream_t>(stream), &variant);
+    return done(s, variant);
+}
+
+kf_status kf_softmax_split_workspace_bytes(kf_dtype x_dtype, int32_t ndim, const int64_t* shape, int64_t dim,
+                                           size_t* bytes) {
+    begin();
+    if (!bytes) return fail(KF_ERR_NULL_POINTER, "bytes is NULL");
+    if (!dtype_ok(x_dtype)) return fail(KF_ERR_BAD_DTYPE, "x dtype %d not supported", (int)x_dtype);
+    kf::SoftmaxArgs a;
+    int64_t n = 0;
+    kf_status s = kf::softmax_view(ndim, shape, dim, &a, &n);
+    if (s != KF_OK) return s;
+    a.xt = a.yt = x_dtype;
+    *bytes = n == 0 ? 0 : softmax_split_workspace_bytes(a);
+    return KF_OK;
+}
+
+kf_status kf_softmax_split(const void* x, kf_dtype x_dtype, void* y, kf_dtype y_dtype, int32_t ndim,
+                           const int64_t* shape, const int64_t* x_strides, const int64_t* y_strides, int64_t dim,
+                           void* workspace, size_t workspace_bytes, void* stream) {
+    begin();
+    kf::SoftmaxArgs a;
+    int64_t n = 0;
+    kf_status s = kf::check_softmax(x, x_dtype, y, y_dtype, ndim, shape, x_strides, y_strides, dim, &a, &n);
+    if (s != KF_OK) return s;
+    if (n == 0) return done(KF_OK, "noop");
+    const size_t need = softmax_split_workspace_bytes(a);
+    if (need > 0) {
+        if (!workspace || workspace_bytes < need)
+            return fail(KF_ERR_WORKSPACE, "workspace of %zu bytes given, %zu needed",
+                        workspace ? workspace_bytes : 0, need);
+        if ((uintptr_t)workspace % 256) return fail(KF_ERR_WORKSPACE, "workspace is not 256-byte aligned");
+        if (overlaps(workspace, (int64_t)need, x, n * elem_bytes(x_dtype)) ||
+            overlaps(workspace, (int64_t)need, y, n * elem_bytes(y_dtype)))
+            return fail(KF_ERR_BAD_ARG, "workspace overlaps x or y");
+    }
+    const char* variant = nullptr;
+    s = softmax_split_launch(a, need > 0 ? workspace : nullptr, static_cast<hipStream_t>(stream), &variant);
     return done(s, variant);
 }
 

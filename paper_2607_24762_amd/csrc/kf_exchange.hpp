@@ -1,0 +1,107 @@
+// kf_exchange.hpp -- cross-workgroup exchange of one 64-bit partial result
+// per workgroup, for kernels that split one reduction unit (a GroupNorm
+// group, a long softmax row) over `parts` workgroups.  Every workgroup of a
+// unit publishes its partial, gathers all `parts` partials of the unit, and
+// merges them in part order, so the merged value does not depend on arrival
+// order and every workgroup of the unit computes it bit for bit the same.
+//
+// Protocol.  A published word is never 0 (the value of an empty slot): the
+// caller's encoding sets a flag bit.  Writing data and flag in one
+// single-copy-atomic 64-bit store means a reader that sees a non-zero word
+// sees the data, so no fences and no cache write-back / invalidation are
+// needed; polls are relaxed agent-scope loads.  The last workgroup of a unit
+// to depart (a per-unit counter) clears the unit's slots and the counter, so
+// every launch leaves the workspace as it found it: all zero.  Waits are
+// bounded by the 100 MHz real-time clock; a workgroup that gives up must
+// recompute the missing partials itself (the kernels do, bit-identically)
+// and records that in the error word, which is informational only.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace kf {
+
+constexpr size_t kCounterStride = 256;  // bytes between two units' counters
+
+struct Exchange {
+    uint64_t* slot;       // [units * parts] published partials, 0 = empty
+    unsigned* depart;     // one counter per unit, kCounterStride bytes apart
+    unsigned* error;      // set to 1 when a wait gave up
+    int32_t parts;        // workgroups per unit
+    uint32_t wait_ticks;  // give up waiting after this many 100 MHz ticks
+};
+
+__device__ __forceinline__ unsigned* ex_counter(const Exchange& ex, int64_t unit) {
+    return reinterpret_cast<unsigned*>(reinterpret_cast<char*>(ex.depart) + unit * (int64_t)kCounterStride);
+}
+
+__device__ __forceinline__ void ex_publish(const Exchange& ex, int64_t unit, int part, uint64_t word) {
+    __hip_atomic_store(ex.slot + unit * ex.parts + part, word, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Slot q of `unit`; with `wait`, polls until it is published or until
+// wait_ticks have passed since t0 (a value of s_memrealtime), in which case
+// it returns 0.
+__device__ __forceinline__ uint64_t ex_poll(const Exchange& ex, int64_t unit, int q, uint64_t t0, bool wait) {
+    uint64_t* at = ex.slot + unit * ex.parts + q;
+    uint64_t w = __hip_atomic_load(at, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (wait) {
+        while (w == 0) {
+            if (__builtin_amdgcn_s_memrealtime() - t0 > ex.wait_ticks) break;
+            __builtin_amdgcn_s_sleep(1);
+            w = __hip_atomic_load(at, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+    }
+    return w;
+}
+
+// Called by one thread of every workgroup of `unit` once the workgroup has
+// read all the unit's slots (its loads returned before the merge that
+// precedes this): the last one to arrive empties the slots and the counter.
+__device__ __forceinline__ void ex_release(const Exchange& ex, int64_t unit) {
+    unsigned* c = ex_counter(ex, unit);
+    const unsigned left = __hip_atomic_fetch_add(c, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (left == (unsigned)ex.parts - 1) {
+        uint64_t* slots = ex.slot + unit * ex.parts;
+        for (int q = 0; q < ex.parts; ++q)
+            __hip_atomic_store(slots + q, (uint64_t)0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(c, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+}
+
+__device__ __forceinline__ void ex_flag_timeout(const Exchange& ex) {
+    __hip_atomic_store(ex.error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// ---------------------------------------------------------------------------
+// Host side: workspace layout.  Slots first, then one 256-byte line per unit
+// for its counter (so different units never share a line), then a 256-byte
+// error block whose first word is the give-up flag.
+struct ExchangeLayout {
+    size_t slot_off, depart_off, error_off, total;
+};
+
+inline ExchangeLayout exchange_layout(int64_t units, int64_t parts) {
+    auto up = [](size_t v) { return (v + 255) & ~(size_t)255; };
+    ExchangeLayout l;
+    l.slot_off = 0;
+    l.depart_off = up((size_t)(units * parts) * sizeof(uint64_t));
+    l.error_off = l.depart_off + (size_t)units * kCounterStride;
+    l.total = l.error_off + 256;
+    return l;
+}
+
+inline Exchange exchange_view(void* workspace, const ExchangeLayout& l, int64_t parts, uint32_t wait_ticks) {
+    char* ws = static_cast<char*>(workspace);
+    Exchange ex;
+    ex.slot = reinterpret_cast<uint64_t*>(ws + l.slot_off);
+    ex.depart = reinterpret_cast<unsigned*>(ws + l.depart_off);
+    ex.error = reinterpret_cast<unsigned*>(ws + l.error_off);
+    ex.parts = (int32_t)parts;
+    ex.wait_ticks = wait_ticks;
+    return ex;
+}
+
+}  // namespace kf

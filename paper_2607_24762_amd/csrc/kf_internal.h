@@ -7,6 +7,8 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include <atomic>
+
 #include "kf355.h"
 
 namespace kf {
@@ -19,6 +21,12 @@ struct SoftmaxArgs {
     int64_t outer, len, inner;
 };
 kf_status softmax_launch(const SoftmaxArgs& a, hipStream_t s, const char** variant);
+// Rows split over several workgroups when few long rows would leave most of
+// the chip idle: workspace bytes the split needs (0 when this view is not
+// split, whatever the pointers), and the launch, which falls back to
+// softmax_launch when it does not split (workspace may then be NULL).
+size_t softmax_split_workspace_bytes(const SoftmaxArgs& a);
+kf_status softmax_split_launch(const SoftmaxArgs& a, void* workspace, hipStream_t s, const char** variant);
 
 // Scaled causal softmax over the last axis of a dense [batch, q, k] view.
 struct CausalSoftmaxArgs {
@@ -70,5 +78,18 @@ kf_status avgpool_launch(const AvgPoolArgs& a, hipStream_t s, const char** varia
 
 // Records the detail text of the current failure (thread-local).
 void set_error(const char* fmt, ...);
+
+// Device properties, cached per device (runtime.cpp).
+int device_multiprocessors(int dev);
+bool device_cooperative(int dev);
+// How many workgroups of `threads` threads of `kernel` can be resident on
+// device `dev` at once (0 if unknown); one cache object per kernel.
+struct ResidencyCache {
+    static constexpr int kDevices = 64;
+    std::atomic<int> v[kDevices];
+};
+int resident_capacity(ResidencyCache& cache, int dev, const void* kernel, int threads);
+// Unsigned value of environment variable `name`, or `dflt` when unset.
+uint32_t env_u32(const char* name, uint32_t dflt);
 
 }  // namespace kf

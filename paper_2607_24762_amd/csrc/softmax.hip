@@ -16,6 +16,7 @@
 #include <math.h>
 
 #include "kf_device.hpp"
+#include "kf_exchange.hpp"
 #include "kf_internal.h"
 
 namespace kf {
@@ -402,6 +403,189 @@ __global__ __launch_bounds__(256) void sm_cols(const void* __restrict__ x, void*
 }
 
 // --------------------------------------------------------------------------
+// Rows split over several workgroups (few long rows, such as decode-step
+// attention scores [batch, heads, 1, kv]: one workgroup per row would leave
+// most of the chip idle).  Part p of a row covers CH = 256 * NV * VEC flat
+// elements starting at the 16-byte boundary at or below the row's start plus
+// p * CH, so every load is an aligned 16-byte vector whatever the row length;
+// elements outside the row are masked to -inf.  Each workgroup keeps its part
+// in registers, reduces it to an online-normaliser state (m, s), exchanges
+// that state with the other parts of its row (one 64-bit word each, see
+// kf_exchange.hpp), merges all parts in part order and writes e^(x - M) / S
+// straight from registers: one HBM read and one write, like sm_block.
+constexpr int kSplitNT = 256;
+
+struct SplitParams {
+    const void* x;
+    void* y;
+    Exchange ex;    // one unit per row, ex.parts workgroups each
+    int64_t len;    // row length
+    int64_t total;  // elements in the tensor (rows * len)
+};
+
+// (m, s) as one never-zero word: m bits low, s bits high with the sign bit
+// forced on (s is a sum of exponentials: never negative).
+__device__ __forceinline__ uint64_t ms_encode(MS a) {
+    return (uint64_t)__float_as_uint(a.m) | ((uint64_t)(__float_as_uint(a.s) | 0x80000000u) << 32);
+}
+__device__ __forceinline__ MS ms_decode(uint64_t w) {
+    return MS{__uint_as_float((uint32_t)w), __uint_as_float((uint32_t)(w >> 32) & 0x7fffffffu)};
+}
+
+template <class TI, int NV>
+struct SplitPart {
+    static constexpr int VEC = TI::vec;
+    static constexpr int NW = kSplitNT / kWave;
+    static constexpr int64_t CH = (int64_t)kSplitNT * NV * VEC;
+    float v[NV][VEC];
+
+    // Flat index of the first element of slot k of this thread in part
+    // `part` of the row starting at r0.  Each wave owns NV*64 consecutive
+    // vectors of the part (the contiguous per-wave stream of sm_block).
+    __device__ __forceinline__ static int64_t at(int64_t r0, int part, int k) {
+        const int seg = (threadIdx.x / kWave) * NV * kWave + (threadIdx.x & (kWave - 1));
+        return (r0 / VEC) * VEC + (int64_t)part * CH + (int64_t)(seg + k * kWave) * VEC;
+    }
+
+    // Loads the part and masks elements outside [r0, r0 + len) to -inf.  All
+    // vector loads are issued unconditionally, from a clamped address when a
+    // vector misses the row or crosses the tensor's end (the row's first
+    // aligned vector, inside the tensor since len >= VEC); the rare edge
+    // vectors are fixed up after every load is in flight.
+    __device__ __forceinline__ void load(const SplitParams& p, int64_t r0, int part) {
+        const int64_t r1 = r0 + p.len;
+        const int64_t safe = (r0 / VEC) * VEC;
+        bool edge = false;
+#pragma unroll
+        for (int k = 0; k < NV; ++k) {
+            const int64_t e = at(r0, part, k);
+            const bool use = e < r1 && e + VEC > r0 && e + VEC <= p.total;
+            load_vec<TI>(p.x, use ? e : safe, v[k]);
+            edge = edge || e < r0 || e + VEC > r1;
+        }
+        if (__any(edge)) {
+#pragma unroll
+            for (int k = 0; k < NV; ++k) {
+                const int64_t e = at(r0, part, k);
+                if (e < r1 && e + VEC > p.total) {  // the tensor's last, partial vector
+#pragma unroll
+                    for (int i = 0; i < VEC; ++i)
+                        if (e + i < r1) v[k][i] = load1<TI>(p.x, e + i);
+                }
+#pragma unroll
+                for (int i = 0; i < VEC; ++i) v[k][i] = (e + i >= r0 && e + i < r1) ? v[k][i] : -INFINITY;
+            }
+        }
+    }
+
+    // The part's (m, s); s accumulates exp_out<TO>, so it carries the same
+    // 2^SHIFT factor as the write.  A part of only -inf (or none of the row)
+    // gives (-inf, 0), which weighs nothing in the merge.  Block-uniform.
+    template <class TO>
+    __device__ __forceinline__ MS stats(float* red) const {
+        float m = -INFINITY;
+#pragma unroll
+        for (int k = 0; k < NV; ++k)
+#pragma unroll
+            for (int i = 0; i < VEC; ++i) m = fmaxf(m, v[k][i]);
+        m = block_reduce<NW>(m, OpMax{}, red);
+        float s = 0.f;
+        if (m != -INFINITY) {
+#pragma unroll
+            for (int k = 0; k < NV; ++k)
+#pragma unroll
+                for (int i = 0; i < VEC; ++i) s += exp_out<TO>(v[k][i], m);
+        }
+        s = block_reduce<NW>(s, OpSum{}, red);
+        return MS{m, s};
+    }
+
+    template <class TO>
+    __device__ __forceinline__ void store(const SplitParams& p, int64_t r0, int part, float mm, float inv) const {
+        const int64_t r1 = r0 + p.len;
+#pragma unroll
+        for (int k = 0; k < NV; ++k) {
+            const int64_t e = at(r0, part, k);
+            float out[VEC];
+#pragma unroll
+            for (int i = 0; i < VEC; ++i) out[i] = exp_out<TO>(v[k][i], mm) * inv;
+            if (e >= r0 && e + VEC <= r1) {
+                store_span<TO, VEC>(p.y, e, out);
+            } else {
+#pragma unroll
+                for (int i = 0; i < VEC; ++i)
+                    if (e + i >= r0 && e + i < r1) store1<TO>(p.y, e + i, out[i]);
+            }
+        }
+    }
+};
+
+template <class TI, class TO, int NV>
+__global__ __launch_bounds__(kSplitNT) void sm_split(SplitParams p) {
+    using P = SplitPart<TI, NV>;
+    __shared__ float red[P::NW];
+    __shared__ float stat[2];
+    __shared__ int gathered;
+    const int64_t row = blockIdx.x / p.ex.parts;
+    const int part = (int)(blockIdx.x - row * p.ex.parts);
+    const int64_t r0 = row * p.len;
+    const int lane = threadIdx.x & (kWave - 1);
+
+    P c;
+    c.load(p, r0, part);
+    const MS own = c.template stats<TO>(red);
+    if (threadIdx.x < kWave) {
+        if (threadIdx.x == 0) ex_publish(p.ex, row, part, ms_encode(own));
+        // Lane l merges parts l, l+64, ... in order, then the wave merges
+        // across lanes (ms_merge is exactly commutative, so every lane and
+        // every workgroup of the row ends with the same bits).
+        const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
+        MS acc{-INFINITY, 0.f};
+        bool all = true;
+        for (int q = lane; q < p.ex.parts; q += kWave) {
+            const uint64_t w = ex_poll(p.ex, row, q, t0, true);
+            all = all && (w != 0);
+            acc = ms_merge(acc, ms_decode(w));
+        }
+        acc = ms_wave(acc);
+        const bool ok = __all(all);
+        if (threadIdx.x == 0) {
+            gathered = ok;
+            stat[0] = acc.m;
+            stat[1] = 1.f / acc.s;
+        }
+    }
+    __syncthreads();
+    if (!gathered) {
+        // Some part of the row was not published in time (its workgroup is
+        // not resident yet).  Recompute every part's state here with the
+        // loads, thread mapping and arithmetic its owner uses and merge in
+        // the same order: the result is bit-identical, so the kernel never
+        // depends on co-residency.  (In-place calls are not split.)
+        MS acc{-INFINITY, 0.f};
+        for (int q = 0; q < p.ex.parts; ++q) {
+            c.load(p, r0, q);
+            const MS mq = c.template stats<TO>(red);
+            if ((q & (kWave - 1)) == lane) acc = ms_merge(acc, mq);
+        }
+        if (threadIdx.x < kWave) {
+            acc = ms_wave(acc);
+            if (threadIdx.x == 0) {
+                stat[0] = acc.m;
+                stat[1] = 1.f / acc.s;
+                ex_flag_timeout(p.ex);
+            }
+        }
+        c.load(p, r0, part);
+        __syncthreads();
+    }
+    // A row of only -inf has M = -inf, so x - M is NaN: a NaN row, as the
+    // definition gives.
+    c.template store<TO>(p, r0, part, stat[0], stat[1]);
+    if (threadIdx.x == 0) ex_release(p.ex, row);  // done reading the row's slots
+}
+
+// --------------------------------------------------------------------------
 // Variant selection.
 template <class TI, class TO, int LPR, int NV, bool VECTOR>
 void go_wave(const SoftmaxArgs& a, hipStream_t s) {
@@ -564,6 +748,88 @@ kf_status run_causal(const CausalSoftmaxArgs& a, hipStream_t s, const char** var
     return KF_OK;
 }
 
+
+// --------------------------------------------------------------------------
+// Split-row plan.  A row is split when the rows alone would occupy fewer
+// than kSplitMaxRows workgroups and it is long enough for at least two
+// parts.  NV is the smallest slot count that keeps rows * parts within
+// kSplitMaxGroups (so the whole grid is resident on the 256 CUs and the
+// exchange completes), giving parts of 2048 (fp32: 1024) elements upwards.
+constexpr int64_t kSplitMaxRows = 128;
+constexpr int64_t kSplitMaxGroups = 1024;
+
+struct SplitPlan {
+    int nv;         // 0: not split
+    int64_t parts;
+};
+
+SplitPlan split_plan(const SoftmaxArgs& a) {
+    SplitPlan none{0, 1};
+    if (a.inner != 1 || a.outer >= kSplitMaxRows || a.outer < 1) return none;
+    const int vec = (a.xt == KF_FLOAT32) ? 4 : 8;
+    // Parts tile the row from the aligned boundary below its start: a row
+    // not starting on one spans up to vec - 1 more elements.
+    const int64_t span = a.len + ((a.len % vec) ? vec - 1 : 0);
+    for (int nv = 1; nv <= 8; nv *= 2) {
+        const int64_t ch = (int64_t)kSplitNT * nv * vec;
+        const int64_t parts = (span + ch - 1) / ch;
+        if (parts < 2) return none;
+        if (a.outer * parts <= kSplitMaxGroups) return SplitPlan{nv, parts};
+    }
+    return none;
+}
+
+uint32_t sm_wait_ticks() {
+    static const uint32_t ticks = env_u32("KF355_SM_WAIT_TICKS", 10000u);
+    return ticks;
+}
+
+template <class TI, class TO, int NV>
+bool launch_split(const SoftmaxArgs& a, const SplitPlan& plan, void* workspace, hipStream_t s,
+                  const char** variant) {
+    const void* kernel = reinterpret_cast<const void*>(sm_split<TI, TO, NV>);
+    static ResidencyCache capacity;
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess) return false;
+    const int64_t grid = a.outer * plan.parts;
+    if ((int64_t)resident_capacity(capacity, dev, kernel, kSplitNT) < grid) return false;
+    SplitParams p;
+    p.x = a.x;
+    p.y = a.y;
+    p.ex = exchange_view(workspace, exchange_layout(a.outer, plan.parts), plan.parts, sm_wait_ticks());
+    p.len = a.len;
+    p.total = a.outer * a.len;
+    hipLaunchKernelGGL((sm_split<TI, TO, NV>), dim3((unsigned)grid), dim3(kSplitNT), 0, s, p);
+    static const char* names[] = {"sm_split_nv1", "sm_split_nv2", "sm_split_nv4", "sm_split_nv8"};
+    *variant = names[NV == 1 ? 0 : NV == 2 ? 1 : NV == 4 ? 2 : 3];
+    return true;
+}
+
+template <class TI, class TO>
+kf_status run_split(const SoftmaxArgs& a, void* workspace, hipStream_t s, const char** variant) {
+    const SplitPlan plan = split_plan(a);
+    // In-place rows are not split (the recompute fallback re-reads x), nor
+    // are buffers off a 16-byte boundary (the parts' vectors would not be).
+    const bool ok = plan.nv != 0 && workspace && a.x != a.y && (uintptr_t)a.x % 16 == 0 &&
+                    (uintptr_t)a.y % 16 == 0;
+    bool launched = false;
+    if (ok) {
+        switch (plan.nv) {
+            case 1: launched = launch_split<TI, TO, 1>(a, plan, workspace, s, variant); break;
+            case 2: launched = launch_split<TI, TO, 2>(a, plan, workspace, s, variant); break;
+            case 4: launched = launch_split<TI, TO, 4>(a, plan, workspace, s, variant); break;
+            default: launched = launch_split<TI, TO, 8>(a, plan, workspace, s, variant); break;
+        }
+    }
+    if (!launched) return run<TI, TO>(a, s, variant);
+    const hipError_t err = hipGetLastError();
+    if (err != hipSuccess) {
+        set_error("softmax split launch failed: %s", hipGetErrorString(err));
+        return KF_ERR_HIP;
+    }
+    return KF_OK;
+}
+
 }  // namespace
 
 kf_status softmax_launch(const SoftmaxArgs& a, hipStream_t s, const char** variant) {
@@ -586,6 +852,23 @@ kf_status softmax_causal_launch(const CausalSoftmaxArgs& a, hipStream_t s, const
     if (a.xt == KF_FLOAT16 && a.yt == KF_FLOAT16) return run_causal<F16, F16>(a, s, variant);
     if (a.xt == KF_FLOAT16 && a.yt == KF_FLOAT32) return run_causal<F16, F32>(a, s, variant);
     set_error("softmax_causal: unsupported dtype pair");
+    return KF_ERR_BAD_DTYPE;
+}
+}  // namespace kf
+
+namespace kf {
+size_t softmax_split_workspace_bytes(const SoftmaxArgs& a) {
+    const SplitPlan plan = split_plan(a);
+    return plan.nv == 0 ? 0 : exchange_layout(a.outer, plan.parts).total;
+}
+
+kf_status softmax_split_launch(const SoftmaxArgs& a, void* workspace, hipStream_t s, const char** variant) {
+    if (a.xt == KF_FLOAT32 && a.yt == KF_FLOAT32) return run_split<F32, F32>(a, workspace, s, variant);
+    if (a.xt == KF_BFLOAT16 && a.yt == KF_BFLOAT16) return run_split<BF16, BF16>(a, workspace, s, variant);
+    if (a.xt == KF_BFLOAT16 && a.yt == KF_FLOAT32) return run_split<BF16, F32>(a, workspace, s, variant);
+    if (a.xt == KF_FLOAT16 && a.yt == KF_FLOAT16) return run_split<F16, F16>(a, workspace, s, variant);
+    if (a.xt == KF_FLOAT16 && a.yt == KF_FLOAT32) return run_split<F16, F32>(a, workspace, s, variant);
+    set_error("softmax: unsupported dtype pair");
     return KF_ERR_BAD_DTYPE;
 }
 }  // namespace kf

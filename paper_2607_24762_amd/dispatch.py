@@ -199,7 +199,7 @@ def _softmax(x, dim=None, dtype=None, orig=None):
         return orig(x, dim, dtype=dtype) if dtype is not None else orig(x, dim)
     out_dtype = dtype or x.dtype
     return _ACTIVE.call("softmax", (x, dim, out_dtype),
-                        lambda: kf355.kf_softmax(x, dim, out_dtype=out_dtype),
+                        lambda: kf355.kf_softmax_split(x, dim, out_dtype=out_dtype),
                         lambda: orig(x, dim, dtype=dtype) if dtype is not None else orig(x, dim))
 
 

@@ -34,6 +34,11 @@ _SIGNATURES = {
     "kf_last_variant": (ctypes.c_char_p, []),
     "kf_softmax": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p, ctypes.c_int, ctypes.c_int32,
                                   _i64p, _i64p, _i64p, ctypes.c_int64, ctypes.c_void_p]),
+    "kf_softmax_split": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p, ctypes.c_int,
+                                        ctypes.c_int32, _i64p, _i64p, _i64p, ctypes.c_int64, ctypes.c_void_p,
+                                        ctypes.c_size_t, ctypes.c_void_p]),
+    "kf_softmax_split_workspace_bytes": (ctypes.c_int, [ctypes.c_int, ctypes.c_int32, _i64p, ctypes.c_int64,
+                                                        ctypes.POINTER(ctypes.c_size_t)]),
     "kf_softmax_causal": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p, ctypes.c_int,
                                          ctypes.c_int32, _i64p, _i64p, _i64p, ctypes.c_double, ctypes.c_void_p]),
     "kf_group_norm": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p, ctypes.c_int32, _i64p, _i64p,
@@ -140,19 +145,50 @@ def kf_softmax_causal(x: torch.Tensor, scale: float = 1.0, out_dtype: torch.dtyp
 _ws_cache: dict = {}
 
 
+def _workspace(x: torch.Tensor, nbytes: int) -> torch.Tensor:
+    """A zero-filled workspace of at least `nbytes`, cached per (device,
+    stream) and grown on demand.  kf_group_norm and kf_softmax_split return
+    the workspace to all-zero after each call, so one cached buffer serves
+    every later call on that stream, of either operator, in stream order."""
+    key = (x.device, torch.cuda.current_stream(x.device).cuda_stream)
+    ws = _ws_cache.get(key)
+    if ws is None or ws.numel() < nbytes:
+        ws = torch.zeros(max(nbytes, 256), dtype=torch.uint8, device=x.device)
+        _ws_cache[key] = ws
+    return ws
+
+
 def group_norm_workspace(x: torch.Tensor, num_groups: int) -> torch.Tensor:
-    """A zero-filled workspace for this shape, cached per (device, stream) and
-    grown on demand; kf_group_norm returns its counters to zero after each
-    call, so the cached buffer stays valid for the next call on that stream."""
+    """The cached zero-filled workspace, large enough for kf_group_norm on x."""
     shape, _s = _arr(list(x.shape))
     nbytes = ctypes.c_size_t(0)
     _check(lib().kf_group_norm_workspace_bytes(_dtype(x), x.dim(), shape, num_groups, ctypes.byref(nbytes)))
-    key = (x.device, torch.cuda.current_stream(x.device).cuda_stream)
-    ws = _ws_cache.get(key)
-    if ws is None or ws.numel() < nbytes.value:
-        ws = torch.zeros(max(nbytes.value, 256), dtype=torch.uint8, device=x.device)
-        _ws_cache[key] = ws
-    return ws
+    return _workspace(x, nbytes.value)
+
+
+def softmax_split_workspace(x: torch.Tensor, dim: int = -1) -> torch.Tensor:
+    """The cached zero-filled workspace, large enough for kf_softmax_split on x."""
+    shape, _s = _arr(list(x.shape))
+    nbytes = ctypes.c_size_t(0)
+    _check(lib().kf_softmax_split_workspace_bytes(_dtype(x), x.dim(), shape, dim, ctypes.byref(nbytes)))
+    return _workspace(x, nbytes.value)
+
+
+def kf_softmax_split(x: torch.Tensor, dim: int = -1, out_dtype: torch.dtype | None = None,
+                     out: torch.Tensor | None = None, workspace: torch.Tensor | None = None) -> torch.Tensor:
+    """softmax(x, dim) through kf_softmax_split: rows split over several
+    workgroups when there are few long ones (decode-step attention scores)."""
+    _need_cuda(x)
+    y = out if out is not None else torch.empty(x.shape, dtype=out_dtype or x.dtype, device=x.device)
+    ws = workspace if workspace is not None else softmax_split_workspace(x, dim)
+    shape, _s = _arr(list(x.shape))
+    xs, _a = _arr(list(x.stride()))
+    ys, _b = _arr(list(y.stride()))
+    with torch.cuda.device(x.device):
+        _check(lib().kf_softmax_split(ctypes.c_void_p(x.data_ptr()), _dtype(x), ctypes.c_void_p(y.data_ptr()),
+                                      _dtype(y), x.dim(), shape, xs, ys, dim, ctypes.c_void_p(ws.data_ptr()),
+                                      ws.numel(), _stream(x)))
+    return y
 
 
 def kf_group_norm(x: torch.Tensor, num_groups: int, weight: torch.Tensor | None = None,
@@ -255,6 +291,18 @@ def prepare_softmax(x: torch.Tensor, y: torch.Tensor, dim: int = -1) -> Prepared
     args = (ctypes.c_void_p(x.data_ptr()), _dtype(x), ctypes.c_void_p(y.data_ptr()), _dtype(y), x.dim(), shape, xs,
             ys, dim, _stream(x))
     return Prepared(lib().kf_softmax, args, (x, y, a0, a1, a2))
+
+
+def prepare_softmax_split(x: torch.Tensor, y: torch.Tensor, dim: int = -1,
+                          workspace: torch.Tensor | None = None) -> Prepared:
+    _need_cuda(x, y)
+    ws = workspace if workspace is not None else softmax_split_workspace(x, dim)
+    shape, a0 = _arr(list(x.shape))
+    xs, a1 = _arr(list(x.stride()))
+    ys, a2 = _arr(list(y.stride()))
+    args = (ctypes.c_void_p(x.data_ptr()), _dtype(x), ctypes.c_void_p(y.data_ptr()), _dtype(y), x.dim(), shape, xs,
+            ys, dim, ctypes.c_void_p(ws.data_ptr()), ws.numel(), _stream(x))
+    return Prepared(lib().kf_softmax_split, args, (x, y, ws, a0, a1, a2))
 
 
 def prepare_softmax_causal(x: torch.Tensor, y: torch.Tensor, scale: float = 1.0) -> Prepared:

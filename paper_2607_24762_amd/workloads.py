@@ -89,6 +89,19 @@ def attn_scores_raw_bf16(seed: int = 4, heads: int = 8, seq: int = 4096) -> dict
     return {"op": "softmax_causal", "x": s, "scale": 1.0 / 16.0, "out_dtype": "bf16"}
 
 
+def attn_decode_bf16(seed: int = 8, batch: int = 1, heads: int = 8, kv: int = 32768,
+                     out_dtype: str = "f32") -> dict:
+    """One greedy decode step of eager attention with a KV cache: the single
+    new query of each head against kv cached keys, bf16 scores
+    [batch, heads, 1, kv] = (3 z) / 16 as in the prefill workload (no mask:
+    the newest query sees every cached key), softmax over the key axis with
+    fp32 output (the dtype=float32 softmax eager attention calls before
+    casting back to bf16)."""
+    rng = np.random.default_rng(seed)
+    s = cast((3.0 * rng.standard_normal((batch, heads, 1, kv))) / 16.0, "bf16")
+    return {"op": "softmax_split", "x": s, "dim": -1, "out_dtype": out_dtype}
+
+
 def layernorm_sd35_bf16(seed: int = 7, tokens: int = 4096, hidden: int = 1536) -> dict:
     """SD3.5 Medium transformer LayerNorm: bf16 [2, tokens, hidden] (the two
     classifier-free-guidance branches of a 1024x1024 image: 4096 patch

@@ -96,6 +96,51 @@ def test_softmax_size_one_dims_may_have_any_stride(lib):
     assert softmax(lib, shape=(1, 0), xs=(12345, 1)) == OK
 
 
+def split(lib, shape=(1, 8, 1, 32768), xt=BF16, yt=F32, x=FAKE, y=FAKE + (1 << 30), ws=FAKE + (2 << 30),
+          wsb=1 << 20, dim=-1, xs=None):
+    return lib.kf_softmax_split(ctypes.c_void_p(x), xt, ctypes.c_void_p(y), yt, len(shape), arr(shape),
+                                arr(xs) if xs else None, None, dim, ctypes.c_void_p(ws), wsb, None)
+
+
+def split_ws(lib, shape, xt=BF16, dim=-1):
+    n = ctypes.c_size_t(0)
+    st = lib.kf_softmax_split_workspace_bytes(xt, len(shape), arr(shape), dim, ctypes.byref(n))
+    return st, n.value
+
+
+def test_softmax_split_rejections(lib):
+    # The argument checks are kf_softmax's ...
+    assert split(lib, xt=F32, yt=BF16) == DTYPE
+    assert split(lib, dim=4) == ARG
+    assert split(lib, x=0) == NULLP
+    assert split(lib, xs=(262144, 32768, 32768, 2)) == LAYOUT
+    assert split(lib, y=FAKE + 64) == ARG
+    # ... plus the workspace, on a view that is split.
+    assert split(lib, ws=0) == WS
+    assert split(lib, wsb=64) == WS and "needed" in err(lib)
+    assert split(lib, ws=FAKE + (2 << 30) + 128) == WS     # not 256-byte aligned
+    assert split(lib, ws=FAKE + 256) == ARG                # overlaps x
+    assert split(lib, shape=(1, 8, 1, 0), ws=0, wsb=0) == OK
+    assert lib.kf_last_variant().decode() == "noop"
+
+
+def test_softmax_split_workspace_query(lib):
+    # 8 rows of 32768 bf16: 16 parts of 2048 elements per row; 8-byte (m, s)
+    # partials, one 256-byte counter line per row, the 256-byte error block.
+    assert split_ws(lib, (1, 8, 1, 32768)) == (OK, 8 * 16 * 8 + 8 * 256 + 256)
+    # A row that does not start on a 16-byte boundary spans one more vector:
+    # 4097 bf16 elements take 3 parts; 9 partials round up to one 256-byte line.
+    assert split_ws(lib, (3, 4097)) == (OK, 256 + 3 * 256 + 256)
+    assert split_ws(lib, (4096, 4096)) == (OK, 0)          # many rows: not split
+    assert split_ws(lib, (4, 2048)) == (OK, 0)             # one part per row: not split
+    assert split_ws(lib, (4, 1000), xt=F32) == (OK, 0)
+    assert split_ws(lib, (1, 32768, 8), dim=1) == (OK, 0)  # not the last dim
+    assert split_ws(lib, (0, 32768)) == (OK, 0)
+    assert split_ws(lib, (4, 8), dim=2)[0] == ARG
+    assert split_ws(lib, (4, 8), xt=9)[0] == DTYPE
+    assert lib.kf_softmax_split_workspace_bytes(BF16, 2, arr((2, 4)), -1, None) == NULLP
+
+
 def causal(lib, shape=(2, 4, 8), scale=0.5, x=FAKE, y=FAKE + (1 << 30), xt=F32, yt=F32, xs=None):
     return lib.kf_softmax_causal(ctypes.c_void_p(x), xt, ctypes.c_void_p(y), yt, len(shape), arr(shape),
                                  arr(xs) if xs else None, None, scale, None)

@@ -143,10 +143,11 @@ def test_wait_timeout_recompute_is_bitwise_identical(tmp_path):
     w = W.groupnorm_vae_bf16()
     y = kf355.kf_group_norm(w["x"].cuda(), 32, w["weight"].cuda(), w["bias"].cuda(), w["eps"])
     torch.cuda.synchronize()
-    child = os.path.join(os.path.dirname(os.path.abspath(__file__)), "gn_child.py")
+    child = os.path.join(os.path.dirname(os.path.abspath(__file__)), "exchange_child.py")
     out = str(tmp_path / "child.npz")
     env = dict(os.environ, KF355_GN_WAIT_TICKS="0")
-    r = subprocess.run([sys.executable, "-u", child, out], env=env, timeout=300, capture_output=True, text=True)
+    r = subprocess.run([sys.executable, "-u", child, "group_norm", out], env=env, timeout=300,
+                       capture_output=True, text=True)
     print(r.stdout, r.stderr[-2000:])
     assert r.returncode == 0
     got = np.load(out)
