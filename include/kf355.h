@@ -125,11 +125,10 @@ kf_status kf_softmax_split(const void* x, kf_dtype x_dtype, void* y, kf_dtype y_
                            const int64_t* shape, const int64_t* x_strides, const int64_t* y_strides, int64_t dim,
                            void* workspace, size_t workspace_bytes, void* stream);
 
-/* Workspace bytes kf_softmax_split needs for this input dtype, shape and dim
- * (written to *bytes; 0 when such a view is never split).  Does not depend on
- * the output dtype. */
-kf_status kf_softmax_split_workspace_bytes(kf_dtype x_dtype, int32_t ndim, const int64_t* shape, int64_t dim,
-                                           size_t* bytes);
+/* Workspace bytes kf_softmax_split needs for these dtypes, shape and dim
+ * (written to *bytes; 0 when such a view is never split). */
+kf_status kf_softmax_split_workspace_bytes(kf_dtype x_dtype, kf_dtype y_dtype, int32_t ndim, const int64_t* shape,
+                                           int64_t dim, size_t* bytes);
 
 /*
  * kf_softmax_causal -- the attention-score softmax of eager attention fused

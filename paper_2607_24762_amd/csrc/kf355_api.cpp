@@ -189,16 +189,18 @@ kf_status kf_softmax(const void* x, kf_dtype x_dtype, void* y, kf_dtype y_dtype,
     return done(s, variant);
 }
 
-kf_status kf_softmax_split_workspace_bytes(kf_dtype x_dtype, int32_t ndim, const int64_t* shape, int64_t dim,
-                                           size_t* bytes) {
+kf_status kf_softmax_split_workspace_bytes(kf_dtype x_dtype, kf_dtype y_dtype, int32_t ndim, const int64_t* shape,
+                                           int64_t dim, size_t* bytes) {
     begin();
     if (!bytes) return fail(KF_ERR_NULL_POINTER, "bytes is NULL");
-    if (!dtype_ok(x_dtype)) return fail(KF_ERR_BAD_DTYPE, "x dtype %d not supported", (int)x_dtype);
+    if (!dtype_ok(x_dtype) || !dtype_ok(y_dtype))
+        return fail(KF_ERR_BAD_DTYPE, "dtype %d -> %d not supported", (int)x_dtype, (int)y_dtype);
     kf::SoftmaxArgs a;
     int64_t n = 0;
     kf_status s = kf::softmax_view(ndim, shape, dim, &a, &n);
     if (s != KF_OK) return s;
-    a.xt = a.yt = x_dtype;
+    a.xt = x_dtype;
+    a.yt = y_dtype;
     *bytes = n == 0 ? 0 : softmax_split_workspace_bytes(a);
     return KF_OK;
 }

@@ -750,13 +750,22 @@ kf_status run_causal(const CausalSoftmaxArgs& a, hipStream_t s, const char** var
 
 
 // --------------------------------------------------------------------------
-// Split-row plan.  A row is split when the rows alone would occupy fewer
-// than kSplitMaxRows workgroups and it is long enough for at least two
-// parts.  NV is the smallest slot count that keeps rows * parts within
-// kSplitMaxGroups (so the whole grid is resident on the 256 CUs and the
-// exchange completes), giving parts of 2048 (fp32: 1024) elements upwards.
+// Split-row plan, from kernel-trace sweeps on MI355X (rows x lengths of
+// bf16 scores with fp32 / bf16 output, cold HBM).  The exchange costs about
+// 2.5 us over a workgroup-per-row launch, so a row is split only when
+//   * the workgroup-per-row path would stream it twice (rows beyond the
+//     register-resident kernels: more than 65536 elements, or 16384 when the
+//     row is not whole 16-byte vectors), where splitting measured 2-7x
+//     faster, or
+//   * it moves at least 160 KiB (input plus output), from where splitting
+//     measured 1.1-1.6x faster up to 64 rows;
+// and only while the rows alone occupy fewer than kSplitMaxRows workgroups.
+// Parts of 16 KiB of input (NV = 4) measured best (up to 1.5x faster than
+// 4 KiB parts at 8-16 rows of 131072); NV = 8 halves the grid when rows x
+// parts would exceed kSplitMaxGroups.
 constexpr int64_t kSplitMaxRows = 128;
 constexpr int64_t kSplitMaxGroups = 1024;
+constexpr int64_t kSplitMinRowBytes = 160 << 10;
 
 struct SplitPlan {
     int nv;         // 0: not split
@@ -766,13 +775,16 @@ struct SplitPlan {
 SplitPlan split_plan(const SoftmaxArgs& a) {
     SplitPlan none{0, 1};
     if (a.inner != 1 || a.outer >= kSplitMaxRows || a.outer < 1) return none;
-    const int vec = (a.xt == KF_FLOAT32) ? 4 : 8;
+    const int xvec = (a.xt == KF_FLOAT32) ? 4 : 8, yvec = (a.yt == KF_FLOAT32) ? 4 : 8;
+    const int64_t row_bytes = a.len * (int64_t)((a.xt == KF_FLOAT32 ? 4 : 2) + (a.yt == KF_FLOAT32 ? 4 : 2));
+    const bool whole_vectors = a.len % xvec == 0 && a.len % yvec == 0;
+    const bool plain_streams = a.len > (whole_vectors ? 65536 : 16384);
+    if (!plain_streams && row_bytes < kSplitMinRowBytes) return none;
     // Parts tile the row from the aligned boundary below its start: a row
-    // not starting on one spans up to vec - 1 more elements.
-    const int64_t span = a.len + ((a.len % vec) ? vec - 1 : 0);
-    for (int nv = 1; nv <= 8; nv *= 2) {
-        const int64_t ch = (int64_t)kSplitNT * nv * vec;
-        const int64_t parts = (span + ch - 1) / ch;
+    // not starting on one spans up to xvec - 1 more elements.
+    const int64_t span = a.len + ((a.len % xvec) ? xvec - 1 : 0);
+    for (int nv = 4; nv <= 8; nv *= 2) {
+        const int64_t parts = (span + (int64_t)kSplitNT * nv * xvec - 1) / ((int64_t)kSplitNT * nv * xvec);
         if (parts < 2) return none;
         if (a.outer * parts <= kSplitMaxGroups) return SplitPlan{nv, parts};
     }
@@ -800,8 +812,7 @@ bool launch_split(const SoftmaxArgs& a, const SplitPlan& plan, void* workspace, 
     p.len = a.len;
     p.total = a.outer * a.len;
     hipLaunchKernelGGL((sm_split<TI, TO, NV>), dim3((unsigned)grid), dim3(kSplitNT), 0, s, p);
-    static const char* names[] = {"sm_split_nv1", "sm_split_nv2", "sm_split_nv4", "sm_split_nv8"};
-    *variant = names[NV == 1 ? 0 : NV == 2 ? 1 : NV == 4 ? 2 : 3];
+    *variant = NV == 4 ? "sm_split_nv4" : "sm_split_nv8";
     return true;
 }
 
@@ -814,12 +825,8 @@ kf_status run_split(const SoftmaxArgs& a, void* workspace, hipStream_t s, const 
                     (uintptr_t)a.y % 16 == 0;
     bool launched = false;
     if (ok) {
-        switch (plan.nv) {
-            case 1: launched = launch_split<TI, TO, 1>(a, plan, workspace, s, variant); break;
-            case 2: launched = launch_split<TI, TO, 2>(a, plan, workspace, s, variant); break;
-            case 4: launched = launch_split<TI, TO, 4>(a, plan, workspace, s, variant); break;
-            default: launched = launch_split<TI, TO, 8>(a, plan, workspace, s, variant); break;
-        }
+        launched = plan.nv == 4 ? launch_split<TI, TO, 4>(a, plan, workspace, s, variant)
+                                : launch_split<TI, TO, 8>(a, plan, workspace, s, variant);
     }
     if (!launched) return run<TI, TO>(a, s, variant);
     const hipError_t err = hipGetLastError();

@@ -37,8 +37,8 @@ _SIGNATURES = {
     "kf_softmax_split": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p, ctypes.c_int,
                                         ctypes.c_int32, _i64p, _i64p, _i64p, ctypes.c_int64, ctypes.c_void_p,
                                         ctypes.c_size_t, ctypes.c_void_p]),
-    "kf_softmax_split_workspace_bytes": (ctypes.c_int, [ctypes.c_int, ctypes.c_int32, _i64p, ctypes.c_int64,
-                                                        ctypes.POINTER(ctypes.c_size_t)]),
+    "kf_softmax_split_workspace_bytes": (ctypes.c_int, [ctypes.c_int, ctypes.c_int, ctypes.c_int32, _i64p,
+                                                        ctypes.c_int64, ctypes.POINTER(ctypes.c_size_t)]),
     "kf_softmax_causal": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p, ctypes.c_int,
                                          ctypes.c_int32, _i64p, _i64p, _i64p, ctypes.c_double, ctypes.c_void_p]),
     "kf_group_norm": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p, ctypes.c_int32, _i64p, _i64p,
@@ -166,11 +166,13 @@ def group_norm_workspace(x: torch.Tensor, num_groups: int) -> torch.Tensor:
     return _workspace(x, nbytes.value)
 
 
-def softmax_split_workspace(x: torch.Tensor, dim: int = -1) -> torch.Tensor:
-    """The cached zero-filled workspace, large enough for kf_softmax_split on x."""
+def softmax_split_workspace(x: torch.Tensor, dim: int = -1, out_dtype: torch.dtype | None = None) -> torch.Tensor:
+    """The cached zero-filled workspace, large enough for kf_softmax_split on
+    x with output dtype out_dtype (x's by default)."""
     shape, _s = _arr(list(x.shape))
     nbytes = ctypes.c_size_t(0)
-    _check(lib().kf_softmax_split_workspace_bytes(_dtype(x), x.dim(), shape, dim, ctypes.byref(nbytes)))
+    yt = DTYPES.get(out_dtype or x.dtype, -1)
+    _check(lib().kf_softmax_split_workspace_bytes(_dtype(x), yt, x.dim(), shape, dim, ctypes.byref(nbytes)))
     return _workspace(x, nbytes.value)
 
 
@@ -180,7 +182,7 @@ def kf_softmax_split(x: torch.Tensor, dim: int = -1, out_dtype: torch.dtype | No
     workgroups when there are few long ones (decode-step attention scores)."""
     _need_cuda(x)
     y = out if out is not None else torch.empty(x.shape, dtype=out_dtype or x.dtype, device=x.device)
-    ws = workspace if workspace is not None else softmax_split_workspace(x, dim)
+    ws = workspace if workspace is not None else softmax_split_workspace(x, dim, y.dtype)
     shape, _s = _arr(list(x.shape))
     xs, _a = _arr(list(x.stride()))
     ys, _b = _arr(list(y.stride()))
@@ -296,7 +298,7 @@ def prepare_softmax(x: torch.Tensor, y: torch.Tensor, dim: int = -1) -> Prepared
 def prepare_softmax_split(x: torch.Tensor, y: torch.Tensor, dim: int = -1,
                           workspace: torch.Tensor | None = None) -> Prepared:
     _need_cuda(x, y)
-    ws = workspace if workspace is not None else softmax_split_workspace(x, dim)
+    ws = workspace if workspace is not None else softmax_split_workspace(x, dim, y.dtype)
     shape, a0 = _arr(list(x.shape))
     xs, a1 = _arr(list(x.stride()))
     ys, a2 = _arr(list(y.stride()))

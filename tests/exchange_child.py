@@ -33,7 +33,7 @@ elif op == "softmax_split":
     x = w["x"].cuda()
     y = kf355.kf_softmax_split(x, -1, out_dtype=torch.float32, workspace=ws)
     shape = (ctypes.c_int64 * 4)(*x.shape)
-    kf355.lib().kf_softmax_split_workspace_bytes(1, 4, shape, -1, ctypes.byref(nb))
+    kf355.lib().kf_softmax_split_workspace_bytes(1, 0, 4, shape, -1, ctypes.byref(nb))
 else:
     raise SystemExit(f"unknown op {op}")
 torch.cuda.synchronize()

@@ -102,9 +102,9 @@ def split(lib, shape=(1, 8, 1, 32768), xt=BF16, yt=F32, x=FAKE, y=FAKE + (1 << 3
                                 arr(xs) if xs else None, None, dim, ctypes.c_void_p(ws), wsb, None)
 
 
-def split_ws(lib, shape, xt=BF16, dim=-1):
+def split_ws(lib, shape, xt=BF16, yt=F32, dim=-1):
     n = ctypes.c_size_t(0)
-    st = lib.kf_softmax_split_workspace_bytes(xt, len(shape), arr(shape), dim, ctypes.byref(n))
+    st = lib.kf_softmax_split_workspace_bytes(xt, yt, len(shape), arr(shape), dim, ctypes.byref(n))
     return st, n.value
 
 
@@ -125,20 +125,30 @@ def test_softmax_split_rejections(lib):
 
 
 def test_softmax_split_workspace_query(lib):
-    # 8 rows of 32768 bf16: 16 parts of 2048 elements per row; 8-byte (m, s)
-    # partials, one 256-byte counter line per row, the 256-byte error block.
-    assert split_ws(lib, (1, 8, 1, 32768)) == (OK, 8 * 16 * 8 + 8 * 256 + 256)
+    # 8 rows of 32768 bf16 -> fp32 (192 KiB of traffic each): 4 parts of 8192
+    # elements per row; 8-byte (m, s) partials padded to a 256-byte line, one
+    # 256-byte counter line per row, the 256-byte error block.
+    assert split_ws(lib, (1, 8, 1, 32768)) == (OK, 256 + 8 * 256 + 256)
+    # The same rows with bf16 output move 128 KiB each: not split.
+    assert split_ws(lib, (1, 8, 1, 32768), yt=BF16) == (OK, 0)
     # A row that does not start on a 16-byte boundary spans one more vector:
-    # 4097 bf16 elements take 3 parts; 9 partials round up to one 256-byte line.
-    assert split_ws(lib, (3, 4097)) == (OK, 256 + 3 * 256 + 256)
+    # 40001 elements take 5 parts.
+    assert split_ws(lib, (3, 40001)) == (OK, 256 + 3 * 256 + 256)
+    # Rows of partial vectors beyond 16384 elements are split at any size
+    # (the per-row path would stream them twice): 16385 -> 3 parts.
+    assert split_ws(lib, (2, 16385), yt=BF16) == (OK, 256 + 2 * 256 + 256)
+    assert split_ws(lib, (2, 16384), yt=BF16) == (OK, 0)
+    # 127 rows of 70000: 9 parts of 8192 would make 1143 workgroups, so
+    # parts of 16384 (5 per row).
+    assert split_ws(lib, (127, 70000)) == (OK, ((127 * 5 * 8 + 255) // 256) * 256 + 127 * 256 + 256)
     assert split_ws(lib, (4096, 4096)) == (OK, 0)          # many rows: not split
-    assert split_ws(lib, (4, 2048)) == (OK, 0)             # one part per row: not split
-    assert split_ws(lib, (4, 1000), xt=F32) == (OK, 0)
-    assert split_ws(lib, (1, 32768, 8), dim=1) == (OK, 0)  # not the last dim
+    assert split_ws(lib, (4, 1000), xt=F32, yt=F32) == (OK, 0)
+    assert split_ws(lib, (1, 32768 * 4, 8), dim=1) == (OK, 0)  # not the last dim
     assert split_ws(lib, (0, 32768)) == (OK, 0)
     assert split_ws(lib, (4, 8), dim=2)[0] == ARG
     assert split_ws(lib, (4, 8), xt=9)[0] == DTYPE
-    assert lib.kf_softmax_split_workspace_bytes(BF16, 2, arr((2, 4)), -1, None) == NULLP
+    assert split_ws(lib, (4, 8), yt=9)[0] == DTYPE
+    assert lib.kf_softmax_split_workspace_bytes(BF16, F32, 2, arr((2, 4)), -1, None) == NULLP
 
 
 def causal(lib, shape=(2, 4, 8), scale=0.5, x=FAKE, y=FAKE + (1 << 30), xt=F32, yt=F32, xs=None):
