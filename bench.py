@@ -110,6 +110,81 @@ def copy_calibration(torch, dev, nbytes: int, reps: int = 50) -> dict:
             "gbps": round(nbytes / (us * 1e-6) / 1e9, 1)}
 
 
+def time_launches(torch, fns, steps, warmup):
+    """Mean µs per call over `steps` back-to-back launches (cycling through
+    fns), between two HIP events on the current stream."""
+    for i in range(warmup):
+        fns[i % len(fns)]()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for i in range(steps):
+        fns[i % len(fns)]()
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) * 1e3 / steps
+
+
+def time_graph(torch, fns, steps, stream):
+    """Mean µs per call of `steps` calls captured in one HIP graph on
+    `stream` (the stream the calls launch on) and replayed: device time
+    without per-launch host cost."""
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=stream):
+        for i in range(steps):
+            fns[i % len(fns)]()
+    g.replay()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    with torch.cuda.stream(stream):
+        e0.record()
+        g.replay()
+        e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) * 1e3 / steps
+
+
+def decode_row(torch, dev, kf355, W, steps, warmup, sets_for):
+    """One decode step of eager attention, bf16 scores [1, 8, 1, 32768] ->
+    fp32 probabilities: kf_softmax_split (rows split over workgroups)
+    against kf_softmax (one workgroup per row) and torch eager, on rotating
+    buffer sets, timed as launched and as a replayed HIP graph."""
+    w = W.attn_decode_bf16()
+    src = w["x"].to(dev)
+    nb = src.numel() * (2 + 4)
+    s = torch.cuda.Stream()
+    xs = [src.clone() for _ in range(sets_for(nb))]
+    ys = [torch.empty(src.shape, dtype=torch.float32, device=dev) for _ in xs]
+    torch.cuda.synchronize()
+    with torch.cuda.stream(s):
+        ws = kf355.softmax_split_workspace(src, -1, torch.float32)
+        split = [kf355.prepare_softmax_split(x, y, -1, workspace=ws) for x, y in zip(xs, ys)]
+        plain = [kf355.prepare_softmax(x, y, -1) for x, y in zip(xs, ys)]
+        eager = [lambda x=x: torch.softmax(x, -1, dtype=torch.float32) for x in xs]
+        split[0]()
+        variant = kf355.last_variant()
+        plain[0]()
+        plain_variant = kf355.last_variant()
+        out = {}
+        for name, fns in (("split", split), ("plain", plain), ("eager", eager)):
+            out[name] = {"launched_us": round(time_launches(torch, fns, steps, warmup), 3),
+                         "graph_us": round(time_graph(torch, fns, steps, s), 3)}
+            if name == "split":
+                # Every replayed call wrote ys[i]; it must equal a direct call.
+                direct = kf355.kf_softmax_split(xs[0], -1, out_dtype=torch.float32)
+                torch.cuda.synchronize()
+                same = bool(torch.equal(ys[0].view(torch.int32), direct.view(torch.int32)))
+    torch.cuda.synchronize()
+    g_us = out["split"]["graph_us"]
+    gbs = nb / (g_us * 1e-6) / 1e9
+    return {"workload": "bf16 [1,8,1,32768] decode-step scores -> fp32 softmax (dtype=float32)",
+            "variant": variant, "plain_variant": plain_variant, "algorithmic_bytes": nb, "buffer_sets": len(xs),
+            "us_per_call": g_us, "gbps": round(gbs, 1), "frac_of_peak": round(gbs / PEAK_HBM_GBS, 4),
+            "timing": "HIP graph of back-to-back calls (graph_us); launched_us = launched from Python",
+            "split": out["split"], "plain": out["plain"], "torch_eager": out["eager"],
+            "vs_plain": round(out["plain"]["graph_us"] / g_us, 3),
+            "vs_torch_eager": round(out["eager"]["graph_us"] / g_us, 3), "graph_output_matches": same}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -117,7 +192,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-eager", action="store_true")
-    ap.add_argument("--no-next", action="store_true", help="skip the fused causal softmax measurement")
+    ap.add_argument("--no-next", action="store_true", help="skip the next-row measurements (fused causal softmax, layer_norm, decode split softmax)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: the operators shard by rows / groups / planes with no exchange, "
@@ -291,6 +366,9 @@ def main():
             "algorithmic_bytes": lbytes, "variant": lvar, "buffer_sets": len(cs),
             "torch_eager_us": round(eager_us, 3), "kf355_speedup": round(eager_us / us, 3)}
         del cs, lx
+
+        next_rows["softmax_decode_split"] = decode_row(torch, dev, kf355, W, args.steps, args.warmup,
+                                                       sets_for)
 
     calib = copy_calibration(torch, dev, nbytes["softmax"])
     sm = per_op["softmax"]
