@@ -142,6 +142,44 @@ void oracle_adaptive_avgpool2d(const double* x, int64_t planes, int64_t h,
     }
 }
 
+/* Max pooling over x viewed as [planes, h, w].  Output (i, j) scans its
+ * window in row-major order -- rows i*sh - ph + a*dh for a = 0..kh-1,
+ * columns j*sw - pw + b*dw for b = 0..kw-1 -- skipping positions outside
+ * the plane (padding is never chosen).  The running choice starts at -inf
+ * on the first in-plane position and moves to an element that is greater,
+ * or that is NaN: so the result is the maximum, the first position wins a
+ * tie, and a window holding NaN gives NaN at its last NaN.  idx, if not
+ * NULL, receives the chosen position as row * w + col. */
+void oracle_max_pool2d(const double* x, int64_t planes, int64_t h, int64_t w, int64_t kh, int64_t kw, int64_t sh,
+                       int64_t sw, int64_t ph, int64_t pw, int64_t dh, int64_t dw, int64_t oh, int64_t ow, double* y,
+                       int64_t* idx) {
+    for (int64_t p = 0; p < planes; ++p) {
+        const double* xp = x + p * h * w;
+        for (int64_t i = 0; i < oh; ++i) {
+            for (int64_t j = 0; j < ow; ++j) {
+                double best = -INFINITY;
+                int64_t at = -1;
+                for (int64_t a = 0; a < kh; ++a) {
+                    const int64_t r = i * sh - ph + a * dh;
+                    if (r < 0 || r >= h) continue;
+                    for (int64_t b = 0; b < kw; ++b) {
+                        const int64_t c = j * sw - pw + b * dw;
+                        if (c < 0 || c >= w) continue;
+                        const double v = xp[r * w + c];
+                        if (at < 0) at = r * w + c;
+                        if (v > best || isnan(v)) {
+                            best = v;
+                            at = r * w + c;
+                        }
+                    }
+                }
+                y[(p * oh + i) * ow + j] = best;
+                if (idx) idx[(p * oh + i) * ow + j] = at;
+            }
+        }
+    }
+}
+
 /* Round one double to the format (mant_bits, exp_bits), ties to even.
  *
  * The exact value |v| is divided by the format's quantum at its binade

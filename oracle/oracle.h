@@ -68,6 +68,19 @@ void oracle_layer_norm(const double* x, int64_t rows, int64_t d, const double* w
 void oracle_adaptive_avgpool2d(const double* x, int64_t planes, int64_t h,
                                int64_t w, int64_t oh, int64_t ow, double* y);
 
+/* max_pool2d over x viewed as [planes, h, w] (PyTorch `max_pool2d`):
+ * output (i, j) is the maximum of its window -- rows i*sh - ph + a*dh
+ * (a < kh), columns j*sw - pw + b*dw (b < kw), positions outside the plane
+ * being padding that is never chosen -- with NaN winning over any number.
+ * The window is scanned row-major from -inf at its first in-plane position,
+ * moving to any greater or NaN element: ties keep the first position, a
+ * window holding NaN reports its last NaN.  y is [planes, oh, ow]; idx (may
+ * be NULL) receives the chosen position as row * w + col within the plane.
+ * Max is exact, so y needs no rounding to the input's format. */
+void oracle_max_pool2d(const double* x, int64_t planes, int64_t h, int64_t w, int64_t kh, int64_t kw, int64_t sh,
+                       int64_t sw, int64_t ph, int64_t pw, int64_t dh, int64_t dw, int64_t oh, int64_t ow, double* y,
+                       int64_t* idx);
+
 /* Round each double to the nearest value of a binary floating-point format
  * with `mant_bits` stored significand bits and `exp_bits` exponent bits,
  * ties to even, directly from double (one rounding).  Returns the format's

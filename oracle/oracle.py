@@ -55,10 +55,12 @@ def _load():
         lib.oracle_group_norm.argtypes = [dp, i64, i64, i64, i64, dp, dp, ctypes.c_double, dp]
         lib.oracle_adaptive_avgpool2d.argtypes = [dp, i64, i64, i64, i64, i64, dp]
         lib.oracle_layer_norm.argtypes = [dp, i64, i64, dp, dp, ctypes.c_double, dp]
+        lib.oracle_max_pool2d.argtypes = [dp] + [i64] * 13 + [dp, ctypes.POINTER(ctypes.c_int64)]
         lib.oracle_round_to_format.argtypes = [dp, i64, ctypes.c_int, ctypes.c_int,
                                                ctypes.POINTER(ctypes.c_uint32)]
         for f in (lib.oracle_softmax_rows, lib.oracle_softmax_causal, lib.oracle_group_norm,
-                  lib.oracle_adaptive_avgpool2d, lib.oracle_layer_norm, lib.oracle_round_to_format):
+                  lib.oracle_adaptive_avgpool2d, lib.oracle_layer_norm, lib.oracle_max_pool2d,
+                  lib.oracle_round_to_format):
             f.restype = None
         _lib = lib
     return _lib
@@ -185,6 +187,49 @@ def adaptive_avg_pool2d(x, output_size) -> np.ndarray:
     if y.size:
         _load().oracle_adaptive_avgpool2d(_dptr(x), planes, h, w, oh, ow, _dptr(y))
     return y
+
+
+def _pair(v):
+    return (v, v) if isinstance(v, int) else tuple(v)
+
+
+def pool_out_size(n: int, k: int, s: int, p: int, d: int, ceil_mode: bool) -> int:
+    """Output length of a pooling window sweep (PyTorch's formula): the
+    number of window starts i*s - p whose effective extent d*(k-1)+1 fits in
+    the padded length, rounded up in ceil mode, where a last window that
+    would start inside the right padding is dropped."""
+    span = n + 2 * p - d * (k - 1) - 1
+    out = (-(-span // s) if ceil_mode else span // s) + 1
+    if ceil_mode and (out - 1) * s >= n + p:
+        out -= 1
+    return out
+
+
+def max_pool2d(x, kernel_size, stride=None, padding=0, dilation=1, ceil_mode=False):
+    """PyTorch max_pool2d(x, ...) with return_indices: (y float64, idx int64)
+    for x [N, C, H, W] or [C, H, W] (any memory layout; the logical tensor is
+    what is pooled)."""
+    x = _f64(x)
+    if x.ndim not in (3, 4):
+        raise ValueError("max_pool2d expects [N, C, H, W] or [C, H, W]")
+    kh, kw = _pair(kernel_size)
+    sh, sw = _pair(stride if stride is not None else kernel_size)
+    ph, pw = _pair(padding)
+    dh, dw = _pair(dilation)
+    if min(kh, kw, sh, sw, dh, dw) < 1 or min(ph, pw) < 0 or ph > kh // 2 or pw > kw // 2:
+        raise ValueError("bad max_pool2d window")
+    h, w = x.shape[-2], x.shape[-1]
+    oh = pool_out_size(h, kh, sh, ph, dh, ceil_mode)
+    ow = pool_out_size(w, kw, sw, pw, dw, ceil_mode)
+    if oh < 1 or ow < 1:
+        raise ValueError("max_pool2d output would be empty")
+    planes = int(np.prod(x.shape[:-2], dtype=np.int64))
+    y = np.empty(x.shape[:-2] + (oh, ow), dtype=np.float64)
+    idx = np.empty(y.shape, dtype=np.int64)
+    if y.size:
+        _load().oracle_max_pool2d(_dptr(x), planes, h, w, kh, kw, sh, sw, ph, pw, dh, dw, oh, ow, _dptr(y),
+                                  idx.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)))
+    return y, idx
 
 
 def round_bits(y: np.ndarray, fmt: str) -> np.ndarray:
