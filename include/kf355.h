@@ -226,6 +226,44 @@ kf_status kf_adaptive_avgpool2d(const void* x, kf_dtype dtype, void* y, int32_t 
                                 const int64_t* x_strides, const int64_t* y_strides, int64_t out_h,
                                 int64_t out_w, void* stream);
 
+/*
+ * kf_max_pool2d -- y = max_pool2d(x, kernel, stride, padding, dilation,
+ * ceil_mode), optionally with return_indices (PyTorch
+ * `torch.nn.functional.max_pool2d`; the paper's ResNet-50 max_pool2d,
+ * Section IV-C).  Output (i, j) of a plane is the maximum over rows
+ * i*sh - ph + a*dh (a < kh) and columns j*sw - pw + b*dw (b < kw) that lie
+ * inside the plane (padding is never chosen); NaN wins over any number.
+ * The result is the selected input element, bit for bit.
+ *
+ *  x        device pointer, shape [N, C, H, W] or [C, H, W], H, W >= 1,
+ *           H * W < 2^31; dtype FLOAT32, BFLOAT16 or FLOAT16; dense NCHW, or
+ *           (4-D) dense channels last (memory order N, H, W, C).
+ *  window   host array {kh, kw, sh, sw, ph, pw, dh, dw}: kernel, stride and
+ *           dilation >= 1, 0 <= padding <= kernel / 2 (PyTorch's rule).
+ *  ceil_mode  non-zero: output sizes rounded up (a last window starting in
+ *           the right padding is dropped), as in PyTorch.
+ *  y        device pointer, shape [N, C, out_h, out_w] (or [C, out_h, out_w])
+ *           from kf_max_pool2d_output_size, x's dtype, dense in x's layout;
+ *           y_strides describe it.  No overlap with x.
+ *  indices  NULL, or device int64 array shaped and laid out like y: the
+ *           selected position as row * W + col within its plane.  In a tie
+ *           the first position in row-major window order; a window holding
+ *           NaN reports its last NaN; a window of only -inf its first
+ *           in-plane position.
+ *  KF_ERR_UNSUPPORTED_LAYOUT for other layouts; KF_ERR_BAD_SHAPE when the
+ *  output would be empty.
+ */
+kf_status kf_max_pool2d(const void* x, kf_dtype dtype, void* y, int64_t* indices, int32_t ndim, const int64_t* shape,
+                        const int64_t* x_strides, const int64_t* y_strides, const int64_t* window, int32_t ceil_mode,
+                        void* stream);
+
+/* Output sizes {out_h, out_w} of kf_max_pool2d for an H x W plane (PyTorch's
+ * formula: out = floor((H + 2*ph - dh*(kh-1) - 1) / sh) + 1, with ceil in
+ * ceil mode, minus one when ceil mode would start the last window at or past
+ * H + ph), written to out_hw[2].  Same checks as kf_max_pool2d. */
+kf_status kf_max_pool2d_output_size(int64_t h, int64_t w, const int64_t* window, int32_t ceil_mode,
+                                    int64_t* out_hw);
+
 #ifdef __cplusplus
 }
 #endif

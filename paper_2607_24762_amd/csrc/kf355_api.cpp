@@ -61,6 +61,47 @@ bool dense(int32_t ndim, const int64_t* shape, const int64_t* strides) {
     return true;
 }
 
+// Dense channels-last [N, C, H, W] (memory order N, H, W, C); dimensions of
+// size 1 may carry any stride.
+bool dense_nhwc(const int64_t* shape, const int64_t* strides) {
+    if (!strides) return false;
+    static const int order[4] = {1, 3, 2, 0};  // innermost first: C, W, H, N
+    int64_t expect = 1;
+    for (int k = 0; k < 4; ++k) {
+        const int i = order[k];
+        if (shape[i] != 1 && strides[i] != expect) return false;
+        expect *= shape[i];
+    }
+    return true;
+}
+
+// PyTorch's pooling output length (see kf_max_pool2d_output_size).
+// Division rounding toward -infinity (b > 0): the span below is negative
+// when the dilated kernel is longer than the padded input, and ceil mode
+// can still produce one window then.
+int64_t floor_div(int64_t a, int64_t b) { return a >= 0 ? a / b : -((-a + b - 1) / b); }
+
+int64_t pool_out(int64_t n, int64_t k, int64_t s, int64_t p, int64_t d, bool ceil_mode) {
+    const int64_t span = n + 2 * p - d * (k - 1) - 1;
+    int64_t out = floor_div(span + (ceil_mode ? s - 1 : 0), s) + 1;
+    if (ceil_mode && (out - 1) * s >= n + p) --out;
+    return out;
+}
+
+// Window {kh, kw, sh, sw, ph, pw, dh, dw}: positive sizes, strides and
+// dilations, padding at most half the kernel (PyTorch's rule).
+kf_status check_window(const int64_t* win) {
+    if (!win) return fail(KF_ERR_NULL_POINTER, "window is NULL");
+    for (int i = 0; i < 8; ++i)
+        if (win[i] > INT32_MAX) return fail(KF_ERR_BAD_ARG, "window entry %d too large", i);
+    if (win[0] < 1 || win[1] < 1) return fail(KF_ERR_BAD_ARG, "kernel size must be >= 1");
+    if (win[2] < 1 || win[3] < 1) return fail(KF_ERR_BAD_ARG, "stride must be >= 1");
+    if (win[6] < 1 || win[7] < 1) return fail(KF_ERR_BAD_ARG, "dilation must be >= 1");
+    if (win[4] < 0 || win[5] < 0 || win[4] > win[0] / 2 || win[5] > win[1] / 2)
+        return fail(KF_ERR_BAD_ARG, "padding must be in [0, kernel / 2]");
+    return KF_OK;
+}
+
 // Byte ranges [a, a+na) and [b, b+nb) share a byte.
 bool overlaps(const void* a, int64_t na, const void* b, int64_t nb) {
     const uintptr_t pa = (uintptr_t)a, pb = (uintptr_t)b;
@@ -370,6 +411,70 @@ kf_status kf_adaptive_avgpool2d(const void* x, kf_dtype dtype, void* y, int32_t 
     AvgPoolArgs a{x, y, dtype, n / (H * W), H, W, out_h, out_w};
     const char* variant = nullptr;
     s = avgpool_launch(a, static_cast<hipStream_t>(stream), &variant);
+    return done(s, variant);
+}
+
+kf_status kf_max_pool2d_output_size(int64_t h, int64_t w, const int64_t* window, int32_t ceil_mode,
+                                     int64_t* out_hw) {
+    begin();
+    if (!out_hw) return fail(KF_ERR_NULL_POINTER, "out_hw is NULL");
+    kf_status s = check_window(window);
+    if (s != KF_OK) return s;
+    if (h < 1 || w < 1) return fail(KF_ERR_BAD_SHAPE, "H and W must be >= 1");
+    out_hw[0] = pool_out(h, window[0], window[2], window[4], window[6], ceil_mode != 0);
+    out_hw[1] = pool_out(w, window[1], window[3], window[5], window[7], ceil_mode != 0);
+    if (out_hw[0] < 1 || out_hw[1] < 1) return fail(KF_ERR_BAD_SHAPE, "output would be empty");
+    return KF_OK;
+}
+
+kf_status kf_max_pool2d(const void* x, kf_dtype dtype, void* y, int64_t* indices, int32_t ndim, const int64_t* shape,
+                        const int64_t* x_strides, const int64_t* y_strides, const int64_t* window, int32_t ceil_mode,
+                        void* stream) {
+    begin();
+    int64_t n = 0;
+    kf_status s = check_shape(ndim, shape, 3, 4, &n);
+    if (s != KF_OK) return s;
+    if (!dtype_ok(dtype)) return fail(KF_ERR_BAD_DTYPE, "dtype %d not supported", (int)dtype);
+    s = check_window(window);
+    if (s != KF_OK) return s;
+    const int64_t H = shape[ndim - 2], W = shape[ndim - 1];
+    if (H < 1 || W < 1) return fail(KF_ERR_BAD_SHAPE, "H and W must be >= 1");
+    if (H * W > INT32_MAX) return fail(KF_ERR_BAD_SHAPE, "a plane of %lld elements is too large", (long long)(H * W));
+    const int64_t oh = pool_out(H, window[0], window[2], window[4], window[6], ceil_mode != 0);
+    const int64_t ow = pool_out(W, window[1], window[3], window[5], window[7], ceil_mode != 0);
+    if (oh < 1 || ow < 1) return fail(KF_ERR_BAD_SHAPE, "output would be empty");
+    int64_t yshape[4];
+    for (int32_t i = 0; i < ndim - 2; ++i) yshape[i] = shape[i];
+    yshape[ndim - 2] = oh;
+    yshape[ndim - 1] = ow;
+    const int64_t ny = count(ndim, yshape);
+    const int64_t N = ndim == 4 ? shape[0] : 1, C = shape[ndim - 3];
+    if (N > INT32_MAX || C > INT32_MAX) return fail(KF_ERR_BAD_SHAPE, "N or C too large");
+    if (n == 0) return done(KF_OK, "noop");
+    if (!x || !y) return fail(KF_ERR_NULL_POINTER, "x or y is NULL");
+    const int64_t eb = elem_bytes(dtype);
+    if ((uintptr_t)x % eb || (uintptr_t)y % eb || (uintptr_t)indices % 8)
+        return fail(KF_ERR_BAD_ARG, "x, y or indices is not element aligned");
+    bool nhwc = false;
+    if (dense(ndim, shape, x_strides)) {
+        if (!dense(ndim, yshape, y_strides))
+            return fail(KF_ERR_UNSUPPORTED_LAYOUT, "y must be dense in x's layout (NCHW)");
+    } else if (ndim == 4 && dense_nhwc(shape, x_strides)) {
+        if (!dense_nhwc(yshape, y_strides))
+            return fail(KF_ERR_UNSUPPORTED_LAYOUT, "y must be dense in x's layout (channels last)");
+        nhwc = true;
+    } else {
+        return fail(KF_ERR_UNSUPPORTED_LAYOUT, "x must be dense NCHW or dense channels last");
+    }
+    if (overlaps(x, n * eb, y, ny * eb)) return fail(KF_ERR_BAD_ARG, "x and y overlap");
+    if (indices && (overlaps(indices, ny * 8, x, n * eb) || overlaps(indices, ny * 8, y, ny * eb)))
+        return fail(KF_ERR_BAD_ARG, "indices overlap x or y");
+
+    MaxPoolArgs a{x, y, indices, dtype, N, C, H, W, oh, ow,
+                  (int32_t)window[0], (int32_t)window[1], (int32_t)window[2], (int32_t)window[3],
+                  (int32_t)window[4], (int32_t)window[5], (int32_t)window[6], (int32_t)window[7], nhwc};
+    const char* variant = nullptr;
+    s = max_pool2d_launch(a, static_cast<hipStream_t>(stream), &variant);
     return done(s, variant);
 }
 

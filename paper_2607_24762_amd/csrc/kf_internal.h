@@ -76,6 +76,19 @@ struct AvgPoolArgs {
 };
 kf_status avgpool_launch(const AvgPoolArgs& a, hipStream_t s, const char** variant);
 
+// max_pool2d over x [n, c, h, w] (NCHW) or [n, h, w, c] (NHWC, channels
+// last); y and idx (optional) are [n, c, oh, ow] in the same layout.
+struct MaxPoolArgs {
+    const void* x;
+    void* y;
+    int64_t* idx;
+    kf_dtype t;
+    int64_t n, c, h, w, oh, ow;
+    int32_t kh, kw, sh, sw, ph, pw, dh, dw;
+    bool nhwc;
+};
+kf_status max_pool2d_launch(const MaxPoolArgs& a, hipStream_t s, const char** variant);
+
 // Records the detail text of the current failure (thread-local).
 void set_error(const char* fmt, ...);
 

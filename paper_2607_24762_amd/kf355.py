@@ -49,6 +49,9 @@ _SIGNATURES = {
     "kf_layer_norm": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p, ctypes.c_int32, _i64p, _i64p,
                                      _i64p, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int,
                                      ctypes.c_double, ctypes.c_void_p]),
+    "kf_max_pool2d": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32,
+                                     _i64p, _i64p, _i64p, _i64p, ctypes.c_int32, ctypes.c_void_p]),
+    "kf_max_pool2d_output_size": (ctypes.c_int, [ctypes.c_int64, ctypes.c_int64, _i64p, ctypes.c_int32, _i64p]),
     "kf_adaptive_avgpool2d": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p, ctypes.c_int32, _i64p,
                                              _i64p, _i64p, ctypes.c_int64, ctypes.c_int64, ctypes.c_void_p]),
 }
@@ -263,11 +266,56 @@ def kf_adaptive_avgpool2d(x: torch.Tensor, output_size, out: torch.Tensor | None
     return y
 
 
+def _pair(v):
+    return (int(v), int(v)) if isinstance(v, int) else (int(v[0]), int(v[1]))
+
+
+def _window(kernel_size, stride, padding, dilation):
+    kh, kw = _pair(kernel_size)
+    sh, sw = _pair(stride if stride is not None and stride != [] else kernel_size)
+    ph, pw = _pair(padding)
+    dh, dw = _pair(dilation)
+    return [kh, kw, sh, sw, ph, pw, dh, dw]
+
+
+def max_pool2d_output_size(h: int, w: int, kernel_size, stride=None, padding=0, dilation=1,
+                           ceil_mode: bool = False) -> tuple:
+    win, _a = _arr(_window(kernel_size, stride, padding, dilation))
+    out, _b = _arr([0, 0])
+    _check(lib().kf_max_pool2d_output_size(h, w, win, int(ceil_mode), out))
+    return int(out[0]), int(out[1])
+
+
+def kf_max_pool2d(x: torch.Tensor, kernel_size, stride=None, padding=0, dilation=1, ceil_mode: bool = False,
+                  return_indices: bool = False, out: torch.Tensor | None = None):
+    """max_pool2d(x, ...) through kf_max_pool2d; x NCHW or channels last
+    (the output keeps x's layout, as PyTorch's does)."""
+    _need_cuda(x)
+    if x.dim() not in (3, 4):
+        raise KfError(2, "max_pool2d expects [N, C, H, W] or [C, H, W]")
+    oh, ow = max_pool2d_output_size(x.shape[-2], x.shape[-1], kernel_size, stride, padding, dilation, ceil_mode)
+    fmt = torch.channels_last if (x.dim() == 4 and not x.is_contiguous()
+                                  and x.is_contiguous(memory_format=torch.channels_last)) else torch.contiguous_format
+    yshape = tuple(x.shape[:-2]) + (oh, ow)
+    y = out if out is not None else torch.empty(yshape, dtype=x.dtype, device=x.device, memory_format=fmt)
+    idx = torch.empty(yshape, dtype=torch.int64, device=x.device, memory_format=fmt) if return_indices else None
+    win, _w = _arr(_window(kernel_size, stride, padding, dilation))
+    shape, _s = _arr(list(x.shape))
+    xs, _a = _arr(list(x.stride()))
+    ys, _b = _arr(list(y.stride()))
+    with torch.cuda.device(x.device):
+        _check(lib().kf_max_pool2d(ctypes.c_void_p(x.data_ptr()), _dtype(x), ctypes.c_void_p(y.data_ptr()),
+                                   ctypes.c_void_p(idx.data_ptr() if idx is not None else None), x.dim(), shape, xs,
+                                   ys, win, int(ceil_mode), _stream(x)))
+    return (y, idx) if return_indices else y
+
+
 softmax = kf_softmax
 softmax_causal = kf_softmax_causal
 layer_norm = kf_layer_norm
 group_norm = kf_group_norm
 adaptive_avg_pool2d = kf_adaptive_avgpool2d
+max_pool2d = kf_max_pool2d
 
 
 class Prepared:
@@ -344,6 +392,19 @@ def prepare_layer_norm(x: torch.Tensor, y: torch.Tensor, normalized_ndim: int, w
             ctypes.c_void_p(bias.data_ptr() if bias is not None else None), _affine_dtype(x, weight, bias),
             float(eps), _stream(x))
     return Prepared(lib().kf_layer_norm, args, (x, y, weight, bias, a0, a1, a2))
+
+
+def prepare_max_pool2d(x: torch.Tensor, y: torch.Tensor, kernel_size, stride=None, padding=0, dilation=1,
+                       ceil_mode: bool = False, indices: torch.Tensor | None = None) -> Prepared:
+    _need_cuda(x, y, indices)
+    win, a3 = _arr(_window(kernel_size, stride, padding, dilation))
+    shape, a0 = _arr(list(x.shape))
+    xs, a1 = _arr(list(x.stride()))
+    ys, a2 = _arr(list(y.stride()))
+    args = (ctypes.c_void_p(x.data_ptr()), _dtype(x), ctypes.c_void_p(y.data_ptr()),
+            ctypes.c_void_p(indices.data_ptr() if indices is not None else None), x.dim(), shape, xs, ys, win,
+            int(ceil_mode), _stream(x))
+    return Prepared(lib().kf_max_pool2d, args, (x, y, indices, a0, a1, a2, a3))
 
 
 def prepare_adaptive_avgpool2d(x: torch.Tensor, y: torch.Tensor) -> Prepared:

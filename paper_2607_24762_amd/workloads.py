@@ -102,6 +102,15 @@ def attn_decode_bf16(seed: int = 8, batch: int = 1, heads: int = 8, kv: int = 32
     return {"op": "softmax_split", "x": s, "dim": -1, "out_dtype": out_dtype}
 
 
+def maxpool_resnet_stem_f32(seed: int = 9, batch: int = 32) -> dict:
+    """ResNet-50 stem pooling: fp32 [batch, 64, 112, 112] NCHW after the
+    stem's BatchNorm + ReLU, so ReLU(z) (about half exact zeros); 3x3 max
+    pooling, stride 2, padding 1 -> [batch, 64, 56, 56]."""
+    rng = np.random.default_rng(seed)
+    x = cast(np.maximum(rng.standard_normal((batch, 64, 112, 112)), 0.0), "f32")
+    return {"op": "max_pool2d", "x": x, "kernel_size": 3, "stride": 2, "padding": 1}
+
+
 def layernorm_sd35_bf16(seed: int = 7, tokens: int = 4096, hidden: int = 1536) -> dict:
     """SD3.5 Medium transformer LayerNorm: bf16 [2, tokens, hidden] (the two
     classifier-free-guidance branches of a 1024x1024 image: 4096 patch

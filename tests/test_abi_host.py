@@ -248,6 +248,51 @@ def test_avgpool_zero_planes_is_a_noop(lib):
     assert lib.kf_last_variant().decode() == "noop"
 
 
+def mp(lib, shape=(2, 3, 9, 9), win=(3, 3, 2, 2, 1, 1, 1, 1), ceil=0, x=FAKE, y=FAKE + (1 << 30), idx=None, xt=F32,
+       xs=None, ys=None):
+    return lib.kf_max_pool2d(ctypes.c_void_p(x), xt, ctypes.c_void_p(y), ctypes.c_void_p(idx), len(shape),
+                             arr(shape), arr(xs) if xs else None, arr(ys) if ys else None,
+                             arr(win) if win is not None else None, ceil, None)
+
+
+def mp_size(lib, h, w, win, ceil=0):
+    out = arr([0, 0])
+    st = lib.kf_max_pool2d_output_size(h, w, arr(win), ceil, out)
+    return st, (out[0], out[1])
+
+
+def test_max_pool2d_rejections(lib):
+    assert mp(lib, shape=(9, 9)) == SHAPE
+    assert mp(lib, win=None) == NULLP
+    assert mp(lib, win=(0, 3, 1, 1, 0, 0, 1, 1)) == ARG
+    assert mp(lib, win=(3, 3, 0, 1, 0, 0, 1, 1)) == ARG
+    assert mp(lib, win=(3, 3, 1, 1, 2, 0, 1, 1)) == ARG and "padding" in err(lib)
+    assert mp(lib, win=(3, 3, 1, 1, 0, 0, 0, 1)) == ARG
+    assert mp(lib, shape=(1, 1, 2, 2), win=(3, 3, 1, 1, 0, 0, 1, 1)) == SHAPE   # empty output
+    assert mp(lib, xt=4) == DTYPE
+    assert mp(lib, x=0) == NULLP
+    assert mp(lib, idx=FAKE + (2 << 30) + 4) == ARG                              # int64 alignment
+    assert mp(lib, y=FAKE + 8) == ARG                                            # overlaps x
+    assert mp(lib, idx=FAKE + 16) == ARG                                         # indices overlap x
+    assert mp(lib, xs=(1, 2, 3, 4)) == LAYOUT
+    assert mp(lib, xs=(243, 1, 27, 3)) == LAYOUT and "channels last" in err(lib)  # y not in x's layout
+    assert mp(lib, shape=(0, 3, 9, 9)) == OK and lib.kf_last_variant().decode() == "noop"
+
+
+def test_max_pool2d_output_size(lib):
+    assert mp_size(lib, 112, 112, (3, 3, 2, 2, 1, 1, 1, 1)) == (OK, (56, 56))   # ResNet-50 stem
+    assert mp_size(lib, 5, 7, (2, 2, 2, 2, 0, 0, 1, 1)) == (OK, (2, 3))
+    assert mp_size(lib, 5, 7, (2, 2, 2, 2, 0, 0, 1, 1), ceil=1) == (OK, (3, 4))
+    assert mp_size(lib, 6, 6, (3, 3, 2, 2, 1, 1, 2, 2)) == (OK, (2, 2))
+    assert mp_size(lib, 2, 2, (3, 3, 1, 1, 0, 0, 1, 1))[0] == SHAPE
+    # The dilated kernel (9) is longer than the input (7): floor mode has no
+    # window, ceil mode one (its span rounds toward -infinity, as PyTorch's).
+    assert mp_size(lib, 7, 7, (5, 5, 3, 3, 0, 0, 2, 2))[0] == SHAPE
+    assert mp_size(lib, 7, 7, (5, 5, 3, 3, 0, 0, 2, 2), ceil=1) == (OK, (1, 1))
+    assert mp_size(lib, 0, 4, (1, 1, 1, 1, 0, 0, 1, 1))[0] == SHAPE
+    assert lib.kf_max_pool2d_output_size(4, 4, arr((1, 1, 1, 1, 0, 0, 1, 1)), 0, None) == NULLP
+
+
 def test_binding_refuses_cpu_tensors(lib):
     import torch
     with pytest.raises(ValueError):

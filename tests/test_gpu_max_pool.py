@@ -1,0 +1,136 @@
+"""GPU parity of kf_max_pool2d against the float64 oracle: bit-exact
+values and indices (max pooling selects an input element, so there is no
+rounding and the tolerance is zero), for the ResNet-50 stem at full size in
+NCHW and channels last, a sweep of window shapes, strides, paddings,
+dilations and ceil mode over every kernel variant (LDS bands with vector and
+element staging, the direct fallback for wide planes, channels last with
+vector and element channel access), every dtype, special values (NaN, -inf,
+ties), 3-D inputs and empty batches."""
+import itertools
+
+import numpy as np
+import pytest
+import torch
+import torch.nn.functional as F
+
+from compare import note
+from oracle import oracle
+from paper_2607_24762_amd import kf355
+from paper_2607_24762_amd import workloads as W
+from paper_2607_24762_amd.workloads import randn
+
+pytestmark = pytest.mark.gpu
+TORCH = {"f32": torch.float32, "bf16": torch.bfloat16, "f16": torch.float16}
+
+
+@pytest.fixture(scope="module", autouse=True)
+def gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU visible")
+    kf355.lib()
+
+
+def check(x_cpu, x_gpu, k, s, p, d, ceil):
+    y, idx = kf355.kf_max_pool2d(x_gpu, k, s, p, d, ceil, return_indices=True)
+    torch.cuda.synchronize()
+    variant = kf355.last_variant()
+    ref, ref_idx = oracle.max_pool2d(x_cpu, k, s, p, d, ceil)
+    got = y.float().cpu().numpy().astype(np.float64)
+    nan_r, nan_g = np.isnan(ref), np.isnan(got)
+    assert np.array_equal(nan_r, nan_g), variant
+    assert np.array_equal(got[~nan_g], ref[~nan_r]), (variant, float(np.abs(got[~nan_g] - ref[~nan_r]).max()))
+    assert np.array_equal(idx.cpu().numpy(), ref_idx), variant
+    assert y.is_contiguous(memory_format=torch.channels_last) == x_gpu.is_contiguous(
+        memory_format=torch.channels_last) or x_gpu.is_contiguous()
+    return y, idx, variant
+
+
+@pytest.mark.parametrize("layout", ["nchw", "nhwc"])
+def test_resnet_stem(layout):
+    w = W.maxpool_resnet_stem_f32()
+    note(f"max_pool2d resnet stem {layout}")
+    x = w["x"].cuda()
+    if layout == "nhwc":
+        x = x.contiguous(memory_format=torch.channels_last)
+    y, idx, variant = check(w["x"], x, 3, 2, 1, 1, False)
+    assert variant == ("mp_band_vec" if layout == "nchw" else "mp_nhwc_vec"), variant
+    # Informational second reference: torch eager on the same GPU agrees bit for bit.
+    ty, ti = F.max_pool2d(x, 3, 2, 1, return_indices=True)
+    assert torch.equal(ty, y) and torch.equal(ti, idx)
+
+
+WINDOWS = [(k, s, p, d, c) for k in (1, 2, 3, 5) for s in (1, 2, 3) for p in sorted({0, k // 2}) for d in (1, 2)
+           for c in (False, True)]
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16", "f16"])
+@pytest.mark.parametrize("hw", [(16, 16), (13, 21), (7, 8), (33, 40)])
+def test_window_sweep_nchw(dt, hw):
+    x_cpu = randn((2, 3) + hw, dt, seed=hw[0] * 100 + hw[1], std=2.0)
+    x = x_cpu.cuda()
+    seen = set()
+    for k, s, p, d, c in WINDOWS:
+        if oracle.pool_out_size(hw[0], k, s, p, d, c) < 1 or oracle.pool_out_size(hw[1], k, s, p, d, c) < 1:
+            continue
+        note(f"max_pool2d nchw {dt} {hw} k={k} s={s} p={p} d={d} ceil={c}")
+        seen.add(check(x_cpu, x, k, s, p, d, c)[2])
+    assert seen <= {"mp_band_vec", "mp_band_scalar"}, seen
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+@pytest.mark.parametrize("c", [64, 24, 5])
+def test_window_sweep_nhwc(dt, c):
+    x_cpu = randn((2, c, 13, 18), dt, seed=c, std=2.0)
+    x = x_cpu.cuda().contiguous(memory_format=torch.channels_last)
+    for k, s, p, d, cm in WINDOWS[::3]:
+        if oracle.pool_out_size(13, k, s, p, d, cm) < 1 or oracle.pool_out_size(18, k, s, p, d, cm) < 1:
+            continue
+        note(f"max_pool2d nhwc {dt} c={c} k={k} s={s} p={p} d={d} ceil={cm}")
+        _, _, variant = check(x_cpu, x, k, s, p, d, cm)
+        vec = 4 if dt == "f32" else 8
+        assert variant == ("mp_nhwc_vec" if c % vec == 0 else "mp_nhwc_scalar"), variant
+
+
+def test_wide_planes_take_the_direct_kernel():
+    note("max_pool2d direct")
+    x_cpu = randn((2, 5, 9000), "f32", seed=4)          # [C, H, W]: a 36 KB row exceeds the band tile
+    _, _, variant = check(x_cpu, x_cpu.cuda(), (3, 3), (2, 2), (1, 1), 1, True)
+    assert variant == "mp_direct"
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16", "f16"])
+@pytest.mark.parametrize("layout", ["nchw", "nhwc"])
+def test_special_values(dt, layout):
+    note(f"max_pool2d special values {dt} {layout}")
+    x = randn((2, 8, 12, 12), "f32", seed=8)
+    x[0, 0] = float("-inf")                             # all -inf planes
+    x[0, 1, 3, 4] = float("nan")
+    x[0, 1, 5, 5] = float("nan")                        # two NaN in overlapping windows
+    x[0, 2] = 0.5                                       # ties everywhere: first position wins
+    x[1, 3, ::2, ::2] = float("inf")
+    x[1, 4] = -1.0                                      # padding must not win over negatives
+    xt = x.to(TORCH[dt])
+    xg = xt.cuda()
+    if layout == "nhwc":
+        xg = xg.contiguous(memory_format=torch.channels_last)
+    check(xt, xg, 3, 2, 1, 1, False)
+    check(xt, xg, 2, 1, 1, 2, True)
+
+
+def test_three_d_input_and_empty_batch():
+    note("max_pool2d 3-D and empty")
+    x_cpu = randn((6, 17, 19), "bf16", seed=12)
+    check(x_cpu, x_cpu.cuda(), 3, 2, 1, 1, True)
+    e = torch.empty(0, 3, 8, 8, device="cuda")
+    y = kf355.kf_max_pool2d(e, 2)
+    torch.cuda.synchronize()
+    assert y.shape == (0, 3, 4, 4)
+
+
+def test_without_indices_matches_with():
+    note("max_pool2d no indices")
+    x = randn((4, 16, 30, 30), "f32", seed=13).cuda()
+    a = kf355.kf_max_pool2d(x, 3, 2, 1)
+    b, _ = kf355.kf_max_pool2d(x, 3, 2, 1, return_indices=True)
+    torch.cuda.synchronize()
+    assert torch.equal(a, b)
