@@ -22,6 +22,8 @@
 //              overlapping windows re-read from cache.
 #include <math.h>
 
+#include <type_traits>
+
 #include "kf_device.hpp"
 #include "kf_internal.h"
 
@@ -30,6 +32,7 @@ namespace {
 
 constexpr int kNT = 256;
 constexpr int kBandBytes = 16 << 10;  // LDS budget of one band tile
+constexpr int64_t kBandGroups = 2048;  // persistent band workgroups (8 per CU)
 
 // Raw storage type of an element and its value as a float (exact).
 template <class T>
@@ -74,7 +77,36 @@ struct Pick {
             at = pos;
         }
     }
+    // The same step without branches, skipped where !valid: callers read
+    // every window position (from a clamped address) before folding, so
+    // the reads issue together instead of one branch and one wait each.
+    __device__ __forceinline__ void consider_if(bool valid, uint32_t raw, int32_t pos) {
+        // Bitwise, not short-circuit, operators: the compiler keeps this
+        // as compares and selects instead of branching around each term.
+        const float v = Raw<T>::value(raw);
+        const bool first = valid & (at < 0);
+        const bool take = valid & ((v > best) | (v != v));
+        best = take ? v : best;
+        bits = take ? raw : bits;
+        at = (take | first) ? pos : at;
+    }
 };
+
+// Merge of two picks over consecutive stretches of the row-major scan (a
+// before b): scanning b's elements after a's moves to b's pick exactly when
+// b holds a greater element or a NaN, so the merged pick equals the pick of
+// the whole scan; an empty a (no in-plane position yet) takes b.
+// (Selected field by field: a select of whole structs would make the
+// compiler keep them in scratch memory.)
+template <class T>
+__device__ __forceinline__ Pick<T> merge(const Pick<T>& a, const Pick<T>& b) {
+    const bool take = (a.at < 0) | (b.best > a.best) | (b.best != b.best);
+    Pick<T> m;
+    m.best = take ? b.best : a.best;
+    m.bits = take ? b.bits : a.bits;
+    m.at = take ? b.at : a.at;
+    return m;
+}
 
 struct MPParams {
     const void* x;
@@ -87,61 +119,251 @@ struct MPParams {
 };
 
 // --------------------------------------------------------------------------
-// NCHW, one workgroup per (plane, band of output rows), input rows in LDS.
-template <class T, bool VECTOR>
+// NCHW, bands of output rows, input rows in LDS.  Work item = (plane, band);
+// a persistent workgroup walks items blockIdx.x, + gridDim.x, ...  In the
+// vector form the next item's input span is loaded into registers while the
+// current one is scanned from LDS and written, so every workgroup keeps
+// loads in flight through its compute and store phases.
+
+// Rows and span of one work item.
+struct Band {
+    int64_t plane;
+    int o0, o1, r_lo, n;  // output rows [o0, o1), first input row, span elements
+};
+__device__ __forceinline__ Band band_of(const MPParams& p, int64_t item) {
+    Band b;
+    b.plane = item / p.bands;
+    const int band = (int)(item - b.plane * p.bands);
+    b.o0 = band * p.band_rows;
+    b.o1 = min(p.oh, b.o0 + p.band_rows);
+    b.r_lo = max(0, b.o0 * p.sh - p.ph);
+    const int r_hi = min(p.h, (b.o1 - 1) * p.sh - p.ph + (p.kh - 1) * p.dh + 1);
+    b.n = max(0, r_hi - b.r_lo) * p.w;
+    return b;
+}
+
+template <class R>
+__device__ __forceinline__ const R* band_src(const MPParams& p, const Band& b) {
+    return static_cast<const R*>(p.x) + b.plane * p.h * p.w + (int64_t)b.r_lo * p.w;
+}
+
+// Scan the band's windows from LDS and write its outputs.  K > 0: a K x K
+// window known at compile time, so the loops unroll and the K*K LDS reads
+// of an output issue together.
+template <class T, int K, class R>
+__device__ __forceinline__ void band_outputs(const MPParams& p, const Band& b, const R* tile) {
+    const int outs = (b.o1 - b.o0) * p.ow;
+    R* dst = static_cast<R*>(p.y) + b.plane * p.oh * p.ow + (int64_t)b.o0 * p.ow;
+    int64_t* idx = p.idx ? p.idx + b.plane * p.oh * p.ow + (int64_t)b.o0 * p.ow : nullptr;
+    // Output q of the band is (o0 + q / ow, q % ow); the quotient is kept
+    // incrementally (q grows by kNT per step) instead of dividing.
+    int i = b.o0 + (int)threadIdx.x / p.ow, j = (int)threadIdx.x - ((int)threadIdx.x / p.ow) * p.ow;
+    const int di = kNT / p.ow, dj = kNT - di * p.ow;
+    for (int q = threadIdx.x; q < outs; q += kNT) {
+        Pick<T> pk;
+        // Positions outside the plane read the tile's first element and
+        // are skipped (the tile always holds at least one row).
+        auto at = [&](int a, int c) {
+            const int r = i * p.sh - p.ph + a * p.dh;
+            const int col = j * p.sw - p.pw + c * p.dw;
+            const bool ok = r >= 0 && r < p.h && col >= 0 && col < p.w;
+            pk.consider_if(ok, tile[ok ? (r - b.r_lo) * p.w + col : 0], r * p.w + col);
+        };
+        if constexpr (K > 0) {
+#pragma unroll
+            for (int a = 0; a < K; ++a)
+#pragma unroll
+                for (int c = 0; c < K; ++c) at(a, c);
+        } else {
+            for (int a = 0; a < p.kh; ++a)
+                for (int c = 0; c < p.kw; ++c) at(a, c);
+        }
+        __builtin_nontemporal_store((R)pk.bits, dst + q);
+        if (idx) __builtin_nontemporal_store((int64_t)pk.at, idx + q);
+        i += di;
+        j += dj;
+        if (j >= p.ow) {
+            j -= p.ow;
+            ++i;
+        }
+    }
+}
+
+// K x K window, stride S in both directions, no dilation: each thread owns a
+// vertical strip of up to kStripRows outputs in one column.  Its K column
+// positions (and whether they are in the plane) are fixed; each input row
+// is reduced to a row pick once, and output i + 1 reuses the K - S row
+// picks it shares with output i.
+constexpr int kStripRows = 4;
+
+// Position of column c inside a staged row: identity, or for stride-2
+// scans the row split into its even columns then its odd columns, so that
+// lanes reading columns 2j-1, 2j, 2j+1 for consecutive j hit consecutive
+// LDS words (no bank conflicts).
+template <int S>
+__device__ __forceinline__ int tile_col(int c, int half) {
+    if constexpr (S == 2) return (c & 1) ? half + (c >> 1) : (c >> 1);
+    else return c;
+}
+
+template <class T, int K, int S, class R>
+__device__ __forceinline__ void band_outputs_strip(const MPParams& p, const Band& b, const R* tile) {
+    const int half = (p.w + 1) >> 1;
+    const int rows = b.o1 - b.o0;
+    const int runs = (rows + kStripRows - 1) / kStripRows;
+    const int tasks = runs * p.ow;
+    R* dst = static_cast<R*>(p.y) + b.plane * p.oh * p.ow;
+    int64_t* idx = p.idx ? p.idx + b.plane * p.oh * p.ow : nullptr;
+    for (int t = threadIdx.x; t < tasks; t += kNT) {
+        const int run = t / p.ow, j = t - run * p.ow;
+        const int i0 = b.o0 + run * kStripRows, i1 = min(b.o1, i0 + kStripRows);
+        int col[K], tcol[K];
+        bool col_ok[K];
+#pragma unroll
+        for (int c = 0; c < K; ++c) {
+            col[c] = j * S - p.pw + c;
+            col_ok[c] = col[c] >= 0 && col[c] < p.w;
+            tcol[c] = tile_col<S>(col_ok[c] ? col[c] : 0, half);  // outside: any in-tile column
+        }
+        // All K reads of a row issue before the fold (rows outside the
+        // plane read the tile's first row and are skipped).
+        auto row_pick = [&](int r) {
+            Pick<T> pk;
+            const bool r_ok = r >= 0 && r < p.h;
+            const R* row = tile + (r_ok ? r - b.r_lo : 0) * p.w;
+            uint32_t raw[K];
+#pragma unroll
+            for (int c = 0; c < K; ++c) raw[c] = row[tcol[c]];
+#pragma unroll
+            for (int c = 0; c < K; ++c) pk.consider_if(r_ok && col_ok[c], raw[c], r * p.w + col[c]);
+            return pk;
+        };
+        Pick<T> rp[K];  // row picks of the current output's K rows
+#pragma unroll
+        for (int a = 0; a < K; ++a) rp[a] = row_pick(i0 * S - p.ph + a);
+        for (int i = i0; i < i1; ++i) {
+            if (i > i0) {
+                if constexpr (S < K) {
+#pragma unroll
+                    for (int a = 0; a < K - S; ++a) rp[a] = rp[a + S];
+#pragma unroll
+                    for (int a = K - S; a < K; ++a) rp[a] = row_pick(i * S - p.ph + a);
+                } else {
+#pragma unroll
+                    for (int a = 0; a < K; ++a) rp[a] = row_pick(i * S - p.ph + a);
+                }
+            }
+            Pick<T> pk = rp[0];
+#pragma unroll
+            for (int a = 1; a < K; ++a) pk = merge(pk, rp[a]);
+            const int64_t o = (int64_t)i * p.ow + j;
+            __builtin_nontemporal_store((R)pk.bits, dst + o);
+            if (idx) __builtin_nontemporal_store((int64_t)pk.at, idx + o);
+        }
+    }
+}
+
+// Vector staging: the span starts on a 16-byte boundary (w and h*w are
+// whole vectors, the base is aligned) and is whole vectors; at most
+// kBandBytes, so kStageVecs 16-byte vectors per thread.
+constexpr int kStageVecs = kBandBytes / 16 / kNT;
+
+template <class R>
+__device__ __forceinline__ void stage_load(const MPParams& p, const Band& b, u32x4 (&r)[kStageVecs]) {
+    const u32x4* s4 = reinterpret_cast<const u32x4*>(band_src<R>(p, b));
+    const int nv = b.n / (16 / (int)sizeof(R));
+#pragma unroll
+    for (int d = 0; d < kStageVecs; ++d) {
+        const int v = threadIdx.x + d * kNT;
+        r[d] = s4[v < nv ? v : 0];
+    }
+}
+
+// Writes the staged vectors into the tile; for S == 2 each row is split
+// into even then odd columns (see tile_col): a vector starts on an even
+// column (w is whole vectors), so its even and odd halves land as two
+// contiguous runs of VEC/2 elements.
+template <class R, int S>
+__device__ __forceinline__ void stage_store(const MPParams& p, const Band& b, const u32x4 (&r)[kStageVecs],
+                                            u32x4* lds) {
+    constexpr int VEC = 16 / (int)sizeof(R);
+    const int nv = b.n / VEC;
+    const int half = p.w >> 1;
+#pragma unroll
+    for (int d = 0; d < kStageVecs; ++d) {
+        const int v = threadIdx.x + d * kNT;
+        if (v < nv) {
+            if constexpr (S == 2) {
+                // Each half is 8 bytes: packed into one 64-bit word and
+                // written with one 8-byte-aligned LDS store (c0 / 2 is a
+                // multiple of VEC / 2, and w / 2 * sizeof(R) of 8).
+                const Lanes<R, VEC> in = __builtin_bit_cast(Lanes<R, VEC>, r[d]);
+                uint64_t ev = 0, od = 0;
+#pragma unroll
+                for (int k = 0; k < VEC / 2; ++k) {
+                    ev |= (uint64_t)in.v[2 * k] << (k * 8 * sizeof(R));
+                    od |= (uint64_t)in.v[2 * k + 1] << (k * 8 * sizeof(R));
+                }
+                const int e = v * VEC, rr = e / p.w, c0 = e - rr * p.w;
+                R* row = reinterpret_cast<R*>(lds) + rr * p.w;
+                *reinterpret_cast<uint64_t*>(row + (c0 >> 1)) = ev;
+                *reinterpret_cast<uint64_t*>(row + half + (c0 >> 1)) = od;
+            } else {
+                lds[v] = r[d];
+            }
+        }
+    }
+}
+
+// S > 0: the strip form above (K x K, stride S, no dilation).
+template <class T, int K, int S, class R>
+__device__ __forceinline__ void band_scan(const MPParams& p, const Band& b, const R* tile) {
+    if constexpr (S > 0) band_outputs_strip<T, K, S>(p, b, tile);
+    else band_outputs<T, K>(p, b, tile);
+}
+
+template <class T, bool VECTOR, int K, int S>
 __global__ __launch_bounds__(kNT) void mp_band(MPParams p) {
     using R = typename Raw<T>::type;
-    constexpr int VEC = 16 / sizeof(R);
     extern __shared__ u32x4 lds_vec[];
     R* tile = reinterpret_cast<R*>(lds_vec);
-    const int64_t plane = blockIdx.x / p.bands;
-    const int band = (int)(blockIdx.x - plane * p.bands);
-    const int o0 = band * p.band_rows;
-    const int o1 = min(p.oh, o0 + p.band_rows);
-    const int r_lo = max(0, o0 * p.sh - p.ph);
-    const int r_hi = min(p.h, (o1 - 1) * p.sh - p.ph + (p.kh - 1) * p.dh + 1);
-    const int n = max(0, r_hi - r_lo) * p.w;
-    const R* src = static_cast<const R*>(p.x) + plane * p.h * p.w + (int64_t)r_lo * p.w;
-
-    // Stage the span; in the vector form every band starts on a 16-byte
-    // boundary (w and h*w are whole vectors, the base is aligned) and the
-    // span is whole vectors.  Four loads in flight per thread.
+    const int64_t items = p.planes * p.bands;
+    int64_t item = blockIdx.x;
+    if (item >= items) return;
+    Band b = band_of(p, item);
     if constexpr (VECTOR) {
-        const u32x4* s4 = reinterpret_cast<const u32x4*>(src);
-        const int nv = n / VEC;
-        for (int v0 = threadIdx.x; v0 < nv; v0 += 4 * kNT) {
-            u32x4 r[4];
-#pragma unroll
-            for (int d = 0; d < 4; ++d) {
-                const int v = v0 + d * kNT;
-                r[d] = s4[v < nv ? v : 0];
+        u32x4 r[kStageVecs];
+        stage_load<R>(p, b, r);
+        while (true) {
+            stage_store<R, S>(p, b, r, lds_vec);
+            __syncthreads();
+            const int64_t next = item + gridDim.x;
+            Band nb = b;
+            if (next < items) {
+                nb = band_of(p, next);
+                stage_load<R>(p, nb, r);  // in flight while this band is scanned
             }
-#pragma unroll
-            for (int d = 0; d < 4; ++d)
-                if (v0 + d * kNT < nv) lds_vec[v0 + d * kNT] = r[d];
+            band_scan<T, K, S>(p, b, tile);
+            if (next >= items) break;
+            __syncthreads();  // the tile is rewritten next
+            item = next;
+            b = nb;
         }
     } else {
-        for (int e = threadIdx.x; e < n; e += kNT) tile[e] = src[e];
-    }
-    __syncthreads();
-
-    const int outs = (o1 - o0) * p.ow;
-    R* dst = static_cast<R*>(p.y) + plane * p.oh * p.ow + (int64_t)o0 * p.ow;
-    for (int q = threadIdx.x; q < outs; q += kNT) {
-        const int i = o0 + q / p.ow, j = q - (q / p.ow) * p.ow;
-        Pick<T> pk;
-        for (int a = 0; a < p.kh; ++a) {
-            const int r = i * p.sh - p.ph + a * p.dh;
-            if (r < 0 || r >= p.h) continue;
-            const R* row = tile + (r - r_lo) * p.w;
-            for (int b = 0; b < p.kw; ++b) {
-                const int col = j * p.sw - p.pw + b * p.dw;
-                if (col < 0 || col >= p.w) continue;
-                pk.consider(row[col], r * p.w + col);
+        while (true) {
+            const R* src = band_src<R>(p, b);
+            const int half = (p.w + 1) >> 1;
+            for (int e = threadIdx.x; e < b.n; e += kNT) {
+                const int rr = e / p.w, c = e - rr * p.w;
+                tile[rr * p.w + tile_col<S>(c, half)] = src[e];
             }
+            __syncthreads();
+            band_scan<T, K, S>(p, b, tile);
+            item += gridDim.x;
+            if (item >= items) break;
+            __syncthreads();
+            b = band_of(p, item);
         }
-        dst[q] = (R)pk.bits;
-        if (p.idx) p.idx[plane * p.oh * p.ow + (int64_t)o0 * p.ow + q] = pk.at;
     }
 }
 
@@ -174,49 +396,76 @@ __global__ __launch_bounds__(kNT) void mp_direct(MPParams p) {
 // --------------------------------------------------------------------------
 // NHWC: thread per (output pixel, VEC channels).  VEC = 16 bytes of
 // channels when c is whole vectors and the bases are aligned, else 1.
-template <class T, int VEC>
+// blockIdx.y is the sample; inside a sample every index fits 32 bits
+// (checked on the host), so the index arithmetic is 32-bit.
+template <class T, int VEC, int K>
 __global__ __launch_bounds__(kNT) void mp_nhwc(MPParams p) {
     using R = typename Raw<T>::type;
-    const int cvs = p.c / VEC;
-    const int64_t t = (int64_t)blockIdx.x * kNT + threadIdx.x;
-    const int64_t total = (int64_t)p.n * p.oh * p.ow * cvs;
-    if (t >= total) return;
-    const int cv = (int)(t % cvs);
-    const int64_t pix = t / cvs;
-    const int j = (int)(pix % p.ow);
-    const int i = (int)((pix / p.ow) % p.oh);
-    const int64_t nn = pix / ((int64_t)p.ow * p.oh);
+    const uint32_t cvs = (uint32_t)p.c / VEC;
+    const uint32_t t = blockIdx.x * kNT + threadIdx.x;
+    if (t >= (uint32_t)p.oh * (uint32_t)p.ow * cvs) return;
+    const uint32_t pix = t / cvs;
+    const int cv = (int)(t - pix * cvs);
+    const int i = (int)(pix / (uint32_t)p.ow);
+    const int j = (int)(pix - (uint32_t)i * (uint32_t)p.ow);
+    const int64_t nn = blockIdx.y;
     const R* xs = static_cast<const R*>(p.x);
     Pick<T> pk[VEC];
-    for (int a = 0; a < p.kh; ++a) {
-        const int r = i * p.sh - p.ph + a * p.dh;
-        if (r < 0 || r >= p.h) continue;
-        for (int b = 0; b < p.kw; ++b) {
-            const int col = j * p.sw - p.pw + b * p.dw;
-            if (col < 0 || col >= p.w) continue;
-            const int64_t e = ((nn * p.h + r) * p.w + col) * p.c + (int64_t)cv * VEC;
-            Lanes<R, VEC> v;
-            if constexpr (VEC == 1) {
-                v.v[0] = xs[e];
-            } else {
-                v = __builtin_bit_cast(Lanes<R, VEC>, *reinterpret_cast<const u32x4*>(xs + e));
+    auto load = [&](int r, int col) {
+        const int64_t e = ((nn * p.h + r) * p.w + col) * p.c + (int64_t)cv * VEC;
+        Lanes<R, VEC> v;
+        if constexpr (VEC == 1) v.v[0] = xs[e];
+        else v = __builtin_bit_cast(Lanes<R, VEC>, *reinterpret_cast<const u32x4*>(xs + e));
+        return v;
+    };
+    if constexpr (K > 0) {
+        // Every window position is loaded first (positions outside the
+        // plane from a clamped in-plane address, then skipped), so all K*K
+        // loads are in flight together.
+        Lanes<R, VEC> v[K * K];
+#pragma unroll
+        for (int a = 0; a < K; ++a)
+#pragma unroll
+            for (int c = 0; c < K; ++c) {
+                const int r = min(max(i * p.sh - p.ph + a * p.dh, 0), p.h - 1);
+                const int col = min(max(j * p.sw - p.pw + c * p.dw, 0), p.w - 1);
+                v[a * K + c] = load(r, col);
             }
 #pragma unroll
-            for (int k = 0; k < VEC; ++k) pk[k].consider(v.v[k], r * p.w + col);
+        for (int a = 0; a < K; ++a)
+#pragma unroll
+            for (int c = 0; c < K; ++c) {
+                const int r = i * p.sh - p.ph + a * p.dh;
+                const int col = j * p.sw - p.pw + c * p.dw;
+                const bool ok = r >= 0 && r < p.h && col >= 0 && col < p.w;
+#pragma unroll
+                for (int k = 0; k < VEC; ++k) pk[k].consider_if(ok, v[a * K + c].v[k], r * p.w + col);
+            }
+    } else {
+        for (int a = 0; a < p.kh; ++a) {
+            const int r = i * p.sh - p.ph + a * p.dh;
+            if (r < 0 || r >= p.h) continue;
+            for (int c = 0; c < p.kw; ++c) {
+                const int col = j * p.sw - p.pw + c * p.dw;
+                if (col < 0 || col >= p.w) continue;
+                const Lanes<R, VEC> v = load(r, col);
+#pragma unroll
+                for (int k = 0; k < VEC; ++k) pk[k].consider(v.v[k], r * p.w + col);
+            }
         }
     }
-    const int64_t o = pix * p.c + (int64_t)cv * VEC;
+    const int64_t o = (nn * p.oh * p.ow + pix) * p.c + (int64_t)cv * VEC;
     Lanes<R, VEC> out;
 #pragma unroll
     for (int k = 0; k < VEC; ++k) out.v[k] = (R)pk[k].bits;
     if constexpr (VEC == 1) {
-        static_cast<R*>(p.y)[o] = out.v[0];
+        __builtin_nontemporal_store(out.v[0], static_cast<R*>(p.y) + o);
     } else {
-        *reinterpret_cast<u32x4*>(static_cast<R*>(p.y) + o) = __builtin_bit_cast(u32x4, out);
+        __builtin_nontemporal_store(__builtin_bit_cast(u32x4, out), reinterpret_cast<u32x4*>(static_cast<R*>(p.y) + o));
     }
     if (p.idx) {
 #pragma unroll
-        for (int k = 0; k < VEC; ++k) p.idx[o + k] = pk[k].at;
+        for (int k = 0; k < VEC; ++k) __builtin_nontemporal_store((int64_t)pk[k].at, p.idx + o + k);
     }
 }
 
@@ -248,18 +497,25 @@ kf_status run(const MaxPoolArgs& a, hipStream_t s, const char** variant) {
     p.band_rows = p.bands = 1;
     if (a.nhwc) {
         const bool vec = a.c % VEC == 0 && (uintptr_t)a.x % 16 == 0 && (uintptr_t)a.y % 16 == 0;
-        const int64_t threads = a.n * a.oh * a.ow * (vec ? a.c / VEC : a.c);
-        const int64_t blocks = (threads + kNT - 1) / kNT;
-        if (blocks > INT32_MAX) {
-            set_error("max_pool2d: grid of %lld workgroups exceeds the launch limit", (long long)blocks);
+        const int64_t per_sample = a.oh * a.ow * (vec ? a.c / VEC : a.c);
+        if (per_sample > INT32_MAX || a.n > 65535) {
+            set_error("max_pool2d: %lld threads per sample or %lld samples exceed the channels-last grid",
+                      (long long)per_sample, (long long)a.n);
             return KF_ERR_UNSUPPORTED_LAYOUT;
         }
+        const dim3 grid((unsigned)((per_sample + kNT - 1) / kNT), (unsigned)a.n);
+        const int k = (a.kh == a.kw && (a.kh == 2 || a.kh == 3)) ? a.kh : 0;
+        auto go = [&](auto kernel) { hipLaunchKernelGGL(kernel, grid, dim3(kNT), 0, s, p); };
         if (vec) {
-            hipLaunchKernelGGL((mp_nhwc<T, VEC>), dim3((unsigned)blocks), dim3(kNT), 0, s, p);
-            *variant = "mp_nhwc_vec";
+            if (k == 3) go(mp_nhwc<T, VEC, 3>);
+            else if (k == 2) go(mp_nhwc<T, VEC, 2>);
+            else go(mp_nhwc<T, VEC, 0>);
+            *variant = k == 3 ? "mp_nhwc_vec_k3" : k == 2 ? "mp_nhwc_vec_k2" : "mp_nhwc_vec";
         } else {
-            hipLaunchKernelGGL((mp_nhwc<T, 1>), dim3((unsigned)blocks), dim3(kNT), 0, s, p);
-            *variant = "mp_nhwc_scalar";
+            if (k == 3) go(mp_nhwc<T, 1, 3>);
+            else if (k == 2) go(mp_nhwc<T, 1, 2>);
+            else go(mp_nhwc<T, 1, 0>);
+            *variant = k == 3 ? "mp_nhwc_scalar_k3" : k == 2 ? "mp_nhwc_scalar_k2" : "mp_nhwc_scalar";
         }
     } else {
         // Output rows per band: as many as keep the band's input rows within
@@ -274,21 +530,39 @@ kf_status run(const MaxPoolArgs& a, hipStream_t s, const char** variant) {
             br = (a.oh + bands - 1) / bands;
             p.band_rows = (int32_t)br;
             p.bands = (int32_t)bands;
-            const int64_t grid = p.planes * bands;
-            if (grid > INT32_MAX) {
-                set_error("max_pool2d: grid of %lld workgroups exceeds the launch limit", (long long)grid);
-                return KF_ERR_UNSUPPORTED_LAYOUT;
-            }
+            // Persistent workgroups: enough to fill every CU several times
+            // over (each walks items with stride gridDim.x).
+            const int64_t items = p.planes * bands;
+            const int64_t grid = items < kBandGroups ? items : kBandGroups;
             const int64_t in_rows = (br - 1) * a.sh + eff;
             const size_t lds = (size_t)(((in_rows * row_bytes) + 15) / 16 * 16);
             const bool vec = a.w % VEC == 0 && (a.h * a.w) % VEC == 0 && (uintptr_t)a.x % 16 == 0;
-            if (vec) {
-                hipLaunchKernelGGL((mp_band<T, true>), dim3((unsigned)grid), dim3(kNT), lds, s, p);
-                *variant = "mp_band_vec";
-            } else {
-                hipLaunchKernelGGL((mp_band<T, false>), dim3((unsigned)grid), dim3(kNT), lds, s, p);
-                *variant = "mp_band_scalar";
-            }
+            // Compile-time forms: square 3x3 / 2x2 windows (unrolled scan);
+            // with equal strides 1 or 2 and no dilation, the strip scan.
+            const int k = (a.kh == a.kw && (a.kh == 2 || a.kh == 3)) ? a.kh : 0;
+            const bool strip = k != 0 && a.sh == a.sw && a.dh == 1 && a.dw == 1 &&
+                               ((k == 3 && (a.sh == 1 || a.sh == 2)) || (k == 2 && a.sh == 2));
+            const int sv = strip ? a.sh : 0;
+            auto go = [&](auto kernel) { hipLaunchKernelGGL(kernel, dim3((unsigned)grid), dim3(kNT), lds, s, p); };
+            auto pick = [&](auto vec_tag) {
+                constexpr bool V = decltype(vec_tag)::value;
+                if (k == 3 && sv == 2) go(mp_band<T, V, 3, 2>);
+                else if (k == 3 && sv == 1) go(mp_band<T, V, 3, 1>);
+                else if (k == 2 && sv == 2) go(mp_band<T, V, 2, 2>);
+                else if (k == 3) go(mp_band<T, V, 3, 0>);
+                else if (k == 2) go(mp_band<T, V, 2, 0>);
+                else go(mp_band<T, V, 0, 0>);
+            };
+            if (vec) pick(std::true_type{});
+            else pick(std::false_type{});
+            static const char* names[2][3][3] = {
+                {{"mp_band_scalar", "mp_band_scalar", "mp_band_scalar"},
+                 {"mp_band_scalar_k2", "mp_band_scalar_k2", "mp_band_scalar_k2_strip_s2"},
+                 {"mp_band_scalar_k3", "mp_band_scalar_k3_strip_s1", "mp_band_scalar_k3_strip_s2"}},
+                {{"mp_band_vec", "mp_band_vec", "mp_band_vec"},
+                 {"mp_band_vec_k2", "mp_band_vec_k2", "mp_band_vec_k2_strip_s2"},
+                 {"mp_band_vec_k3", "mp_band_vec_k3_strip_s1", "mp_band_vec_k3_strip_s2"}}};
+            *variant = names[vec ? 1 : 0][k == 0 ? 0 : k - 1][sv];
         } else {
             const int64_t blocks = (p.planes * a.oh * a.ow + kNT - 1) / kNT;
             if (blocks > INT32_MAX) {
