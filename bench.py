@@ -185,6 +185,32 @@ def decode_row(torch, dev, kf355, W, steps, warmup, sets_for):
             "vs_torch_eager": round(out["eager"]["graph_us"] / g_us, 3), "graph_output_matches": same}
 
 
+def maxpool_row(torch, F, dev, kf355, W, steps, warmup, sets_for):
+    """ResNet-50 stem max pooling, fp32 [32,64,112,112] 3x3 / 2 / 1 ->
+    [32,64,56,56], NCHW and channels last, libkf355 against torch eager on
+    the same rotating buffer sets (launched back to back)."""
+    w = W.maxpool_resnet_stem_f32()
+    src = w["x"].to(dev)
+    out_shape = (src.shape[0], src.shape[1], 56, 56)
+    nb = src.numel() * 4 + src.shape[0] * src.shape[1] * 56 * 56 * 4
+    row = {"workload": "fp32 [32,64,112,112] kernel 3 stride 2 padding 1 (ResNet-50 stem)", "algorithmic_bytes": nb}
+    for layout, fmt in (("nchw", torch.contiguous_format), ("channels_last", torch.channels_last)):
+        xs = [src.contiguous(memory_format=fmt).clone(memory_format=fmt) for _ in range(sets_for(nb))]
+        ys = [torch.empty(out_shape, device=dev, memory_format=fmt) for _ in xs]
+        fns = [kf355.prepare_max_pool2d(x, y, 3, 2, 1) for x, y in zip(xs, ys)]
+        fns[0]()
+        variant = kf355.last_variant()
+        us = time_launches(torch, fns, steps, warmup)
+        eager_us = time_launches(torch, [lambda x=x: F.max_pool2d(x, 3, 2, 1) for x in xs], min(steps, 50), warmup)
+        gbs = nb / (us * 1e-6) / 1e9
+        row[layout] = {"variant": variant, "us_per_call": round(us, 3), "gbps": round(gbs, 1),
+                       "frac_of_peak": round(gbs / PEAK_HBM_GBS, 4), "torch_eager_us": round(eager_us, 3),
+                       "kf355_speedup": round(eager_us / us, 3), "buffer_sets": len(xs)}
+        del xs, ys, fns
+        torch.cuda.empty_cache()
+    return row
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -192,7 +218,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-eager", action="store_true")
-    ap.add_argument("--no-next", action="store_true", help="skip the next-row measurements (fused causal softmax, layer_norm, decode split softmax)")
+    ap.add_argument("--no-next", action="store_true", help="skip the next-row measurements (fused causal softmax, layer_norm, decode split softmax, max_pool2d)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: the operators shard by rows / groups / planes with no exchange, "
@@ -369,6 +395,7 @@ def main():
 
         next_rows["softmax_decode_split"] = decode_row(torch, dev, kf355, W, args.steps, args.warmup,
                                                        sets_for)
+        next_rows["max_pool2d_stem"] = maxpool_row(torch, F, dev, kf355, W, args.steps, args.warmup, sets_for)
 
     calib = copy_calibration(torch, dev, nbytes["softmax"])
     sm = per_op["softmax"]

@@ -16,7 +16,8 @@ Section III-A).  This module applies that policy to libkf355:
   take the recorded path.
 * `install()` / `uninstall()` (or the `installed()` context manager) route
   `torch.softmax`, `torch.Tensor.softmax`, `F.softmax`, `F.layer_norm`,
-  `F.group_norm` and `F.adaptive_avg_pool2d` through a dispatcher for CUDA
+  `F.group_norm`, `F.adaptive_avg_pool2d` and `F.max_pool2d` through a
+  dispatcher for CUDA
   tensors in inference (no autograd); anything else goes straight to the
   original function.
 * `save()` / `load()` write and read the decisions as JSON, the package a
@@ -70,13 +71,22 @@ class Decision:
         return f"{self.backend} ({self.reason})"
 
 
-def agree(y_kf: torch.Tensor, y_ref: torch.Tensor) -> tuple[bool, float]:
+def agree(y_kf, y_ref) -> tuple[bool, float]:
     """(every element within TOLERANCES of the eager result, max |difference|).
-    NaN must sit at the same positions on both sides; infinities must match."""
+    NaN must sit at the same positions on both sides; infinities must match.
+    Integer outputs (pooling indices) must be equal; tuples agree element by
+    element."""
+    if isinstance(y_ref, (tuple, list)):
+        if not isinstance(y_kf, (tuple, list)) or len(y_kf) != len(y_ref):
+            return False, float("inf")
+        results = [agree(a, b) for a, b in zip(y_kf, y_ref)]
+        return all(ok for ok, _ in results), max((d for _, d in results), default=0.0)
     if y_kf.shape != y_ref.shape or y_kf.dtype != y_ref.dtype:
         return False, float("inf")
     if y_ref.numel() == 0:
         return True, 0.0
+    if not y_ref.dtype.is_floating_point:
+        return bool(torch.equal(y_kf, y_ref)), float((y_kf.double() - y_ref.double()).abs().max().item())
     rtol, stol = TOLERANCES.get(y_ref.dtype, (1e-5, 1e-6))
     a, b = y_kf.double(), y_ref.double()
     nan_a, nan_b = torch.isnan(a), torch.isnan(b)
@@ -250,6 +260,20 @@ def _f_adaptive_avg_pool2d(input, output_size):
                         lambda: orig(input, output_size))
 
 
+def _f_max_pool2d(input, kernel_size, stride=None, padding=0, dilation=1, ceil_mode=False, return_indices=False):
+    orig = _ORIG["F.max_pool2d"]
+    args = (input, kernel_size, stride, padding, dilation)
+    if not _eligible(input) or input.dim() not in (3, 4):
+        return orig(*args, ceil_mode=ceil_mode, return_indices=return_indices)
+    norm = lambda v: tuple(v) if isinstance(v, (tuple, list)) else v  # noqa: E731
+    st = None if stride is None or (isinstance(stride, (tuple, list)) and len(stride) == 0) else norm(stride)
+    return _ACTIVE.call("max_pool2d", (input, norm(kernel_size), st, norm(padding), norm(dilation), bool(ceil_mode),
+                                       bool(return_indices)),
+                        lambda: kf355.kf_max_pool2d(input, kernel_size, st, padding, dilation, ceil_mode,
+                                                    return_indices),
+                        lambda: orig(*args, ceil_mode=ceil_mode, return_indices=return_indices))
+
+
 def install(dispatcher: GuardedDispatcher | None = None) -> GuardedDispatcher:
     """Route the supported PyTorch operators through `dispatcher` (a new one
     by default).  Raises if libkf355 is not built."""
@@ -260,13 +284,14 @@ def install(dispatcher: GuardedDispatcher | None = None) -> GuardedDispatcher:
     _ACTIVE = dispatcher or GuardedDispatcher()
     _ORIG.update({"torch.softmax": torch.softmax, "Tensor.softmax": torch.Tensor.softmax,
                   "F.softmax": F.softmax, "F.layer_norm": F.layer_norm, "F.group_norm": F.group_norm,
-                  "F.adaptive_avg_pool2d": F.adaptive_avg_pool2d})
+                  "F.adaptive_avg_pool2d": F.adaptive_avg_pool2d, "F.max_pool2d": F.max_pool2d})
     torch.softmax = _torch_softmax
     torch.Tensor.softmax = _tensor_softmax
     F.softmax = _f_softmax
     F.layer_norm = _f_layer_norm
     F.group_norm = _f_group_norm
     F.adaptive_avg_pool2d = _f_adaptive_avg_pool2d
+    F.max_pool2d = _f_max_pool2d
     return _ACTIVE
 
 
@@ -280,6 +305,7 @@ def uninstall():
     F.layer_norm = _ORIG["F.layer_norm"]
     F.group_norm = _ORIG["F.group_norm"]
     F.adaptive_avg_pool2d = _ORIG["F.adaptive_avg_pool2d"]
+    F.max_pool2d = _ORIG["F.max_pool2d"]
     _ORIG.clear()
     _ACTIVE = None
 

@@ -114,7 +114,8 @@ def test_variant_key_distinguishes_layouts_and_arguments():
 def test_install_restores_and_passes_cpu_tensors_through():
     if not os.path.exists(kf355.LIB_PATH):
         pytest.skip("libkf355.so not built")
-    originals = (torch.softmax, torch.Tensor.softmax, F.softmax, F.layer_norm, F.group_norm, F.adaptive_avg_pool2d)
+    originals = (torch.softmax, torch.Tensor.softmax, F.softmax, F.layer_norm, F.group_norm, F.adaptive_avg_pool2d,
+                 F.max_pool2d)
     x = torch.randn(2, 8, 4, 4)
     with dispatch.installed() as d:
         assert torch.softmax is not originals[0]
@@ -124,9 +125,12 @@ def test_install_restores_and_passes_cpu_tensors_through():
         assert torch.equal(F.group_norm(x, 2), originals[4](x, 2))
         assert torch.equal(F.layer_norm(x, (4,)), originals[3](x, (4,)))
         assert torch.equal(F.adaptive_avg_pool2d(x, 1), originals[5](x, 1))
+        y, i = F.max_pool2d(x, 2, return_indices=True)
+        ty, ti = originals[6](x, 2, return_indices=True)
+        assert torch.equal(y, ty) and torch.equal(i, ti)
         assert d.decisions == {}
     assert (torch.softmax, torch.Tensor.softmax, F.softmax, F.layer_norm, F.group_norm,
-            F.adaptive_avg_pool2d) == originals
+            F.adaptive_avg_pool2d, F.max_pool2d) == originals
 
 
 def test_agree_scales_with_the_output_and_checks_specials():
@@ -144,3 +148,12 @@ def test_agree_scales_with_the_output_and_checks_specials():
     assert not dispatch.agree(torch.zeros(2), torch.zeros(3))[0]
     assert not dispatch.agree(torch.zeros(2), torch.zeros(2, dtype=torch.float64))[0]
     assert dispatch.agree(torch.zeros(0), torch.zeros(0))[0]
+
+
+def test_agree_on_tuples_and_integer_outputs():
+    y = torch.tensor([1.0, 2.0])
+    i = torch.tensor([3, 4])
+    assert dispatch.agree((y, i), (y.clone(), i.clone()))[0]
+    assert not dispatch.agree((y, i), (y, torch.tensor([3, 5])))[0]     # indices must be equal
+    assert not dispatch.agree((y,), (y, i))[0]
+    assert not dispatch.agree(y, (y, i))[0]

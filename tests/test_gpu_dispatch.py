@@ -36,7 +36,8 @@ def net(x, t, gw, gb):
     p = torch.softmax(s, dim=-1)
     q = s.softmax(-1)
     r = F.softmax(s.bfloat16(), dim=-1, dtype=torch.float32)
-    return h, pooled, u, p, q, r
+    m, mi = F.max_pool2d(x, 3, 2, 1, return_indices=True)
+    return h, pooled, u, p, q, r, m, mi
 
 
 def inputs():
@@ -64,7 +65,7 @@ def test_network_matches_eager_and_labels_every_variant(measure):
         check_close(a, c)
         check_close(b, c)
     ops = sorted(r["op"] for r in d.report())
-    assert ops == ["adaptive_avg_pool2d", "group_norm", "layer_norm", "softmax", "softmax"], ops
+    assert ops == ["adaptive_avg_pool2d", "group_norm", "layer_norm", "max_pool2d", "softmax", "softmax"], ops
     for r in d.report():
         assert r["backend"] in ("kf355", "eager") and r["label"].startswith(r["backend"])
         assert not r["reason"].startswith(("invalid", "unsupported")), r
