@@ -211,6 +211,25 @@ def maxpool_row(torch, F, dev, kf355, W, steps, warmup, sets_for):
     return row
 
 
+def avgpool_cl_row(torch, F, dev, kf355, W, steps, warmup, sets_for):
+    """The ResNet-50 head pooling on a channels-last tensor: fp32
+    [32,2048,7,7] -> 1x1, libkf355 against torch eager, rotating sets."""
+    src = W.avgpool_resnet_head_f32()["x"].to(dev).contiguous(memory_format=torch.channels_last)
+    nb = src.numel() * 4 + src.shape[0] * src.shape[1] * 4
+    xs = [src.clone(memory_format=torch.channels_last) for _ in range(sets_for(nb))]
+    ys = [torch.empty(src.shape[0], src.shape[1], 1, 1, device=dev, memory_format=torch.channels_last) for _ in xs]
+    fns = [kf355.prepare_adaptive_avgpool2d(x, y) for x, y in zip(xs, ys)]
+    fns[0]()
+    variant = kf355.last_variant()
+    us = time_launches(torch, fns, steps, warmup)
+    eager_us = time_launches(torch, [lambda x=x: F.adaptive_avg_pool2d(x, 1) for x in xs], min(steps, 50), warmup)
+    gbs = nb / (us * 1e-6) / 1e9
+    return {"workload": "fp32 [32,2048,7,7] channels last -> 1x1 (ResNet-50 head)", "variant": variant,
+            "algorithmic_bytes": nb, "us_per_call": round(us, 3), "gbps": round(gbs, 1),
+            "frac_of_peak": round(gbs / PEAK_HBM_GBS, 4), "torch_eager_us": round(eager_us, 3),
+            "kf355_speedup": round(eager_us / us, 3), "buffer_sets": len(xs)}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -396,6 +415,8 @@ def main():
         next_rows["softmax_decode_split"] = decode_row(torch, dev, kf355, W, args.steps, args.warmup,
                                                        sets_for)
         next_rows["max_pool2d_stem"] = maxpool_row(torch, F, dev, kf355, W, args.steps, args.warmup, sets_for)
+        next_rows["avgpool_channels_last"] = avgpool_cl_row(torch, F, dev, kf355, W, args.steps, args.warmup,
+                                                            sets_for)
 
     calib = copy_calibration(torch, dev, nbytes["softmax"])
     sm = per_op["softmax"]

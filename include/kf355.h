@@ -215,12 +215,14 @@ kf_status kf_layer_norm(const void* x, kf_dtype x_dtype, void* y, int32_t ndim, 
  * [floor(j*W/out_w), ceil((j+1)*W/out_w)).
  *
  *  x        device pointer, shape [N, C, H, W] or [C, H, W] with H, W >= 1,
- *           dtype FLOAT32, BFLOAT16 or FLOAT16 (fp32 accumulation).
+ *           dtype FLOAT32, BFLOAT16 or FLOAT16 (fp32 accumulation); dense
+ *           NCHW, or (4-D) dense channels last (memory order N, H, W, C).
  *  out_h,   >= 1 each (may exceed H, W, as in PyTorch).
  *  out_w
  *  y        device pointer, shape [N, C, out_h, out_w] (or [C, out_h,
- *           out_w]), x's dtype; y_strides describe that shape.  y must not
- *           overlap x.
+ *           out_w]), x's dtype, dense in x's layout; y_strides describe
+ *           it.  y must not overlap x.  Other layouts:
+ *           KF_ERR_UNSUPPORTED_LAYOUT.
  */
 kf_status kf_adaptive_avgpool2d(const void* x, kf_dtype dtype, void* y, int32_t ndim, const int64_t* shape,
                                 const int64_t* x_strides, const int64_t* y_strides, int64_t out_h,

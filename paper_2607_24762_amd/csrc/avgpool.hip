@@ -12,6 +12,11 @@
 //   ap_plane  1x1 output for large planes: one workgroup per plane reads it
 //             with coalesced loads and reduces in registers.
 //   ap_window any output size: one thread per output cell.
+//   ap_nhwc   channels last, any output size: a workgroup owns one output
+//             cell of one sample and 64 vectors of 16 bytes of channels;
+//             its four thread groups sum interleaved window pixels, so
+//             every load is a coalesced 1 KiB channel run, and the four
+//             partials are added in group order through LDS.
 #include "kf_device.hpp"
 #include "kf_internal.h"
 
@@ -137,6 +142,72 @@ __global__ __launch_bounds__(kNT) void ap_window(const void* __restrict__ x, voi
     store1<T>(y, idx, sum / (float)((h1 - h0) * (w1 - w0)));
 }
 
+constexpr int kCB = 64;         // channel vectors per ap_nhwc workgroup
+constexpr int kPG = kNT / kCB;  // pixel groups per workgroup
+
+template <class T, int VEC>
+__global__ __launch_bounds__(kNT) void ap_nhwc(const void* __restrict__ x, void* __restrict__ y, int32_t H,
+                                               int32_t W, int32_t C, int32_t OH, int32_t OW) {
+    __shared__ float part[kPG - 1][kCB][VEC];
+    const int lc = threadIdx.x % kCB, g = threadIdx.x / kCB;
+    const int cv = blockIdx.x * kCB + lc;
+    const bool active = cv < C / VEC;
+    const int i = blockIdx.y / OW, j = blockIdx.y - (blockIdx.y / OW) * OW;
+    const int64_t n = blockIdx.z;
+    const int h0 = (int)(((int64_t)i * H) / OH), h1 = (int)((((int64_t)i + 1) * H + OH - 1) / OH);
+    const int w0 = (int)(((int64_t)j * W) / OW), w1 = (int)((((int64_t)j + 1) * W + OW - 1) / OW);
+    const int ww = w1 - w0, count = (h1 - h0) * ww;
+    const int64_t base = n * H * W * (int64_t)C + (int64_t)cv * VEC;
+    auto at = [&](int q) {
+        const int r = h0 + q / ww, c = w0 + (q - (q / ww) * ww);
+        return base + ((int64_t)r * W + c) * C;
+    };
+    float acc[VEC];
+#pragma unroll
+    for (int k = 0; k < VEC; ++k) acc[k] = 0.f;
+    if (active) {
+        // Window pixels g, g + 4, ... in order, DEPTH loads in flight (64
+        // floats of registers: a 7x7 window's 13 pixels per group go out
+        // in one or two batches); a slot past the window re-reads the
+        // first pixel and is not added.
+        constexpr int DEPTH = 64 / VEC < 16 ? 64 / VEC : 16;
+        for (int q0 = g; q0 < count; q0 += DEPTH * kPG) {
+            float v[DEPTH][VEC];
+#pragma unroll
+            for (int d = 0; d < DEPTH; ++d) {
+                const int q = q0 + d * kPG;
+                const int64_t e = at(q < count ? q : 0);
+                if constexpr (VEC > 1) load_vec<T>(x, e, v[d]);
+                else v[d][0] = load1<T>(x, e);
+            }
+#pragma unroll
+            for (int d = 0; d < DEPTH; ++d)
+                if (q0 + d * kPG < count) {
+#pragma unroll
+                    for (int k = 0; k < VEC; ++k) acc[k] += v[d][k];
+                }
+        }
+    }
+    if (g > 0) {
+#pragma unroll
+        for (int k = 0; k < VEC; ++k) part[g - 1][lc][k] = acc[k];
+    }
+    __syncthreads();
+    if (g == 0 && active) {
+        const float cnt = (float)count;
+#pragma unroll
+        for (int k = 0; k < VEC; ++k) {
+            float s = acc[k];
+#pragma unroll
+            for (int gg = 0; gg < kPG - 1; ++gg) s += part[gg][lc][k];
+            acc[k] = s / cnt;
+        }
+        const int64_t o = ((n * OH + i) * OW + j) * (int64_t)C + (int64_t)cv * VEC;
+        if constexpr (VEC > 1) store_vec<T, false>(y, o, acc);
+        else store1<T>(y, o, acc[0]);
+    }
+}
+
 template <class T, int TPS>
 void launch_flat(const AvgPoolArgs& a, hipStream_t s, const char** variant, const char* name) {
     constexpr int P = kNT / TPS;
@@ -157,7 +228,24 @@ void launch_flat(const AvgPoolArgs& a, hipStream_t s, const char** variant, cons
 template <class T>
 kf_status run(const AvgPoolArgs& a, hipStream_t s, const char** variant) {
     const int64_t S = a.h * a.w;
-    if (a.oh == 1 && a.ow == 1) {
+    if (a.nhwc) {
+        const bool vec = a.c % T::vec == 0 && (uintptr_t)a.x % 16 == 0 && (uintptr_t)a.y % 16 == 0;
+        const int64_t cvs = vec ? a.c / T::vec : a.c;
+        const int64_t gx = (cvs + kCB - 1) / kCB, gy = a.oh * a.ow;
+        if (gx > INT32_MAX || gy > INT32_MAX || a.n > 65535 || a.h * a.w * a.c > INT64_MAX / 2 ||
+            a.h > INT32_MAX || a.w > INT32_MAX || a.c > INT32_MAX) {
+            set_error("adaptive_avgpool2d: channels-last problem exceeds the grid limits");
+            return KF_ERR_UNSUPPORTED_LAYOUT;
+        }
+        const dim3 grid((unsigned)gx, (unsigned)gy, (unsigned)a.n);
+        if (vec)
+            hipLaunchKernelGGL((ap_nhwc<T, T::vec>), grid, dim3(kNT), 0, s, a.x, a.y, (int32_t)a.h, (int32_t)a.w,
+                               (int32_t)a.c, (int32_t)a.oh, (int32_t)a.ow);
+        else
+            hipLaunchKernelGGL((ap_nhwc<T, 1>), grid, dim3(kNT), 0, s, a.x, a.y, (int32_t)a.h, (int32_t)a.w,
+                               (int32_t)a.c, (int32_t)a.oh, (int32_t)a.ow);
+        *variant = vec ? "ap_nhwc_vec" : "ap_nhwc_scalar";
+    } else if (a.oh == 1 && a.ow == 1) {
         // Planes per workgroup: the largest power of two (<= 256) whose span
         // fits the staging tile; a plane too big for it gets a workgroup.
         int64_t P = 256;

@@ -404,11 +404,20 @@ kf_status kf_adaptive_avgpool2d(const void* x, kf_dtype dtype, void* y, int32_t 
     if (!x || !y) return fail(KF_ERR_NULL_POINTER, "x or y is NULL");
     const int64_t eb = elem_bytes(dtype);
     if ((uintptr_t)x % eb || (uintptr_t)y % eb) return fail(KF_ERR_BAD_ARG, "x or y is not element aligned");
-    if (!dense(ndim, shape, x_strides) || !dense(ndim, yshape, y_strides))
-        return fail(KF_ERR_UNSUPPORTED_LAYOUT, "only dense row-major (NCHW) tensors are supported");
+    bool nhwc = false;
+    if (dense(ndim, shape, x_strides)) {
+        if (!dense(ndim, yshape, y_strides))
+            return fail(KF_ERR_UNSUPPORTED_LAYOUT, "y must be dense in x's layout (NCHW)");
+    } else if (ndim == 4 && dense_nhwc(shape, x_strides)) {
+        if (!dense_nhwc(yshape, y_strides))
+            return fail(KF_ERR_UNSUPPORTED_LAYOUT, "y must be dense in x's layout (channels last)");
+        nhwc = true;
+    } else {
+        return fail(KF_ERR_UNSUPPORTED_LAYOUT, "x must be dense NCHW or dense channels last");
+    }
     if (overlaps(x, n * eb, y, ny * eb)) return fail(KF_ERR_BAD_ARG, "x and y overlap");
 
-    AvgPoolArgs a{x, y, dtype, n / (H * W), H, W, out_h, out_w};
+    AvgPoolArgs a{x, y, dtype, n / (H * W), H, W, out_h, out_w, nhwc, ndim == 4 ? shape[0] : 1, shape[ndim - 3]};
     const char* variant = nullptr;
     s = avgpool_launch(a, static_cast<hipStream_t>(stream), &variant);
     return done(s, variant);

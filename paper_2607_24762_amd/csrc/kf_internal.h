@@ -67,12 +67,16 @@ struct LayerNormArgs {
 };
 kf_status layer_norm_launch(const LayerNormArgs& a, hipStream_t s, const char** variant);
 
-// adaptive_avg_pool2d over a dense [planes, h, w] view -> [planes, oh, ow].
+// adaptive_avg_pool2d over a dense [planes, h, w] view -> [planes, oh, ow]
+// (NCHW), or with nhwc over x [n, h, w, c] -> y [n, oh, ow, c] (channels
+// last; planes = n * c).
 struct AvgPoolArgs {
     const void* x;
     void* y;
     kf_dtype t;
     int64_t planes, h, w, oh, ow;
+    bool nhwc;
+    int64_t n, c;
 };
 kf_status avgpool_launch(const AvgPoolArgs& a, hipStream_t s, const char** variant);
 

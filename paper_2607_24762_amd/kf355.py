@@ -256,7 +256,10 @@ def kf_adaptive_avgpool2d(x: torch.Tensor, output_size, out: torch.Tensor | None
     """adaptive_avg_pool2d(x, output_size) through kf_adaptive_avgpool2d."""
     _need_cuda(x)
     oh, ow = (output_size, output_size) if isinstance(output_size, int) else output_size
-    y = out if out is not None else torch.empty(tuple(x.shape[:-2]) + (oh, ow), dtype=x.dtype, device=x.device)
+    fmt = torch.channels_last if (x.dim() == 4 and not x.is_contiguous()
+                                  and x.is_contiguous(memory_format=torch.channels_last)) else torch.contiguous_format
+    y = out if out is not None else torch.empty(tuple(x.shape[:-2]) + (oh, ow), dtype=x.dtype, device=x.device,
+                                                memory_format=fmt)
     shape, _s = _arr(list(x.shape))
     xs, _a = _arr(list(x.stride()))
     ys, _b = _arr(list(y.stride()))

@@ -238,7 +238,8 @@ def test_avgpool_rejections(lib):
     assert ap(lib, shape=(2, 3, 0, 7)) == SHAPE
     assert ap(lib, oh=0) == ARG
     assert ap(lib, y=FAKE + 64) == ARG                    # overlaps x
-    assert ap(lib, xs=(147, 1, 21, 3)) == LAYOUT          # channels-last
+    assert ap(lib, xs=(147, 1, 21, 3)) == LAYOUT          # channels-last x, NCHW y
+    assert ap(lib, xs=(147, 49, 1, 7)) == LAYOUT          # neither layout
     assert ap(lib, xt=5) == DTYPE
     assert ap(lib, x=0) == NULLP
 

@@ -85,3 +85,34 @@ def test_constant_input_is_exact():
     y = kf355.kf_adaptive_avgpool2d(x, 1)
     torch.cuda.synchronize()
     assert (y == 0.375).all()
+
+
+CHANNELS_LAST = [
+    ((32, 2048, 7, 7), 1),          # the ResNet-50 head, channels last
+    ((2, 64, 14, 14), 7),           # divisible windows
+    ((2, 48, 7, 7), (3, 5)),        # overlapping adaptive windows
+    ((1, 24, 5, 9), (8, 4)),        # output taller than the input
+    ((3, 5, 6, 6), 2),              # channels not whole 16-byte vectors: scalar path
+    ((2, 200, 9, 11), (1, 3)),      # channels beyond one 64-vector block
+]
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16", "f16"])
+@pytest.mark.parametrize("shape,out", CHANNELS_LAST, ids=lambda v: str(v))
+def test_channels_last(shape, out, dt):
+    note(f"avgpool channels last {shape} -> {out} {dt}")
+    x_cpu = relu_input(shape, dt, seed=shape[1])
+    x = x_cpu.cuda().contiguous(memory_format=torch.channels_last)
+    variant = run(x_cpu, out, dt, x_gpu=x)
+    vec = 4 if dt == "f32" else 8
+    assert variant == ("ap_nhwc_vec" if shape[1] % vec == 0 else "ap_nhwc_scalar"), variant
+
+
+def test_channels_last_output_keeps_the_layout():
+    note("avgpool channels last layout")
+    x = relu_input((2, 16, 9, 9), "f32", seed=3).cuda().contiguous(memory_format=torch.channels_last)
+    y = kf355.kf_adaptive_avgpool2d(x, (3, 3))
+    torch.cuda.synchronize()
+    assert y.is_contiguous(memory_format=torch.channels_last)
+    ref = torch.nn.functional.adaptive_avg_pool2d(x, (3, 3))
+    assert torch.allclose(y, ref, atol=1e-6, rtol=0)
