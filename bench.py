@@ -230,6 +230,27 @@ def avgpool_cl_row(torch, F, dev, kf355, W, steps, warmup, sets_for):
             "kf355_speedup": round(eager_us / us, 3), "buffer_sets": len(xs)}
 
 
+def gn_cl_row(torch, F, dev, kf355, W, steps, warmup, sets_for):
+    """The SD3.5 VAE GroupNorm on a channels-last tensor: bf16
+    [1,512,128,128], 32 groups, bf16 affine, libkf355 against torch eager."""
+    gn = W.groupnorm_vae_bf16()
+    src = gn["x"].to(dev).contiguous(memory_format=torch.channels_last)
+    gw, gb = gn["weight"].to(dev), gn["bias"].to(dev)
+    nb = src.numel() * 2 * 2 + 2 * src.shape[1] * 2
+    xs = [src.clone(memory_format=torch.channels_last) for _ in range(sets_for(nb))]
+    fns = [kf355.prepare_group_norm(x, torch.empty_like(x), 32, gw, gb, gn["eps"]) for x in xs]
+    fns[0]()
+    variant = kf355.last_variant()
+    us = time_launches(torch, fns, steps, warmup)
+    eager_us = time_launches(torch, [lambda x=x: F.group_norm(x, 32, gw, gb, gn["eps"]) for x in xs],
+                             min(steps, 50), warmup)
+    gbs = nb / (us * 1e-6) / 1e9
+    return {"workload": "bf16 [1,512,128,128] channels last, 32 groups, affine, eps 1e-6 (SD3.5 VAE)",
+            "variant": variant, "algorithmic_bytes": nb, "us_per_call": round(us, 3), "gbps": round(gbs, 1),
+            "frac_of_peak": round(gbs / PEAK_HBM_GBS, 4), "torch_eager_us": round(eager_us, 3),
+            "kf355_speedup": round(eager_us / us, 3), "buffer_sets": len(xs)}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -417,6 +438,8 @@ def main():
         next_rows["max_pool2d_stem"] = maxpool_row(torch, F, dev, kf355, W, args.steps, args.warmup, sets_for)
         next_rows["avgpool_channels_last"] = avgpool_cl_row(torch, F, dev, kf355, W, args.steps, args.warmup,
                                                             sets_for)
+        next_rows["group_norm_channels_last"] = gn_cl_row(torch, F, dev, kf355, W, args.steps, args.warmup,
+                                                          sets_for)
 
     calib = copy_calibration(torch, dev, nbytes["softmax"])
     sm = per_op["softmax"]

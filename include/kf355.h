@@ -159,7 +159,10 @@ kf_status kf_softmax_causal(const void* x, kf_dtype x_dtype, void* y, kf_dtype y
  * y = (x - mu) / sqrt(var + eps) * weight[c] + bias[c].
  *
  *  x, y          device pointers, shape [N, C, *] (2 <= ndim <= 8), same dtype
- *                (FLOAT32, BFLOAT16 or FLOAT16); statistics are fp32.
+ *                (FLOAT32, BFLOAT16 or FLOAT16); statistics are fp32.  Dense
+ *                row-major, or for 4-D [N, C, H, W] dense channels last
+ *                (memory order N, H, W, C); y in x's layout.  Other layouts:
+ *                KF_ERR_UNSUPPORTED_LAYOUT.
  *  num_groups    >= 1 and divides C, else KF_ERR_BAD_ARG.
  *  weight, bias  device pointers to C elements each, or NULL (weight 1 /
  *                bias 0); both use `affine_dtype`, which is x_dtype or

@@ -3,10 +3,13 @@
 // affine), the operator behind the paper's SD3.5 Medium group_norm result
 // (Section IV-C).
 //
-// Layout: x is dense [n, c, spatial]; group g of sample i is the contiguous
-// span of (c/G)*spatial elements starting at (i*G + g) * (c/G)*spatial.  Each
-// group is cut into `parts` chunks of CH = 256 threads * NV * VEC elements and
-// one workgroup owns one chunk.
+// Layout: x is dense [n, c, spatial] (NCHW) or dense [n, spatial, c]
+// (channels last).  A group's (c/G)*spatial elements are numbered o = 0, 1,
+// ...: NCHW in memory order (the group is one contiguous span), channels
+// last pixel-major (element o is channel g*cpg + o % cpg of pixel o / cpg),
+// so VEC consecutive elements are VEC adjacent channels of one pixel: 16
+// contiguous bytes either way.  Each group is cut into `parts` chunks of
+// CH = 256 threads * NV * VEC elements and one workgroup owns one chunk.
 //
 //   gn_fused  (one launch, one HBM read + one write)  Each workgroup keeps its
 //             chunk in registers, computes its (count, mean, M2) moments,
@@ -46,6 +49,7 @@ struct GNParams {
     Exchange ex;           // one unit per (sample, group), ex.parts chunks each
     int64_t group_elems;   // (c/G) * spatial
     int64_t spatial;
+    int64_t channels;      // c
     int32_t cpg;           // channels per group
     int32_t groups;        // G
     float eps;
@@ -57,7 +61,7 @@ __device__ __forceinline__ float part_count(const GNParams& p, int64_t chunk, in
     return (float)(left < chunk ? left : chunk);
 }
 
-template <class T, bool VECTOR>
+template <class T, bool VECTOR, bool NHWC>
 struct Chunk {
     static constexpr int VEC = VECTOR ? T::vec : 1;
     static constexpr int NV = kFloatsPerThread / VEC;
@@ -68,16 +72,30 @@ struct Chunk {
     __device__ __forceinline__ static int64_t off(int part, int k) {
         return (int64_t)part * CH + ((int64_t)k * kNT + threadIdx.x) * VEC;
     }
+    // Element index in x / y of offset o of group ng (= sample * G + g).  A
+    // group holds fewer than 2^31 elements (checked on the host), so the
+    // channels-last split of o is a 32-bit division.
+    __device__ __forceinline__ static int64_t at(const GNParams& p, int64_t ng, int64_t o) {
+        if constexpr (!NHWC) {
+            return ng * p.group_elems + o;
+        } else {
+            const int64_t n = ng / p.groups;
+            const int g = (int)(ng - n * p.groups);
+            const uint32_t pix = (uint32_t)o / (uint32_t)p.cpg;
+            const uint32_t ch = (uint32_t)o - pix * (uint32_t)p.cpg;
+            return (n * p.spatial + pix) * p.channels + (int64_t)g * p.cpg + ch;
+        }
+    }
     // All slots load unconditionally so the loads issue back to back; a slot
     // past the group's end re-reads the group's first element and is never
     // used afterwards.
-    __device__ __forceinline__ void load(const GNParams& p, int64_t gbase, int part) {
+    __device__ __forceinline__ void load(const GNParams& p, int64_t ng, int part) {
 #pragma unroll
         for (int k = 0; k < NV; ++k) {
             const int64_t o = off(part, k);
-            const int64_t at = gbase + (o < p.group_elems ? o : 0);
-            if constexpr (VECTOR) load_vec<T>(p.x, at, v[k]);
-            else v[k][0] = load1<T>(p.x, at);
+            const int64_t e = at(p, ng, o < p.group_elems ? o : 0);
+            if constexpr (VECTOR) load_vec<T>(p.x, e, v[k]);
+            else v[k][0] = load1<T>(p.x, e);
         }
     }
     // Thread-local moments of the valid elements from sums shifted by K, the
@@ -111,11 +129,17 @@ struct Chunk {
         const float d1 = s1 * r;
         return Moments{cnt, K + d1, fmaxf(fmaf(-s1, d1, s2), 0.f)};
     }
-    // Raw w[c] and b[c] for every slot, loaded before the statistics are
-    // known (they do not depend on them), so their latency hides behind the
-    // cross-workgroup wait.  A group holds fewer than 2^31 elements (checked
-    // on the host), so the channel index is a 32-bit division.
+    // Raw w[c] and b[c], loaded before the statistics are known (they do
+    // not depend on them), so their latency hides behind the cross-workgroup
+    // wait.  NCHW, and scalar channels last: the channel of each slot
+    // (a 16-byte NCHW vector lies inside one channel).  Vector channels
+    // last: element i of every slot of this thread is channel
+    // g*cpg + (thread*VEC) % cpg + i (the host requires cpg | 256*VEC, so
+    // the channels do not change from slot to slot): wv[i], bv[i] for
+    // i < VEC.  A group holds fewer than 2^31 elements (checked on the
+    // host), so the channel index is a 32-bit division.
     float wv[NV], bv[NV];
+    static constexpr bool kFixedChannels = NHWC && VECTOR;
     template <class A>
     __device__ __forceinline__ void load_affine(const GNParams& p, int part, int g) {
         int64_t c[NV];
@@ -123,7 +147,12 @@ struct Chunk {
         for (int k = 0; k < NV; ++k) {
             const int64_t o = off(part, k);
             const uint32_t oc = o < p.group_elems ? (uint32_t)o : 0u;
-            c[k] = (int64_t)g * p.cpg + (int64_t)(oc / (uint32_t)p.spatial);
+            if constexpr (kFixedChannels)
+                c[k] = (int64_t)g * p.cpg + (int64_t)((threadIdx.x * VEC) % (uint32_t)p.cpg) + (k < VEC ? k : 0);
+            else if constexpr (NHWC)
+                c[k] = (int64_t)g * p.cpg + (int64_t)(oc % (uint32_t)p.cpg);
+            else
+                c[k] = (int64_t)g * p.cpg + (int64_t)(oc / (uint32_t)p.spatial);
         }
         if (p.w) {
 #pragma unroll
@@ -141,18 +170,33 @@ struct Chunk {
         }
     }
     // y = (x - mean) * (rstd * w[c]) + b[c], non-temporal stores.
-    __device__ __forceinline__ void normalise_store(const GNParams& p, int64_t gbase, int part, float mean,
+    __device__ __forceinline__ void normalise_store(const GNParams& p, int64_t ng, int part, float mean,
                                                     float rstd) {
+        float ai[VEC];
+        if constexpr (kFixedChannels) {
+#pragma unroll
+            for (int i = 0; i < VEC; ++i) ai[i] = rstd * wv[i];
+        }
 #pragma unroll
         for (int k = 0; k < NV; ++k) {
             const int64_t o = off(part, k);
             if (o < p.group_elems) {
-                const float a = rstd * wv[k];
                 float out[VEC];
+                if constexpr (kFixedChannels) {
 #pragma unroll
-                for (int i = 0; i < VEC; ++i) out[i] = fmaf(v[k][i] - mean, a, bv[k]);
-                if constexpr (VECTOR) store_vec<T, true>(p.y, gbase + o, out);
-                else store1<T>(p.y, gbase + o, out[0]);
+                    for (int i = 0; i < VEC; ++i) out[i] = fmaf(v[k][i] - mean, ai[i], bv[i]);
+                } else {
+                    const float a = rstd * wv[k];
+#pragma unroll
+                    for (int i = 0; i < VEC; ++i) out[i] = fmaf(v[k][i] - mean, a, bv[k]);
+                }
+                // Non-temporal stores for NCHW (each workgroup writes whole
+                // lines).  Channels last, a group's 16-byte runs share their
+                // lines with neighbouring groups written by other workgroups:
+                // ordinary stores let L2 merge those before writing back
+                // (non-temporal ones measured twice the HBM write traffic).
+                if constexpr (VECTOR) store_vec<T, !NHWC>(p.y, at(p, ng, o), out);
+                else store1<T>(p.y, at(p, ng, o), out[0]);
             }
         }
     }
@@ -191,19 +235,18 @@ __device__ __forceinline__ Moments gather_parts(const GNParams& p, int64_t ng, i
     return moments_wave(acc);
 }
 
-template <class T, class A, bool VECTOR>
+template <class T, class A, bool VECTOR, bool NHWC>
 __global__ __launch_bounds__(kNT) void gn_fused(GNParams p) {
-    using C = Chunk<T, VECTOR>;
+    using C = Chunk<T, VECTOR, NHWC>;
     __shared__ Moments lds[kNT / kWave];
     __shared__ float stats[2];
     __shared__ int gathered;
     const int64_t ng = blockIdx.x / p.ex.parts;
     const int part = blockIdx.x - (int)(ng * p.ex.parts);
     const int g = (int)(ng % p.groups);
-    const int64_t gbase = ng * p.group_elems;
 
     C c;
-    c.load(p, gbase, part);
+    c.load(p, ng, part);
     c.template load_affine<A>(p, part, g);
     Moments m = moments_block<kNT / kWave>(c.moments(p, part), lds);
 
@@ -232,7 +275,7 @@ __global__ __launch_bounds__(kNT) void gn_fused(GNParams p) {
         Moments acc{0.f, 0.f, 0.f};
         const int lane = threadIdx.x & (kWave - 1);
         for (int q = 0; q < p.ex.parts; ++q) {
-            c.load(p, gbase, q);
+            c.load(p, ng, q);
             const Moments mq = moments_block<kNT / kWave>(c.moments(p, q), lds);
             if ((q & (kWave - 1)) == lane) acc = chan(acc, mq);
         }
@@ -244,38 +287,37 @@ __global__ __launch_bounds__(kNT) void gn_fused(GNParams p) {
                 ex_flag_timeout(p.ex);
             }
         }
-        c.load(p, gbase, part);
+        c.load(p, ng, part);
         __syncthreads();
     }
-    c.normalise_store(p, gbase, part, stats[0], stats[1]);
+    c.normalise_store(p, ng, part, stats[0], stats[1]);
     // Off the critical path: this workgroup is done reading its group's slots.
     if (p.ex.parts > 1 && threadIdx.x == 0) ex_release(p.ex, ng);
 }
 
-template <class T, bool VECTOR>
+template <class T, bool VECTOR, bool NHWC>
 __global__ __launch_bounds__(kNT) void gn_stats(GNParams p) {
-    using C = Chunk<T, VECTOR>;
+    using C = Chunk<T, VECTOR, NHWC>;
     __shared__ Moments lds[kNT / kWave];
     const int64_t ng = blockIdx.x / p.ex.parts;
     const int part = blockIdx.x - (int)(ng * p.ex.parts);
     C c;
-    c.load(p, ng * p.group_elems, part);
+    c.load(p, ng, part);
     Moments m = moments_block<kNT / kWave>(c.moments(p, part), lds);
     if (threadIdx.x == 0) ex_publish(p.ex, ng, part, encode(m));
 }
 
-template <class T, class A, bool VECTOR>
+template <class T, class A, bool VECTOR, bool NHWC>
 __global__ __launch_bounds__(kNT) void gn_apply(GNParams p) {
-    using C = Chunk<T, VECTOR>;
+    using C = Chunk<T, VECTOR, NHWC>;
     __shared__ float stats[2];
     const int64_t ng = blockIdx.x / p.ex.parts;
     const int part = blockIdx.x - (int)(ng * p.ex.parts);
     const int g = (int)(ng % p.groups);
-    const int64_t gbase = ng * p.group_elems;
     // Chunk and affine loads first, so they are in flight while wave 0
     // gathers the statistics.
     C c;
-    c.load(p, gbase, part);
+    c.load(p, ng, part);
     c.template load_affine<A>(p, part, g);
     if (threadIdx.x < kWave) {
         bool ok;
@@ -287,7 +329,7 @@ __global__ __launch_bounds__(kNT) void gn_apply(GNParams p) {
         }
     }
     __syncthreads();
-    c.normalise_store(p, gbase, part, stats[0], stats[1]);
+    c.normalise_store(p, ng, part, stats[0], stats[1]);
 }
 
 // --------------------------------------------------------------------------
@@ -299,9 +341,16 @@ int64_t chunk_elems(kf_dtype xt, bool vector) {
     return (int64_t)kNT * (kFloatsPerThread / vec) * vec;
 }
 
+// 16-byte vectors: NCHW needs each channel's span to be whole vectors;
+// channels last needs each group's channel run to be whole vectors and the
+// channels of a thread to stay fixed across its slots (cpg divides
+// 256 * VEC).  Both need 16-byte aligned bases.
 bool vector_ok(const GroupNormArgs& a) {
     const int vec = a.xt == KF_FLOAT32 ? 4 : 8;
-    return (a.spatial % vec == 0) && ((uintptr_t)a.x % 16 == 0) && ((uintptr_t)a.y % 16 == 0);
+    if ((uintptr_t)a.x % 16 || (uintptr_t)a.y % 16) return false;
+    const int64_t cpg = a.c / a.groups;
+    if (a.nhwc) return cpg % vec == 0 && ((int64_t)kNT * vec) % cpg == 0;
+    return a.spatial % vec == 0;
 }
 
 struct Layout {
@@ -343,7 +392,7 @@ uint32_t gn_wait_ticks() {
     return ticks;
 }
 
-template <class T, class A, bool VECTOR>
+template <class T, class A, bool VECTOR, bool NHWC>
 kf_status run(const GroupNormArgs& a, hipStream_t s, const char** variant) {
     const Layout l = layout(a.n, a.c, a.spatial, a.groups, a.xt, VECTOR);
     GNParams p;
@@ -354,6 +403,7 @@ kf_status run(const GroupNormArgs& a, hipStream_t s, const char** variant) {
     p.ex = exchange_view(a.workspace, l.ex, l.parts, gn_wait_ticks());
     p.group_elems = (a.c / a.groups) * a.spatial;
     p.spatial = a.spatial;
+    p.channels = a.c;
     p.cpg = (int32_t)(a.c / a.groups);
     p.groups = (int32_t)a.groups;
     p.eps = a.eps;
@@ -382,31 +432,35 @@ kf_status run(const GroupNormArgs& a, hipStream_t s, const char** variant) {
             set_error("group_norm: no current HIP device");
             return KF_ERR_HIP;
         }
-        const void* kernel = reinterpret_cast<const void*>(gn_fused<T, A, VECTOR>);
+        const void* kernel = reinterpret_cast<const void*>(gn_fused<T, A, VECTOR, NHWC>);
         if ((int64_t)resident_capacity(capacity_cache, dev, kernel, kNT) >= grid) {
             if (mode == kModeCoop && device_cooperative(dev)) path = FUSED_COOP;
             else if (mode != kModeCoop) path = FUSED_PLAIN;
         }
     }
+    // Variant names: [layout][vector][path].
+    static const char* names[2][2][4] = {
+        {{"gn_fused_scalar_single", "gn_fused_scalar", "gn_fused_scalar_coop", "gn_two_pass_scalar"},
+         {"gn_fused_vec_single", "gn_fused_vec", "gn_fused_vec_coop", "gn_two_pass_vec"}},
+        {{"gn_nhwc_fused_scalar_single", "gn_nhwc_fused_scalar", "gn_nhwc_fused_scalar_coop",
+          "gn_nhwc_two_pass_scalar"},
+         {"gn_nhwc_fused_vec_single", "gn_nhwc_fused_vec", "gn_nhwc_fused_vec_coop", "gn_nhwc_two_pass_vec"}}};
+    *variant = names[NHWC ? 1 : 0][VECTOR ? 1 : 0][path];
     hipError_t err;
     if (path == FUSED_SINGLE || path == FUSED_PLAIN) {
-        hipLaunchKernelGGL((gn_fused<T, A, VECTOR>), dim3((unsigned)grid), dim3(kNT), 0, s, p);
+        hipLaunchKernelGGL((gn_fused<T, A, VECTOR, NHWC>), dim3((unsigned)grid), dim3(kNT), 0, s, p);
         err = hipGetLastError();
-        *variant = path == FUSED_SINGLE ? (VECTOR ? "gn_fused_vec_single" : "gn_fused_scalar_single")
-                                        : (VECTOR ? "gn_fused_vec" : "gn_fused_scalar");
     } else if (path == FUSED_COOP) {
         void* args[] = {&p};
-        err = hipLaunchCooperativeKernel(reinterpret_cast<const void*>(gn_fused<T, A, VECTOR>), dim3((unsigned)grid),
-                                         dim3(kNT), args, 0, s);
-        *variant = VECTOR ? "gn_fused_vec_coop" : "gn_fused_scalar_coop";
+        err = hipLaunchCooperativeKernel(reinterpret_cast<const void*>(gn_fused<T, A, VECTOR, NHWC>),
+                                         dim3((unsigned)grid), dim3(kNT), args, 0, s);
     } else {
-        hipLaunchKernelGGL((gn_stats<T, VECTOR>), dim3((unsigned)grid), dim3(kNT), 0, s, p);
+        hipLaunchKernelGGL((gn_stats<T, VECTOR, NHWC>), dim3((unsigned)grid), dim3(kNT), 0, s, p);
         err = hipGetLastError();
         if (err == hipSuccess) {
-            hipLaunchKernelGGL((gn_apply<T, A, VECTOR>), dim3((unsigned)grid), dim3(kNT), 0, s, p);
+            hipLaunchKernelGGL((gn_apply<T, A, VECTOR, NHWC>), dim3((unsigned)grid), dim3(kNT), 0, s, p);
             err = hipGetLastError();
         }
-        *variant = VECTOR ? "gn_two_pass_vec" : "gn_two_pass_scalar";
     }
     if (err != hipSuccess) {
         set_error("group_norm launch failed: %s", hipGetErrorString(err));
@@ -417,7 +471,9 @@ kf_status run(const GroupNormArgs& a, hipStream_t s, const char** variant) {
 
 template <class T, class A>
 kf_status run_layout(const GroupNormArgs& a, hipStream_t s, const char** variant) {
-    return vector_ok(a) ? run<T, A, true>(a, s, variant) : run<T, A, false>(a, s, variant);
+    const bool vec = vector_ok(a);
+    if (a.nhwc) return vec ? run<T, A, true, true>(a, s, variant) : run<T, A, false, true>(a, s, variant);
+    return vec ? run<T, A, true, false>(a, s, variant) : run<T, A, false, false>(a, s, variant);
 }
 
 }  // namespace

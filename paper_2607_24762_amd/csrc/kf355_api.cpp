@@ -326,8 +326,17 @@ kf_status kf_group_norm(const void* x, kf_dtype x_dtype, void* y, int32_t ndim, 
     if (!x || !y) return fail(KF_ERR_NULL_POINTER, "x or y is NULL");
     const int64_t eb = elem_bytes(x_dtype);
     if ((uintptr_t)x % eb || (uintptr_t)y % eb) return fail(KF_ERR_BAD_ARG, "x or y is not element aligned");
-    if (!dense(ndim, shape, x_strides) || !dense(ndim, shape, y_strides))
-        return fail(KF_ERR_UNSUPPORTED_LAYOUT, "only dense row-major (NC*) tensors are supported");
+    bool nhwc = false;
+    if (dense(ndim, shape, x_strides)) {
+        if (!dense(ndim, shape, y_strides))
+            return fail(KF_ERR_UNSUPPORTED_LAYOUT, "y must be dense in x's layout (NC*)");
+    } else if (ndim == 4 && dense_nhwc(shape, x_strides)) {
+        if (!dense_nhwc(shape, y_strides))
+            return fail(KF_ERR_UNSUPPORTED_LAYOUT, "y must be dense in x's layout (channels last)");
+        nhwc = true;
+    } else {
+        return fail(KF_ERR_UNSUPPORTED_LAYOUT, "x must be dense NC* or dense channels last [N, C, H, W]");
+    }
     const int64_t xb = n * eb;
     if (x != y && overlaps(x, xb, y, xb)) return fail(KF_ERR_BAD_ARG, "x and y partially overlap");
     const int64_t ab = shape[1] * ((weight || bias) ? elem_bytes(affine_dtype) : 0);
@@ -343,7 +352,7 @@ kf_status kf_group_norm(const void* x, kf_dtype x_dtype, void* y, int32_t ndim, 
         return fail(KF_ERR_BAD_ARG, "workspace overlaps x or y");
 
     GroupNormArgs a{x,     y,    x_dtype,      shape[0],         shape[1], spatial, num_groups, weight, bias,
-                    affine_dtype, (float)eps, workspace, workspace_bytes};
+                    affine_dtype, (float)eps, workspace, workspace_bytes, nhwc};
     const char* variant = nullptr;
     s = group_norm_launch(a, static_cast<hipStream_t>(stream), &variant);
     return done(s, variant);

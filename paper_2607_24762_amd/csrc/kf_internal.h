@@ -50,6 +50,7 @@ struct GroupNormArgs {
     float eps;
     void* workspace;
     size_t workspace_bytes;
+    bool nhwc;  // x, y dense [n, spatial, c] (channels last) instead of [n, c, spatial]
 };
 size_t group_norm_workspace_bytes(int64_t n, int64_t c, int64_t spatial, int64_t groups, kf_dtype xt);
 kf_status group_norm_launch(const GroupNormArgs& a, hipStream_t s, const char** variant);

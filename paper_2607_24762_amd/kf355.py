@@ -201,7 +201,9 @@ def kf_group_norm(x: torch.Tensor, num_groups: int, weight: torch.Tensor | None 
                   workspace: torch.Tensor | None = None) -> torch.Tensor:
     """group_norm(x, num_groups, weight, bias, eps) through kf_group_norm."""
     _need_cuda(x, weight, bias)
-    y = out if out is not None else torch.empty_like(x, memory_format=torch.contiguous_format)
+    fmt = torch.channels_last if (x.dim() == 4 and not x.is_contiguous()
+                                  and x.is_contiguous(memory_format=torch.channels_last)) else torch.contiguous_format
+    y = out if out is not None else torch.empty_like(x, memory_format=fmt)
     ws = workspace if workspace is not None else group_norm_workspace(x, num_groups)
     affine = weight if weight is not None else bias
     at = _dtype(affine) if affine is not None else _dtype(x)

@@ -6,7 +6,7 @@ workgroup give up at once and recompute the partials itself), and saves the
 output bits, the workspace's give-up word and the count of other non-zero
 workspace bytes.
 
-usage: exchange_child.py group_norm|softmax_split OUT.npz"""
+usage: exchange_child.py group_norm|group_norm_nhwc|softmax_split OUT.npz"""
 import ctypes
 import os
 import sys
@@ -23,9 +23,12 @@ print(f"[child] op={op} KF355_GN_WAIT_TICKS={os.environ.get('KF355_GN_WAIT_TICKS
       f"KF355_SM_WAIT_TICKS={os.environ.get('KF355_SM_WAIT_TICKS')}", flush=True)
 ws = torch.zeros(1 << 20, dtype=torch.uint8, device="cuda")
 nb = ctypes.c_size_t(0)
-if op == "group_norm":
+if op in ("group_norm", "group_norm_nhwc"):
     w = W.groupnorm_vae_bf16()
-    y = kf355.kf_group_norm(w["x"].cuda(), 32, w["weight"].cuda(), w["bias"].cuda(), w["eps"], workspace=ws)
+    x = w["x"].cuda()
+    if op == "group_norm_nhwc":
+        x = x.contiguous(memory_format=torch.channels_last)
+    y = kf355.kf_group_norm(x, 32, w["weight"].cuda(), w["bias"].cuda(), w["eps"], workspace=ws)
     shape = (ctypes.c_int64 * 4)(1, 512, 128, 128)
     kf355.lib().kf_group_norm_workspace_bytes(1, 4, shape, 32, ctypes.byref(nb))
 elif op == "softmax_split":

@@ -208,7 +208,8 @@ def test_group_norm_rejections(lib):
     assert gn(lib, ws=0) == WS
     assert gn(lib, wsb=16) == WS
     assert gn(lib, ws=FAKE + (2 << 30) + 64) == WS         # not 256-byte aligned
-    assert gn(lib, xs=(128, 16, 4, 2)) == LAYOUT          # channels-last strides
+    assert gn(lib, xs=(128, 16, 4, 2)) == LAYOUT          # not dense in any layout
+    assert gn(lib, xs=(128, 1, 32, 8)) == LAYOUT and "channels last" in err(lib)  # channels-last x, NCHW y
     assert gn(lib, y=FAKE + 128) == ARG                   # partial overlap
     assert gn(lib, w=FAKE + (1 << 30) + 64) == ARG        # weight inside y
     assert gn(lib, ws=FAKE) == ARG                        # workspace overlaps x

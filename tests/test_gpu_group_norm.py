@@ -42,13 +42,16 @@ def check(y, ref, dt):
     assert_close(y, ref, dt, floor=FLOOR)
 
 
-def run(shape, groups, dt, affine="same", eps=1e-6, seed=0, mean=0.3, std=1.5, in_place=False):
+def run(shape, groups, dt, affine="same", eps=1e-6, seed=0, mean=0.3, std=1.5, in_place=False,
+        channels_last=False):
     c = shape[1]
     x_cpu = randn(shape, dt, seed=seed, mean=mean, std=std)
     adt = dt if affine == "same" else "f32"
     w_cpu = randn((c,), adt, seed=seed + 1, mean=1.0, std=0.1) if affine in ("same", "f32", "w") else None
     b_cpu = randn((c,), adt, seed=seed + 2, std=0.1) if affine in ("same", "f32", "b") else None
     x = x_cpu.cuda()
+    if channels_last:
+        x = x.contiguous(memory_format=torch.channels_last)
     w = w_cpu.cuda() if w_cpu is not None else None
     b = b_cpu.cuda() if b_cpu is not None else None
     y = kf355.kf_group_norm(x, groups, w, b, eps, out=x if in_place else None)
@@ -187,3 +190,71 @@ def test_paths_share_one_workspace(mode_shape):
         torch.cuda.synchronize()
         assert_close(y, oracle.group_norm(x_cpu, groups, None, None, 1e-6), "bf16", floor=FLOOR)
     assert int(ws.count_nonzero().item()) == 0
+
+
+CHANNELS_LAST = [
+    ((1, 512, 128, 128), 32),    # the SD3.5 VAE block, channels last: 16-chunk groups
+    ((2, 64, 15, 17), 8),        # 8-channel groups, ragged pixel count
+    ((2, 96, 9, 7), 96),         # one channel per group: scalar layout
+    ((1, 24, 64, 64), 2),        # 12-channel groups: scalar layout, 3 chunks
+    ((3, 256, 10, 5), 1),        # one group of every channel
+    ((2, 32, 60, 50), 2),        # 16-channel groups, 3 chunks
+]
+
+
+@pytest.mark.parametrize("dt", ["bf16", "f32", "f16"])
+@pytest.mark.parametrize("shape,groups", CHANNELS_LAST, ids=lambda v: str(v))
+def test_channels_last(shape, groups, dt):
+    note(f"group_norm channels last {shape} G={groups} {dt}")
+    y, variant = run(shape, groups, dt, channels_last=True)
+    assert variant.startswith("gn_nhwc_"), variant
+    assert y.is_contiguous(memory_format=torch.channels_last)
+    vec = 4 if dt == "f32" else 8
+    cpg = shape[1] // groups
+    assert ("_vec" in variant) == (cpg % vec == 0 and (256 * vec) % cpg == 0), variant
+
+
+@pytest.mark.parametrize("affine", ["none", "w", "b", "f32"])
+def test_channels_last_affine_and_in_place(affine):
+    note(f"group_norm channels last affine={affine}")
+    run((2, 64, 32, 32), 4, "bf16", affine=affine, channels_last=True)
+    _, variant = run((1, 128, 64, 64), 8, "bf16", affine=affine, channels_last=True, in_place=True)
+    assert variant == "gn_nhwc_two_pass_vec", variant     # multi-chunk in place: two kernels
+
+
+def test_channels_last_matches_nchw_statistics():
+    # The same logical tensor in both layouts normalises to the same values
+    # within the tolerance (the moment merges visit elements in different orders).
+    note("group_norm channels last vs NCHW")
+    w = W.groupnorm_vae_bf16()
+    x = w["x"].cuda()
+    a = kf355.kf_group_norm(x, 32, w["weight"].cuda(), w["bias"].cuda(), w["eps"])
+    b = kf355.kf_group_norm(x.contiguous(memory_format=torch.channels_last), 32, w["weight"].cuda(),
+                            w["bias"].cuda(), w["eps"])
+    torch.cuda.synchronize()
+    assert b.is_contiguous(memory_format=torch.channels_last)
+    ref = oracle.group_norm(w["x"], 32, w["weight"], w["bias"], w["eps"])
+    check(a, ref, "bf16")
+    check(b, ref, "bf16")
+
+
+def test_channels_last_gave_up_waiting_recomputes_bit_identically(tmp_path):
+    import os
+    import subprocess
+    import sys
+    note("group_norm channels last forced recompute (child process)")
+    w = W.groupnorm_vae_bf16()
+    x = w["x"].cuda().contiguous(memory_format=torch.channels_last)
+    y = kf355.kf_group_norm(x, 32, w["weight"].cuda(), w["bias"].cuda(), w["eps"])
+    torch.cuda.synchronize()
+    child = os.path.join(os.path.dirname(os.path.abspath(__file__)), "exchange_child.py")
+    out = str(tmp_path / "child.npz")
+    env = dict(os.environ, KF355_GN_WAIT_TICKS="0")
+    r = subprocess.run([sys.executable, "-u", child, "group_norm_nhwc", out], env=env, timeout=300,
+                       capture_output=True, text=True)
+    print(r.stdout, r.stderr[-2000:])
+    assert r.returncode == 0
+    got = np.load(out)
+    assert str(got["variant"]) == "gn_nhwc_fused_vec"
+    assert int(got["flag"]) == 1 and int(got["rest"]) == 0
+    assert np.array_equal(got["bits"], y.contiguous().view(torch.int16).cpu().numpy())
