@@ -94,8 +94,27 @@ def _check(status: int):
         raise KfError(status, lib().kf_last_error().decode())
 
 
+_ARRS: dict = {}
+
+
 def _arr(vals):
-    a = (ctypes.c_int64 * max(len(vals), 1))(*vals)
+    """A read-only int64 array for shapes, strides and windows, cached by
+    value (the library never writes through these pointers): building
+    ctypes arrays is a noticeable part of a call's host cost."""
+    key = tuple(int(v) for v in vals)
+    hit = _ARRS.get(key)
+    if hit is None:
+        a = (ctypes.c_int64 * max(len(key), 1))(*key)
+        hit = (ctypes.cast(a, _i64p), a)
+        if len(_ARRS) > 4096:
+            _ARRS.clear()
+        _ARRS[key] = hit
+    return hit
+
+
+def _out_arr(n: int):
+    """A fresh int64 array the library writes into."""
+    a = (ctypes.c_int64 * n)()
     return ctypes.cast(a, _i64p), a
 
 
@@ -105,8 +124,30 @@ def _dtype(t: torch.Tensor) -> int:
     return DTYPES[t.dtype]
 
 
-def _stream(t: torch.Tensor):
-    return ctypes.c_void_p(torch.cuda.current_stream(t.device).cuda_stream)
+_raw_stream = getattr(torch._C, "_cuda_getCurrentRawStream", None)
+
+
+def _stream(t: torch.Tensor) -> int:
+    """The current HIP stream of t's device, as an address."""
+    if _raw_stream is not None:
+        return _raw_stream(t.device.index)
+    return torch.cuda.current_stream(t.device).cuda_stream
+
+
+class _NoSwitch:
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        return False
+
+
+_NO_SWITCH = _NoSwitch()
+
+
+def _on(t: torch.Tensor):
+    """Make t's device current for the call (a no-op when it already is)."""
+    return _NO_SWITCH if t.device.index == torch.cuda.current_device() else torch.cuda.device(t.device)
 
 
 def _need_cuda(*ts):
@@ -120,11 +161,12 @@ def kf_softmax(x: torch.Tensor, dim: int = -1, out_dtype: torch.dtype | None = N
     """softmax(x, dim) on the GPU through kf_softmax; out_dtype=torch.float32
     with a bf16/fp16 input matches torch.softmax(x, dim, dtype=torch.float32)."""
     _need_cuda(x)
-    y = out if out is not None else torch.empty(x.shape, dtype=out_dtype or x.dtype, device=x.device)
-    shape, _s = _arr(list(x.shape))
-    xs, _a = _arr(list(x.stride()))
-    ys, _b = _arr(list(y.stride()))
-    with torch.cuda.device(x.device):
+    y = out if out is not None else torch.empty_like(x, dtype=out_dtype or x.dtype,
+                                                     memory_format=torch.contiguous_format)
+    shape, _s = _arr(x.shape)
+    xs, _a = _arr(x.stride())
+    ys, _b = _arr(y.stride())
+    with _on(x):
         _check(lib().kf_softmax(ctypes.c_void_p(x.data_ptr()), _dtype(x), ctypes.c_void_p(y.data_ptr()), _dtype(y),
                                 x.dim(), shape, xs, ys, dim, _stream(x)))
     return y
@@ -135,17 +177,19 @@ def kf_softmax_causal(x: torch.Tensor, scale: float = 1.0, out_dtype: torch.dtyp
     """softmax(scale * x + causal mask, -1) over x [..., q, k] through
     kf_softmax_causal (query i sees keys j <= i + k - q)."""
     _need_cuda(x)
-    y = out if out is not None else torch.empty(x.shape, dtype=out_dtype or x.dtype, device=x.device)
-    shape, _s = _arr(list(x.shape))
-    xs, _a = _arr(list(x.stride()))
-    ys, _b = _arr(list(y.stride()))
-    with torch.cuda.device(x.device):
+    y = out if out is not None else torch.empty_like(x, dtype=out_dtype or x.dtype,
+                                                     memory_format=torch.contiguous_format)
+    shape, _s = _arr(x.shape)
+    xs, _a = _arr(x.stride())
+    ys, _b = _arr(y.stride())
+    with _on(x):
         _check(lib().kf_softmax_causal(ctypes.c_void_p(x.data_ptr()), _dtype(x), ctypes.c_void_p(y.data_ptr()),
                                        _dtype(y), x.dim(), shape, xs, ys, float(scale), _stream(x)))
     return y
 
 
 _ws_cache: dict = {}
+_ws_bytes: dict = {}
 
 
 def _workspace(x: torch.Tensor, nbytes: int) -> torch.Tensor:
@@ -153,7 +197,7 @@ def _workspace(x: torch.Tensor, nbytes: int) -> torch.Tensor:
     stream) and grown on demand.  kf_group_norm and kf_softmax_split return
     the workspace to all-zero after each call, so one cached buffer serves
     every later call on that stream, of either operator, in stream order."""
-    key = (x.device, torch.cuda.current_stream(x.device).cuda_stream)
+    key = (x.device.index, _stream(x))
     ws = _ws_cache.get(key)
     if ws is None or ws.numel() < nbytes:
         ws = torch.zeros(max(nbytes, 256), dtype=torch.uint8, device=x.device)
@@ -161,22 +205,36 @@ def _workspace(x: torch.Tensor, nbytes: int) -> torch.Tensor:
     return ws
 
 
+def _query_bytes(key, query) -> int:
+    """Workspace size for a (function, dtypes, shape, arguments) key, asked
+    of the library once and remembered."""
+    n = _ws_bytes.get(key)
+    if n is None:
+        nbytes = ctypes.c_size_t(0)
+        _check(query(ctypes.byref(nbytes)))
+        n = nbytes.value
+        if len(_ws_bytes) > 4096:
+            _ws_bytes.clear()
+        _ws_bytes[key] = n
+    return n
+
+
 def group_norm_workspace(x: torch.Tensor, num_groups: int) -> torch.Tensor:
     """The cached zero-filled workspace, large enough for kf_group_norm on x."""
-    shape, _s = _arr(list(x.shape))
-    nbytes = ctypes.c_size_t(0)
-    _check(lib().kf_group_norm_workspace_bytes(_dtype(x), x.dim(), shape, num_groups, ctypes.byref(nbytes)))
-    return _workspace(x, nbytes.value)
+    shape, _s = _arr(x.shape)
+    n = _query_bytes(("gn", _dtype(x), tuple(x.shape), num_groups),
+                     lambda out: lib().kf_group_norm_workspace_bytes(_dtype(x), x.dim(), shape, num_groups, out))
+    return _workspace(x, n)
 
 
 def softmax_split_workspace(x: torch.Tensor, dim: int = -1, out_dtype: torch.dtype | None = None) -> torch.Tensor:
     """The cached zero-filled workspace, large enough for kf_softmax_split on
     x with output dtype out_dtype (x's by default)."""
-    shape, _s = _arr(list(x.shape))
-    nbytes = ctypes.c_size_t(0)
+    shape, _s = _arr(x.shape)
     yt = DTYPES.get(out_dtype or x.dtype, -1)
-    _check(lib().kf_softmax_split_workspace_bytes(_dtype(x), yt, x.dim(), shape, dim, ctypes.byref(nbytes)))
-    return _workspace(x, nbytes.value)
+    n = _query_bytes(("sm", _dtype(x), yt, tuple(x.shape), dim),
+                     lambda out: lib().kf_softmax_split_workspace_bytes(_dtype(x), yt, x.dim(), shape, dim, out))
+    return _workspace(x, n)
 
 
 def kf_softmax_split(x: torch.Tensor, dim: int = -1, out_dtype: torch.dtype | None = None,
@@ -184,12 +242,13 @@ def kf_softmax_split(x: torch.Tensor, dim: int = -1, out_dtype: torch.dtype | No
     """softmax(x, dim) through kf_softmax_split: rows split over several
     workgroups when there are few long ones (decode-step attention scores)."""
     _need_cuda(x)
-    y = out if out is not None else torch.empty(x.shape, dtype=out_dtype or x.dtype, device=x.device)
+    y = out if out is not None else torch.empty_like(x, dtype=out_dtype or x.dtype,
+                                                     memory_format=torch.contiguous_format)
     ws = workspace if workspace is not None else softmax_split_workspace(x, dim, y.dtype)
-    shape, _s = _arr(list(x.shape))
-    xs, _a = _arr(list(x.stride()))
-    ys, _b = _arr(list(y.stride()))
-    with torch.cuda.device(x.device):
+    shape, _s = _arr(x.shape)
+    xs, _a = _arr(x.stride())
+    ys, _b = _arr(y.stride())
+    with _on(x):
         _check(lib().kf_softmax_split(ctypes.c_void_p(x.data_ptr()), _dtype(x), ctypes.c_void_p(y.data_ptr()),
                                       _dtype(y), x.dim(), shape, xs, ys, dim, ctypes.c_void_p(ws.data_ptr()),
                                       ws.numel(), _stream(x)))
@@ -212,10 +271,10 @@ def kf_group_norm(x: torch.Tensor, num_groups: int, weight: torch.Tensor | None 
     for p in (weight, bias):
         if p is not None and (p.dim() != 1 or not p.is_contiguous()):
             raise KfError(5, "weight and bias must be contiguous 1-D tensors")
-    shape, _s = _arr(list(x.shape))
-    xs, _a = _arr(list(x.stride()))
-    ys, _b = _arr(list(y.stride()))
-    with torch.cuda.device(x.device):
+    shape, _s = _arr(x.shape)
+    xs, _a = _arr(x.stride())
+    ys, _b = _arr(y.stride())
+    with _on(x):
         _check(lib().kf_group_norm(
             ctypes.c_void_p(x.data_ptr()), _dtype(x), ctypes.c_void_p(y.data_ptr()), x.dim(), shape, xs, ys,
             num_groups, ctypes.c_void_p(weight.data_ptr() if weight is not None else None),
@@ -242,10 +301,10 @@ def kf_layer_norm(x: torch.Tensor, normalized_shape, weight: torch.Tensor | None
         if p is not None and (tuple(p.shape) != nshape or not p.is_contiguous()):
             raise KfError(5, "weight and bias must be contiguous with the normalised shape")
     y = out if out is not None else torch.empty_like(x, memory_format=torch.contiguous_format)
-    shape, _s = _arr(list(x.shape))
-    xs, _a = _arr(list(x.stride()))
-    ys, _b = _arr(list(y.stride()))
-    with torch.cuda.device(x.device):
+    shape, _s = _arr(x.shape)
+    xs, _a = _arr(x.stride())
+    ys, _b = _arr(y.stride())
+    with _on(x):
         _check(lib().kf_layer_norm(
             ctypes.c_void_p(x.data_ptr()), _dtype(x), ctypes.c_void_p(y.data_ptr()), x.dim(), shape, xs, ys,
             len(nshape), ctypes.c_void_p(weight.data_ptr() if weight is not None else None),
@@ -262,10 +321,10 @@ def kf_adaptive_avgpool2d(x: torch.Tensor, output_size, out: torch.Tensor | None
                                   and x.is_contiguous(memory_format=torch.channels_last)) else torch.contiguous_format
     y = out if out is not None else torch.empty(tuple(x.shape[:-2]) + (oh, ow), dtype=x.dtype, device=x.device,
                                                 memory_format=fmt)
-    shape, _s = _arr(list(x.shape))
-    xs, _a = _arr(list(x.stride()))
-    ys, _b = _arr(list(y.stride()))
-    with torch.cuda.device(x.device):
+    shape, _s = _arr(x.shape)
+    xs, _a = _arr(x.stride())
+    ys, _b = _arr(y.stride())
+    with _on(x):
         _check(lib().kf_adaptive_avgpool2d(ctypes.c_void_p(x.data_ptr()), _dtype(x), ctypes.c_void_p(y.data_ptr()),
                                            x.dim(), shape, xs, ys, oh, ow, _stream(x)))
     return y
@@ -286,7 +345,7 @@ def _window(kernel_size, stride, padding, dilation):
 def max_pool2d_output_size(h: int, w: int, kernel_size, stride=None, padding=0, dilation=1,
                            ceil_mode: bool = False) -> tuple:
     win, _a = _arr(_window(kernel_size, stride, padding, dilation))
-    out, _b = _arr([0, 0])
+    out, _b = _out_arr(2)
     _check(lib().kf_max_pool2d_output_size(h, w, win, int(ceil_mode), out))
     return int(out[0]), int(out[1])
 
@@ -305,10 +364,10 @@ def kf_max_pool2d(x: torch.Tensor, kernel_size, stride=None, padding=0, dilation
     y = out if out is not None else torch.empty(yshape, dtype=x.dtype, device=x.device, memory_format=fmt)
     idx = torch.empty(yshape, dtype=torch.int64, device=x.device, memory_format=fmt) if return_indices else None
     win, _w = _arr(_window(kernel_size, stride, padding, dilation))
-    shape, _s = _arr(list(x.shape))
-    xs, _a = _arr(list(x.stride()))
-    ys, _b = _arr(list(y.stride()))
-    with torch.cuda.device(x.device):
+    shape, _s = _arr(x.shape)
+    xs, _a = _arr(x.stride())
+    ys, _b = _arr(y.stride())
+    with _on(x):
         _check(lib().kf_max_pool2d(ctypes.c_void_p(x.data_ptr()), _dtype(x), ctypes.c_void_p(y.data_ptr()),
                                    ctypes.c_void_p(idx.data_ptr() if idx is not None else None), x.dim(), shape, xs,
                                    ys, win, int(ceil_mode), _stream(x)))
@@ -340,9 +399,9 @@ class Prepared:
 
 def prepare_softmax(x: torch.Tensor, y: torch.Tensor, dim: int = -1) -> Prepared:
     _need_cuda(x, y)
-    shape, a0 = _arr(list(x.shape))
-    xs, a1 = _arr(list(x.stride()))
-    ys, a2 = _arr(list(y.stride()))
+    shape, a0 = _arr(x.shape)
+    xs, a1 = _arr(x.stride())
+    ys, a2 = _arr(y.stride())
     args = (ctypes.c_void_p(x.data_ptr()), _dtype(x), ctypes.c_void_p(y.data_ptr()), _dtype(y), x.dim(), shape, xs,
             ys, dim, _stream(x))
     return Prepared(lib().kf_softmax, args, (x, y, a0, a1, a2))
@@ -352,9 +411,9 @@ def prepare_softmax_split(x: torch.Tensor, y: torch.Tensor, dim: int = -1,
                           workspace: torch.Tensor | None = None) -> Prepared:
     _need_cuda(x, y)
     ws = workspace if workspace is not None else softmax_split_workspace(x, dim, y.dtype)
-    shape, a0 = _arr(list(x.shape))
-    xs, a1 = _arr(list(x.stride()))
-    ys, a2 = _arr(list(y.stride()))
+    shape, a0 = _arr(x.shape)
+    xs, a1 = _arr(x.stride())
+    ys, a2 = _arr(y.stride())
     args = (ctypes.c_void_p(x.data_ptr()), _dtype(x), ctypes.c_void_p(y.data_ptr()), _dtype(y), x.dim(), shape, xs,
             ys, dim, ctypes.c_void_p(ws.data_ptr()), ws.numel(), _stream(x))
     return Prepared(lib().kf_softmax_split, args, (x, y, ws, a0, a1, a2))
@@ -362,9 +421,9 @@ def prepare_softmax_split(x: torch.Tensor, y: torch.Tensor, dim: int = -1,
 
 def prepare_softmax_causal(x: torch.Tensor, y: torch.Tensor, scale: float = 1.0) -> Prepared:
     _need_cuda(x, y)
-    shape, a0 = _arr(list(x.shape))
-    xs, a1 = _arr(list(x.stride()))
-    ys, a2 = _arr(list(y.stride()))
+    shape, a0 = _arr(x.shape)
+    xs, a1 = _arr(x.stride())
+    ys, a2 = _arr(y.stride())
     args = (ctypes.c_void_p(x.data_ptr()), _dtype(x), ctypes.c_void_p(y.data_ptr()), _dtype(y), x.dim(), shape, xs,
             ys, float(scale), _stream(x))
     return Prepared(lib().kf_softmax_causal, args, (x, y, a0, a1, a2))
@@ -376,9 +435,9 @@ def prepare_group_norm(x: torch.Tensor, y: torch.Tensor, num_groups: int, weight
     ws = workspace if workspace is not None else group_norm_workspace(x, num_groups)
     affine = weight if weight is not None else bias
     at = _dtype(affine) if affine is not None else _dtype(x)
-    shape, a0 = _arr(list(x.shape))
-    xs, a1 = _arr(list(x.stride()))
-    ys, a2 = _arr(list(y.stride()))
+    shape, a0 = _arr(x.shape)
+    xs, a1 = _arr(x.stride())
+    ys, a2 = _arr(y.stride())
     args = (ctypes.c_void_p(x.data_ptr()), _dtype(x), ctypes.c_void_p(y.data_ptr()), x.dim(), shape, xs, ys,
             num_groups, ctypes.c_void_p(weight.data_ptr() if weight is not None else None),
             ctypes.c_void_p(bias.data_ptr() if bias is not None else None), at, float(eps),
@@ -389,9 +448,9 @@ def prepare_group_norm(x: torch.Tensor, y: torch.Tensor, num_groups: int, weight
 def prepare_layer_norm(x: torch.Tensor, y: torch.Tensor, normalized_ndim: int, weight=None, bias=None,
                        eps: float = 1e-5) -> Prepared:
     _need_cuda(x, y, weight, bias)
-    shape, a0 = _arr(list(x.shape))
-    xs, a1 = _arr(list(x.stride()))
-    ys, a2 = _arr(list(y.stride()))
+    shape, a0 = _arr(x.shape)
+    xs, a1 = _arr(x.stride())
+    ys, a2 = _arr(y.stride())
     args = (ctypes.c_void_p(x.data_ptr()), _dtype(x), ctypes.c_void_p(y.data_ptr()), x.dim(), shape, xs, ys,
             normalized_ndim, ctypes.c_void_p(weight.data_ptr() if weight is not None else None),
             ctypes.c_void_p(bias.data_ptr() if bias is not None else None), _affine_dtype(x, weight, bias),
@@ -403,9 +462,9 @@ def prepare_max_pool2d(x: torch.Tensor, y: torch.Tensor, kernel_size, stride=Non
                        ceil_mode: bool = False, indices: torch.Tensor | None = None) -> Prepared:
     _need_cuda(x, y, indices)
     win, a3 = _arr(_window(kernel_size, stride, padding, dilation))
-    shape, a0 = _arr(list(x.shape))
-    xs, a1 = _arr(list(x.stride()))
-    ys, a2 = _arr(list(y.stride()))
+    shape, a0 = _arr(x.shape)
+    xs, a1 = _arr(x.stride())
+    ys, a2 = _arr(y.stride())
     args = (ctypes.c_void_p(x.data_ptr()), _dtype(x), ctypes.c_void_p(y.data_ptr()),
             ctypes.c_void_p(indices.data_ptr() if indices is not None else None), x.dim(), shape, xs, ys, win,
             int(ceil_mode), _stream(x))
@@ -415,9 +474,9 @@ def prepare_max_pool2d(x: torch.Tensor, y: torch.Tensor, kernel_size, stride=Non
 def prepare_adaptive_avgpool2d(x: torch.Tensor, y: torch.Tensor) -> Prepared:
     _need_cuda(x, y)
     oh, ow = y.shape[-2], y.shape[-1]
-    shape, a0 = _arr(list(x.shape))
-    xs, a1 = _arr(list(x.stride()))
-    ys, a2 = _arr(list(y.stride()))
+    shape, a0 = _arr(x.shape)
+    xs, a1 = _arr(x.stride())
+    ys, a2 = _arr(y.stride())
     args = (ctypes.c_void_p(x.data_ptr()), _dtype(x), ctypes.c_void_p(y.data_ptr()), x.dim(), shape, xs, ys, oh, ow,
             _stream(x))
     return Prepared(lib().kf_adaptive_avgpool2d, args, (x, y, a0, a1, a2))
