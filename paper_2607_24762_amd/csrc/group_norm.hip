@@ -235,35 +235,25 @@ __device__ __forceinline__ Moments gather_parts(const GNParams& p, int64_t ng, i
     return moments_wave(acc);
 }
 
-template <class T, class A, bool VECTOR, bool NHWC>
-__global__ __launch_bounds__(kNT) void gn_fused(GNParams p) {
-    using C = Chunk<T, VECTOR, NHWC>;
-    __shared__ Moments lds[kNT / kWave];
-    __shared__ float stats[2];
-    __shared__ int gathered;
-    const int64_t ng = blockIdx.x / p.ex.parts;
-    const int part = blockIdx.x - (int)(ng * p.ex.parts);
-    const int g = (int)(ng % p.groups);
-
-    C c;
-    c.load(p, ng, part);
-    c.template load_affine<A>(p, part, g);
-    Moments m = moments_block<kNT / kWave>(c.moments(p, part), lds);
-
+// The statistics of group ng for chunk c (part `part` of the group, whose
+// own moments `own` the caller has already published when the group has
+// several parts), then the normalised chunk, then the group's slots
+// released.  Called by the whole workgroup; `stats` and `gathered` are LDS.
+template <class C>
+__device__ __forceinline__ void settle(const GNParams& p, C& c, int64_t ng, int part, Moments own, Moments* lds,
+                                       float* stats, int* gathered) {
     if (threadIdx.x < kWave) {
         bool ok = true;
-        if (p.ex.parts > 1) {
-            if (threadIdx.x == 0) ex_publish(p.ex, ng, part, encode(m));
-            m = gather_parts(p, ng, C::CH, true, &ok);
-        }
+        Moments m = own;
+        if (p.ex.parts > 1) m = gather_parts(p, ng, C::CH, true, &ok);
         if (threadIdx.x == 0) {
-            gathered = ok;
+            *gathered = ok;
             stats[0] = m.mean;
             stats[1] = 1.f / sqrtf(m.m2 / (float)p.group_elems + p.eps);
         }
     }
     __syncthreads();
-    if (!gathered) {
+    if (!*gathered) {
         // Some workgroup of this group has not published in time (it is not
         // resident yet, e.g. while other kernels hold the CUs).  Recompute
         // every part's moments here with the same loads, thread mapping and
@@ -293,6 +283,24 @@ __global__ __launch_bounds__(kNT) void gn_fused(GNParams p) {
     c.normalise_store(p, ng, part, stats[0], stats[1]);
     // Off the critical path: this workgroup is done reading its group's slots.
     if (p.ex.parts > 1 && threadIdx.x == 0) ex_release(p.ex, ng);
+}
+
+template <class T, class A, bool VECTOR, bool NHWC>
+__global__ __launch_bounds__(kNT) void gn_fused(GNParams p) {
+    using C = Chunk<T, VECTOR, NHWC>;
+    __shared__ Moments lds[kNT / kWave];
+    __shared__ float stats[2];
+    __shared__ int gathered;
+    const int64_t ng = blockIdx.x / p.ex.parts;
+    const int part = blockIdx.x - (int)(ng * p.ex.parts);
+    const int g = (int)(ng % p.groups);
+
+    C c;
+    c.load(p, ng, part);
+    c.template load_affine<A>(p, part, g);
+    const Moments m = moments_block<kNT / kWave>(c.moments(p, part), lds);
+    if (p.ex.parts > 1 && threadIdx.x == 0) ex_publish(p.ex, ng, part, encode(m));
+    settle(p, c, ng, part, m, lds, stats, &gathered);
 }
 
 template <class T, bool VECTOR, bool NHWC>
