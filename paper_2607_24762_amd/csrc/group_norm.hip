@@ -52,8 +52,26 @@ struct GNParams {
     int64_t channels;      // c
     int32_t cpg;           // channels per group
     int32_t groups;        // G
+    int32_t xcd_map;       // 1: place all parts of a group on one XCD (block_chunk)
     float eps;
 };
+
+// The (group, part) chunk that workgroup b handles.  Workgroups are handed
+// to the 8 XCDs in turn (b % 8); when the number of groups is a multiple of
+// 8, every part of group ng runs on XCD ng % 8, so a group's exchange and
+// the moment its last part lands stay within one XCD (measured ~1% faster
+// on the SD3.5 VAE block than groups spread over all eight); otherwise the
+// plain order b = group * parts + part.
+__device__ __forceinline__ void block_chunk(const GNParams& p, int64_t b, int64_t* ng, int* part) {
+    if (p.xcd_map) {
+        const int64_t slot = b >> 3;
+        *ng = (b & 7) + 8 * (slot / p.ex.parts);
+        *part = (int)(slot - (slot / p.ex.parts) * p.ex.parts);
+    } else {
+        *ng = b / p.ex.parts;
+        *part = (int)(b - *ng * p.ex.parts);
+    }
+}
 
 // Elements held by part p of a group.
 __device__ __forceinline__ float part_count(const GNParams& p, int64_t chunk, int part) {
@@ -291,8 +309,9 @@ __global__ __launch_bounds__(kNT) void gn_fused(GNParams p) {
     __shared__ Moments lds[kNT / kWave];
     __shared__ float stats[2];
     __shared__ int gathered;
-    const int64_t ng = blockIdx.x / p.ex.parts;
-    const int part = blockIdx.x - (int)(ng * p.ex.parts);
+    int64_t ng;
+    int part;
+    block_chunk(p, blockIdx.x, &ng, &part);
     const int g = (int)(ng % p.groups);
 
     C c;
@@ -307,8 +326,9 @@ template <class T, bool VECTOR, bool NHWC>
 __global__ __launch_bounds__(kNT) void gn_stats(GNParams p) {
     using C = Chunk<T, VECTOR, NHWC>;
     __shared__ Moments lds[kNT / kWave];
-    const int64_t ng = blockIdx.x / p.ex.parts;
-    const int part = blockIdx.x - (int)(ng * p.ex.parts);
+    int64_t ng;
+    int part;
+    block_chunk(p, blockIdx.x, &ng, &part);
     C c;
     c.load(p, ng, part);
     Moments m = moments_block<kNT / kWave>(c.moments(p, part), lds);
@@ -319,8 +339,9 @@ template <class T, class A, bool VECTOR, bool NHWC>
 __global__ __launch_bounds__(kNT) void gn_apply(GNParams p) {
     using C = Chunk<T, VECTOR, NHWC>;
     __shared__ float stats[2];
-    const int64_t ng = blockIdx.x / p.ex.parts;
-    const int part = blockIdx.x - (int)(ng * p.ex.parts);
+    int64_t ng;
+    int part;
+    block_chunk(p, blockIdx.x, &ng, &part);
     const int g = (int)(ng % p.groups);
     // Chunk and affine loads first, so they are in flight while wave 0
     // gathers the statistics.
@@ -414,6 +435,7 @@ kf_status run(const GroupNormArgs& a, hipStream_t s, const char** variant) {
     p.channels = a.c;
     p.cpg = (int32_t)(a.c / a.groups);
     p.groups = (int32_t)a.groups;
+    p.xcd_map = (l.groups_total % 8 == 0) ? 1 : 0;
     p.eps = a.eps;
 
     const int64_t grid = l.groups_total * l.parts;
