@@ -298,9 +298,13 @@ __device__ __forceinline__ void settle(const GNParams& p, C& c, int64_t ng, int 
         c.load(p, ng, part);
         __syncthreads();
     }
+    // This workgroup is done reading its group's slots: count it out before
+    // the stores, so the atomic's round trip overlaps them.
+    const bool leaves = p.ex.parts > 1 && threadIdx.x == 0;
+    unsigned before = 0;
+    if (leaves) before = ex_depart(p.ex, ng);
     c.normalise_store(p, ng, part, stats[0], stats[1]);
-    // Off the critical path: this workgroup is done reading its group's slots.
-    if (p.ex.parts > 1 && threadIdx.x == 0) ex_release(p.ex, ng);
+    if (leaves) ex_leave(p.ex, ng, before);
 }
 
 template <class T, class A, bool VECTOR, bool NHWC>

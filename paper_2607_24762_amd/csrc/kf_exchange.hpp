@@ -57,19 +57,27 @@ __device__ __forceinline__ uint64_t ex_poll(const Exchange& ex, int64_t unit, in
     return w;
 }
 
-// Called by one thread of every workgroup of `unit` once the workgroup has
-// read all the unit's slots (its loads returned before the merge that
-// precedes this): the last one to arrive empties the slots and the counter.
-__device__ __forceinline__ void ex_release(const Exchange& ex, int64_t unit) {
-    unsigned* c = ex_counter(ex, unit);
-    const unsigned left = __hip_atomic_fetch_add(c, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    if (left == (unsigned)ex.parts - 1) {
+// Departure, in two steps, by one thread of every workgroup of `unit` once
+// the workgroup has read all the unit's slots (its loads returned before the
+// merge that precedes this).  ex_depart counts the workgroup out and returns
+// how many had left before it; ex_leave, given that count, lets the last one
+// empty the slots and the counter.  Callers put their own stores between the
+// two, so the atomic's round trip overlaps them instead of ending the
+// workgroup's life.
+__device__ __forceinline__ unsigned ex_depart(const Exchange& ex, int64_t unit) {
+    return __hip_atomic_fetch_add(ex_counter(ex, unit), 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ __forceinline__ void ex_leave(const Exchange& ex, int64_t unit, unsigned departed_before) {
+    if (departed_before == (unsigned)ex.parts - 1) {
         uint64_t* slots = ex.slot + unit * ex.parts;
         for (int q = 0; q < ex.parts; ++q)
             __hip_atomic_store(slots + q, (uint64_t)0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        __hip_atomic_store(c, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(ex_counter(ex, unit), 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
 }
+
+__device__ __forceinline__ void ex_release(const Exchange& ex, int64_t unit) { ex_leave(ex, unit, ex_depart(ex, unit)); }
 
 __device__ __forceinline__ void ex_flag_timeout(const Exchange& ex) {
     __hip_atomic_store(ex.error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);

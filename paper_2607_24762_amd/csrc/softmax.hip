@@ -579,10 +579,13 @@ __global__ __launch_bounds__(kSplitNT) void sm_split(SplitParams p) {
         c.load(p, r0, part);
         __syncthreads();
     }
-    // A row of only -inf has M = -inf, so x - M is NaN: a NaN row, as the
-    // definition gives.
+    // Done reading the row's slots: count this workgroup out before the
+    // stores, so the atomic's round trip overlaps them.  A row of only -inf
+    // has M = -inf, so x - M is NaN: a NaN row, as the definition gives.
+    unsigned before = 0;
+    if (threadIdx.x == 0) before = ex_depart(p.ex, row);
     c.template store<TO>(p, r0, part, stat[0], stat[1]);
-    if (threadIdx.x == 0) ex_release(p.ex, row);  // done reading the row's slots
+    if (threadIdx.x == 0) ex_leave(p.ex, row, before);
 }
 
 // --------------------------------------------------------------------------
