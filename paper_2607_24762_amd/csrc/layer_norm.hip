@@ -18,6 +18,8 @@
 // the sums); stores are non-temporal.
 #include <math.h>
 
+#include <type_traits>
+
 #include "kf_device.hpp"
 #include "kf_internal.h"
 
@@ -36,6 +38,11 @@ __device__ __forceinline__ void load_affine_span(const void* p, int64_t e, float
         for (int i = 0; i < VEC; ++i) out[i] = load1<A>(p, e + i);
     }
 }
+
+// Affine type of a call with neither weight nor bias: the kernels then hold
+// no affine registers (no 16-byte weight / bias slots per element), which
+// raises occupancy.
+struct NoAffine {};
 
 struct LNArgsDev {
     const void* x;
@@ -79,25 +86,37 @@ template <class T, class A, int NV, int VEC, bool VECTOR>
 __device__ __forceinline__ void normalise_slots(const LNArgsDev& p, int64_t base, const int (&e0)[NV],
                                                 const bool (&ok)[NV], float (&v)[NV][VEC], float mean,
                                                 float rstd) {
-    float wv[NV][VEC], bv[NV][VEC];
-    if (p.w) {
+    if constexpr (std::is_same_v<A, NoAffine>) {
 #pragma unroll
-        for (int k = 0; k < NV; ++k) load_affine_span<A, VEC, VECTOR>(p.w, ok[k] ? e0[k] : 0, wv[k]);
-    }
-    if (p.b) {
+        for (int k = 0; k < NV; ++k) {
+            if (ok[k]) {
 #pragma unroll
-        for (int k = 0; k < NV; ++k) load_affine_span<A, VEC, VECTOR>(p.b, ok[k] ? e0[k] : 0, bv[k]);
-    }
-#pragma unroll
-    for (int k = 0; k < NV; ++k) {
-        if (ok[k]) {
-#pragma unroll
-            for (int i = 0; i < VEC; ++i) {
-                const float a = p.w ? rstd * wv[k][i] : rstd;
-                v[k][i] = fmaf(v[k][i] - mean, a, p.b ? bv[k][i] : 0.f);
+                for (int i = 0; i < VEC; ++i) v[k][i] = (v[k][i] - mean) * rstd;
+                if constexpr (VECTOR) store_vec<T, true>(p.y, base + e0[k], v[k]);
+                else store1<T>(p.y, base + e0[k], v[k][0]);
             }
-            if constexpr (VECTOR) store_vec<T, true>(p.y, base + e0[k], v[k]);
-            else store1<T>(p.y, base + e0[k], v[k][0]);
+        }
+    } else {
+        float wv[NV][VEC], bv[NV][VEC];
+        if (p.w) {
+#pragma unroll
+            for (int k = 0; k < NV; ++k) load_affine_span<A, VEC, VECTOR>(p.w, ok[k] ? e0[k] : 0, wv[k]);
+        }
+        if (p.b) {
+#pragma unroll
+            for (int k = 0; k < NV; ++k) load_affine_span<A, VEC, VECTOR>(p.b, ok[k] ? e0[k] : 0, bv[k]);
+        }
+#pragma unroll
+        for (int k = 0; k < NV; ++k) {
+            if (ok[k]) {
+#pragma unroll
+                for (int i = 0; i < VEC; ++i) {
+                    const float a = p.w ? rstd * wv[k][i] : rstd;
+                    v[k][i] = fmaf(v[k][i] - mean, a, p.b ? bv[k][i] : 0.f);
+                }
+                if constexpr (VECTOR) store_vec<T, true>(p.y, base + e0[k], v[k]);
+                else store1<T>(p.y, base + e0[k], v[k][0]);
+            }
         }
     }
 }
@@ -230,6 +249,12 @@ const char* launch(const LNArgsDev& p, hipStream_t s) {
     KF_LN_WAVE(16, 2)
     KF_LN_WAVE(16, 4)
     KF_LN_WAVE(32, 4)
+    // Rows of 129-192 slots (the SD3.5 width): two rows per wave measured
+    // 9.4 us against 10.2 us for one (bf16 [2,4096,1536], no affine); with
+    // affine registers it would drop to 3 waves per SIMD, so only then.
+    if constexpr (std::is_same_v<A, NoAffine>) {
+        KF_LN_WAVE(32, 6)
+    }
     KF_LN_WAVE(64, 3)
     KF_LN_WAVE(64, 4)
     KF_LN_BLOCK(128, 3)
@@ -271,12 +296,15 @@ kf_status run(const LayerNormArgs& a, hipStream_t s, const char** variant) {
 
 kf_status layer_norm_launch(const LayerNormArgs& a, hipStream_t s, const char** variant) {
     const bool f32_affine = (a.at == KF_FLOAT32);
+    const bool affine = a.weight || a.bias;
     switch (a.xt) {
         case KF_FLOAT32:
-            return run<F32, F32>(a, s, variant);
+            return affine ? run<F32, F32>(a, s, variant) : run<F32, NoAffine>(a, s, variant);
         case KF_BFLOAT16:
+            if (!affine) return run<BF16, NoAffine>(a, s, variant);
             return f32_affine ? run<BF16, F32>(a, s, variant) : run<BF16, BF16>(a, s, variant);
         case KF_FLOAT16:
+            if (!affine) return run<F16, NoAffine>(a, s, variant);
             return f32_affine ? run<F16, F32>(a, s, variant) : run<F16, F16>(a, s, variant);
     }
     set_error("layer_norm: unsupported dtype");

@@ -73,6 +73,19 @@ def test_widths(d, dt):
     assert variant.startswith("ln_"), variant
 
 
+@pytest.mark.parametrize("dt", ["bf16", "f32"])
+@pytest.mark.parametrize("d", [8, 256, 1000, 1024, 1536, 1544, 2048, 4096, 16384, 65536])
+def test_widths_without_affine(d, dt):
+    # No weight and no bias select the kernels that hold no affine registers
+    # (and, for rows of 129-192 slots, two rows per wave).
+    rows = 37 if d <= 8192 else 3
+    note(f"layer_norm no affine rows={rows} d={d} {dt}")
+    _, variant = run((rows, d), 1, dt, affine="none", seed=d + 1)
+    assert variant.startswith("ln_"), variant
+    if d == 1536 and dt == "bf16":
+        assert variant == "ln_wave_vec_lpr32_nv6", variant
+
+
 @pytest.mark.parametrize("affine", ["f32", "w", "b", "none"])
 def test_affine_variants(affine):
     note(f"layer_norm affine={affine}")
