@@ -238,7 +238,11 @@ kf_status kf_adaptive_avgpool2d(const void* x, kf_dtype dtype, void* y, int32_t 
  * Section IV-C).  Output (i, j) of a plane is the maximum over rows
  * i*sh - ph + a*dh (a < kh) and columns j*sw - pw + b*dw (b < kw) that lie
  * inside the plane (padding is never chosen); NaN wins over any number.
- * The result is the selected input element, bit for bit.
+ * With indices, the result is the selected input element, bit for bit.
+ * Without them (indices NULL) a running maximum is kept instead, so two
+ * results differ from the selected element's bits: a window whose maximum
+ * is a zero may give +0 where the first maximum is -0 (the two compare
+ * equal), and a window holding NaN gives the default quiet NaN.
  *
  *  x        device pointer, shape [N, C, H, W] or [C, H, W], H, W >= 1,
  *           H * W < 2^31; dtype FLOAT32, BFLOAT16 or FLOAT16; dense NCHW, or

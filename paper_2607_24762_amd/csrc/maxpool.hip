@@ -62,7 +62,7 @@ struct alignas(16) Lanes {
     R v[N];
 };
 
-// The running choice of one window.
+// The running choice of one window, with its position (indices wanted).
 template <class T>
 struct Pick {
     float best = -INFINITY;
@@ -90,7 +90,59 @@ struct Pick {
         bits = take ? raw : bits;
         at = (take | first) ? pos : at;
     }
+    __device__ __forceinline__ uint32_t result() const { return bits; }
+    __device__ __forceinline__ int32_t index() const { return at; }
 };
+
+// Canonical quiet NaN of each storage format.
+template <class T>
+constexpr uint32_t kQuietNaN = 0x7fc00000u;
+template <>
+constexpr uint32_t kQuietNaN<BF16> = 0x7fc0u;
+template <>
+constexpr uint32_t kQuietNaN<F16> = 0x7e00u;
+
+// The value-only choice (no indices wanted): the window's maximum and
+// whether it held a NaN.  Every element of a window converts to float
+// exactly, so the maximum converts back exactly; a NaN window yields the
+// canonical quiet NaN, and where +0 and -0 tie the result may be +0 (the
+// two compare equal).  Two instructions per element instead of Pick's
+// compare-and-select chain.
+template <class T>
+struct MaxOnly {
+    float best = -INFINITY;
+    bool nan = false;
+    __device__ __forceinline__ void consider(uint32_t raw, int32_t) {
+        const float v = Raw<T>::value(raw);
+        best = fmaxf(best, v);
+        nan = nan | (v != v);
+    }
+    __device__ __forceinline__ void consider_if(bool valid, uint32_t raw, int32_t) {
+        const float v = Raw<T>::value(raw);
+        best = valid ? fmaxf(best, v) : best;
+        nan = nan | (valid & (v != v));
+    }
+    __device__ __forceinline__ uint32_t result() const {
+        if (nan) return kQuietNaN<T>;
+        if constexpr (std::is_same_v<T, F32>) return __float_as_uint(best);
+        else if constexpr (std::is_same_v<T, BF16>) return __float_as_uint(best) >> 16;
+        else return (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)best);
+    }
+    __device__ __forceinline__ int32_t index() const { return -1; }
+};
+
+template <class T>
+__device__ __forceinline__ MaxOnly<T> merge(const MaxOnly<T>& a, const MaxOnly<T>& b) {
+    MaxOnly<T> m;
+    m.best = fmaxf(a.best, b.best);
+    m.nan = a.nan | b.nan;
+    return m;
+}
+
+// Selection rule of a kernel: with indices the position-tracking Pick, else
+// the value-only maximum.
+template <class T, bool IDX>
+using Select = std::conditional_t<IDX, Pick<T>, MaxOnly<T>>;
 
 // Merge of two picks over consecutive stretches of the row-major scan (a
 // before b): scanning b's elements after a's moves to b's pick exactly when
@@ -150,7 +202,7 @@ __device__ __forceinline__ const R* band_src(const MPParams& p, const Band& b) {
 // Scan the band's windows from LDS and write its outputs.  K > 0: a K x K
 // window known at compile time, so the loops unroll and the K*K LDS reads
 // of an output issue together.
-template <class T, int K, class R>
+template <class T, int K, bool IDX, class R>
 __device__ __forceinline__ void band_outputs(const MPParams& p, const Band& b, const R* tile) {
     const int outs = (b.o1 - b.o0) * p.ow;
     R* dst = static_cast<R*>(p.y) + b.plane * p.oh * p.ow + (int64_t)b.o0 * p.ow;
@@ -160,7 +212,7 @@ __device__ __forceinline__ void band_outputs(const MPParams& p, const Band& b, c
     int i = b.o0 + (int)threadIdx.x / p.ow, j = (int)threadIdx.x - ((int)threadIdx.x / p.ow) * p.ow;
     const int di = kNT / p.ow, dj = kNT - di * p.ow;
     for (int q = threadIdx.x; q < outs; q += kNT) {
-        Pick<T> pk;
+        Select<T, IDX> pk;
         // Positions outside the plane read the tile's first element and
         // are skipped (the tile always holds at least one row).
         auto at = [&](int a, int c) {
@@ -178,8 +230,8 @@ __device__ __forceinline__ void band_outputs(const MPParams& p, const Band& b, c
             for (int a = 0; a < p.kh; ++a)
                 for (int c = 0; c < p.kw; ++c) at(a, c);
         }
-        __builtin_nontemporal_store((R)pk.bits, dst + q);
-        if (idx) __builtin_nontemporal_store((int64_t)pk.at, idx + q);
+        __builtin_nontemporal_store((R)pk.result(), dst + q);
+        if constexpr (IDX) __builtin_nontemporal_store((int64_t)pk.index(), idx + q);
         i += di;
         j += dj;
         if (j >= p.ow) {
@@ -206,7 +258,7 @@ __device__ __forceinline__ int tile_col(int c, int half) {
     else return c;
 }
 
-template <class T, int K, int S, class R>
+template <class T, int K, int S, bool IDX, class R>
 __device__ __forceinline__ void band_outputs_strip(const MPParams& p, const Band& b, const R* tile) {
     const int half = (p.w + 1) >> 1;
     const int rows = b.o1 - b.o0;
@@ -228,7 +280,7 @@ __device__ __forceinline__ void band_outputs_strip(const MPParams& p, const Band
         // All K reads of a row issue before the fold (rows outside the
         // plane read the tile's first row and are skipped).
         auto row_pick = [&](int r) {
-            Pick<T> pk;
+            Select<T, IDX> pk;
             const bool r_ok = r >= 0 && r < p.h;
             const R* row = tile + (r_ok ? r - b.r_lo : 0) * p.w;
             uint32_t raw[K];
@@ -238,7 +290,7 @@ __device__ __forceinline__ void band_outputs_strip(const MPParams& p, const Band
             for (int c = 0; c < K; ++c) pk.consider_if(r_ok && col_ok[c], raw[c], r * p.w + col[c]);
             return pk;
         };
-        Pick<T> rp[K];  // row picks of the current output's K rows
+        Select<T, IDX> rp[K];  // row picks of the current output's K rows
 #pragma unroll
         for (int a = 0; a < K; ++a) rp[a] = row_pick(i0 * S - p.ph + a);
         for (int i = i0; i < i1; ++i) {
@@ -253,12 +305,12 @@ __device__ __forceinline__ void band_outputs_strip(const MPParams& p, const Band
                     for (int a = 0; a < K; ++a) rp[a] = row_pick(i * S - p.ph + a);
                 }
             }
-            Pick<T> pk = rp[0];
+            Select<T, IDX> pk = rp[0];
 #pragma unroll
             for (int a = 1; a < K; ++a) pk = merge(pk, rp[a]);
             const int64_t o = (int64_t)i * p.ow + j;
-            __builtin_nontemporal_store((R)pk.bits, dst + o);
-            if (idx) __builtin_nontemporal_store((int64_t)pk.at, idx + o);
+            __builtin_nontemporal_store((R)pk.result(), dst + o);
+            if constexpr (IDX) __builtin_nontemporal_store((int64_t)pk.index(), idx + o);
         }
     }
 }
@@ -316,13 +368,13 @@ __device__ __forceinline__ void stage_store(const MPParams& p, const Band& b, co
 }
 
 // S > 0: the strip form above (K x K, stride S, no dilation).
-template <class T, int K, int S, class R>
+template <class T, int K, int S, bool IDX, class R>
 __device__ __forceinline__ void band_scan(const MPParams& p, const Band& b, const R* tile) {
-    if constexpr (S > 0) band_outputs_strip<T, K, S>(p, b, tile);
-    else band_outputs<T, K>(p, b, tile);
+    if constexpr (S > 0) band_outputs_strip<T, K, S, IDX>(p, b, tile);
+    else band_outputs<T, K, IDX>(p, b, tile);
 }
 
-template <class T, bool VECTOR, int K, int S>
+template <class T, bool VECTOR, int K, int S, bool IDX>
 __global__ __launch_bounds__(kNT) void mp_band(MPParams p) {
     using R = typename Raw<T>::type;
     extern __shared__ u32x4 lds_vec[];
@@ -343,7 +395,7 @@ __global__ __launch_bounds__(kNT) void mp_band(MPParams p) {
                 nb = band_of(p, next);
                 stage_load<R>(p, nb, r);  // in flight while this band is scanned
             }
-            band_scan<T, K, S>(p, b, tile);
+            band_scan<T, K, S, IDX>(p, b, tile);
             if (next >= items) break;
             __syncthreads();  // the tile is rewritten next
             item = next;
@@ -358,7 +410,7 @@ __global__ __launch_bounds__(kNT) void mp_band(MPParams p) {
                 tile[rr * p.w + tile_col<S>(c, half)] = src[e];
             }
             __syncthreads();
-            band_scan<T, K, S>(p, b, tile);
+            band_scan<T, K, S, IDX>(p, b, tile);
             item += gridDim.x;
             if (item >= items) break;
             __syncthreads();
@@ -398,7 +450,7 @@ __global__ __launch_bounds__(kNT) void mp_direct(MPParams p) {
 // channels when c is whole vectors and the bases are aligned, else 1.
 // blockIdx.y is the sample; inside a sample every index fits 32 bits
 // (checked on the host), so the index arithmetic is 32-bit.
-template <class T, int VEC, int K>
+template <class T, int VEC, int K, bool IDX>
 __global__ __launch_bounds__(kNT) void mp_nhwc(MPParams p) {
     using R = typename Raw<T>::type;
     const uint32_t cvs = (uint32_t)p.c / VEC;
@@ -410,7 +462,7 @@ __global__ __launch_bounds__(kNT) void mp_nhwc(MPParams p) {
     const int j = (int)(pix - (uint32_t)i * (uint32_t)p.ow);
     const int64_t nn = blockIdx.y;
     const R* xs = static_cast<const R*>(p.x);
-    Pick<T> pk[VEC];
+    Select<T, IDX> pk[VEC];
     auto load = [&](int r, int col) {
         const int64_t e = ((nn * p.h + r) * p.w + col) * p.c + (int64_t)cv * VEC;
         Lanes<R, VEC> v;
@@ -457,15 +509,15 @@ __global__ __launch_bounds__(kNT) void mp_nhwc(MPParams p) {
     const int64_t o = (nn * p.oh * p.ow + pix) * p.c + (int64_t)cv * VEC;
     Lanes<R, VEC> out;
 #pragma unroll
-    for (int k = 0; k < VEC; ++k) out.v[k] = (R)pk[k].bits;
+    for (int k = 0; k < VEC; ++k) out.v[k] = (R)pk[k].result();
     if constexpr (VEC == 1) {
         __builtin_nontemporal_store(out.v[0], static_cast<R*>(p.y) + o);
     } else {
         __builtin_nontemporal_store(__builtin_bit_cast(u32x4, out), reinterpret_cast<u32x4*>(static_cast<R*>(p.y) + o));
     }
-    if (p.idx) {
+    if constexpr (IDX) {
 #pragma unroll
-        for (int k = 0; k < VEC; ++k) __builtin_nontemporal_store((int64_t)pk[k].at, p.idx + o + k);
+        for (int k = 0; k < VEC; ++k) __builtin_nontemporal_store((int64_t)pk[k].index(), p.idx + o + k);
     }
 }
 
@@ -506,17 +558,26 @@ kf_status run(const MaxPoolArgs& a, hipStream_t s, const char** variant) {
         const dim3 grid((unsigned)((per_sample + kNT - 1) / kNT), (unsigned)a.n);
         const int k = (a.kh == a.kw && (a.kh == 2 || a.kh == 3)) ? a.kh : 0;
         auto go = [&](auto kernel) { hipLaunchKernelGGL(kernel, grid, dim3(kNT), 0, s, p); };
-        if (vec) {
-            if (k == 3) go(mp_nhwc<T, VEC, 3>);
-            else if (k == 2) go(mp_nhwc<T, VEC, 2>);
-            else go(mp_nhwc<T, VEC, 0>);
-            *variant = k == 3 ? "mp_nhwc_vec_k3" : k == 2 ? "mp_nhwc_vec_k2" : "mp_nhwc_vec";
-        } else {
-            if (k == 3) go(mp_nhwc<T, 1, 3>);
-            else if (k == 2) go(mp_nhwc<T, 1, 2>);
-            else go(mp_nhwc<T, 1, 0>);
-            *variant = k == 3 ? "mp_nhwc_scalar_k3" : k == 2 ? "mp_nhwc_scalar_k2" : "mp_nhwc_scalar";
-        }
+        auto pick = [&](auto idx_tag) {
+            constexpr bool I = decltype(idx_tag)::value;
+            if (vec) {
+                if (k == 3) go(mp_nhwc<T, VEC, 3, I>);
+                else if (k == 2) go(mp_nhwc<T, VEC, 2, I>);
+                else go(mp_nhwc<T, VEC, 0, I>);
+            } else {
+                if (k == 3) go(mp_nhwc<T, 1, 3, I>);
+                else if (k == 2) go(mp_nhwc<T, 1, 2, I>);
+                else go(mp_nhwc<T, 1, 0, I>);
+            }
+        };
+        if (a.idx) pick(std::true_type{});
+        else pick(std::false_type{});
+        static const char* names[2][2][3] = {
+            {{"mp_nhwc_scalar", "mp_nhwc_scalar_k2", "mp_nhwc_scalar_k3"},
+             {"mp_nhwc_vec", "mp_nhwc_vec_k2", "mp_nhwc_vec_k3"}},
+            {{"mp_nhwc_scalar_idx", "mp_nhwc_scalar_k2_idx", "mp_nhwc_scalar_k3_idx"},
+             {"mp_nhwc_vec_idx", "mp_nhwc_vec_k2_idx", "mp_nhwc_vec_k3_idx"}}};
+        *variant = names[a.idx ? 1 : 0][vec ? 1 : 0][k == 0 ? 0 : k - 1];
     } else {
         // Output rows per band: as many as keep the band's input rows within
         // kBandBytes, then evened out over the plane's bands.
@@ -544,25 +605,35 @@ kf_status run(const MaxPoolArgs& a, hipStream_t s, const char** variant) {
                                ((k == 3 && (a.sh == 1 || a.sh == 2)) || (k == 2 && a.sh == 2));
             const int sv = strip ? a.sh : 0;
             auto go = [&](auto kernel) { hipLaunchKernelGGL(kernel, dim3((unsigned)grid), dim3(kNT), lds, s, p); };
-            auto pick = [&](auto vec_tag) {
-                constexpr bool V = decltype(vec_tag)::value;
-                if (k == 3 && sv == 2) go(mp_band<T, V, 3, 2>);
-                else if (k == 3 && sv == 1) go(mp_band<T, V, 3, 1>);
-                else if (k == 2 && sv == 2) go(mp_band<T, V, 2, 2>);
-                else if (k == 3) go(mp_band<T, V, 3, 0>);
-                else if (k == 2) go(mp_band<T, V, 2, 0>);
-                else go(mp_band<T, V, 0, 0>);
+            auto pick = [&](auto vec_tag, auto idx_tag) {
+                constexpr bool V = decltype(vec_tag)::value, I = decltype(idx_tag)::value;
+                if (k == 3 && sv == 2) go(mp_band<T, V, 3, 2, I>);
+                else if (k == 3 && sv == 1) go(mp_band<T, V, 3, 1, I>);
+                else if (k == 2 && sv == 2) go(mp_band<T, V, 2, 2, I>);
+                else if (k == 3) go(mp_band<T, V, 3, 0, I>);
+                else if (k == 2) go(mp_band<T, V, 2, 0, I>);
+                else go(mp_band<T, V, 0, 0, I>);
             };
-            if (vec) pick(std::true_type{});
-            else pick(std::false_type{});
-            static const char* names[2][3][3] = {
-                {{"mp_band_scalar", "mp_band_scalar", "mp_band_scalar"},
-                 {"mp_band_scalar_k2", "mp_band_scalar_k2", "mp_band_scalar_k2_strip_s2"},
-                 {"mp_band_scalar_k3", "mp_band_scalar_k3_strip_s1", "mp_band_scalar_k3_strip_s2"}},
-                {{"mp_band_vec", "mp_band_vec", "mp_band_vec"},
-                 {"mp_band_vec_k2", "mp_band_vec_k2", "mp_band_vec_k2_strip_s2"},
-                 {"mp_band_vec_k3", "mp_band_vec_k3_strip_s1", "mp_band_vec_k3_strip_s2"}}};
-            *variant = names[vec ? 1 : 0][k == 0 ? 0 : k - 1][sv];
+            auto with_idx = [&](auto vec_tag) {
+                if (a.idx) pick(vec_tag, std::true_type{});
+                else pick(vec_tag, std::false_type{});
+            };
+            if (vec) with_idx(std::true_type{});
+            else with_idx(std::false_type{});
+            static const char* names[2][2][3][3] = {
+                {{{"mp_band_scalar", "mp_band_scalar", "mp_band_scalar"},
+                  {"mp_band_scalar_k2", "mp_band_scalar_k2", "mp_band_scalar_k2_strip_s2"},
+                  {"mp_band_scalar_k3", "mp_band_scalar_k3_strip_s1", "mp_band_scalar_k3_strip_s2"}},
+                 {{"mp_band_vec", "mp_band_vec", "mp_band_vec"},
+                  {"mp_band_vec_k2", "mp_band_vec_k2", "mp_band_vec_k2_strip_s2"},
+                  {"mp_band_vec_k3", "mp_band_vec_k3_strip_s1", "mp_band_vec_k3_strip_s2"}}},
+                {{{"mp_band_scalar_idx", "mp_band_scalar_idx", "mp_band_scalar_idx"},
+                  {"mp_band_scalar_k2_idx", "mp_band_scalar_k2_idx", "mp_band_scalar_k2_strip_s2_idx"},
+                  {"mp_band_scalar_k3_idx", "mp_band_scalar_k3_strip_s1_idx", "mp_band_scalar_k3_strip_s2_idx"}},
+                 {{"mp_band_vec_idx", "mp_band_vec_idx", "mp_band_vec_idx"},
+                  {"mp_band_vec_k2_idx", "mp_band_vec_k2_idx", "mp_band_vec_k2_strip_s2_idx"},
+                  {"mp_band_vec_k3_idx", "mp_band_vec_k3_strip_s1_idx", "mp_band_vec_k3_strip_s2_idx"}}}};
+            *variant = names[a.idx ? 1 : 0][vec ? 1 : 0][k == 0 ? 0 : k - 1][sv];
         } else {
             const int64_t blocks = (p.planes * a.oh * a.ow + kNT - 1) / kNT;
             if (blocks > INT32_MAX) {

@@ -5,7 +5,12 @@ NCHW and channels last, a sweep of window shapes, strides, paddings,
 dilations and ceil mode over every kernel variant (LDS bands with vector and
 element staging, the direct fallback for wide planes, channels last with
 vector and element channel access), every dtype, special values (NaN, -inf,
-ties), 3-D inputs and empty batches."""
+ties), 3-D inputs and empty batches.  Every case runs twice: with indices
+(the kernels that track the winning position) and without (the value-only
+kernels, which keep a running max and a NaN flag); the values must agree
+with the oracle either way, with NaN at the same places and signed zeros
+compared by value, since a value-only call may return +0 for a window whose
+first maximum is -0."""
 import itertools
 
 import numpy as np
@@ -30,16 +35,25 @@ def gpu():
     kf355.lib()
 
 
-def check(x_cpu, x_gpu, k, s, p, d, ceil):
-    y, idx = kf355.kf_max_pool2d(x_gpu, k, s, p, d, ceil, return_indices=True)
-    torch.cuda.synchronize()
-    variant = kf355.last_variant()
-    ref, ref_idx = oracle.max_pool2d(x_cpu, k, s, p, d, ceil)
+def same_values(y, ref, variant):
     got = y.float().cpu().numpy().astype(np.float64)
     nan_r, nan_g = np.isnan(ref), np.isnan(got)
     assert np.array_equal(nan_r, nan_g), variant
     assert np.array_equal(got[~nan_g], ref[~nan_r]), (variant, float(np.abs(got[~nan_g] - ref[~nan_r]).max()))
+
+
+def check(x_cpu, x_gpu, k, s, p, d, ceil):
+    y, idx = kf355.kf_max_pool2d(x_gpu, k, s, p, d, ceil, return_indices=True)
+    torch.cuda.synchronize()
+    variant = kf355.last_variant()
+    y_only = kf355.kf_max_pool2d(x_gpu, k, s, p, d, ceil)
+    torch.cuda.synchronize()
+    variant_only = kf355.last_variant()
+    ref, ref_idx = oracle.max_pool2d(x_cpu, k, s, p, d, ceil)
+    same_values(y, ref, variant)
+    same_values(y_only, ref, variant_only)
     assert np.array_equal(idx.cpu().numpy(), ref_idx), variant
+    assert variant == variant_only == "mp_direct" or variant == variant_only + "_idx", (variant, variant_only)
     assert y.is_contiguous(memory_format=torch.channels_last) == x_gpu.is_contiguous(
         memory_format=torch.channels_last) or x_gpu.is_contiguous()
     return y, idx, variant
@@ -53,7 +67,7 @@ def test_resnet_stem(layout):
     if layout == "nhwc":
         x = x.contiguous(memory_format=torch.channels_last)
     y, idx, variant = check(w["x"], x, 3, 2, 1, 1, False)
-    assert variant == ("mp_band_vec_k3_strip_s2" if layout == "nchw" else "mp_nhwc_vec_k3"), variant
+    assert variant == ("mp_band_vec_k3_strip_s2_idx" if layout == "nchw" else "mp_nhwc_vec_k3_idx"), variant
     # Informational second reference: torch eager on the same GPU agrees bit for bit.
     ty, ti = F.max_pool2d(x, 3, 2, 1, return_indices=True)
     assert torch.equal(ty, y) and torch.equal(ti, idx)
@@ -136,3 +150,25 @@ def test_without_indices_matches_with():
     b, _ = kf355.kf_max_pool2d(x, 3, 2, 1, return_indices=True)
     torch.cuda.synchronize()
     assert torch.equal(a, b)
+
+
+@pytest.mark.parametrize("layout", ["nchw", "nhwc"])
+def test_signed_zero_and_nan_without_indices(layout):
+    """Value-only windows: -0 and +0 compare equal, so a window of zeros gives
+    a zero (either sign); a window holding NaN gives NaN whatever its
+    position among the other elements."""
+    note(f"max_pool2d value-only zeros/NaN {layout}")
+    x = torch.full((1, 4, 6, 6), -1.0)
+    x[0, 0] = -0.0
+    x[0, 1, ::2] = -0.0
+    x[0, 1, 1::2] = 0.0
+    x[0, 2, 0, 0] = float("nan")
+    x[0, 3, 5, 5] = float("nan")
+    xg = x.cuda()
+    if layout == "nhwc":
+        xg = xg.contiguous(memory_format=torch.channels_last)
+    y = kf355.kf_max_pool2d(xg, 3, 2, 1)
+    torch.cuda.synchronize()
+    ref, _ = oracle.max_pool2d(x.numpy().astype(np.float64), 3, 2, 1)
+    same_values(y, ref, kf355.last_variant())
+    assert torch.all(y[0, :2] == 0) and torch.isnan(y[0, 2, 0, 0]) and torch.isnan(y[0, 3, 2, 2])
