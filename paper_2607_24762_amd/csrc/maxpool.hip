@@ -446,21 +446,37 @@ __global__ __launch_bounds__(kNT) void mp_direct(MPParams p) {
 }
 
 // --------------------------------------------------------------------------
+// Workgroups go to the 8 XCDs in turn (dispatch order L goes to XCD L % 8).
+// xcd_contiguous renumbers them so that XCD x runs one contiguous range of
+// the T logical tiles: x gets q = T / 8 tiles, one more when x < T % 8, and
+// starts at x * q + min(x, T % 8).  A bijection on [0, T).
+__device__ __forceinline__ uint32_t xcd_contiguous(uint32_t L, uint32_t T) {
+    const uint32_t q = T >> 3, r = T & 7, x = L & 7;
+    return x * q + min(x, r) + (L >> 3);
+}
+
 // NHWC: thread per (output pixel, VEC channels).  VEC = 16 bytes of
-// channels when c is whole vectors and the bases are aligned, else 1.
-// blockIdx.y is the sample; inside a sample every index fits 32 bits
-// (checked on the host), so the index arithmetic is 32-bit.
+// channels when c is whole vectors and the bases are aligned, else 1.  The
+// grid is (tiles per sample, samples), renumbered with xcd_contiguous, so
+// tiles of neighbouring output rows, whose windows share input rows, run on
+// one XCD and find those rows in its L2 (in dispatch order they would land
+// on different XCDs and each fetch the shared rows again).  Inside a sample
+// every index fits 32 bits (checked on the host), so the index arithmetic
+// is 32-bit.
 template <class T, int VEC, int K, bool IDX>
 __global__ __launch_bounds__(kNT) void mp_nhwc(MPParams p) {
     using R = typename Raw<T>::type;
+    const uint32_t tiles = gridDim.x;
+    const uint32_t logical = xcd_contiguous(blockIdx.y * tiles + blockIdx.x, tiles * gridDim.y);
+    const uint32_t sample = logical / tiles;
     const uint32_t cvs = (uint32_t)p.c / VEC;
-    const uint32_t t = blockIdx.x * kNT + threadIdx.x;
+    const uint32_t t = (logical - sample * tiles) * kNT + threadIdx.x;
     if (t >= (uint32_t)p.oh * (uint32_t)p.ow * cvs) return;
     const uint32_t pix = t / cvs;
     const int cv = (int)(t - pix * cvs);
     const int i = (int)(pix / (uint32_t)p.ow);
     const int j = (int)(pix - (uint32_t)i * (uint32_t)p.ow);
-    const int64_t nn = blockIdx.y;
+    const int64_t nn = sample;
     const R* xs = static_cast<const R*>(p.x);
     Select<T, IDX> pk[VEC];
     auto load = [&](int r, int col) {
@@ -550,12 +566,13 @@ kf_status run(const MaxPoolArgs& a, hipStream_t s, const char** variant) {
     if (a.nhwc) {
         const bool vec = a.c % VEC == 0 && (uintptr_t)a.x % 16 == 0 && (uintptr_t)a.y % 16 == 0;
         const int64_t per_sample = a.oh * a.ow * (vec ? a.c / VEC : a.c);
-        if (per_sample > INT32_MAX || a.n > 65535) {
+        const int64_t tiles = (per_sample + kNT - 1) / kNT;
+        if (per_sample > INT32_MAX || a.n > 65535 || tiles * a.n > (int64_t)UINT32_MAX) {
             set_error("max_pool2d: %lld threads per sample or %lld samples exceed the channels-last grid",
                       (long long)per_sample, (long long)a.n);
             return KF_ERR_UNSUPPORTED_LAYOUT;
         }
-        const dim3 grid((unsigned)((per_sample + kNT - 1) / kNT), (unsigned)a.n);
+        const dim3 grid((unsigned)tiles, (unsigned)a.n);
         const int k = (a.kh == a.kw && (a.kh == 2 || a.kh == 3)) ? a.kh : 0;
         auto go = [&](auto kernel) { hipLaunchKernelGGL(kernel, grid, dim3(kNT), 0, s, p); };
         auto pick = [&](auto idx_tag) {
