@@ -38,7 +38,8 @@ __global__ __launch_bounds__(kNT) void ap_flat(const void* __restrict__ x, void*
     constexpr int P = kNT / TPS;  // planes per workgroup
     constexpr int VEC = VECTOR ? T::vec : 1;
     constexpr int NV = slots<VEC>();
-    extern __shared__ float tile[];  // P * S floats
+    extern __shared__ float4 tile4[];  // P * S floats, 16-byte aligned
+    float* tile = reinterpret_cast<float*>(tile4);
     const int64_t p0 = (int64_t)blockIdx.x * P;
     const int64_t np = (planes - p0) < P ? (planes - p0) : P;
     const int32_t span = (int32_t)(np * S);  // elements this workgroup owns
@@ -47,7 +48,9 @@ __global__ __launch_bounds__(kNT) void ap_flat(const void* __restrict__ x, void*
 
     // Stage the span in LDS as fp32.  Every load is issued before the first
     // LDS store, so a thread has all its requests in flight at once; only the
-    // last workgroup can have a remainder that is not whole vectors.
+    // last workgroup can have a remainder that is not whole vectors.  A lane
+    // writes its four fp32 values with one 16-byte LDS store: as 4-byte
+    // stores, lanes 16 apart would hit the same bank.
     float v[NV][VEC];
 #pragma unroll
     for (int k = 0; k < NV; ++k) {
@@ -61,8 +64,13 @@ __global__ __launch_bounds__(kNT) void ap_flat(const void* __restrict__ x, void*
     for (int k = 0; k < NV; ++k) {
         const int32_t e = (k * kNT + (int)threadIdx.x) * VEC;
         if (e < whole) {
+            if constexpr (VEC % 4 == 0) {
 #pragma unroll
-            for (int i = 0; i < VEC; ++i) tile[e + i] = v[k][i];
+                for (int i = 0; i < VEC; i += 4)
+                    tile4[(e + i) / 4] = make_float4(v[k][i], v[k][i + 1], v[k][i + 2], v[k][i + 3]);
+            } else {
+                tile[e] = v[k][0];
+            }
         }
     }
     for (int32_t e = whole + threadIdx.x; e < span; e += kNT) tile[e] = load1<T>(x, base + e);
