@@ -242,7 +242,8 @@ kf_status kf_adaptive_avgpool2d(const void* x, kf_dtype dtype, void* y, int32_t 
  * Without them (indices NULL) a running maximum is kept instead, so two
  * results differ from the selected element's bits: a window whose maximum
  * is a zero may give +0 where the first maximum is -0 (the two compare
- * equal), and a window holding NaN gives the default quiet NaN.
+ * equal), and a window holding NaN gives a quiet NaN that need not carry
+ * the NaN element's bits.
  *
  *  x        device pointer, shape [N, C, H, W] or [C, H, W], H, W >= 1,
  *           H * W < 2^31; dtype FLOAT32, BFLOAT16 or FLOAT16; dense NCHW, or

@@ -15,6 +15,10 @@
 //              staged into LDS with coalesced 16-byte loads; windows are
 //              scanned from LDS and consecutive threads write consecutive
 //              outputs.
+//   mp_tile    NCHW 3x3 windows at stride 2 without dilation (the ResNet
+//              stem's pooling) on rows of whole 16-byte vectors: a thread
+//              owns 16 bytes of consecutive outputs and folds its windows
+//              from registers (vector loads, no LDS).
 //   mp_direct  NCHW planes whose band tile does not fit in LDS: one thread
 //              per output, window loads from global memory.
 //   mp_nhwc    channels last: one thread per (output pixel, 16-byte vector
@@ -33,6 +37,11 @@ namespace {
 constexpr int kNT = 256;
 constexpr int kBandBytes = 16 << 10;  // LDS budget of one band tile
 constexpr int64_t kBandGroups = 2048;  // persistent band workgroups (8 per CU)
+// mp_tile: output rows per thread.  On the ResNet stem one row (25.1 us)
+// beats reusing the shared input row across two (27.4 us) or four (30.4 us):
+// the extra threads keep more loads in flight, and the shared row comes
+// from L2.
+constexpr int kTileRows = 1;
 
 // Raw storage type of an element and its value as a float (exact).
 template <class T>
@@ -102,6 +111,20 @@ constexpr uint32_t kQuietNaN<BF16> = 0x7fc0u;
 template <>
 constexpr uint32_t kQuietNaN<F16> = 0x7e00u;
 
+// Storage bits of a float that holds a value of T exactly.
+template <class T>
+__device__ __forceinline__ uint32_t raw_of(float f) {
+    if constexpr (std::is_same_v<T, F32>) return __float_as_uint(f);
+    else if constexpr (std::is_same_v<T, BF16>) return __float_as_uint(f) >> 16;
+    else return (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)f);
+}
+
+// IEEE 754-2019 maximum of three (NaN propagates, -0 < +0): one
+// v_maximum3_f32 on gfx950.
+__device__ __forceinline__ float maximum3(float a, float b, float c) {
+    return __builtin_elementwise_maximum(__builtin_elementwise_maximum(a, b), c);
+}
+
 // The value-only choice (no indices wanted): the window's maximum and
 // whether it held a NaN.  Every element of a window converts to float
 // exactly, so the maximum converts back exactly; a NaN window yields the
@@ -122,12 +145,7 @@ struct MaxOnly {
         best = valid ? fmaxf(best, v) : best;
         nan = nan | (valid & (v != v));
     }
-    __device__ __forceinline__ uint32_t result() const {
-        if (nan) return kQuietNaN<T>;
-        if constexpr (std::is_same_v<T, F32>) return __float_as_uint(best);
-        else if constexpr (std::is_same_v<T, BF16>) return __float_as_uint(best) >> 16;
-        else return (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)best);
-    }
+    __device__ __forceinline__ uint32_t result() const { return nan ? kQuietNaN<T> : raw_of<T>(best); }
     __device__ __forceinline__ int32_t index() const { return -1; }
 };
 
@@ -538,6 +556,148 @@ __global__ __launch_bounds__(kNT) void mp_nhwc(MPParams p) {
 }
 
 // --------------------------------------------------------------------------
+// NCHW 3x3 windows, stride 2, no dilation, padding PW = 0 or 1 across (any
+// padding down): the ResNet stem's pooling, on planes whose rows are whole
+// 16-byte vectors.  A thread owns E = 16 / sizeof(T) consecutive outputs in
+// each of ROWS consecutive output rows of one plane.  Its windows span
+// 2 * ROWS + 1 input rows and 2E + 1 columns: per row two 16-byte vectors
+// (columns 2 * j0 .. 2 * j0 + 2E - 1) and one halo element (the column to
+// the left with padding 1, to the right without), all loaded before any
+// folding, from clamped addresses where a row or column lies outside the
+// plane.  Each input row is folded into E row picks (three columns per
+// output), and output rows that share an input row reuse its picks, so no
+// element is read twice from registers or memory by one thread.  Lanes run
+// along an output row, so a wave's vector loads cover input rows
+// contiguously; workgroups are numbered XCD-contiguously, so neighbouring
+// row groups, which share one input row, run on one XCD.  No LDS, no
+// barrier.
+//
+// EXACT (value only, no indices; the host sets it when no vector column
+// lies right of the plane, 2 * E * ceil(ow / E) <= w): then every clamped
+// load is a duplicate of an element of the same window (a window is an
+// interval of rows and of columns that meets the plane, and clamping moves
+// an outside row or column to the nearest one inside), which cannot change
+// a maximum, so the folds need no masks: one maximum3 per output per row
+// and one across rows.  Such a NaN result is a quiet NaN (an input NaN's
+// payload, quieted), not necessarily the canonical one.
+template <class T, bool IDX, int ROWS, int PW, bool EXACT>
+__global__ __launch_bounds__(kNT) void mp_tile(MPParams p) {
+    static_assert(!(IDX && EXACT), "positions need the masked fold");
+    using R = typename Raw<T>::type;
+    constexpr int E = 16 / sizeof(R);
+    constexpr int IN = 2 * ROWS + 1;  // input rows under a thread's windows
+    constexpr int COLS = 2 * E + 1;   // input columns under them
+    const uint32_t gw = ((uint32_t)p.ow + E - 1) / E;        // column groups per output row
+    const uint32_t rg = ((uint32_t)p.oh + ROWS - 1) / ROWS;  // row groups per plane
+    const uint32_t t = xcd_contiguous(blockIdx.x, gridDim.x) * kNT + threadIdx.x;
+    if (t >= (uint32_t)p.planes * rg * gw) return;  // the host keeps this product below 2^31
+    const uint32_t g = t % gw;
+    const uint32_t rest = t / gw;
+    const uint32_t plane = rest / rg;
+    const int i0 = (int)(rest - plane * rg) * ROWS;  // first output row
+    const int j0 = (int)g * E;                       // first output column
+    const int c0 = 2 * j0 - PW;                      // column of value 0 below
+    const int r0 = 2 * i0 - p.ph;                    // input row of row 0 below
+    const R* xp = static_cast<const R*>(p.x) + (int64_t)plane * p.h * p.w;
+
+    // v[a][m]: input row r0 + a, column c0 + m.  With PW = 1 the halo is
+    // m = 0 and the vectors m = 1 .. 2E; with PW = 0 the vectors are
+    // m = 0 .. 2E - 1 and the halo m = 2E.  A vector starts at a multiple
+    // of E, so it lies wholly inside or wholly outside the row (w % E == 0).
+    R v[IN][COLS];
+    const int va = 2 * j0, vb = 2 * j0 + E, hc = PW ? 2 * j0 - 1 : 2 * j0 + 2 * E;
+    const int va_c = min(va, p.w - E), vb_c = min(vb, p.w - E), hc_c = min(max(hc, 0), p.w - 1);
+#pragma unroll
+    for (int a = 0; a < IN; ++a) {
+        const R* row = xp + (int64_t)min(max(r0 + a, 0), p.h - 1) * p.w;
+        const Lanes<R, E> A = __builtin_bit_cast(Lanes<R, E>, *reinterpret_cast<const u32x4*>(row + va_c));
+        const Lanes<R, E> B = __builtin_bit_cast(Lanes<R, E>, *reinterpret_cast<const u32x4*>(row + vb_c));
+#pragma unroll
+        for (int k = 0; k < E; ++k) {
+            v[a][PW + k] = A.v[k];
+            v[a][PW + E + k] = B.v[k];
+        }
+        v[a][PW ? 0 : 2 * E] = row[hc_c];
+    }
+
+    Lanes<R, E> out[ROWS];
+    int32_t at[ROWS][E];
+    if constexpr (EXACT) {
+        float hm[IN][E];  // row maxima of each output's three columns
+#pragma unroll
+        for (int a = 0; a < IN; ++a)
+#pragma unroll
+            for (int k = 0; k < E; ++k)
+                hm[a][k] = maximum3(Raw<T>::value(v[a][2 * k]), Raw<T>::value(v[a][2 * k + 1]),
+                                    Raw<T>::value(v[a][2 * k + 2]));
+#pragma unroll
+        for (int q = 0; q < ROWS; ++q)
+#pragma unroll
+            for (int k = 0; k < E; ++k)
+                out[q].v[k] = (R)raw_of<T>(maximum3(hm[2 * q][k], hm[2 * q + 1][k], hm[2 * q + 2][k]));
+    } else {
+        // Row picks: rp[a][k] folds columns 2k, 2k + 1, 2k + 2 of row a, in
+        // order, skipping positions outside the plane.
+        Select<T, IDX> rp[IN][E];
+#pragma unroll
+        for (int a = 0; a < IN; ++a) {
+            const int r = r0 + a;
+            const bool row_ok = (r >= 0) & (r < p.h);
+#pragma unroll
+            for (int k = 0; k < E; ++k)
+#pragma unroll
+                for (int m = 2 * k; m < 2 * k + 3; ++m) {
+                    const int col = c0 + m;
+                    rp[a][k].consider_if(row_ok & (col >= 0) & (col < p.w), v[a][m], r * p.w + col);
+                }
+        }
+#pragma unroll
+        for (int q = 0; q < ROWS; ++q)
+#pragma unroll
+            for (int k = 0; k < E; ++k) {
+                const Select<T, IDX> s = merge(merge(rp[2 * q][k], rp[2 * q + 1][k]), rp[2 * q + 2][k]);
+                out[q].v[k] = (R)s.result();
+                at[q][k] = s.index();
+            }
+    }
+
+    R* yp = static_cast<R*>(p.y) + (int64_t)plane * p.oh * p.ow;
+    const bool whole = (p.ow % E == 0);  // output rows are whole 16-byte vectors
+#pragma unroll
+    for (int q = 0; q < ROWS; ++q) {
+        const int i = i0 + q;
+        if (i >= p.oh) break;
+        const int64_t o = (int64_t)i * p.ow + j0;
+        if (whole) {
+            __builtin_nontemporal_store(__builtin_bit_cast(u32x4, out[q]), reinterpret_cast<u32x4*>(yp + o));
+        } else {
+#pragma unroll
+            for (int k = 0; k < E; ++k)
+                if (j0 + k < p.ow) yp[o + k] = out[q].v[k];
+        }
+        if constexpr (IDX) {
+            // A lane's E indices are 8E contiguous bytes: written as 16-byte
+            // stores that the cache merges into whole lines with the
+            // neighbouring lanes' (8-byte non-temporal stores at a 32-byte
+            // lane stride measured 2.3x slower).
+            int64_t* ip = p.idx + (int64_t)plane * p.oh * p.ow + o;
+            if (whole) {
+#pragma unroll
+                for (int k = 0; k < E; k += 2) {
+                    const u32x4 pair = {(uint32_t)at[q][k], at[q][k] < 0 ? ~0u : 0u, (uint32_t)at[q][k + 1],
+                                        at[q][k + 1] < 0 ? ~0u : 0u};
+                    *reinterpret_cast<u32x4*>(ip + k) = pair;
+                }
+            } else {
+#pragma unroll
+                for (int k = 0; k < E; ++k)
+                    if (j0 + k < p.ow) ip[k] = at[q][k];
+            }
+        }
+    }
+}
+
+// --------------------------------------------------------------------------
 // Host side.
 template <class T>
 kf_status run(const MaxPoolArgs& a, hipStream_t s, const char** variant) {
@@ -595,6 +755,26 @@ kf_status run(const MaxPoolArgs& a, hipStream_t s, const char** variant) {
             {{"mp_nhwc_scalar_idx", "mp_nhwc_scalar_k2_idx", "mp_nhwc_scalar_k3_idx"},
              {"mp_nhwc_vec_idx", "mp_nhwc_vec_k2_idx", "mp_nhwc_vec_k3_idx"}}};
         *variant = names[a.idx ? 1 : 0][vec ? 1 : 0][k == 0 ? 0 : k - 1];
+    } else if (a.kh == 3 && a.kw == 3 && a.sh == 2 && a.sw == 2 && a.dh == 1 && a.dw == 1 && a.w % VEC == 0 &&
+               (uintptr_t)a.x % 16 == 0 && (uintptr_t)a.y % 16 == 0 && (uintptr_t)a.idx % 16 == 0 &&
+               p.planes * ((a.oh + kTileRows - 1) / kTileRows) * ((a.ow + VEC - 1) / VEC) < INT32_MAX) {
+        const int64_t threads = p.planes * ((a.oh + kTileRows - 1) / kTileRows) * ((a.ow + VEC - 1) / VEC);
+        const dim3 grid((unsigned)((threads + kNT - 1) / kNT));
+        auto go = [&](auto kernel) { hipLaunchKernelGGL(kernel, grid, dim3(kNT), 0, s, p); };
+        const bool exact = 2 * VEC * ((a.ow + VEC - 1) / VEC) <= a.w;
+        if (a.idx) {
+            if (a.pw) go(mp_tile<T, true, kTileRows, 1, false>);
+            else go(mp_tile<T, true, kTileRows, 0, false>);
+            *variant = "mp_tile_idx";
+        } else if (exact) {
+            if (a.pw) go(mp_tile<T, false, kTileRows, 1, true>);
+            else go(mp_tile<T, false, kTileRows, 0, true>);
+            *variant = "mp_tile_exact";
+        } else {
+            if (a.pw) go(mp_tile<T, false, kTileRows, 1, false>);
+            else go(mp_tile<T, false, kTileRows, 0, false>);
+            *variant = "mp_tile";
+        }
     } else {
         // Output rows per band: as many as keep the band's input rows within
         // kBandBytes, then evened out over the plane's bands.
