@@ -230,6 +230,34 @@ def avgpool_cl_row(torch, F, dev, kf355, W, steps, warmup, sets_for):
             "kf355_speedup": round(eager_us / us, 3), "buffer_sets": len(xs)}
 
 
+def avgpool_general_row(torch, F, dev, kf355, W, steps, warmup, sets_for):
+    """adaptive_avgpool2d to general output sizes, fp32 NCHW: [32,512,14,14]
+    -> 7x7 (2x2 windows) and [32,256,13,13] -> 6x6 (overlapping 3x3
+    windows), libkf355 against torch eager, rotating sets."""
+    row = {}
+    for key, shape, out in (("vgg_14x14_to_7x7", (32, 512, 14, 14), (7, 7)),
+                            ("alexnet_13x13_to_6x6", (32, 256, 13, 13), (6, 6))):
+        w = W.avgpool_general_f32(shape=shape, output_size=out)
+        src = w["x"].to(dev)
+        nb = src.numel() * 4 + shape[0] * shape[1] * out[0] * out[1] * 4
+        xs = [src.clone() for _ in range(sets_for(nb))]
+        ys = [torch.empty(shape[0], shape[1], out[0], out[1], device=dev) for _ in xs]
+        fns = [kf355.prepare_adaptive_avgpool2d(x, y) for x, y in zip(xs, ys)]
+        fns[0]()
+        variant = kf355.last_variant()
+        us = time_launches(torch, fns, steps, warmup)
+        eager_us = time_launches(torch, [lambda x=x: F.adaptive_avg_pool2d(x, out) for x in xs], min(steps, 50),
+                                 warmup)
+        gbs = nb / (us * 1e-6) / 1e9
+        row[key] = {"workload": f"fp32 {list(shape)} -> {out[0]}x{out[1]}", "variant": variant,
+                    "algorithmic_bytes": nb, "us_per_call": round(us, 3), "gbps": round(gbs, 1),
+                    "frac_of_peak": round(gbs / PEAK_HBM_GBS, 4), "torch_eager_us": round(eager_us, 3),
+                    "kf355_speedup": round(eager_us / us, 3), "buffer_sets": len(xs)}
+        del xs, ys, fns
+        torch.cuda.empty_cache()
+    return row
+
+
 def gn_cl_row(torch, F, dev, kf355, W, steps, warmup, sets_for):
     """The SD3.5 VAE GroupNorm on a channels-last tensor: bf16
     [1,512,128,128], 32 groups, bf16 affine, libkf355 against torch eager."""
@@ -258,7 +286,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-eager", action="store_true")
-    ap.add_argument("--no-next", action="store_true", help="skip the next-row measurements (fused causal softmax, layer_norm, decode split softmax, max_pool2d)")
+    ap.add_argument("--no-next", action="store_true", help="skip the next-row measurements (fused causal softmax, layer_norm, decode split softmax, max_pool2d, channels-last and general-size pooling, channels-last group_norm)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: the operators shard by rows / groups / planes with no exchange, "
@@ -436,6 +464,8 @@ def main():
         next_rows["softmax_decode_split"] = decode_row(torch, dev, kf355, W, args.steps, args.warmup,
                                                        sets_for)
         next_rows["max_pool2d_stem"] = maxpool_row(torch, F, dev, kf355, W, args.steps, args.warmup, sets_for)
+        next_rows["avgpool_general_sizes"] = avgpool_general_row(torch, F, dev, kf355, W, args.steps, args.warmup,
+                                                                  sets_for)
         next_rows["avgpool_channels_last"] = avgpool_cl_row(torch, F, dev, kf355, W, args.steps, args.warmup,
                                                             sets_for)
         next_rows["group_norm_channels_last"] = gn_cl_row(torch, F, dev, kf355, W, args.steps, args.warmup,

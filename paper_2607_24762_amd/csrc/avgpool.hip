@@ -11,12 +11,18 @@
 //             writes the mean.
 //   ap_plane  1x1 output for large planes: one workgroup per plane reads it
 //             with coalesced loads and reduces in registers.
-//   ap_window any output size: one thread per output cell.
+//   ap_staged any output size, planes of at most 4096 elements: P planes
+//             staged in LDS as in ap_flat, then one thread per output cell
+//             sums its window from LDS.
+//   ap_window any output size, larger planes: one thread per output cell.
 //   ap_nhwc   channels last, any output size: a workgroup owns one output
 //             cell of one sample and 64 vectors of 16 bytes of channels;
 //             its four thread groups sum interleaved window pixels, so
 //             every load is a coalesced 1 KiB channel run, and the four
 //             partials are added in group order through LDS.
+#include <algorithm>
+#include <type_traits>
+
 #include "kf_device.hpp"
 #include "kf_internal.h"
 
@@ -25,6 +31,10 @@ namespace {
 
 constexpr int kNT = 256;
 constexpr int kSpanMax = 4096;  // fp32 staging per workgroup: 16 KiB of LDS
+#ifndef KF_STAGED_BLOCKS
+#define KF_STAGED_BLOCKS 2048
+#endif
+constexpr int64_t kStagedBlocks = KF_STAGED_BLOCKS;  // ap_staged: target workgroups
 
 // Loads issued per thread to cover a span of kSpanMax elements.
 template <int VEC>
@@ -32,25 +42,18 @@ constexpr int slots() {
     return (kSpanMax + kNT * VEC - 1) / (kNT * VEC);
 }
 
-template <class T, int TPS, bool VECTOR>
-__global__ __launch_bounds__(kNT) void ap_flat(const void* __restrict__ x, void* __restrict__ y, int64_t planes,
-                                               int32_t S) {
-    constexpr int P = kNT / TPS;  // planes per workgroup
+// Stage elements [base, base + span) of x in LDS as fp32 (span <= kSpanMax).
+// Every load is issued before the first LDS store, so a thread has all its
+// requests in flight at once; only the last workgroup can have a remainder
+// that is not whole vectors (VECTOR needs x + base 16-byte aligned).  A lane
+// writes its four fp32 values with one 16-byte LDS store: as 4-byte stores,
+// lanes 16 apart would hit the same bank.  Ends with a barrier.
+template <class T, bool VECTOR>
+__device__ __forceinline__ void stage_span(const void* __restrict__ x, int64_t base, int32_t span, float4* tile4) {
     constexpr int VEC = VECTOR ? T::vec : 1;
     constexpr int NV = slots<VEC>();
-    extern __shared__ float4 tile4[];  // P * S floats, 16-byte aligned
     float* tile = reinterpret_cast<float*>(tile4);
-    const int64_t p0 = (int64_t)blockIdx.x * P;
-    const int64_t np = (planes - p0) < P ? (planes - p0) : P;
-    const int32_t span = (int32_t)(np * S);  // elements this workgroup owns
     const int32_t whole = span - span % VEC;
-    const int64_t base = p0 * S;
-
-    // Stage the span in LDS as fp32.  Every load is issued before the first
-    // LDS store, so a thread has all its requests in flight at once; only the
-    // last workgroup can have a remainder that is not whole vectors.  A lane
-    // writes its four fp32 values with one 16-byte LDS store: as 4-byte
-    // stores, lanes 16 apart would hit the same bank.
     float v[NV][VEC];
 #pragma unroll
     for (int k = 0; k < NV; ++k) {
@@ -75,6 +78,17 @@ __global__ __launch_bounds__(kNT) void ap_flat(const void* __restrict__ x, void*
     }
     for (int32_t e = whole + threadIdx.x; e < span; e += kNT) tile[e] = load1<T>(x, base + e);
     __syncthreads();
+}
+
+template <class T, int TPS, bool VECTOR>
+__global__ __launch_bounds__(kNT) void ap_flat(const void* __restrict__ x, void* __restrict__ y, int64_t planes,
+                                               int32_t S) {
+    constexpr int P = kNT / TPS;  // planes per workgroup
+    extern __shared__ float4 tile4[];  // P * S floats, 16-byte aligned
+    float* tile = reinterpret_cast<float*>(tile4);
+    const int64_t p0 = (int64_t)blockIdx.x * P;
+    const int64_t np = (planes - p0) < P ? (planes - p0) : P;
+    stage_span<T, VECTOR>(x, p0 * S, (int32_t)(np * S), tile4);
 
     // TPS threads sum each plane at stride TPS, four accumulators each.
     const int q = threadIdx.x / TPS;
@@ -130,6 +144,70 @@ __global__ __launch_bounds__(kNT) void ap_plane(const void* __restrict__ x, void
 #pragma unroll
         for (int i = 1; i < kNT / kWave; ++i) t += red[i];
         store1<T>(y, blockIdx.x, t / (float)S);
+    }
+}
+
+// Any output size, planes of S = H * W <= kSpanMax elements: a workgroup
+// stages P consecutive planes (one contiguous span) in LDS as ap_flat does,
+// then its threads take the P * OH * OW output cells in order (consecutive
+// threads, consecutive cells, coalesced stores) and sum each window from LDS
+// row by row.  Window bounds are PyTorch's adaptive ones, computed once per
+// workgroup into LDS tables (row i: h0 | h1 << 16, column j: w0 | w1 << 16;
+// every bound is at most 4096); a thread steps its (plane, row, column) by
+// the workgroup size with carries instead of dividing per cell.  KMAX > 0:
+// no window is more than KMAX rows or columns, and the window is read as a
+// fixed KMAX x KMAX block (reads outside the window clamped and added as 0,
+// in the same row-major order), so its LDS reads issue together instead of
+// one loop trip and one wait each.
+template <class T, bool VECTOR, int KMAX>
+__global__ __launch_bounds__(kNT) void ap_staged(const void* __restrict__ x, void* __restrict__ y, int64_t planes,
+                                                 int32_t P, int32_t H, int32_t W, int32_t OH, int32_t OW) {
+    extern __shared__ float4 tile4[];  // P * H * W floats, then OH + OW bounds
+    const float* tile = reinterpret_cast<const float*>(tile4);
+    const int32_t S = H * W, cells = OH * OW;
+    uint32_t* rows = reinterpret_cast<uint32_t*>(reinterpret_cast<float*>(tile4) + P * S);
+    uint32_t* cols = rows + OH;
+    for (int32_t t = threadIdx.x; t < OH + OW; t += kNT) {
+        const int32_t k = t < OH ? t : t - OH, n = t < OH ? H : W, m = t < OH ? OH : OW;
+        rows[t] = (uint32_t)((k * n) / m) | ((uint32_t)(((k + 1) * n + m - 1) / m) << 16);
+    }
+    const int64_t p0 = (int64_t)blockIdx.x * P;
+    const int32_t np = (int32_t)((planes - p0) < P ? (planes - p0) : P);
+    stage_span<T, VECTOR>(x, p0 * S, np * S, tile4);  // its barrier also publishes the tables
+    // This thread's first cell, and the step kNT = dq * cells + di * OW + dj.
+    int32_t q = (int32_t)threadIdx.x / cells;
+    int32_t i = ((int32_t)threadIdx.x - q * cells) / OW;
+    int32_t j = (int32_t)threadIdx.x - q * cells - i * OW;
+    const int32_t dq = kNT / cells, di = (kNT - dq * cells) / OW, dj = kNT - dq * cells - di * OW;
+    for (int32_t o = threadIdx.x; o < np * cells; o += kNT) {
+        const uint32_t rb = rows[i], cb = cols[j];
+        const int32_t h0 = (int32_t)(rb & 0xffff), h1 = (int32_t)(rb >> 16);
+        const int32_t w0 = (int32_t)(cb & 0xffff), w1 = (int32_t)(cb >> 16);
+        const float* plane = tile + q * S;
+        float sum = 0.f;
+        if constexpr (KMAX > 0) {
+            float v[KMAX][KMAX];
+#pragma unroll
+            for (int a = 0; a < KMAX; ++a)
+#pragma unroll
+                for (int b = 0; b < KMAX; ++b)
+                    v[a][b] = plane[min(h0 + a, H - 1) * W + min(w0 + b, W - 1)];
+#pragma unroll
+            for (int a = 0; a < KMAX; ++a)
+#pragma unroll
+                for (int b = 0; b < KMAX; ++b) sum += (h0 + a < h1 && w0 + b < w1) ? v[a][b] : 0.f;
+        } else {
+            for (int32_t rr = h0; rr < h1; ++rr)
+                for (int32_t c = w0; c < w1; ++c) sum += plane[rr * W + c];
+        }
+        store1<T>(y, p0 * cells + o, sum / (float)((h1 - h0) * (w1 - w0)));
+        j += dj;
+        const int32_t cj = j >= OW;
+        j -= cj * OW;
+        i += di + cj;
+        const int32_t ci = i >= OH;
+        i -= ci * OH;
+        q += dq + ci;
     }
 }
 
@@ -282,6 +360,48 @@ kf_status run(const AvgPoolArgs& a, hipStream_t s, const char** variant) {
                 *variant = "ap_plane";
             }
         }
+    } else if (S <= kSpanMax && a.oh + a.ow <= 4096 &&
+               (kSpanMax / S) * a.oh * a.ow <= INT32_MAX && (a.planes + kSpanMax / S - 1) / (kSpanMax / S) <= INT32_MAX) {
+        // Planes per workgroup: as many as fit the staging tile, but no more
+        // than leave kStagedBlocks workgroups (enough to keep every CU busy
+        // with several), rounded down so the span stays whole 16-byte vectors
+        // when it can.
+        int64_t P = kSpanMax / S;
+        const int64_t spread = a.planes / kStagedBlocks;
+        P = spread < 1 ? 1 : (spread < P ? spread : P);
+        const int64_t vec_elems = T::vec;
+        while (P > 1 && (P * S) % vec_elems != 0) --P;
+        const int64_t blocks = (a.planes + P - 1) / P;
+        const bool vec = ((P * S) % vec_elems == 0) && ((uintptr_t)a.x % 16 == 0);
+        const size_t lds = (size_t)(P * S) * sizeof(float) + (size_t)(a.oh + a.ow) * sizeof(uint32_t);
+        // Largest window extent along either axis.
+        auto extent = [](int64_t n, int64_t m) {
+            int64_t e = 0;
+            for (int64_t k = 0; k < m; ++k) {
+                const int64_t d = ((k + 1) * n + m - 1) / m - (k * n) / m;
+                e = d > e ? d : e;
+            }
+            return e;
+        };
+        const int64_t ext = std::max(extent(a.h, a.oh), extent(a.w, a.ow));
+        const int kmax = ext <= 2 ? 2 : ext <= 3 ? 3 : ext <= 4 ? 4 : 0;
+        auto go = [&](auto kernel) {
+            hipLaunchKernelGGL(kernel, dim3((unsigned)blocks), dim3(kNT), lds, s, a.x, a.y, a.planes, (int32_t)P,
+                               (int32_t)a.h, (int32_t)a.w, (int32_t)a.oh, (int32_t)a.ow);
+        };
+        auto pick = [&](auto vec_tag) {
+            constexpr bool V = decltype(vec_tag)::value;
+            if (kmax == 2) go(ap_staged<T, V, 2>);
+            else if (kmax == 3) go(ap_staged<T, V, 3>);
+            else if (kmax == 4) go(ap_staged<T, V, 4>);
+            else go(ap_staged<T, V, 0>);
+        };
+        if (vec) pick(std::true_type{});
+        else pick(std::false_type{});
+        static const char* names[2][5] = {
+            {"ap_staged_scalar", "", "ap_staged_scalar_k2", "ap_staged_scalar_k3", "ap_staged_scalar_k4"},
+            {"ap_staged_vec", "", "ap_staged_vec_k2", "ap_staged_vec_k3", "ap_staged_vec_k4"}};
+        *variant = names[vec ? 1 : 0][kmax];
     } else {
         const int64_t blocks = (a.planes * a.oh * a.ow + kNT - 1) / kNT;
         if (blocks > INT32_MAX) {

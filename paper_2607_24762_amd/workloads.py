@@ -59,6 +59,16 @@ def avgpool_resnet_head_f32(seed: int = 2) -> dict:
     return {"op": "adaptive_avgpool2d", "x": x, "output_size": (1, 1)}
 
 
+def avgpool_general_f32(seed: int = 10, shape=(32, 512, 14, 14), output_size=(7, 7)) -> dict:
+    """Adaptive average pooling to a general output size, fp32 NCHW,
+    ReLU(z) like the head input: by default a VGG-style 7x7 head on a 14x14
+    map (2x2 windows); (32, 256, 13, 13) -> (6, 6) gives overlapping 3x3
+    windows (an AlexNet-style head)."""
+    rng = np.random.default_rng(seed)
+    x = cast(np.maximum(rng.standard_normal(shape), 0.0), "f32")
+    return {"op": "adaptive_avgpool2d", "x": x, "output_size": tuple(output_size)}
+
+
 def groupnorm_vae_bf16(seed: int = 3) -> dict:
     """SD3.5 VAE-style GroupNorm: bf16 [1, 512, 128, 128], 32 groups,
     eps 1e-6; x ~ N(0.3, 1.5^2), weight ~ N(1, 0.1^2), bias ~ N(0, 0.1^2),

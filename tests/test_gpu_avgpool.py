@@ -1,7 +1,8 @@
 """GPU parity of kf_adaptive_avgpool2d against the float64 oracle: 1x1
 outputs over plane sizes that select each LDS tiling (1, 4, 16 and 64
 threads per plane) and the plane-per-workgroup kernel, ragged plane counts,
-misaligned inputs, generic output sizes and 3-D inputs, in fp32 / bf16 /
+misaligned inputs, generic output sizes (staged planes, vector and element
+staging, and a thread per cell for large planes) and 3-D inputs, in fp32 / bf16 /
 fp16.  Tolerances: fp32 max abs error <= 1e-6; bf16 / fp16 within 1 unit in
 the last place of the oracle rounded once."""
 import pytest
@@ -61,12 +62,48 @@ def test_one_by_one(shape, variant, dt):
     assert run(relu_input(shape, dt, 1), (1, 1), dt) == variant
 
 
-@pytest.mark.parametrize("shape,out", [((2, 3, 7, 7), (3, 3)), ((1, 2, 13, 17), (5, 7)), ((1, 1, 4, 6), (8, 9)),
-                                       ((3, 10, 9), (4, 2)), ((2, 4, 7, 7), (7, 7)), ((1, 2, 5, 5), (1, 3))])
-@pytest.mark.parametrize("dt", ["f32", "bf16"])
+GENERIC = [
+    ((2, 3, 7, 7), (3, 3)), ((1, 2, 13, 17), (5, 7)), ((1, 1, 4, 6), (8, 9)), ((3, 10, 9), (4, 2)),
+    ((2, 4, 7, 7), (7, 7)), ((1, 2, 5, 5), (1, 3)),
+    ((2, 512, 14, 14), (7, 7)),      # 2x2 windows (a VGG-style head at twice the resolution)
+    ((2, 256, 13, 13), (6, 6)),      # overlapping 3x3 windows (AlexNet-style)
+    ((3, 7, 9, 11), (4, 5)),         # 21 planes, odd spans: ragged workgroups
+    ((1, 5, 64, 64), (3, 3)),        # one plane per workgroup
+    ((1, 3, 1, 1), (5, 6)),          # one element spread over a larger output
+    ((1, 2, 70, 70), (5, 5)),        # planes beyond the staging tile
+]
+
+
+def staged_variant(shape, out, dt, x):
+    """The kernel the host picks: staged planes when a plane fits the 4096-element tile (vector staging when the
+    planes per workgroup make whole 16-byte spans and x is aligned; a fixed k x k window read when no window
+    is more than k <= 4 rows or columns), else a thread per output cell."""
+    h, w = shape[-2], shape[-1]
+    s = h * w
+    if s > 4096:
+        return "ap_window"
+    vec = 4 if dt == "f32" else 8
+    planes = 1
+    for d in shape[:-2]:
+        planes *= d
+    p = max(1, min(4096 // s, planes // 2048))
+    while p > 1 and (p * s) % vec:
+        p -= 1
+    name = "ap_staged_vec" if (p * s) % vec == 0 and x.data_ptr() % 16 == 0 else "ap_staged_scalar"
+
+    def extent(n, m):
+        return max(((k + 1) * n + m - 1) // m - (k * n) // m for k in range(m))
+    e = max(extent(h, out[0]), extent(w, out[1]))
+    return name + (f"_k{e if e > 1 else 2}" if e <= 4 else "")
+
+
+@pytest.mark.parametrize("shape,out", GENERIC, ids=lambda v: str(v))
+@pytest.mark.parametrize("dt", ["f32", "bf16", "f16"])
 def test_generic_sizes(shape, out, dt):
     note(f"avgpool {shape}->{out} {dt}")
-    assert run(relu_input(shape, dt, 2), out, dt) == "ap_window"
+    x_cpu = relu_input(shape, dt, 2)
+    x = x_cpu.cuda()
+    assert run(x_cpu, out, dt, x_gpu=x) == staged_variant(shape, out, dt, x)
 
 
 @pytest.mark.parametrize("dt", ["f32", "bf16"])
@@ -77,6 +114,7 @@ def test_misaligned_input(dt):
     x_cpu = big[1:].view(3, 100, 7, 7)
     x = big.cuda()[1:].view(3, 100, 7, 7)
     run(x_cpu, (1, 1), dt, x_gpu=x)
+    assert run(x_cpu, (3, 3), dt, x_gpu=x) == "ap_staged_scalar_k3"
 
 
 def test_constant_input_is_exact():

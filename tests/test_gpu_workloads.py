@@ -72,3 +72,17 @@ def test_avgpool_resnet_head_f32():
     y = kf355.kf_adaptive_avgpool2d(w["x"].cuda(), w["output_size"])
     torch.cuda.synchronize()
     report(name, compare(y, oracle.adaptive_avg_pool2d(w["x"], w["output_size"]), "f32"))
+
+
+@pytest.mark.parametrize("shape,out", [((32, 512, 14, 14), (7, 7)), ((32, 256, 13, 13), (6, 6))])
+def test_avgpool_general_sizes_f32(shape, out):
+    """The general-size pooling rows at the shapes the benchmark times."""
+    name = f"avgpool_f32_{'x'.join(map(str, shape))}_to_{out[0]}x{out[1]}"
+    note(name)
+    w = W.avgpool_general_f32(shape=shape, output_size=out)
+    x = w["x"].cuda()
+    y = torch.empty(shape[0], shape[1], *out, device="cuda")
+    kf355.prepare_adaptive_avgpool2d(x, y)()
+    torch.cuda.synchronize()
+    assert kf355.last_variant().startswith("ap_staged_vec_k"), kf355.last_variant()
+    report(name, compare(y, oracle.adaptive_avg_pool2d(w["x"], out), "f32"))
