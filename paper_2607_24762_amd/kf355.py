@@ -91,17 +91,22 @@ def last_variant() -> str:
 
 def _check(status: int):
     if status != KF_OK:
-        raise KfError(status, lib().kf_last_error().decode())
+        _raise(status)
+
+
+def _raise(status: int):
+    raise KfError(status, lib().kf_last_error().decode())
 
 
 _ARRS: dict = {}
 
 
 def _arr(vals):
-    """A read-only int64 array for shapes, strides and windows, cached by
-    value (the library never writes through these pointers): building
-    ctypes arrays is a noticeable part of a call's host cost."""
-    key = tuple(int(v) for v in vals)
+    """A read-only int64 array for shapes, strides and windows (tuples of
+    Python ints: torch.Size, Tensor.stride(), _window), cached by value (the
+    library never writes through these pointers): building ctypes arrays is
+    a noticeable part of a call's host cost."""
+    key = vals if type(vals) is tuple else tuple(vals)
     hit = _ARRS.get(key)
     if hit is None:
         a = (ctypes.c_int64 * max(len(key), 1))(*key)
@@ -167,7 +172,7 @@ def kf_softmax(x: torch.Tensor, dim: int = -1, out_dtype: torch.dtype | None = N
     xs, _a = _arr(x.stride())
     ys, _b = _arr(y.stride())
     with _on(x):
-        _check(lib().kf_softmax(ctypes.c_void_p(x.data_ptr()), _dtype(x), ctypes.c_void_p(y.data_ptr()), _dtype(y),
+        _check(lib().kf_softmax(x.data_ptr(), _dtype(x), y.data_ptr(), _dtype(y),
                                 x.dim(), shape, xs, ys, dim, _stream(x)))
     return y
 
@@ -183,7 +188,7 @@ def kf_softmax_causal(x: torch.Tensor, scale: float = 1.0, out_dtype: torch.dtyp
     xs, _a = _arr(x.stride())
     ys, _b = _arr(y.stride())
     with _on(x):
-        _check(lib().kf_softmax_causal(ctypes.c_void_p(x.data_ptr()), _dtype(x), ctypes.c_void_p(y.data_ptr()),
+        _check(lib().kf_softmax_causal(x.data_ptr(), _dtype(x), y.data_ptr(),
                                        _dtype(y), x.dim(), shape, xs, ys, float(scale), _stream(x)))
     return y
 
@@ -249,8 +254,8 @@ def kf_softmax_split(x: torch.Tensor, dim: int = -1, out_dtype: torch.dtype | No
     xs, _a = _arr(x.stride())
     ys, _b = _arr(y.stride())
     with _on(x):
-        _check(lib().kf_softmax_split(ctypes.c_void_p(x.data_ptr()), _dtype(x), ctypes.c_void_p(y.data_ptr()),
-                                      _dtype(y), x.dim(), shape, xs, ys, dim, ctypes.c_void_p(ws.data_ptr()),
+        _check(lib().kf_softmax_split(x.data_ptr(), _dtype(x), y.data_ptr(),
+                                      _dtype(y), x.dim(), shape, xs, ys, dim, ws.data_ptr(),
                                       ws.numel(), _stream(x)))
     return y
 
@@ -276,10 +281,10 @@ def kf_group_norm(x: torch.Tensor, num_groups: int, weight: torch.Tensor | None 
     ys, _b = _arr(y.stride())
     with _on(x):
         _check(lib().kf_group_norm(
-            ctypes.c_void_p(x.data_ptr()), _dtype(x), ctypes.c_void_p(y.data_ptr()), x.dim(), shape, xs, ys,
-            num_groups, ctypes.c_void_p(weight.data_ptr() if weight is not None else None),
-            ctypes.c_void_p(bias.data_ptr() if bias is not None else None), at, float(eps),
-            ctypes.c_void_p(ws.data_ptr()), ws.numel(), _stream(x)))
+            x.data_ptr(), _dtype(x), y.data_ptr(), x.dim(), shape, xs, ys,
+            num_groups, weight.data_ptr() if weight is not None else None,
+            bias.data_ptr() if bias is not None else None, at, float(eps),
+            ws.data_ptr(), ws.numel(), _stream(x)))
     return y
 
 
@@ -306,9 +311,9 @@ def kf_layer_norm(x: torch.Tensor, normalized_shape, weight: torch.Tensor | None
     ys, _b = _arr(y.stride())
     with _on(x):
         _check(lib().kf_layer_norm(
-            ctypes.c_void_p(x.data_ptr()), _dtype(x), ctypes.c_void_p(y.data_ptr()), x.dim(), shape, xs, ys,
-            len(nshape), ctypes.c_void_p(weight.data_ptr() if weight is not None else None),
-            ctypes.c_void_p(bias.data_ptr() if bias is not None else None), _affine_dtype(x, weight, bias),
+            x.data_ptr(), _dtype(x), y.data_ptr(), x.dim(), shape, xs, ys,
+            len(nshape), weight.data_ptr() if weight is not None else None,
+            bias.data_ptr() if bias is not None else None, _affine_dtype(x, weight, bias),
             float(eps), _stream(x)))
     return y
 
@@ -325,7 +330,7 @@ def kf_adaptive_avgpool2d(x: torch.Tensor, output_size, out: torch.Tensor | None
     xs, _a = _arr(x.stride())
     ys, _b = _arr(y.stride())
     with _on(x):
-        _check(lib().kf_adaptive_avgpool2d(ctypes.c_void_p(x.data_ptr()), _dtype(x), ctypes.c_void_p(y.data_ptr()),
+        _check(lib().kf_adaptive_avgpool2d(x.data_ptr(), _dtype(x), y.data_ptr(),
                                            x.dim(), shape, xs, ys, oh, ow, _stream(x)))
     return y
 
@@ -334,20 +339,36 @@ def _pair(v):
     return (int(v), int(v)) if isinstance(v, int) else (int(v[0]), int(v[1]))
 
 
-def _window(kernel_size, stride, padding, dilation):
+def _window(kernel_size, stride, padding, dilation) -> tuple:
     kh, kw = _pair(kernel_size)
     sh, sw = _pair(stride if stride is not None and stride != [] else kernel_size)
     ph, pw = _pair(padding)
     dh, dw = _pair(dilation)
-    return [kh, kw, sh, sw, ph, pw, dh, dw]
+    return (kh, kw, sh, sw, ph, pw, dh, dw)
+
+
+_OUT_SIZES: dict = {}
+
+
+def _pool_out(h: int, w: int, win: tuple, ceil_mode: bool) -> tuple:
+    """kf_max_pool2d_output_size for a window tuple, asked of the library once
+    per (plane, window, mode) and remembered."""
+    key = (h, w, win, ceil_mode)
+    hit = _OUT_SIZES.get(key)
+    if hit is None:
+        warr, _a = _arr(win)
+        out, _b = _out_arr(2)
+        _check(lib().kf_max_pool2d_output_size(h, w, warr, int(ceil_mode), out))
+        hit = (int(out[0]), int(out[1]))
+        if len(_OUT_SIZES) > 4096:
+            _OUT_SIZES.clear()
+        _OUT_SIZES[key] = hit
+    return hit
 
 
 def max_pool2d_output_size(h: int, w: int, kernel_size, stride=None, padding=0, dilation=1,
                            ceil_mode: bool = False) -> tuple:
-    win, _a = _arr(_window(kernel_size, stride, padding, dilation))
-    out, _b = _out_arr(2)
-    _check(lib().kf_max_pool2d_output_size(h, w, win, int(ceil_mode), out))
-    return int(out[0]), int(out[1])
+    return _pool_out(int(h), int(w), _window(kernel_size, stride, padding, dilation), bool(ceil_mode))
 
 
 def kf_max_pool2d(x: torch.Tensor, kernel_size, stride=None, padding=0, dilation=1, ceil_mode: bool = False,
@@ -357,19 +378,20 @@ def kf_max_pool2d(x: torch.Tensor, kernel_size, stride=None, padding=0, dilation
     _need_cuda(x)
     if x.dim() not in (3, 4):
         raise KfError(2, "max_pool2d expects [N, C, H, W] or [C, H, W]")
-    oh, ow = max_pool2d_output_size(x.shape[-2], x.shape[-1], kernel_size, stride, padding, dilation, ceil_mode)
+    window = _window(kernel_size, stride, padding, dilation)
+    oh, ow = _pool_out(x.shape[-2], x.shape[-1], window, bool(ceil_mode))
     fmt = torch.channels_last if (x.dim() == 4 and not x.is_contiguous()
                                   and x.is_contiguous(memory_format=torch.channels_last)) else torch.contiguous_format
     yshape = tuple(x.shape[:-2]) + (oh, ow)
     y = out if out is not None else torch.empty(yshape, dtype=x.dtype, device=x.device, memory_format=fmt)
     idx = torch.empty(yshape, dtype=torch.int64, device=x.device, memory_format=fmt) if return_indices else None
-    win, _w = _arr(_window(kernel_size, stride, padding, dilation))
+    win, _w = _arr(window)
     shape, _s = _arr(x.shape)
     xs, _a = _arr(x.stride())
     ys, _b = _arr(y.stride())
     with _on(x):
-        _check(lib().kf_max_pool2d(ctypes.c_void_p(x.data_ptr()), _dtype(x), ctypes.c_void_p(y.data_ptr()),
-                                   ctypes.c_void_p(idx.data_ptr() if idx is not None else None), x.dim(), shape, xs,
+        _check(lib().kf_max_pool2d(x.data_ptr(), _dtype(x), y.data_ptr(),
+                                   idx.data_ptr() if idx is not None else None, x.dim(), shape, xs,
                                    ys, win, int(ceil_mode), _stream(x)))
     return (y, idx) if return_indices else y
 
@@ -402,7 +424,7 @@ def prepare_softmax(x: torch.Tensor, y: torch.Tensor, dim: int = -1) -> Prepared
     shape, a0 = _arr(x.shape)
     xs, a1 = _arr(x.stride())
     ys, a2 = _arr(y.stride())
-    args = (ctypes.c_void_p(x.data_ptr()), _dtype(x), ctypes.c_void_p(y.data_ptr()), _dtype(y), x.dim(), shape, xs,
+    args = (x.data_ptr(), _dtype(x), y.data_ptr(), _dtype(y), x.dim(), shape, xs,
             ys, dim, _stream(x))
     return Prepared(lib().kf_softmax, args, (x, y, a0, a1, a2))
 
@@ -414,8 +436,8 @@ def prepare_softmax_split(x: torch.Tensor, y: torch.Tensor, dim: int = -1,
     shape, a0 = _arr(x.shape)
     xs, a1 = _arr(x.stride())
     ys, a2 = _arr(y.stride())
-    args = (ctypes.c_void_p(x.data_ptr()), _dtype(x), ctypes.c_void_p(y.data_ptr()), _dtype(y), x.dim(), shape, xs,
-            ys, dim, ctypes.c_void_p(ws.data_ptr()), ws.numel(), _stream(x))
+    args = (x.data_ptr(), _dtype(x), y.data_ptr(), _dtype(y), x.dim(), shape, xs,
+            ys, dim, ws.data_ptr(), ws.numel(), _stream(x))
     return Prepared(lib().kf_softmax_split, args, (x, y, ws, a0, a1, a2))
 
 
@@ -424,7 +446,7 @@ def prepare_softmax_causal(x: torch.Tensor, y: torch.Tensor, scale: float = 1.0)
     shape, a0 = _arr(x.shape)
     xs, a1 = _arr(x.stride())
     ys, a2 = _arr(y.stride())
-    args = (ctypes.c_void_p(x.data_ptr()), _dtype(x), ctypes.c_void_p(y.data_ptr()), _dtype(y), x.dim(), shape, xs,
+    args = (x.data_ptr(), _dtype(x), y.data_ptr(), _dtype(y), x.dim(), shape, xs,
             ys, float(scale), _stream(x))
     return Prepared(lib().kf_softmax_causal, args, (x, y, a0, a1, a2))
 
@@ -438,10 +460,10 @@ def prepare_group_norm(x: torch.Tensor, y: torch.Tensor, num_groups: int, weight
     shape, a0 = _arr(x.shape)
     xs, a1 = _arr(x.stride())
     ys, a2 = _arr(y.stride())
-    args = (ctypes.c_void_p(x.data_ptr()), _dtype(x), ctypes.c_void_p(y.data_ptr()), x.dim(), shape, xs, ys,
-            num_groups, ctypes.c_void_p(weight.data_ptr() if weight is not None else None),
-            ctypes.c_void_p(bias.data_ptr() if bias is not None else None), at, float(eps),
-            ctypes.c_void_p(ws.data_ptr()), ws.numel(), _stream(x))
+    args = (x.data_ptr(), _dtype(x), y.data_ptr(), x.dim(), shape, xs, ys,
+            num_groups, weight.data_ptr() if weight is not None else None,
+            bias.data_ptr() if bias is not None else None, at, float(eps),
+            ws.data_ptr(), ws.numel(), _stream(x))
     return Prepared(lib().kf_group_norm, args, (x, y, weight, bias, ws, a0, a1, a2))
 
 
@@ -451,9 +473,9 @@ def prepare_layer_norm(x: torch.Tensor, y: torch.Tensor, normalized_ndim: int, w
     shape, a0 = _arr(x.shape)
     xs, a1 = _arr(x.stride())
     ys, a2 = _arr(y.stride())
-    args = (ctypes.c_void_p(x.data_ptr()), _dtype(x), ctypes.c_void_p(y.data_ptr()), x.dim(), shape, xs, ys,
-            normalized_ndim, ctypes.c_void_p(weight.data_ptr() if weight is not None else None),
-            ctypes.c_void_p(bias.data_ptr() if bias is not None else None), _affine_dtype(x, weight, bias),
+    args = (x.data_ptr(), _dtype(x), y.data_ptr(), x.dim(), shape, xs, ys,
+            normalized_ndim, weight.data_ptr() if weight is not None else None,
+            bias.data_ptr() if bias is not None else None, _affine_dtype(x, weight, bias),
             float(eps), _stream(x))
     return Prepared(lib().kf_layer_norm, args, (x, y, weight, bias, a0, a1, a2))
 
@@ -465,8 +487,8 @@ def prepare_max_pool2d(x: torch.Tensor, y: torch.Tensor, kernel_size, stride=Non
     shape, a0 = _arr(x.shape)
     xs, a1 = _arr(x.stride())
     ys, a2 = _arr(y.stride())
-    args = (ctypes.c_void_p(x.data_ptr()), _dtype(x), ctypes.c_void_p(y.data_ptr()),
-            ctypes.c_void_p(indices.data_ptr() if indices is not None else None), x.dim(), shape, xs, ys, win,
+    args = (x.data_ptr(), _dtype(x), y.data_ptr(),
+            indices.data_ptr() if indices is not None else None, x.dim(), shape, xs, ys, win,
             int(ceil_mode), _stream(x))
     return Prepared(lib().kf_max_pool2d, args, (x, y, indices, a0, a1, a2, a3))
 
@@ -477,6 +499,6 @@ def prepare_adaptive_avgpool2d(x: torch.Tensor, y: torch.Tensor) -> Prepared:
     shape, a0 = _arr(x.shape)
     xs, a1 = _arr(x.stride())
     ys, a2 = _arr(y.stride())
-    args = (ctypes.c_void_p(x.data_ptr()), _dtype(x), ctypes.c_void_p(y.data_ptr()), x.dim(), shape, xs, ys, oh, ow,
+    args = (x.data_ptr(), _dtype(x), y.data_ptr(), x.dim(), shape, xs, ys, oh, ow,
             _stream(x))
     return Prepared(lib().kf_adaptive_avgpool2d, args, (x, y, a0, a1, a2))
