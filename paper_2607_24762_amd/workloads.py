@@ -33,6 +33,17 @@ def randn(shape, dtype: str, seed: int, mean: float = 0.0, std: float = 1.0) -> 
     return cast(mean + std * rng.standard_normal(tuple(shape)), dtype)
 
 
+def randn_device(shape, dtype: str, seed: int, device="cuda", mean: float = 0.0, std: float = 1.0) -> torch.Tensor:
+    """mean + std * N(0, 1) drawn on the device from a seeded torch generator
+    (for tensors too large to draw on the host), cast to dtype."""
+    g = torch.Generator(device=device)
+    g.manual_seed(seed)
+    t = torch.randn(tuple(shape), generator=g, device=device, dtype=torch.float32)
+    if mean != 0.0 or std != 1.0:
+        t.mul_(std).add_(mean)
+    return t.to({"f32": torch.float32, "bf16": torch.bfloat16, "f16": torch.float16}[dtype])
+
+
 def causal_mask_(s: torch.Tensor) -> torch.Tensor:
     """Set the strict upper triangle (key j > query i) of the last two dims
     to -inf, in place; the diagonal stays, so every row keeps an entry."""
