@@ -149,24 +149,38 @@ def host_cpu() -> dict:
             "usable_cpus": len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else None}
 
 
-def copy_calibration(torch, dev, nbytes: int, reps: int = 50) -> dict:
+def copy_calibration(torch, dev, nbytes: int, reps: int = 48, pairs: int = 3) -> dict:
     """A plain device-to-device copy moving the same bytes as the attention
     softmax (half read, half written): what this machine's HBM sustains for a
-    pure stream, as context for the roofline fraction."""
-    src = torch.empty(nbytes // 2, dtype=torch.uint8, device=dev)
-    dst = torch.empty_like(src)
-    for _ in range(5):
-        dst.copy_(src)
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
-    for a, b in ev:
-        a.record()
-        dst.copy_(src)
-        b.record()
-    torch.cuda.synchronize()
-    us = sum(a.elapsed_time(b) for a, b in ev) * 1e3 / reps
-    del src, dst
-    return {"kind": "torch copy_ of 256 MiB (512 MiB moved)", "us_per_call": round(us, 3),
-            "gbps": round(nbytes / (us * 1e-6) / 1e9, 1)}
+    pure stream, as context for the roofline fraction.  Copies rotate over
+    `pairs` source / destination pairs (1.5 GiB in all), so, like the
+    operators' timings, they read HBM rather than the 256 MB Infinity Cache.
+    Timed for torch's copy_ and for the library's own streaming copy
+    (kf_stream_copy: 4 KiB per wave, non-temporal stores)."""
+    from paper_2607_24762_amd import kf355
+
+    srcs = [torch.empty(nbytes // 2, dtype=torch.uint8, device=dev) for _ in range(pairs)]
+    dsts = [torch.empty_like(s) for s in srcs]
+
+    def timed(copy):
+        for i in range(5):
+            copy(srcs[i % pairs], dsts[i % pairs])
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+        for i, (a, b) in enumerate(ev):
+            a.record()
+            copy(srcs[i % pairs], dsts[i % pairs])
+            b.record()
+        torch.cuda.synchronize()
+        return sum(a.elapsed_time(b) for a, b in ev) * 1e3 / reps
+
+    us = timed(lambda s, d: d.copy_(s))
+    own_us = timed(lambda s, d: kf355.stream_copy(s, d))
+    del srcs, dsts
+    return {"kind": f"torch copy_ of 256 MiB (512 MiB moved), {pairs} rotating pairs", "us_per_call": round(us, 3),
+            "gbps": round(nbytes / (us * 1e-6) / 1e9, 1),
+            "own_copy": {"kind": "kf_stream_copy of the same 256 MiB (4 KiB per wave, non-temporal stores)",
+                         "us_per_call": round(own_us, 3), "gbps": round(nbytes / (own_us * 1e-6) / 1e9, 1),
+                         "frac_of_peak": round(nbytes / (own_us * 1e-6) / 1e9 / PEAK_HBM_GBS, 4)}}
 
 
 def time_launches(torch, fns, steps, warmup):

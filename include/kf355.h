@@ -274,6 +274,20 @@ kf_status kf_max_pool2d(const void* x, kf_dtype dtype, void* y, int64_t* indices
 kf_status kf_max_pool2d_output_size(int64_t h, int64_t w, const int64_t* window, int32_t ceil_mode,
                                     int64_t* out_hw);
 
+/*
+ * kf_stream_copy -- measurement aid, not an operator: copies `bytes` from src
+ * to dst with the library's own streaming kernel (each wave moves 4 KiB of
+ * consecutive 16-byte vectors, non-temporal stores), so a benchmark can state
+ * what the HBM of this GPU sustains for a plain copy beside the operators'
+ * achieved bandwidth.
+ *
+ *  src, dst  device pointers, 16-byte aligned, not overlapping; the caller
+ *            owns both.
+ *  bytes     a multiple of 16 (0 is a no-op), else KF_ERR_BAD_SHAPE.
+ *  Misaligned pointers or overlap: KF_ERR_BAD_ARG.  Asynchronous on stream.
+ */
+kf_status kf_stream_copy(const void* src, void* dst, int64_t bytes, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -16,7 +16,7 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libkf355.so")
 
-SOURCES = ["kf355_api.cpp", "runtime.cpp", "softmax.hip", "group_norm.hip", "layer_norm.hip", "avgpool.hip", "maxpool.hip"]
+SOURCES = ["kf355_api.cpp", "runtime.cpp", "softmax.hip", "group_norm.hip", "layer_norm.hip", "avgpool.hip", "maxpool.hip", "calibrate.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 

@@ -445,6 +445,16 @@ kf_status kf_max_pool2d_output_size(int64_t h, int64_t w, const int64_t* window,
     return KF_OK;
 }
 
+kf_status kf_stream_copy(const void* src, void* dst, int64_t bytes, void* stream) {
+    begin();
+    if (bytes < 0 || bytes % 16) return fail(KF_ERR_BAD_SHAPE, "bytes must be a non-negative multiple of 16");
+    if (bytes == 0) return done(KF_OK, "noop");
+    if (!src || !dst) return fail(KF_ERR_NULL_POINTER, "src or dst is NULL");
+    if ((uintptr_t)src % 16 || (uintptr_t)dst % 16) return fail(KF_ERR_BAD_ARG, "src and dst must be 16-byte aligned");
+    if (overlaps(src, bytes, dst, bytes)) return fail(KF_ERR_BAD_ARG, "src and dst overlap");
+    return done(stream_copy_launch(src, dst, bytes, static_cast<hipStream_t>(stream)), "stream_copy");
+}
+
 kf_status kf_max_pool2d(const void* x, kf_dtype dtype, void* y, int64_t* indices, int32_t ndim, const int64_t* shape,
                         const int64_t* x_strides, const int64_t* y_strides, const int64_t* window, int32_t ceil_mode,
                         void* stream) {

@@ -94,6 +94,10 @@ struct MaxPoolArgs {
 };
 kf_status max_pool2d_launch(const MaxPoolArgs& a, hipStream_t s, const char** variant);
 
+// Calibration copy of `bytes` (a multiple of 16) between 16-byte aligned,
+// non-overlapping device buffers.
+kf_status stream_copy_launch(const void* src, void* dst, int64_t bytes, hipStream_t s);
+
 // Records the detail text of the current failure (thread-local).
 void set_error(const char* fmt, ...);
 

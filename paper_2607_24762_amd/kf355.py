@@ -54,6 +54,7 @@ _SIGNATURES = {
     "kf_max_pool2d_output_size": (ctypes.c_int, [ctypes.c_int64, ctypes.c_int64, _i64p, ctypes.c_int32, _i64p]),
     "kf_adaptive_avgpool2d": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p, ctypes.c_int32, _i64p,
                                              _i64p, _i64p, ctypes.c_int64, ctypes.c_int64, ctypes.c_void_p]),
+    "kf_stream_copy": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p]),
 }
 
 _lib = None
@@ -394,6 +395,18 @@ def kf_max_pool2d(x: torch.Tensor, kernel_size, stride=None, padding=0, dilation
                                    idx.data_ptr() if idx is not None else None, x.dim(), shape, xs,
                                    ys, win, int(ceil_mode), _stream(x)))
     return (y, idx) if return_indices else y
+
+
+def stream_copy(src: torch.Tensor, dst: torch.Tensor) -> torch.Tensor:
+    """Calibration copy through kf_stream_copy (a measurement aid, no
+    operator): dst[:] = src for two contiguous GPU tensors of equal byte size."""
+    _need_cuda(src, dst)
+    nbytes = src.numel() * src.element_size()
+    if not (src.is_contiguous() and dst.is_contiguous()) or dst.numel() * dst.element_size() != nbytes:
+        raise KfError(2, "stream_copy needs contiguous tensors of equal byte size")
+    with _on(src):
+        _check(lib().kf_stream_copy(src.data_ptr(), dst.data_ptr(), nbytes, _stream(src)))
+    return dst
 
 
 softmax = kf_softmax

@@ -299,3 +299,13 @@ def test_binding_refuses_cpu_tensors(lib):
     import torch
     with pytest.raises(ValueError):
         kf355.kf_softmax(torch.zeros(4, 4))
+
+
+def test_stream_copy_rejections(lib):
+    # The calibration copy checks its arguments on the host like the operators.
+    assert lib.kf_stream_copy(FAKE, FAKE + (1 << 30), 0, None) == OK          # no-op
+    assert lib.kf_stream_copy(FAKE, FAKE + (1 << 30), 24, None) == SHAPE      # not a multiple of 16
+    assert lib.kf_stream_copy(FAKE, FAKE + (1 << 30), -16, None) == SHAPE
+    assert lib.kf_stream_copy(None, FAKE, 64, None) == NULLP
+    assert lib.kf_stream_copy(FAKE + 4, FAKE + (1 << 30), 64, None) == ARG    # misaligned
+    assert lib.kf_stream_copy(FAKE, FAKE + 32, 64, None) == ARG               # overlap
