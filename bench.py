@@ -331,6 +331,30 @@ def avgpool_general_row(torch, F, dev, kf355, W, steps, warmup, sets_for):
     return row
 
 
+def small_softmax_row(torch, dev, kf355, W, steps, warmup, sets_for):
+    """The fp32 softmax configurations reported beside the large one: a
+    square [1024, 1024] and the MoE router logits [16384, 256] and [16384,
+    257] (rows not whole 16-byte vectors), libkf355 against torch eager."""
+    row = {}
+    for name in ("softmax_f32_1024x1024", "router_softmax_f32_16384x256", "router_softmax_f32_16384x257"):
+        src = W.WORKLOADS[name]()["x"].to(dev)
+        nb = src.numel() * 4 * 2
+        xs = [src.clone() for _ in range(sets_for(nb))]
+        fns = [kf355.prepare_softmax(x, torch.empty_like(x), -1) for x in xs]
+        fns[0]()
+        variant = kf355.last_variant()
+        us = time_launches(torch, fns, steps, warmup)
+        eager_us = time_launches(torch, [lambda x=x: torch.softmax(x, -1) for x in xs], min(steps, 50), warmup)
+        gbs = nb / (us * 1e-6) / 1e9
+        row[name] = {"workload": f"fp32 {list(src.shape)} softmax over the last dim", "variant": variant,
+                     "algorithmic_bytes": nb, "us_per_call": round(us, 3), "gbps": round(gbs, 1),
+                     "frac_of_peak": round(gbs / PEAK_HBM_GBS, 4), "torch_eager_us": round(eager_us, 3),
+                     "kf355_speedup": round(eager_us / us, 3), "buffer_sets": len(xs)}
+        del xs, fns
+        torch.cuda.empty_cache()
+    return row
+
+
 def gn_cl_row(torch, F, dev, kf355, W, steps, warmup, sets_for):
     """The SD3.5 VAE GroupNorm on a channels-last tensor: bf16
     [1,512,128,128], 32 groups, bf16 affine, libkf355 against torch eager."""
@@ -550,6 +574,7 @@ def main():
         next_rows["softmax_decode_split"] = decode_row(torch, dev, kf355, W, args.steps, args.warmup,
                                                        sets_for)
         next_rows["max_pool2d_stem"] = maxpool_row(torch, F, dev, kf355, W, args.steps, args.warmup, sets_for)
+        next_rows["softmax_fp32_configs"] = small_softmax_row(torch, dev, kf355, W, args.steps, args.warmup, sets_for)
         next_rows["avgpool_general_sizes"] = avgpool_general_row(torch, F, dev, kf355, W, args.steps, args.warmup,
                                                                   sets_for)
         next_rows["avgpool_channels_last"] = avgpool_cl_row(torch, F, dev, kf355, W, args.steps, args.warmup,

@@ -11,9 +11,16 @@
 //             are combined through LDS.
 //   sm_stream one workgroup per row of any length: an online (max, sum) pass,
 //             then a write pass that reads the row again.
+//   sm_span   short rows that are not whole 16-byte vectors (e.g. 257
+//             router logits): R consecutive rows, chosen so that their span
+//             starts 16-byte aligned for input and output, are staged in LDS
+//             with 16-byte loads; LPR lanes per row reduce and normalise in
+//             LDS; the span is written back with 16-byte stores.
 //   sm_cols   softmax over a non-innermost axis: one thread per column,
 //             online pass then write pass, coalesced across the inner axis.
 #include <math.h>
+
+#include <type_traits>
 
 #include "kf_device.hpp"
 #include "kf_exchange.hpp"
@@ -199,6 +206,90 @@ __global__ __launch_bounds__(NT) void sm_block(const void* __restrict__ x, void*
             else store1<TO>(y, base + e0, v[k][0]);
         }
     }
+}
+
+// --------------------------------------------------------------------------
+// Rows of `len` elements that are not whole 16-byte vectors, R rows per
+// workgroup (R * len <= kSpanFloats, R a multiple of what makes r0 * len a
+// whole number of input and output vectors, so every span starts aligned).
+constexpr int kSpanFloats = 4096;  // 16 KiB of fp32 staging per workgroup
+
+template <class TI, class TO, int LPR, int NPL>
+__global__ __launch_bounds__(256) void sm_span(const void* __restrict__ x, void* __restrict__ y, int64_t rows,
+                                               int32_t len, int32_t R) {
+    extern __shared__ float4 tile4[];  // R * len floats
+    float* tile = reinterpret_cast<float*>(tile4);
+    const int64_t r0 = (int64_t)blockIdx.x * R;
+    const int32_t nr = (int32_t)((rows - r0) < R ? (rows - r0) : R);
+    const int32_t span = nr * len;
+    const int64_t base = r0 * len;
+
+    // Stage: whole input vectors first (all loads before the LDS stores),
+    // then the span's last partial vector element by element.
+    constexpr int VI = TI::vec;
+    constexpr int NL = (kSpanFloats + 256 * VI - 1) / (256 * VI);
+    const int32_t whole_in = span - span % VI;
+    float v[NL][VI];
+#pragma unroll
+    for (int k = 0; k < NL; ++k) {
+        const int32_t e = (k * 256 + (int)threadIdx.x) * VI;
+        if (e < whole_in) load_vec<TI>(x, base + e, v[k]);
+    }
+#pragma unroll
+    for (int k = 0; k < NL; ++k) {
+        const int32_t e = (k * 256 + (int)threadIdx.x) * VI;
+        if (e < whole_in) {
+#pragma unroll
+            for (int i = 0; i < VI; i += 4)
+                tile4[(e + i) / 4] = make_float4(v[k][i], v[k][i + 1], v[k][i + 2], v[k][i + 3]);
+        }
+    }
+    for (int32_t e = whole_in + threadIdx.x; e < span; e += 256) tile[e] = load1<TI>(x, base + e);
+    __syncthreads();
+
+    // Row q: elements lr, lr + LPR, ... (at most NPL of them) of the LPR
+    // lanes that own it, read from LDS into registers in one batch (slots
+    // past the row are -inf), reduced and normalised there, written back
+    // once.  Lanes of rows past nr take part in the reductions and write
+    // nothing.
+    const int q = threadIdx.x / LPR, lr = threadIdx.x % LPR;
+    const bool row_ok = q < nr;
+    float* row = tile + (row_ok ? q : 0) * len;
+    float v2[NPL];
+#pragma unroll
+    for (int k = 0; k < NPL; ++k) {
+        const int32_t e = lr + k * LPR;
+        v2[k] = (row_ok && e < len) ? row[e] : -INFINITY;
+    }
+    float m = -INFINITY;
+#pragma unroll
+    for (int k = 0; k < NPL; ++k) m = fmaxf(m, v2[k]);
+    m = group_reduce<LPR>(m, OpMax{});
+    float sum = 0.f;
+#pragma unroll
+    for (int k = 0; k < NPL; ++k) {
+        v2[k] = exp_out<TO>(v2[k], m);
+        sum += v2[k];
+    }
+    sum = group_reduce<LPR>(sum, OpSum{});
+    const float inv = 1.f / sum;
+#pragma unroll
+    for (int k = 0; k < NPL; ++k) {
+        const int32_t e = lr + k * LPR;
+        if (row_ok && e < len) row[e] = v2[k] * inv;
+    }
+    __syncthreads();
+
+    // Store the span: whole output vectors, then the partial tail.
+    constexpr int VO = TO::vec;
+    const int32_t whole_out = span - span % VO;
+    for (int32_t e = (int32_t)threadIdx.x * VO; e < whole_out; e += 256 * VO) {
+        float o[VO];
+#pragma unroll
+        for (int i = 0; i < VO; ++i) o[i] = tile[e + i];
+        store_vec<TO, true>(y, base + e, o);
+    }
+    for (int32_t e = whole_out + threadIdx.x; e < span; e += 256) store1<TO>(y, base + e, tile[e]);
 }
 
 // --------------------------------------------------------------------------
@@ -659,6 +750,75 @@ Choice pick_resident(int64_t len) {
     return Choice{nullptr, nullptr};
 }
 
+// sm_span for rows of `len` elements that are not whole vectors, when both
+// bases are 16-byte aligned and at least the aligning row count fits the
+// staging tile.  Returns false (nothing launched) otherwise.
+template <class TI, class TO>
+bool run_span(const SoftmaxArgs& a, hipStream_t s, const char** variant) {
+    if ((uintptr_t)a.x % 16 || (uintptr_t)a.y % 16 || a.len < 1 || a.len > kSpanFloats) return false;
+    auto rows_for = [&](int64_t vec) {  // fewest rows whose span is a whole number of vectors
+        int64_t r = 1;
+        while ((a.len * r) % vec != 0) ++r;  // ends by r = vec
+        return r;
+    };
+    const int64_t ra = rows_for(TI::vec), rb = rows_for(TO::vec);
+    const int64_t align = ra > rb ? ra : rb;  // both are powers of two, so the larger is their lcm
+    // Rows per workgroup: as many as fit the staging tile, fewer while a lane
+    // would hold more than 16 of a row's elements (on [16384, 257] fp32:
+    // 12 rows and 17 per lane 8.27 us, 8 rows and 9 per lane 7.23 us, 4 rows
+    // and 5 per lane 8.88 us).
+    int64_t R = kSpanFloats / a.len;
+    R = R > 256 ? 256 : R;
+    R -= R % align;
+    if (R < align) return false;
+    auto lanes_for = [](int64_t rows) {  // the largest power of two <= 256 / rows, at most 64
+        int l = 1;
+        while (l < 64 && 2 * l * rows <= 256) l *= 2;
+        return l;
+    };
+    while (R - align >= align && (a.len + lanes_for(R) - 1) / lanes_for(R) > 16) R -= align;
+    const int64_t blocks = (a.outer + R - 1) / R;
+    if (blocks > INT32_MAX) return false;
+    const size_t lds = (size_t)(R * a.len) * sizeof(float);
+    auto go = [&](auto kernel) {
+        hipLaunchKernelGGL(kernel, dim3((unsigned)blocks), dim3(256), lds, s, a.x, a.y, a.outer, (int32_t)a.len,
+                           (int32_t)R);
+    };
+    // Lanes per row, then elements per lane: R * len <= 4096 and LPR > 128 / R
+    // give at most 32.
+    const int lpr = lanes_for(R);
+    const int64_t per_lane = (a.len + lpr - 1) / lpr;
+    const int npl = per_lane <= 8 ? 8 : per_lane <= 16 ? 16 : 32;
+    if (per_lane > 32) return false;
+    auto with_npl = [&](auto lpr_tag) {
+        constexpr int L = decltype(lpr_tag)::value;
+        if (npl == 8) go(sm_span<TI, TO, L, 8>);
+        else if (npl == 16) go(sm_span<TI, TO, L, 16>);
+        else go(sm_span<TI, TO, L, 32>);
+    };
+    switch (lpr) {
+        case 64: with_npl(std::integral_constant<int, 64>{}); break;
+        case 32: with_npl(std::integral_constant<int, 32>{}); break;
+        case 16: with_npl(std::integral_constant<int, 16>{}); break;
+        case 8: with_npl(std::integral_constant<int, 8>{}); break;
+        case 4: with_npl(std::integral_constant<int, 4>{}); break;
+        case 2: with_npl(std::integral_constant<int, 2>{}); break;
+        default: with_npl(std::integral_constant<int, 1>{}); break;
+    }
+    static const char* names[7][3] = {
+        {"sm_span_lpr1_npl8", "sm_span_lpr1_npl16", "sm_span_lpr1_npl32"},
+        {"sm_span_lpr2_npl8", "sm_span_lpr2_npl16", "sm_span_lpr2_npl32"},
+        {"sm_span_lpr4_npl8", "sm_span_lpr4_npl16", "sm_span_lpr4_npl32"},
+        {"sm_span_lpr8_npl8", "sm_span_lpr8_npl16", "sm_span_lpr8_npl32"},
+        {"sm_span_lpr16_npl8", "sm_span_lpr16_npl16", "sm_span_lpr16_npl32"},
+        {"sm_span_lpr32_npl8", "sm_span_lpr32_npl16", "sm_span_lpr32_npl32"},
+        {"sm_span_lpr64_npl8", "sm_span_lpr64_npl16", "sm_span_lpr64_npl32"}};
+    int li = 0;
+    while ((1 << li) < lpr) ++li;
+    *variant = names[li][npl == 8 ? 0 : npl == 16 ? 1 : 2];
+    return true;
+}
+
 template <class TI, class TO>
 kf_status run(const SoftmaxArgs& a, hipStream_t s, const char** variant) {
     if (a.inner != 1) {
@@ -682,20 +842,24 @@ kf_status run(const SoftmaxArgs& a, hipStream_t s, const char** variant) {
         // input and the output, and both base pointers 16-byte aligned.
         const bool vec_ok = (a.len % TI::vec == 0) && (a.len % TO::vec == 0) &&
                             ((uintptr_t)a.x % 16 == 0) && ((uintptr_t)a.y % 16 == 0);
-        Choice c{nullptr, nullptr};
-        if (a.len <= INT32_MAX)
-            c = vec_ok ? pick_resident<TI, TO, true>(a.len) : pick_resident<TI, TO, false>(a.len);
-        if (c.fn) {
-            c.fn(a, s);
-            *variant = c.name;
-        } else if (vec_ok) {
-            hipLaunchKernelGGL((sm_stream<TI, TO, 1024, true>), dim3((unsigned)a.outer), dim3(1024), 0, s,
-                               a.x, a.y, a.len);
-            *variant = "sm_stream_vec";
+        if (!vec_ok && run_span<TI, TO>(a, s, variant)) {
+            // short rows that are not whole vectors: staged spans
         } else {
-            hipLaunchKernelGGL((sm_stream<TI, TO, 1024, false>), dim3((unsigned)a.outer), dim3(1024), 0, s,
-                               a.x, a.y, a.len);
-            *variant = "sm_stream_scalar";
+            Choice c{nullptr, nullptr};
+            if (a.len <= INT32_MAX)
+                c = vec_ok ? pick_resident<TI, TO, true>(a.len) : pick_resident<TI, TO, false>(a.len);
+            if (c.fn) {
+                c.fn(a, s);
+                *variant = c.name;
+            } else if (vec_ok) {
+                hipLaunchKernelGGL((sm_stream<TI, TO, 1024, true>), dim3((unsigned)a.outer), dim3(1024), 0, s,
+                                   a.x, a.y, a.len);
+                *variant = "sm_stream_vec";
+            } else {
+                hipLaunchKernelGGL((sm_stream<TI, TO, 1024, false>), dim3((unsigned)a.outer), dim3(1024), 0, s,
+                                   a.x, a.y, a.len);
+                *variant = "sm_stream_scalar";
+            }
         }
     }
     const hipError_t err = hipGetLastError();

@@ -1,8 +1,10 @@
 """GPU parity of kf_softmax against the float64 oracle: row-length sweep
 across every kernel variant (one-row-per-lane-group, workgroup, streaming,
-strided axis), every dtype pair, misaligned rows, special values and in-place
-use.  Tolerances: fp32 outputs max abs error <= 1e-6; bf16 / fp16 outputs
+strided axis, staged spans of rows that are not whole vectors), every dtype
+pair, misaligned rows, special values and in-place use.  Tolerances: fp32 outputs max abs error <= 1e-6; bf16 / fp16 outputs
 within 1 unit in the last place of the oracle rounded once to the format."""
+import math
+
 import numpy as np
 import pytest
 import torch
@@ -76,7 +78,7 @@ def test_non_last_dim(shape, dim, pair):
 
 
 @pytest.mark.parametrize("dt", ["f32", "bf16", "f16"])
-@pytest.mark.parametrize("length", [5, 256, 4096, 70000])
+@pytest.mark.parametrize("length", [5, 256, 257, 4096, 70000])
 def test_special_rows(dt, length):
     note(f"softmax special rows {dt} len={length}")
     x = randn((8, length), "f32", seed=5, std=2.0)
@@ -99,15 +101,39 @@ def test_special_rows(dt, length):
         assert (yc[6] == 1.0 / length).all()  # a power-of-two uniform row is exact
 
 
+@pytest.mark.parametrize("length", [1000, 257])
 @pytest.mark.parametrize("dt", ["f32", "bf16"])
-def test_in_place(dt):
-    note(f"softmax in place {dt}")
-    x_cpu = randn((64, 1000), dt, seed=9)
+def test_in_place(dt, length):
+    note(f"softmax in place {dt} len={length}")
+    x_cpu = randn((64, length), dt, seed=9)
     x = x_cpu.cuda()
     y = kf355.kf_softmax(x, -1, out=x)
     torch.cuda.synchronize()
     assert y.data_ptr() == x.data_ptr()
     assert_close(x, oracle.softmax(x_cpu, -1), dt)
+
+
+def span_rows(length, pair):
+    """Rows per workgroup of the staged-span kernel for rows that are not
+    whole 16-byte vectors, or 0 when it does not apply: the fewest rows whose
+    span is whole input and output vectors, times as many as fit 4096 fp32."""
+    vin, vout = (4 if pair[0] == "f32" else 8), (4 if pair[1] == "f32" else 8)
+    if length % vin == 0 and length % vout == 0:
+        return 0
+    align = max(v // math.gcd(length, v) for v in (vin, vout))
+    r = min(256, 4096 // length)
+    r -= r % align
+    return r if r >= align else 0
+
+
+@pytest.mark.parametrize("pair", PAIRS, ids=lambda p: f"{p[0]}-{p[1]}")
+@pytest.mark.parametrize("length", [1, 3, 5, 257, 1023, 1025, 4095])
+def test_ragged_rows_take_staged_spans(pair, length):
+    rows = 1000                                   # not a multiple of any span's rows: a partial last workgroup
+    note(f"softmax staged spans {pair} len={length}")
+    x = randn((rows, length), pair[0], seed=length + 7, std=3.0)
+    _, variant, _ = run_case(x, -1, pair[1])
+    assert variant.startswith("sm_span") == (span_rows(length, pair) > 0), variant
 
 
 def test_zero_d_and_empty():
