@@ -927,11 +927,16 @@ kf_status run_causal(const CausalSoftmaxArgs& a, hipStream_t s, const char** var
 //   * it moves at least 160 KiB (input plus output), from where splitting
 //     measured 1.1-1.6x faster up to 64 rows;
 // and only while the rows alone occupy fewer than kSplitMaxRows workgroups.
-// Parts of 16 KiB of input (NV = 4) measured best (up to 1.5x faster than
-// 4 KiB parts at 8-16 rows of 131072); NV = 8 halves the grid when rows x
-// parts would exceed kSplitMaxGroups.
+// Part size: the smallest (NV = 1, 2, 4, 8 16-byte vectors per thread, 4-32
+// KiB of bf16) that leaves at most kSplitMaxParts parts per row: 16 KiB
+// parts measured up to 1.5x faster than 4 KiB ones at 8-16 rows of 131072
+// (64 parts per row is too many to gather), while for the decode step
+// [1, 8, 1, 32768] 4 KiB parts (16 per row) beat 16 KiB ones, 4.95 against
+// 5.41 us.  A larger NV halves the grid when rows x parts would exceed
+// kSplitMaxGroups.
 constexpr int64_t kSplitMaxRows = 128;
 constexpr int64_t kSplitMaxGroups = 1024;
+constexpr int64_t kSplitMaxParts = 16;
 constexpr int64_t kSplitMinRowBytes = 160 << 10;
 
 struct SplitPlan {
@@ -950,9 +955,10 @@ SplitPlan split_plan(const SoftmaxArgs& a) {
     // Parts tile the row from the aligned boundary below its start: a row
     // not starting on one spans up to xvec - 1 more elements.
     const int64_t span = a.len + ((a.len % xvec) ? xvec - 1 : 0);
-    for (int nv = 4; nv <= 8; nv *= 2) {
+    for (int nv = 1; nv <= 8; nv *= 2) {
         const int64_t parts = (span + (int64_t)kSplitNT * nv * xvec - 1) / ((int64_t)kSplitNT * nv * xvec);
         if (parts < 2) return none;
+        if (parts > kSplitMaxParts && nv < 8) continue;
         if (a.outer * parts <= kSplitMaxGroups) return SplitPlan{nv, parts};
     }
     return none;
@@ -979,7 +985,7 @@ bool launch_split(const SoftmaxArgs& a, const SplitPlan& plan, void* workspace, 
     p.len = a.len;
     p.total = a.outer * a.len;
     hipLaunchKernelGGL((sm_split<TI, TO, NV>), dim3((unsigned)grid), dim3(kSplitNT), 0, s, p);
-    *variant = NV == 4 ? "sm_split_nv4" : "sm_split_nv8";
+    *variant = NV == 1 ? "sm_split_nv1" : NV == 2 ? "sm_split_nv2" : NV == 4 ? "sm_split_nv4" : "sm_split_nv8";
     return true;
 }
 
@@ -992,8 +998,12 @@ kf_status run_split(const SoftmaxArgs& a, void* workspace, hipStream_t s, const 
                     (uintptr_t)a.y % 16 == 0;
     bool launched = false;
     if (ok) {
-        launched = plan.nv == 4 ? launch_split<TI, TO, 4>(a, plan, workspace, s, variant)
-                                : launch_split<TI, TO, 8>(a, plan, workspace, s, variant);
+        switch (plan.nv) {
+            case 1: launched = launch_split<TI, TO, 1>(a, plan, workspace, s, variant); break;
+            case 2: launched = launch_split<TI, TO, 2>(a, plan, workspace, s, variant); break;
+            case 4: launched = launch_split<TI, TO, 4>(a, plan, workspace, s, variant); break;
+            default: launched = launch_split<TI, TO, 8>(a, plan, workspace, s, variant); break;
+        }
     }
     if (!launched) return run<TI, TO>(a, s, variant);
     const hipError_t err = hipGetLastError();
