@@ -532,7 +532,7 @@ def main():
         us = e0.elapsed_time(e1) * 1e3 / args.steps
         gbs = cbytes / (us * 1e-6) / 1e9
         next_rows = {"softmax_causal_fused": {
-            "workload": "bf16 [1,8,4096,4096] raw scores, scale 1/16, causal; same output as the step's softmax",
+            "workload": "bf16 [1,8,4096,4096] raw scores, scale 1/16, causal; the step's softmax with scale and mask fused",
             "us_per_call": round(us, 3), "gbps": round(gbs, 1), "frac_of_peak": round(gbs / PEAK_HBM_GBS, 4),
             "algorithmic_bytes": cbytes, "variant": cvar,
             "vs_unfused_softmax": round(per_op["softmax"]["us_per_call"] / us, 3)}}

@@ -9,7 +9,7 @@ import numpy as np
 import pytest
 import torch
 
-from compare import assert_close, compare, note
+from compare import assert_close, compare, gpu_bits, note, ordered
 from oracle import oracle
 from paper_2607_24762_amd import kf355
 from paper_2607_24762_amd import workloads as W
@@ -40,15 +40,20 @@ def test_attention_workload_matches_oracle_and_unfused_path():
     x = w["x"].cuda()
     y = kf355.kf_softmax_causal(x, w["scale"])
     torch.cuda.synchronize()
-    assert kf355.last_variant() == "sm_causal_vec_nt256_nv2"
+    assert kf355.last_variant() == "sm_causal_vec_nt128_nv4"
     r = compare(y.cpu(), oracle.softmax_causal(w["x"], w["scale"]), "bf16")
     print("[parity] softmax_causal attention:", r, flush=True)
     assert r["ok"], r
-    # Scaling by 1/16 is exact, so the fused result must equal the unfused
-    # softmax of the pre-scaled, pre-masked scores bit for bit.
+    # Scaling by 1/16 is exact, so the fused result agrees with the unfused
+    # softmax of the pre-scaled, pre-masked scores to within the rounding of
+    # their fp32 sums, which the two kernels accumulate in different orders
+    # (128 threads x 4 vectors per row against 256 x 2): at most 1 bf16 ulp,
+    # and the masked entries are +0 in both.
     ref = kf355.kf_softmax(W.attn_softmax_causal_bf16()["x"].cuda(), -1)
     torch.cuda.synchronize()
-    assert torch.equal(y.view(torch.int16), ref.view(torch.int16))
+    a, b = ordered(gpu_bits(y)), ordered(gpu_bits(ref))
+    assert int(np.abs(a - b).max()) <= 1
+    assert np.array_equal(a == 0, b == 0)
 
 
 @pytest.mark.parametrize("pair", [("f32", "f32"), ("bf16", "bf16"), ("bf16", "f32"), ("f16", "f16"), ("f16", "f32")],
