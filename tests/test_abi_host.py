@@ -125,21 +125,22 @@ def test_softmax_split_rejections(lib):
 
 
 def test_softmax_split_workspace_query(lib):
-    # 8 rows of 32768 bf16 -> fp32 (192 KiB of traffic each): 4 parts of 8192
-    # elements per row; 8-byte (m, s) partials padded to a 256-byte line, one
+    # 8 rows of 32768 bf16 -> fp32 (192 KiB of traffic each): the smallest
+    # parts that leave at most 16 per row, 16 parts of 2048 elements; 8-byte
+    # (m, s) partials (1024 bytes, a whole number of 256-byte lines), one
     # 256-byte counter line per row, the 256-byte error block.
-    assert split_ws(lib, (1, 8, 1, 32768)) == (OK, 256 + 8 * 256 + 256)
+    assert split_ws(lib, (1, 8, 1, 32768)) == (OK, 1024 + 8 * 256 + 256)
     # The same rows with bf16 output move 128 KiB each: not split.
     assert split_ws(lib, (1, 8, 1, 32768), yt=BF16) == (OK, 0)
     # A row that does not start on a 16-byte boundary spans one more vector:
-    # 40001 elements take 5 parts.
+    # 40001 elements take 10 parts of 4096.
     assert split_ws(lib, (3, 40001)) == (OK, 256 + 3 * 256 + 256)
     # Rows of partial vectors beyond 16384 elements are split at any size
-    # (the per-row path would stream them twice): 16385 -> 3 parts.
+    # (the per-row path would stream them twice): 16385 -> 9 parts of 2048.
     assert split_ws(lib, (2, 16385), yt=BF16) == (OK, 256 + 2 * 256 + 256)
     assert split_ws(lib, (2, 16384), yt=BF16) == (OK, 0)
-    # 127 rows of 70000: 9 parts of 8192 would make 1143 workgroups, so
-    # parts of 16384 (5 per row).
+    # 127 rows of 70000: 9 parts of 8192 (the first size with at most 16 per
+    # row) would make 1143 workgroups, so parts of 16384 (5 per row).
     assert split_ws(lib, (127, 70000)) == (OK, ((127 * 5 * 8 + 255) // 256) * 256 + 127 * 256 + 256)
     assert split_ws(lib, (4096, 4096)) == (OK, 0)          # many rows: not split
     assert split_ws(lib, (4, 1000), xt=F32, yt=F32) == (OK, 0)
