@@ -331,6 +331,37 @@ def avgpool_general_row(torch, F, dev, kf355, W, steps, warmup, sets_for):
     return row
 
 
+def resnet_fp16_row(torch, F, dev, kf355, W, steps, warmup, sets_for):
+    """The ResNet-50 pooling shapes in fp16 (the precision the paper's
+    ResNet-50 ran in): head adaptive_avgpool2d [32,2048,7,7] -> 1x1 and stem
+    max_pool2d [32,64,112,112] 3x3 / 2 / 1, NCHW, libkf355 against torch
+    eager, rotating sets."""
+    row = {}
+    head = W.avgpool_resnet_head_f32()["x"].to(dev).half()
+    stem = W.maxpool_resnet_stem_f32()["x"].to(dev).half()
+    for key, src, out_shape, prep, eager in (
+            ("avgpool_head", head, (32, 2048, 1, 1), lambda x, y: kf355.prepare_adaptive_avgpool2d(x, y),
+             lambda x: F.adaptive_avg_pool2d(x, 1)),
+            ("max_pool_stem", stem, (32, 64, 56, 56), lambda x, y: kf355.prepare_max_pool2d(x, y, 3, 2, 1),
+             lambda x: F.max_pool2d(x, 3, 2, 1))):
+        nb = (src.numel() + out_shape[0] * out_shape[1] * out_shape[2] * out_shape[3]) * 2
+        xs = [src.clone() for _ in range(sets_for(nb))]
+        ys = [torch.empty(out_shape, dtype=torch.float16, device=dev) for _ in xs]
+        fns = [prep(x, y) for x, y in zip(xs, ys)]
+        fns[0]()
+        variant = kf355.last_variant()
+        us = time_launches(torch, fns, steps, warmup)
+        eager_us = time_launches(torch, [lambda x=x: eager(x) for x in xs], min(steps, 50), warmup)
+        gbs = nb / (us * 1e-6) / 1e9
+        row[key] = {"workload": f"fp16 {list(src.shape)} -> {list(out_shape)}", "variant": variant,
+                    "algorithmic_bytes": nb, "us_per_call": round(us, 3), "gbps": round(gbs, 1),
+                    "frac_of_peak": round(gbs / PEAK_HBM_GBS, 4), "torch_eager_us": round(eager_us, 3),
+                    "kf355_speedup": round(eager_us / us, 3), "buffer_sets": len(xs)}
+        del xs, ys, fns
+        torch.cuda.empty_cache()
+    return row
+
+
 def small_softmax_row(torch, dev, kf355, W, steps, warmup, sets_for):
     """The fp32 softmax configurations reported beside the large one: a
     square [1024, 1024] and the MoE router logits [16384, 256] and [16384,
@@ -574,6 +605,7 @@ def main():
         next_rows["softmax_decode_split"] = decode_row(torch, dev, kf355, W, args.steps, args.warmup,
                                                        sets_for)
         next_rows["max_pool2d_stem"] = maxpool_row(torch, F, dev, kf355, W, args.steps, args.warmup, sets_for)
+        next_rows["resnet50_fp16"] = resnet_fp16_row(torch, F, dev, kf355, W, args.steps, args.warmup, sets_for)
         next_rows["softmax_fp32_configs"] = small_softmax_row(torch, dev, kf355, W, args.steps, args.warmup, sets_for)
         next_rows["avgpool_general_sizes"] = avgpool_general_row(torch, F, dev, kf355, W, args.steps, args.warmup,
                                                                   sets_for)
