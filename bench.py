@@ -368,7 +368,8 @@ def small_softmax_row(torch, dev, kf355, W, steps, warmup, sets_for):
     257] (rows not whole 16-byte vectors), libkf355 against torch eager."""
     row = {}
     for name in ("softmax_f32_1024x1024", "router_softmax_f32_16384x256", "router_softmax_f32_16384x257"):
-        src = W.WORKLOADS[name]()["x"].to(dev)
+        wl = W.WORKLOADS[name]()
+        src = wl["x"].to(dev)
         nb = src.numel() * 4 * 2
         xs = [src.clone() for _ in range(sets_for(nb))]
         fns = [kf355.prepare_softmax(x, torch.empty_like(x), -1) for x in xs]
@@ -380,8 +381,11 @@ def small_softmax_row(torch, dev, kf355, W, steps, warmup, sets_for):
         row[name] = {"workload": f"fp32 {list(src.shape)} softmax over the last dim", "variant": variant,
                      "algorithmic_bytes": nb, "us_per_call": round(us, 3), "gbps": round(gbs, 1),
                      "frac_of_peak": round(gbs / PEAK_HBM_GBS, 4), "torch_eager_us": round(eager_us, 3),
-                     "kf355_speedup": round(eager_us / us, 3), "buffer_sets": len(xs)}
-        del xs, fns
+                     "kf355_speedup": round(eager_us / us, 3), "buffer_sets": len(xs),
+                     "input_sha256": W.sha256(wl["x"])}
+        if "outliers" in wl:
+            row[name]["outliers"] = wl["outliers"]
+        del xs, fns, wl
         torch.cuda.empty_cache()
     return row
 
@@ -432,6 +436,11 @@ def main():
          "softmax": W.attn_softmax_causal_bf16()}
     nbytes = algorithmic_bytes(w)
     step_bytes = sum(nbytes.values())
+    # The exact input bits of the step, so a run can be matched to the
+    # oracle's inputs (every consumer draws them from the same generators).
+    inputs = {"adaptive_avgpool2d": {"x": W.sha256(w["avgpool"]["x"])},
+              "group_norm": {k: W.sha256(w["group_norm"][k]) for k in ("x", "weight", "bias")},
+              "softmax": {"x": W.sha256(w["softmax"]["x"])}}
 
     # Rotating buffer sets: each operator cycles through enough distinct
     # input/output sets (>= 1 GiB in total) that no call finds its input in
@@ -636,7 +645,7 @@ def main():
         "data": "synthetic (seeded, shapes and distributions of the paper's workloads)",
         "config": {"workload": WORKLOAD, "step_algorithmic_bytes": step_bytes},
         "per_op": per_op, "roofline": roofline, "cpu_baseline": base, "cpu_baseline_parallel": base_mt,
-        "torch_eager": eager,
+        "torch_eager": eager, "inputs_sha256": inputs,
         "calibration": calib, "next_rows": next_rows,
     }
     print(json.dumps(out), flush=True)

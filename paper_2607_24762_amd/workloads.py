@@ -44,6 +44,13 @@ def randn_device(shape, dtype: str, seed: int, device="cuda", mean: float = 0.0,
     return t.to({"f32": torch.float32, "bf16": torch.bfloat16, "f16": torch.float16}[dtype])
 
 
+def sha256(t: torch.Tensor) -> str:
+    """SHA-256 of a CPU tensor's bytes in C order (the exact input bits)."""
+    import hashlib
+
+    return hashlib.sha256(t.contiguous().view(torch.uint8).numpy().tobytes()).hexdigest()
+
+
 def causal_mask_(s: torch.Tensor) -> torch.Tensor:
     """Set the strict upper triangle (key j > query i) of the last two dims
     to -inf, in place; the diagonal stays, so every row keeps an entry."""
@@ -148,8 +155,9 @@ def router_softmax_f32(seed: int = 5, experts: int = 256, tokens: int = 16384) -
     rng = np.random.default_rng(seed)
     z = rng.standard_normal((tokens, experts))
     u = rng.random((tokens, experts))
-    x = cast(z + 4.0 * (u < 0.05), "f32")
-    return {"op": "softmax", "x": x, "dim": -1, "out_dtype": "f32"}
+    outlier = u < 0.05
+    x = cast(z + 4.0 * outlier, "f32")
+    return {"op": "softmax", "x": x, "dim": -1, "out_dtype": "f32", "outliers": int(outlier.sum())}
 
 
 WORKLOADS = {
