@@ -16,6 +16,10 @@
 //             starts 16-byte aligned for input and output, are staged in LDS
 //             with 16-byte loads; LPR lanes per row reduce and normalise in
 //             LDS; the span is written back with 16-byte stores.
+//   sm_wave_edge / sm_block_edge  longer rows that are not whole vectors,
+//             on aligned bases: the aligned 16-byte vectors covering the row,
+//             neighbouring rows' elements masked, the two end vectors
+//             written element by element.
 //   sm_cols   softmax over a non-innermost axis: one thread per column,
 //             online pass then write pass, coalesced across the inner axis.
 #include <math.h>
@@ -206,6 +210,152 @@ __global__ __launch_bounds__(NT) void sm_block(const void* __restrict__ x, void*
             else store1<TO>(y, base + e0, v[k][0]);
         }
     }
+}
+
+// --------------------------------------------------------------------------
+// Rows that are not whole 16-byte vectors (len >= TI::vec, both bases
+// 16-byte aligned).  A row [r0, r1) is covered by the aligned vectors from
+// the one at or below r0: slot s of the row is the vector at
+// a0 + s * VEC, a0 = floor(r0 / VEC) * VEC, so every load is a 16-byte load
+// and at most ceil((len - 1) / VEC) + 1 slots are needed.  Elements of the
+// neighbouring rows in the two end vectors are set to -inf after the loads
+// (they weigh nothing), and only the row's own elements are written: whole
+// vectors inside the row with 16-byte stores, the two end vectors element by
+// element, so two rows sharing a vector never overwrite each other's values.
+
+// Loads slots s0 + k * STRIDE (k < NV) of the row.  Offsets are 32-bit,
+// relative to a0 (the row spans fewer than 2^31 elements): lo and hi are
+// the row's bounds and room the elements left in the tensor from a0.  Every
+// vector load is issued unconditionally: a slot past the row, a vector
+// crossing the end of the tensor, or a row past the last reads the vector at
+// a0 (for a row past the last, a0 = 0), which lies inside the tensor because
+// len >= VEC.  The tensor's last vector, when partial, is then read element
+// by element.
+template <class TI, int NV, int STRIDE>
+__device__ __forceinline__ void edge_load(const void* x, int64_t a0, int s0, int32_t lo, int32_t hi,
+                                          int32_t room, bool row_ok, float (&v)[NV][TI::vec]) {
+    constexpr int VEC = TI::vec;
+    const void* xa = static_cast<const char*>(x) + a0 * TI::bytes;
+#pragma unroll
+    for (int k = 0; k < NV; ++k) {
+        const int32_t e = (s0 + k * STRIDE) * VEC;
+        const bool use = row_ok && e < hi && e <= room - VEC;
+        load_vec<TI>(xa, use ? e : 0, v[k]);
+    }
+#pragma unroll
+    for (int k = 0; k < NV; ++k) {
+        const int32_t e = (s0 + k * STRIDE) * VEC;
+        if (row_ok && e < hi && e > room - VEC) {
+#pragma unroll
+            for (int i = 0; i < VEC; ++i)
+                if (e + i < hi) v[k][i] = load1<TI>(xa, e + i);
+        }
+#pragma unroll
+        for (int i = 0; i < VEC; ++i) v[k][i] = (row_ok && e + i >= lo && e + i < hi) ? v[k][i] : -INFINITY;
+    }
+}
+
+// Scales slots s0 + k * STRIDE by inv and writes the row's own elements.
+template <class TO, int VEC, int NV, int STRIDE>
+__device__ __forceinline__ void edge_store(void* y, int64_t a0, int s0, int32_t lo, int32_t hi, bool row_ok,
+                                           float (&v)[NV][VEC], float inv) {
+    void* ya = static_cast<char*>(y) + a0 * TO::bytes;
+#pragma unroll
+    for (int k = 0; k < NV; ++k) {
+        const int32_t e = (s0 + k * STRIDE) * VEC;
+        if (row_ok && e < hi) {
+#pragma unroll
+            for (int i = 0; i < VEC; ++i) v[k][i] *= inv;
+            if (e >= lo && e + VEC <= hi) {
+                store_span<TO, VEC>(ya, e, v[k]);
+            } else {
+#pragma unroll
+                for (int i = 0; i < VEC; ++i)
+                    if (e + i >= lo && e + i < hi) store1<TO>(ya, e + i, v[k][i]);
+            }
+        }
+    }
+}
+
+// Row bounds relative to its first aligned vector, and the elements left in
+// the tensor from there (capped at 2^31 - 1).
+struct EdgeRow {
+    int64_t a0;
+    int32_t lo, hi, room;
+    template <int VEC>
+    __device__ __forceinline__ static EdgeRow make(int64_t r0, int32_t len, int64_t total, bool row_ok) {
+        EdgeRow r;
+        r.a0 = row_ok ? (r0 / VEC) * VEC : 0;
+        r.lo = (int32_t)(r0 - r.a0);
+        r.hi = r.lo + len;
+        const int64_t left = total - r.a0;
+        r.room = left < (int64_t)INT32_MAX ? (int32_t)left : INT32_MAX;
+        return r;
+    }
+};
+
+// sm_wave for such rows: LPR lanes own a row, lane lr holds slots
+// lr + k * LPR.
+template <class TI, class TO, int LPR, int NV>
+__global__ __launch_bounds__(256) void sm_wave_edge(const void* __restrict__ x, void* __restrict__ y,
+                                                    int64_t rows, int32_t len) {
+    constexpr int VEC = TI::vec;
+    constexpr int RPW = kWave / LPR;
+    const int lane = threadIdx.x & (kWave - 1);
+    const int lr = lane & (LPR - 1);
+    const int64_t row = ((int64_t)blockIdx.x * (blockDim.x / kWave) + (threadIdx.x / kWave)) * RPW + lane / LPR;
+    const bool row_ok = row < rows;
+    const EdgeRow er = EdgeRow::make<VEC>(row * (int64_t)len, len, rows * (int64_t)len, row_ok);
+
+    float v[NV][VEC];
+    edge_load<TI, NV, LPR>(x, er.a0, lr, er.lo, er.hi, er.room, row_ok, v);
+    float m = -INFINITY;
+#pragma unroll
+    for (int k = 0; k < NV; ++k)
+#pragma unroll
+        for (int i = 0; i < VEC; ++i) m = fmaxf(m, v[k][i]);
+    m = group_reduce<LPR>(m, OpMax{});
+    float s = 0.f;
+#pragma unroll
+    for (int k = 0; k < NV; ++k)
+#pragma unroll
+        for (int i = 0; i < VEC; ++i) {
+            v[k][i] = exp_out<TO>(v[k][i], m);
+            s += v[k][i];
+        }
+    s = group_reduce<LPR>(s, OpSum{});
+    edge_store<TO, VEC, NV, LPR>(y, er.a0, lr, er.lo, er.hi, row_ok, v, 1.f / s);
+}
+
+// sm_block for such rows: one workgroup per row, each wave owning NV * 64
+// consecutive slots.
+template <class TI, class TO, int NT, int NV>
+__global__ __launch_bounds__(NT) void sm_block_edge(const void* __restrict__ x, void* __restrict__ y,
+                                                    int32_t len) {
+    constexpr int VEC = TI::vec;
+    constexpr int NW = NT / kWave;
+    __shared__ float red[NW];
+    const EdgeRow er = EdgeRow::make<VEC>((int64_t)blockIdx.x * len, len, (int64_t)gridDim.x * len, true);
+    const int seg = (threadIdx.x / kWave) * NV * kWave + (threadIdx.x & (kWave - 1));
+
+    float v[NV][VEC];
+    edge_load<TI, NV, kWave>(x, er.a0, seg, er.lo, er.hi, er.room, true, v);
+    float m = -INFINITY;
+#pragma unroll
+    for (int k = 0; k < NV; ++k)
+#pragma unroll
+        for (int i = 0; i < VEC; ++i) m = fmaxf(m, v[k][i]);
+    m = block_reduce<NW>(m, OpMax{}, red);
+    float s = 0.f;
+#pragma unroll
+    for (int k = 0; k < NV; ++k)
+#pragma unroll
+        for (int i = 0; i < VEC; ++i) {
+            v[k][i] = exp_out<TO>(v[k][i], m);
+            s += v[k][i];
+        }
+    s = block_reduce<NW>(s, OpSum{}, red);
+    edge_store<TO, VEC, NV, kWave>(y, er.a0, seg, er.lo, er.hi, true, v, 1.f / s);
 }
 
 // --------------------------------------------------------------------------
@@ -750,6 +900,57 @@ Choice pick_resident(int64_t len) {
     return Choice{nullptr, nullptr};
 }
 
+template <class TI, class TO, int LPR, int NV>
+void go_wave_edge(const SoftmaxArgs& a, hipStream_t s) {
+    constexpr int rows_per_block = (256 / kWave) * (kWave / LPR);
+    const int64_t blocks = (a.outer + rows_per_block - 1) / rows_per_block;
+    hipLaunchKernelGGL((sm_wave_edge<TI, TO, LPR, NV>), dim3((unsigned)blocks), dim3(256), 0, s, a.x, a.y, a.outer,
+                       (int32_t)a.len);
+}
+template <class TI, class TO, int NT, int NV>
+void go_block_edge(const SoftmaxArgs& a, hipStream_t s) {
+    hipLaunchKernelGGL((sm_block_edge<TI, TO, NT, NV>), dim3((unsigned)a.outer), dim3(NT), 0, s, a.x, a.y,
+                       (int32_t)a.len);
+}
+
+// Register-resident configuration for rows that are not whole vectors
+// (bases 16-byte aligned, len >= TI::vec): the smallest whose slots cover
+// the ceil((len - 1) / VEC) + 1 aligned vectors a row can touch.  Lane
+// groups up to 256 slots, then a workgroup per row, as for whole-vector rows.
+// The shortest rows that get here are 16-bit rows of more than 512 elements
+// (shorter ones are staged spans), so lane groups start at 80 slots.
+template <class TI, class TO>
+Choice pick_edge(int64_t len) {
+    constexpr int VEC = TI::vec;
+    const int64_t slots = (len - 1 + VEC - 1) / VEC + 1;
+#define KF_WAVE(LPR, NV)         \
+    if (slots <= (int64_t)(LPR) * (NV)) \
+        return Choice{go_wave_edge<TI, TO, LPR, NV>, "sm_wave_edge_lpr" #LPR "_nv" #NV};
+#define KF_BLOCK(NT, NV)         \
+    if (slots <= (int64_t)(NT) * (NV)) \
+        return Choice{go_block_edge<TI, TO, NT, NV>, "sm_block_edge_nt" #NT "_nv" #NV};
+    KF_WAVE(16, 5)
+    KF_WAVE(32, 3)
+    KF_WAVE(32, 4)
+    KF_WAVE(32, 5)
+    KF_WAVE(64, 3)
+    KF_WAVE(64, 4)
+    KF_BLOCK(256, 2)
+    KF_BLOCK(256, 3)
+    KF_BLOCK(512, 2)
+    KF_BLOCK(512, 3)
+    KF_BLOCK(1024, 2)
+    KF_BLOCK(1024, 3)
+    KF_BLOCK(1024, 4)
+    KF_BLOCK(1024, 5)
+    if constexpr (VEC == 4) {  // 16-element slots would spill at 9 per lane
+        KF_BLOCK(1024, 9)
+    }
+#undef KF_WAVE
+#undef KF_BLOCK
+    return Choice{nullptr, nullptr};
+}
+
 // sm_span for rows of `len` elements that are not whole vectors, when both
 // bases are 16-byte aligned and at least the aligning row count fits the
 // staging tile.  Returns false (nothing launched) otherwise.
@@ -842,12 +1043,26 @@ kf_status run(const SoftmaxArgs& a, hipStream_t s, const char** variant) {
         // input and the output, and both base pointers 16-byte aligned.
         const bool vec_ok = (a.len % TI::vec == 0) && (a.len % TO::vec == 0) &&
                             ((uintptr_t)a.x % 16 == 0) && ((uintptr_t)a.y % 16 == 0);
+        // Rows that are not whole vectors: staged spans where they apply;
+        // otherwise, on 16-byte aligned bases, aligned vectors with masked
+        // ends for 16-bit inputs (element-wise 2-byte loads move half the
+        // bytes per instruction: bf16 [32768, 4097] 185 us element-wise,
+        // 107 us with masked vectors) and for fp32 rows too long for the
+        // element-wise resident kernels; fp32 rows within their reach stay
+        // element-wise, which measured faster ([16384, 1025]: 26.6 against
+        // 30.3 us).
+        const bool edge_ok = !vec_ok && a.len >= TI::vec && ((uintptr_t)a.x % 16 == 0) &&
+                             ((uintptr_t)a.y % 16 == 0) && a.len <= INT32_MAX;
+        Choice c{nullptr, nullptr};
         if (!vec_ok && run_span<TI, TO>(a, s, variant)) {
-            // short rows that are not whole vectors: staged spans
+            // staged spans launched
         } else {
-            Choice c{nullptr, nullptr};
-            if (a.len <= INT32_MAX)
-                c = vec_ok ? pick_resident<TI, TO, true>(a.len) : pick_resident<TI, TO, false>(a.len);
+            if (a.len <= INT32_MAX) {
+                if (vec_ok) c = pick_resident<TI, TO, true>(a.len);
+                else if (edge_ok && TI::vec == 8) c = pick_edge<TI, TO>(a.len);
+                if (!c.fn && !vec_ok) c = pick_resident<TI, TO, false>(a.len);
+                if (!c.fn && edge_ok) c = pick_edge<TI, TO>(a.len);
+            }
             if (c.fn) {
                 c.fn(a, s);
                 *variant = c.name;

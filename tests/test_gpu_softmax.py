@@ -1,6 +1,7 @@
 """GPU parity of kf_softmax against the float64 oracle: row-length sweep
 across every kernel variant (one-row-per-lane-group, workgroup, streaming,
-strided axis, staged spans of rows that are not whole vectors), every dtype
+strided axis, staged spans and masked vectors for rows that are not whole
+vectors), every dtype
 pair, misaligned rows, special values and in-place use.  Tolerances: fp32 outputs max abs error <= 1e-6; bf16 / fp16 outputs
 within 1 unit in the last place of the oracle rounded once to the format."""
 import math
@@ -134,6 +135,62 @@ def test_ragged_rows_take_staged_spans(pair, length):
     x = randn((rows, length), pair[0], seed=length + 7, std=3.0)
     _, variant, _ = run_case(x, -1, pair[1])
     assert variant.startswith("sm_span") == (span_rows(length, pair) > 0), variant
+
+
+# Rows that are not whole 16-byte vectors, too long for staged spans: the
+# aligned vectors covering each row with the neighbours' elements masked.
+# Lengths reach every lane-group and workgroup configuration for 16-bit
+# inputs (ceil((L - 1) / 8) + 1 slots) and the fp32 ones past the
+# element-wise kernels' 16384; row counts leave a partial last workgroup and
+# a tensor that ends inside a vector.
+EDGE_16 = [515, 701, 1001, 1201, 1501, 2001, 3001, 4097, 8001, 12001, 16001, 24001, 32001, 40001]
+EDGE_32 = [16385, 20001, 30001]
+
+
+def edge_rows(length):
+    return 37 if length <= 8192 else 5
+
+
+@pytest.mark.parametrize("pair", [p for p in PAIRS if p[0] != "f32"], ids=lambda p: f"{p[0]}-{p[1]}")
+@pytest.mark.parametrize("length", EDGE_16)
+def test_masked_vector_rows_16bit(pair, length):
+    rows = edge_rows(length)
+    note(f"softmax masked-vector rows {pair} rows={rows} len={length}")
+    x = randn((rows, length), pair[0], seed=length + 3, std=3.0)
+    _, variant, _ = run_case(x, -1, pair[1])
+    assert variant.startswith(("sm_wave_edge", "sm_block_edge")), variant
+
+
+@pytest.mark.parametrize("length", EDGE_32)
+def test_masked_vector_rows_fp32(length):
+    note(f"softmax masked-vector rows f32 len={length}")
+    x = randn((5, length), "f32", seed=length + 3, std=3.0)
+    _, variant, _ = run_case(x, -1, "f32")
+    assert variant.startswith("sm_block_edge"), variant
+
+
+@pytest.mark.parametrize("dt", ["bf16", "f16"])
+def test_masked_vector_rows_special_and_in_place(dt):
+    note(f"softmax masked-vector rows special values in place {dt}")
+    length = 4097
+    x = randn((9, length), "f32", seed=21, std=2.0)
+    x[0] = float("-inf")                      # fully masked -> NaN row
+    x[1, 7] = float("nan")                    # NaN in the row's first vector
+    x[2, length - 1] = float("inf")           # +inf in the row's last vector
+    x[3] = float("-inf")
+    x[3, 0] = 0.5                             # one finite entry -> exact one-hot
+    x[4, 1::2] = float("-inf")                # masked entries -> exact +0
+    x[5] = 1.25                               # uniform row
+    x_cpu = x.to(TORCH[dt])
+    xd = x_cpu.cuda()
+    y = kf355.kf_softmax(xd, -1, out=xd)
+    torch.cuda.synchronize()
+    assert y.data_ptr() == xd.data_ptr() and kf355.last_variant().startswith("sm_block_edge")
+    assert_close(y, oracle.softmax(x_cpu, -1), dt)
+    yc = y.float().cpu()
+    assert torch.isnan(yc[:3]).all() and not torch.isnan(yc[3:]).any()
+    assert yc[3, 0].item() == 1.0 and (yc[3, 1:] == 0).all() and not torch.signbit(yc[3]).any()
+    assert (yc[4, 1::2] == 0).all()
 
 
 def test_zero_d_and_empty():
