@@ -223,7 +223,8 @@ __global__ __launch_bounds__(NT) void sm_block(const void* __restrict__ x, void*
 // vectors inside the row with 16-byte stores, the two end vectors element by
 // element, so two rows sharing a vector never overwrite each other's values.
 
-// Loads slots s0 + k * STRIDE (k < NV) of the row.  Offsets are 32-bit,
+// Loads slots s0 + k * STRIDE (k < NV) of the row (elements [lo, hi)
+// relative to a0), multiplied by `scale` when SCALED.  Offsets are 32-bit,
 // relative to a0 (the row spans fewer than 2^31 elements): lo and hi are
 // the row's bounds and room the elements left in the tensor from a0.  Every
 // vector load is issued unconditionally: a slot past the row, a vector
@@ -231,9 +232,10 @@ __global__ __launch_bounds__(NT) void sm_block(const void* __restrict__ x, void*
 // a0 (for a row past the last, a0 = 0), which lies inside the tensor because
 // len >= VEC.  The tensor's last vector, when partial, is then read element
 // by element.
-template <class TI, int NV, int STRIDE>
+template <class TI, int NV, int STRIDE, bool SCALED = false>
 __device__ __forceinline__ void edge_load(const void* x, int64_t a0, int s0, int32_t lo, int32_t hi,
-                                          int32_t room, bool row_ok, float (&v)[NV][TI::vec]) {
+                                          int32_t room, bool row_ok, float (&v)[NV][TI::vec],
+                                          float scale = 1.f) {
     constexpr int VEC = TI::vec;
     const void* xa = static_cast<const char*>(x) + a0 * TI::bytes;
 #pragma unroll
@@ -251,7 +253,10 @@ __device__ __forceinline__ void edge_load(const void* x, int64_t a0, int s0, int
                 if (e + i < hi) v[k][i] = load1<TI>(xa, e + i);
         }
 #pragma unroll
-        for (int i = 0; i < VEC; ++i) v[k][i] = (row_ok && e + i >= lo && e + i < hi) ? v[k][i] : -INFINITY;
+        for (int i = 0; i < VEC; ++i) {
+            const float z = SCALED ? v[k][i] * scale : v[k][i];
+            v[k][i] = (row_ok && e + i >= lo && e + i < hi) ? z : -INFINITY;
+        }
     }
 }
 
@@ -512,6 +517,51 @@ __global__ __launch_bounds__(NT) void sm_causal(const void* __restrict__ x, void
             else store1<TO>(y, base + e0, v[kk][0]);
         }
     }
+}
+
+// sm_causal for rows that are not whole vectors (k >= TI::vec, aligned
+// bases): the masked-vector row layout of sm_block_edge, with the visible
+// prefix [lo, lo + live) loaded (scaled, masked to -inf past it) and every
+// element of the row [lo, hi) written.
+template <class TI, class TO, int NT, int NV>
+__global__ __launch_bounds__(NT) void sm_causal_edge(const void* __restrict__ x, void* __restrict__ y, int32_t q,
+                                                     int32_t k, float scale) {
+    constexpr int VEC = TI::vec;
+    constexpr int NW = NT / kWave;
+    __shared__ float red[NW];
+    const int64_t row = blockIdx.x;
+    const int32_t i = (int32_t)(row % q);
+    const int32_t live = max(0, min(k, i + (k - q) + 1));
+    const EdgeRow er = EdgeRow::make<VEC>(row * k, k, (int64_t)gridDim.x * k, true);
+    const int wave = threadIdx.x / kWave;
+    const int seg = wave * NV * kWave + (threadIdx.x & (kWave - 1));
+    const int32_t vis = er.lo + live;
+
+    float v[NV][VEC];
+    if (wave * NV * kWave * VEC < vis) {  // uniform per wave: segments past the visible prefix load nothing
+        edge_load<TI, NV, kWave, true>(x, er.a0, seg, er.lo, vis, er.room, true, v, scale);
+    } else {
+#pragma unroll
+        for (int kk = 0; kk < NV; ++kk)
+#pragma unroll
+            for (int ii = 0; ii < VEC; ++ii) v[kk][ii] = -INFINITY;
+    }
+    float m = -INFINITY;
+#pragma unroll
+    for (int kk = 0; kk < NV; ++kk)
+#pragma unroll
+        for (int ii = 0; ii < VEC; ++ii) m = fmaxf(m, v[kk][ii]);
+    m = block_reduce<NW>(m, OpMax{}, red);
+    float s = 0.f;
+#pragma unroll
+    for (int kk = 0; kk < NV; ++kk)
+#pragma unroll
+        for (int ii = 0; ii < VEC; ++ii) {
+            v[kk][ii] = exp_out<TO>(v[kk][ii], m);
+            s += v[kk][ii];
+        }
+    s = block_reduce<NW>(s, OpSum{}, red);
+    edge_store<TO, VEC, NV, kWave>(y, er.a0, seg, er.lo, er.hi, true, v, 1.f / s);
 }
 
 // --------------------------------------------------------------------------
@@ -1091,6 +1141,12 @@ void go_causal(const CausalSoftmaxArgs& a, hipStream_t s) {
                        a.y, (int32_t)a.q, (int32_t)a.k, a.scale);
 }
 
+template <class TI, class TO, int NT, int NV>
+void go_causal_edge(const CausalSoftmaxArgs& a, hipStream_t s) {
+    hipLaunchKernelGGL((sm_causal_edge<TI, TO, NT, NV>), dim3((unsigned)(a.batch * a.q)), dim3(NT), 0, s, a.x,
+                       a.y, (int32_t)a.q, (int32_t)a.k, a.scale);
+}
+
 template <class TI, class TO>
 kf_status run_causal(const CausalSoftmaxArgs& a, hipStream_t s, const char** variant) {
     if (a.batch * a.q > (int64_t)INT32_MAX || a.k > (int64_t)INT32_MAX || a.q > (int64_t)INT32_MAX) {
@@ -1100,8 +1156,33 @@ kf_status run_causal(const CausalSoftmaxArgs& a, hipStream_t s, const char** var
     }
     const bool vec = (a.k % TI::vec == 0) && (a.k % TO::vec == 0) && ((uintptr_t)a.x % 16 == 0) &&
                      ((uintptr_t)a.y % 16 == 0);
+    // Rows that are not whole vectors, on aligned bases: masked vectors
+    // covering each row (at most ceil((k - 1) / VEC) + 1 of them).
+    const bool edge = !vec && a.k >= TI::vec && ((uintptr_t)a.x % 16 == 0) && ((uintptr_t)a.y % 16 == 0);
     const int64_t slots = vec ? a.k / TI::vec : a.k;
     bool done = false;
+    if (edge) {
+        const int64_t eslots = (a.k - 1 + TI::vec - 1) / TI::vec + 1;
+#define KF_CAUSAL_EDGE(NT, NV)                                                \
+    if (!done && eslots <= (int64_t)(NT) * (NV)) {                            \
+        go_causal_edge<TI, TO, NT, NV>(a, s);                                 \
+        *variant = "sm_causal_edge_nt" #NT "_nv" #NV;                         \
+        done = true;                                                          \
+    }
+        KF_CAUSAL_EDGE(64, 2)
+        KF_CAUSAL_EDGE(128, 2)
+        KF_CAUSAL_EDGE(128, 3)
+        KF_CAUSAL_EDGE(128, 5)
+        KF_CAUSAL_EDGE(512, 2)
+        KF_CAUSAL_EDGE(512, 3)
+        KF_CAUSAL_EDGE(1024, 2)
+        KF_CAUSAL_EDGE(1024, 3)
+        KF_CAUSAL_EDGE(1024, 5)
+        if constexpr (TI::vec == 4) {
+            KF_CAUSAL_EDGE(1024, 9)
+        }
+#undef KF_CAUSAL_EDGE
+    }
 #define KF_CAUSAL(NT, NV)                                                                                    \
     if (!done && slots <= (int64_t)(NT) * (NV)) {                                                            \
         if (vec) go_causal<TI, TO, NT, NV, true>(a, s);                                                      \

@@ -1,7 +1,8 @@
 """GPU parity of kf_softmax_causal (scale + causal mask + softmax in one
 pass) against the float64 oracle: the attention workload shape, query /
 key lengths that differ (mask aligned to the end of the key axis), every
-dtype pair, row lengths across the kernel table, unaligned rows, garbage in
+dtype pair, row lengths across the kernel table, rows that are not whole
+vectors, misaligned bases, garbage in
 the masked triangle, rows with no visible key, and in-place use.
 Tolerances as for kf_softmax: fp32 max abs error <= 1e-6, bf16 / fp16
 within 1 unit in the last place of the oracle rounded once."""
@@ -85,6 +86,49 @@ def test_unaligned_rows_use_element_access():
     torch.cuda.synchronize()
     assert "scalar" in kf355.last_variant()
     assert_close(y, oracle.softmax_causal(x_cpu, 0.5), "bf16")
+
+
+PAIRS = [("f32", "f32"), ("bf16", "bf16"), ("bf16", "f32"), ("f16", "f16"), ("f16", "f32")]
+
+
+@pytest.mark.parametrize("pair", PAIRS, ids=lambda p: f"{p[0]}-{p[1]}")
+@pytest.mark.parametrize("qk", [(3, 9), (9, 9), (33, 257), (40, 1001), (12, 4097), (3, 12001), (2, 30001),
+                                (1, 40001)])
+def test_rows_that_are_not_whole_vectors(pair, qk):
+    """Aligned bases, k not a multiple of the 16-byte vector: masked vectors
+    covering each row (q < k puts the visible boundary mid-row; two batches
+    so rows share end vectors across the batch boundary too)."""
+    q, k = qk
+    if pair[0] == "f32" and k > 36864:
+        pytest.skip("fp32 rows that are not whole vectors above 36864 are outside the table")
+    note(f"softmax_causal masked-vector rows {pair} q={q} k={k}")
+    x = randn((2, q, k), pair[0], seed=q * k, std=3.0)
+    _, variant = run(x, 0.37, pair[1])
+    assert variant.startswith("sm_causal_edge"), variant
+
+
+def test_rows_that_are_not_whole_vectors_ignore_the_masked_triangle_in_place():
+    note("softmax_causal masked-vector rows: NaN in the masked triangle, in place")
+    q = k = 515
+    x = randn((2, q, k), "bf16", seed=18, std=2.0)
+    poisoned = x.clone()
+    poisoned[:, torch.ones(q, k, dtype=torch.bool).triu(1)] = float("nan")
+    a = kf355.kf_softmax_causal(x.cuda(), 0.25)
+    pd = poisoned.cuda()
+    b = kf355.kf_softmax_causal(pd, 0.25, out=pd)
+    torch.cuda.synchronize()
+    assert kf355.last_variant().startswith("sm_causal_edge")
+    assert torch.equal(a.view(torch.int16), b.view(torch.int16))
+    assert_close(b, oracle.softmax_causal(x, 0.25), "bf16")
+
+
+@pytest.mark.parametrize("dt,k", [("bf16", 40961), ("f32", 36865)])
+def test_rows_beyond_the_masked_vector_table_are_refused(dt, k):
+    note(f"softmax_causal {dt} k={k} refused")
+    x = torch.zeros((1, k), dtype=TORCH[dt], device="cuda")
+    with pytest.raises(kf355.KfError) as e:
+        kf355.kf_softmax_causal(x, 1.0)
+    assert e.value.status == 5  # KF_ERR_UNSUPPORTED_LAYOUT
 
 
 def test_masked_triangle_is_never_used():
