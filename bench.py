@@ -331,6 +331,40 @@ def avgpool_general_row(torch, F, dev, kf355, W, steps, warmup, sets_for):
     return row
 
 
+def unaligned_softmax_row(torch, dev, kf355, W, steps, warmup, sets_for):
+    """Attention scores whose key length is not a multiple of the 16-byte
+    vector (a prompt one token past a power of two): bf16 [1, 8, 4097, 4097]
+    drawn on the device (3z/16), through kf_softmax on causally pre-masked
+    scores and kf_softmax_causal on the raw scores (scale 1), against torch
+    eager softmax of the pre-masked scores."""
+    q = k = 4097
+    raw = W.randn_device((1, 8, q, k), "bf16", seed=13, std=3.0 / 16.0)
+    masked = raw.masked_fill(torch.ones(q, k, dtype=torch.bool, device=dev).triu_(1), float("-inf"))
+    numel = raw.numel()
+    visible = 8 * (q * (q + 1) // 2)
+    plain_bytes, causal_bytes = numel * 2 * 2, visible * 2 + numel * 2
+    row = {"workload": "bf16 [1,8,4097,4097] attention scores (rows not whole 16-byte vectors)"}
+    for name, src, nb, prep in (
+            ("softmax", masked, plain_bytes, lambda x: kf355.prepare_softmax(x, torch.empty_like(x), -1)),
+            ("softmax_causal", raw, causal_bytes,
+             lambda x: kf355.prepare_softmax_causal(x, torch.empty_like(x), 1.0))):
+        xs = [src.clone() for _ in range(sets_for(nb))]
+        fns = [prep(x) for x in xs]
+        fns[0]()
+        variant = kf355.last_variant()
+        us = time_launches(torch, fns, steps, warmup)
+        gbs = nb / (us * 1e-6) / 1e9
+        row[name] = {"variant": variant, "algorithmic_bytes": nb, "us_per_call": round(us, 3),
+                     "gbps": round(gbs, 1), "frac_of_peak": round(gbs / PEAK_HBM_GBS, 4), "buffer_sets": len(xs)}
+        if name == "softmax":
+            eager_us = time_launches(torch, [lambda x=x: torch.softmax(x, -1) for x in xs], min(steps, 50), warmup)
+            row[name]["torch_eager_us"] = round(eager_us, 3)
+            row[name]["kf355_speedup"] = round(eager_us / us, 3)
+        del xs, fns
+        torch.cuda.empty_cache()
+    return row
+
+
 def resnet_fp16_row(torch, F, dev, kf355, W, steps, warmup, sets_for):
     """The ResNet-50 pooling shapes in fp16 (the precision the paper's
     ResNet-50 ran in): head adaptive_avgpool2d [32,2048,7,7] -> 1x1 and stem
@@ -418,7 +452,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-eager", action="store_true")
-    ap.add_argument("--no-next", action="store_true", help="skip the next-row measurements (fused causal softmax, layer_norm, decode split softmax, max_pool2d, channels-last and general-size pooling, channels-last group_norm)")
+    ap.add_argument("--no-next", action="store_true", help="skip the next-row measurements (fused causal softmax, layer_norm, decode split softmax, max_pool2d, channels-last and general-size pooling, channels-last group_norm, rows that are not whole vectors)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: the operators shard by rows / groups / planes with no exchange, "
@@ -438,7 +472,7 @@ def main():
     step_bytes = sum(nbytes.values())
     # The exact input bits of the step, so a run can be matched to the
     # oracle's inputs (every consumer draws them from the same generators).
-    inputs = {"adaptive_avgpool2d": {"x": W.sha256(w["avgpool"]["x"])},
+    input_hashes = {"adaptive_avgpool2d": {"x": W.sha256(w["avgpool"]["x"])},
               "group_norm": {k: W.sha256(w["group_norm"][k]) for k in ("x", "weight", "bias")},
               "softmax": {"x": W.sha256(w["softmax"]["x"])}}
 
@@ -615,6 +649,8 @@ def main():
                                                        sets_for)
         next_rows["max_pool2d_stem"] = maxpool_row(torch, F, dev, kf355, W, args.steps, args.warmup, sets_for)
         next_rows["resnet50_fp16"] = resnet_fp16_row(torch, F, dev, kf355, W, args.steps, args.warmup, sets_for)
+        next_rows["softmax_unaligned_rows"] = unaligned_softmax_row(torch, dev, kf355, W, args.steps, args.warmup,
+                                                                    sets_for)
         next_rows["softmax_fp32_configs"] = small_softmax_row(torch, dev, kf355, W, args.steps, args.warmup, sets_for)
         next_rows["avgpool_general_sizes"] = avgpool_general_row(torch, F, dev, kf355, W, args.steps, args.warmup,
                                                                   sets_for)
@@ -645,7 +681,7 @@ def main():
         "data": "synthetic (seeded, shapes and distributions of the paper's workloads)",
         "config": {"workload": WORKLOAD, "step_algorithmic_bytes": step_bytes},
         "per_op": per_op, "roofline": roofline, "cpu_baseline": base, "cpu_baseline_parallel": base_mt,
-        "torch_eager": eager, "inputs_sha256": inputs,
+        "torch_eager": eager, "inputs_sha256": input_hashes,
         "calibration": calib, "next_rows": next_rows,
     }
     print(json.dumps(out), flush=True)
