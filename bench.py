@@ -304,17 +304,20 @@ def avgpool_cl_row(torch, F, dev, kf355, W, steps, warmup, sets_for):
 
 
 def avgpool_general_row(torch, F, dev, kf355, W, steps, warmup, sets_for):
-    """adaptive_avgpool2d to general output sizes, fp32 NCHW: [32,512,14,14]
-    -> 7x7 (2x2 windows) and [32,256,13,13] -> 6x6 (overlapping 3x3
-    windows), libkf355 against torch eager, rotating sets."""
+    """adaptive_avgpool2d to general output sizes, fp32: [32,512,14,14] -> 7x7
+    (2x2 windows) and [32,256,13,13] -> 6x6 (overlapping 3x3 windows), NCHW
+    and channels last, libkf355 against torch eager, rotating sets."""
     row = {}
-    for key, shape, out in (("vgg_14x14_to_7x7", (32, 512, 14, 14), (7, 7)),
-                            ("alexnet_13x13_to_6x6", (32, 256, 13, 13), (6, 6))):
+    for key, shape, out, cl in (("vgg_14x14_to_7x7", (32, 512, 14, 14), (7, 7), False),
+                                ("alexnet_13x13_to_6x6", (32, 256, 13, 13), (6, 6), False),
+                                ("vgg_14x14_to_7x7_channels_last", (32, 512, 14, 14), (7, 7), True),
+                                ("alexnet_13x13_to_6x6_channels_last", (32, 256, 13, 13), (6, 6), True)):
+        fmt = torch.channels_last if cl else torch.contiguous_format
         w = W.avgpool_general_f32(shape=shape, output_size=out)
-        src = w["x"].to(dev)
+        src = w["x"].to(dev).contiguous(memory_format=fmt)
         nb = src.numel() * 4 + shape[0] * shape[1] * out[0] * out[1] * 4
-        xs = [src.clone() for _ in range(sets_for(nb))]
-        ys = [torch.empty(shape[0], shape[1], out[0], out[1], device=dev) for _ in xs]
+        xs = [src.clone(memory_format=fmt) for _ in range(sets_for(nb))]
+        ys = [torch.empty(shape[0], shape[1], out[0], out[1], device=dev, memory_format=fmt) for _ in xs]
         fns = [kf355.prepare_adaptive_avgpool2d(x, y) for x, y in zip(xs, ys)]
         fns[0]()
         variant = kf355.last_variant()
@@ -322,7 +325,8 @@ def avgpool_general_row(torch, F, dev, kf355, W, steps, warmup, sets_for):
         eager_us = time_launches(torch, [lambda x=x: F.adaptive_avg_pool2d(x, out) for x in xs], min(steps, 50),
                                  warmup)
         gbs = nb / (us * 1e-6) / 1e9
-        row[key] = {"workload": f"fp32 {list(shape)} -> {out[0]}x{out[1]}", "variant": variant,
+        row[key] = {"workload": f"fp32 {list(shape)}{' channels last' if cl else ''} -> {out[0]}x{out[1]}",
+                    "variant": variant,
                     "algorithmic_bytes": nb, "us_per_call": round(us, 3), "gbps": round(gbs, 1),
                     "frac_of_peak": round(gbs / PEAK_HBM_GBS, 4), "torch_eager_us": round(eager_us, 3),
                     "kf355_speedup": round(eager_us / us, 3), "buffer_sets": len(xs)}

@@ -15,6 +15,8 @@
 //             staged in LDS as in ap_flat, then one thread per output cell
 //             sums its window from LDS.
 //   ap_window any output size, larger planes: one thread per output cell.
+//   ap_nhwc_cell  channels last, windows of at most 4 x 4: a thread per
+//             output cell and 16-byte channel vector.
 //   ap_nhwc   channels last, any output size: a workgroup owns one output
 //             cell of one sample and 64 vectors of 16 bytes of channels;
 //             its four thread groups sum interleaved window pixels, so
@@ -294,6 +296,69 @@ __global__ __launch_bounds__(kNT) void ap_nhwc(const void* __restrict__ x, void*
     }
 }
 
+// Channels last, windows of at most K x K pixels (ap_nhwc_cell): one thread
+// per (sample, output cell, 16-byte channel vector), consecutive threads on
+// consecutive channel vectors, so every window pixel is read as a coalesced
+// run of channels.  The K x K block is read from clamped addresses (a pixel
+// past the window repeats the window's last row or column), all loads
+// issued before the adds, and the pixels inside the window are added in
+// row-major order.  No LDS and no barrier: small windows leave too little
+// work per output cell to split it over thread groups as ap_nhwc does.
+template <class T, int VEC, int K>
+__global__ __launch_bounds__(kNT) void ap_nhwc_cell(const void* __restrict__ x, void* __restrict__ y, int64_t total,
+                                                    int32_t CV, int32_t H, int32_t W, int32_t C, int32_t OH,
+                                                    int32_t OW) {
+    const int64_t idx = (int64_t)blockIdx.x * kNT + threadIdx.x;
+    if (idx >= total) return;
+    const int32_t cv = (int32_t)(idx % CV);
+    const int64_t cell = idx / CV;
+    const int32_t j = (int32_t)(cell % OW);
+    const int64_t t = cell / OW;
+    const int32_t i = (int32_t)(t % OH);
+    const int64_t n = t / OH;
+    const int h0 = (int)(((int64_t)i * H) / OH), h1 = (int)((((int64_t)i + 1) * H + OH - 1) / OH);
+    const int w0 = (int)(((int64_t)j * W) / OW), w1 = (int)((((int64_t)j + 1) * W + OW - 1) / OW);
+    const int hh = h1 - h0, ww = w1 - w0;
+    const int64_t base = n * H * W * (int64_t)C + (int64_t)cv * VEC;
+    float v[K][K][VEC];
+#pragma unroll
+    for (int a = 0; a < K; ++a)
+#pragma unroll
+        for (int b = 0; b < K; ++b) {
+            const int r = h0 + (a < hh ? a : hh - 1), c = w0 + (b < ww ? b : ww - 1);
+            const int64_t e = base + ((int64_t)r * W + c) * C;
+            if constexpr (VEC > 1) load_vec<T>(x, e, v[a][b]);
+            else v[a][b][0] = load1<T>(x, e);
+        }
+    float acc[VEC];
+#pragma unroll
+    for (int k = 0; k < VEC; ++k) acc[k] = 0.f;
+#pragma unroll
+    for (int a = 0; a < K; ++a)
+#pragma unroll
+        for (int b = 0; b < K; ++b)
+            if (a < hh && b < ww) {
+#pragma unroll
+                for (int k = 0; k < VEC; ++k) acc[k] += v[a][b][k];
+            }
+    const float cnt = (float)(hh * ww);
+#pragma unroll
+    for (int k = 0; k < VEC; ++k) acc[k] = acc[k] / cnt;
+    const int64_t o = ((n * OH + i) * OW + j) * (int64_t)C + (int64_t)cv * VEC;
+    if constexpr (VEC > 1) store_vec<T, false>(y, o, acc);
+    else store1<T>(y, o, acc[0]);
+}
+
+// Largest window extent of an adaptive pooling of n positions into m.
+int64_t window_extent(int64_t n, int64_t m) {
+    int64_t e = 0;
+    for (int64_t k = 0; k < m; ++k) {
+        const int64_t d = ((k + 1) * n + m - 1) / m - (k * n) / m;
+        e = d > e ? d : e;
+    }
+    return e;
+}
+
 template <class T, int TPS>
 void launch_flat(const AvgPoolArgs& a, hipStream_t s, const char** variant, const char* name) {
     constexpr int P = kNT / TPS;
@@ -322,6 +387,39 @@ kf_status run(const AvgPoolArgs& a, hipStream_t s, const char** variant) {
             a.h > INT32_MAX || a.w > INT32_MAX || a.c > INT32_MAX) {
             set_error("adaptive_avgpool2d: channels-last problem exceeds the grid limits");
             return KF_ERR_UNSUPPORTED_LAYOUT;
+        }
+        // Windows of at most 4 x 4 pixels: a thread per output cell and
+        // channel vector ([32, 512, 14, 14] -> 7 x 7: 16.0 us with ap_nhwc's
+        // split windows, which suit large windows such as the 7 x 7 -> 1 x 1
+        // head).
+        const int64_t ext = (a.oh <= 4096 && a.ow <= 4096)
+                                ? std::max(window_extent(a.h, a.oh), window_extent(a.w, a.ow)) : 0;
+        const int kc = ext == 0 ? 0 : ext <= 2 ? 2 : ext <= 3 ? 3 : ext <= 4 ? 4 : 0;
+        const int64_t total = a.n * a.oh * a.ow * cvs;
+        if (kc > 0 && (total + kNT - 1) / kNT <= INT32_MAX) {
+            const unsigned blocks = (unsigned)((total + kNT - 1) / kNT);
+            auto go = [&](auto kernel) {
+                hipLaunchKernelGGL(kernel, dim3(blocks), dim3(kNT), 0, s, a.x, a.y, total, (int32_t)cvs,
+                                   (int32_t)a.h, (int32_t)a.w, (int32_t)a.c, (int32_t)a.oh, (int32_t)a.ow);
+            };
+            auto pick = [&](auto vec_tag) {
+                constexpr int V = decltype(vec_tag)::value;
+                if (kc == 2) go(ap_nhwc_cell<T, V, 2>);
+                else if (kc == 3) go(ap_nhwc_cell<T, V, 3>);
+                else go(ap_nhwc_cell<T, V, 4>);
+            };
+            if (vec) pick(std::integral_constant<int, T::vec>{});
+            else pick(std::integral_constant<int, 1>{});
+            static const char* names[2][5] = {
+                {"", "", "ap_nhwc_cell_scalar_k2", "ap_nhwc_cell_scalar_k3", "ap_nhwc_cell_scalar_k4"},
+                {"", "", "ap_nhwc_cell_vec_k2", "ap_nhwc_cell_vec_k3", "ap_nhwc_cell_vec_k4"}};
+            *variant = names[vec ? 1 : 0][kc];
+            const hipError_t err = hipGetLastError();
+            if (err != hipSuccess) {
+                set_error("adaptive_avgpool2d launch failed: %s", hipGetErrorString(err));
+                return KF_ERR_HIP;
+            }
+            return KF_OK;
         }
         const dim3 grid((unsigned)gx, (unsigned)gy, (unsigned)a.n);
         if (vec)
@@ -375,15 +473,7 @@ kf_status run(const AvgPoolArgs& a, hipStream_t s, const char** variant) {
         const bool vec = ((P * S) % vec_elems == 0) && ((uintptr_t)a.x % 16 == 0);
         const size_t lds = (size_t)(P * S) * sizeof(float) + (size_t)(a.oh + a.ow) * sizeof(uint32_t);
         // Largest window extent along either axis.
-        auto extent = [](int64_t n, int64_t m) {
-            int64_t e = 0;
-            for (int64_t k = 0; k < m; ++k) {
-                const int64_t d = ((k + 1) * n + m - 1) / m - (k * n) / m;
-                e = d > e ? d : e;
-            }
-            return e;
-        };
-        const int64_t ext = std::max(extent(a.h, a.oh), extent(a.w, a.ow));
+        const int64_t ext = std::max(window_extent(a.h, a.oh), window_extent(a.w, a.ow));
         const int kmax = ext <= 2 ? 2 : ext <= 3 ? 3 : ext <= 4 ? 4 : 0;
         auto go = [&](auto kernel) {
             hipLaunchKernelGGL(kernel, dim3((unsigned)blocks), dim3(kNT), lds, s, a.x, a.y, a.planes, (int32_t)P,

@@ -132,7 +132,26 @@ CHANNELS_LAST = [
     ((1, 24, 5, 9), (8, 4)),        # output taller than the input
     ((3, 5, 6, 6), 2),              # channels not whole 16-byte vectors: scalar path
     ((2, 200, 9, 11), (1, 3)),      # channels beyond one 64-vector block
+    ((4, 512, 14, 14), 7),          # 2 x 2 windows, many channel vectors
+    ((2, 256, 13, 13), 6),          # overlapping 3 x 3 windows
+    ((2, 64, 8, 8), 2),             # 4 x 4 windows
+    ((2, 64, 10, 10), 2),           # 5 x 5 windows: split over thread groups
 ]
+
+
+def window_extent(n, m):
+    """Largest adaptive window extent pooling n positions into m."""
+    return max(((k + 1) * n + m - 1) // m - (k * n) // m for k in range(m))
+
+
+def nhwc_variant(shape, out, dt):
+    oh, ow = (out, out) if isinstance(out, int) else out
+    vec = 4 if dt == "f32" else 8
+    kind = "vec" if shape[1] % vec == 0 else "scalar"
+    ext = max(window_extent(shape[2], oh), window_extent(shape[3], ow))
+    if ext <= 4:
+        return f"ap_nhwc_cell_{kind}_k{max(ext, 2)}"
+    return f"ap_nhwc_{kind}"
 
 
 @pytest.mark.parametrize("dt", ["f32", "bf16", "f16"])
@@ -142,8 +161,7 @@ def test_channels_last(shape, out, dt):
     x_cpu = relu_input(shape, dt, seed=shape[1])
     x = x_cpu.cuda().contiguous(memory_format=torch.channels_last)
     variant = run(x_cpu, out, dt, x_gpu=x)
-    vec = 4 if dt == "f32" else 8
-    assert variant == ("ap_nhwc_vec" if shape[1] % vec == 0 else "ap_nhwc_scalar"), variant
+    assert variant == nhwc_variant(shape, out, dt), variant
 
 
 def test_channels_last_output_keeps_the_layout():
