@@ -22,8 +22,10 @@ import subprocess
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-_SRC = os.path.join(_HERE, "oracle.c")
-_LIB = os.path.join(_HERE, "liboracle.so")
+# KF_ORACLE_SRC names another copy of oracle.c, built next to it: the pin
+# tests use it to check that a mistake planted in the oracle makes them fail.
+_SRC = os.environ.get("KF_ORACLE_SRC") or os.path.join(_HERE, "oracle.c")
+_LIB = os.path.join(os.path.dirname(os.path.abspath(_SRC)), "liboracle.so")
 
 # Stored significand bits and exponent bits of the narrow output formats.
 FORMATS = {"bf16": (7, 8), "f16": (10, 5)}
@@ -36,7 +38,7 @@ def compile_oracle(force: bool = False) -> str:
         tmp = _LIB + ".tmp%d" % os.getpid()
         subprocess.check_call([
             "gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-ffp-contract=off",
-            "-fno-fast-math", "-Wall", "-Wextra", "-o", tmp, _SRC, "-lm"])
+            "-fno-fast-math", "-Wall", "-Wextra", "-I", _HERE, "-o", tmp, _SRC, "-lm"])
         os.replace(tmp, _LIB)
     return _LIB
 
