@@ -183,6 +183,53 @@ def copy_calibration(torch, dev, nbytes: int, reps: int = 48, pairs: int = 3) ->
                          "frac_of_peak": round(nbytes / (own_us * 1e-6) / 1e9 / PEAK_HBM_GBS, 4)}}
 
 
+def floors_row(torch, dev, kf355, w, steps, sets_for):
+    """What this box does for the same bytes with no operator arithmetic and
+    no exchange: the library's plain read of the pooling input
+    (kf_stream_read, 16 bytes out per 4 KiB in) and its plain copy of the
+    GroupNorm and softmax inputs (kf_stream_copy), each over rotating buffers
+    like the operator, and a one-wave read (the cost of a launch by itself).
+    Floors and operators are both timed as replayed HIP graphs of
+    back-to-back calls, so host launch cost (comparable to these kernels)
+    is out of both."""
+    gn = w["group_norm"]
+    ap_x, gn_x, sm_x = w["avgpool"]["x"].to(dev), gn["x"].to(dev), w["softmax"]["x"].to(dev)
+    gw, gb = gn["weight"].to(dev), gn["bias"].to(dev)
+    st = torch.cuda.Stream()
+    st.wait_stream(torch.cuda.current_stream())
+    row = {"timing": "HIP graph of back-to-back calls, rotating buffer sets"}
+    with torch.cuda.stream(st):
+        def floor_fns(src_bytes, reader, n):
+            srcs = [torch.empty(src_bytes, dtype=torch.uint8, device=dev) for _ in range(n)]
+            if reader:
+                dsts = [torch.empty(-(-src_bytes // 4096) * 16, dtype=torch.uint8, device=dev) for _ in srcs]
+                return [lambda s=s, d=d: kf355.stream_read(s, d) for s, d in zip(srcs, dsts)]
+            dsts = [torch.empty_like(s) for s in srcs]
+            return [lambda s=s, d=d: kf355.stream_copy(s, d) for s, d in zip(srcs, dsts)]
+
+        row["launch_us"] = round(time_graph(torch, floor_fns(4096, True, 1), steps, st), 3)
+        row["launch_kind"] = "kf_stream_read of 4 KiB (one wave)"
+        cases = (
+            ("adaptive_avgpool2d", ap_x, True, "kf_stream_read of its input",
+             lambda x: kf355.prepare_adaptive_avgpool2d(x, torch.empty(x.shape[0], x.shape[1], 1, 1, device=dev))),
+            ("group_norm", gn_x, False, "kf_stream_copy of its input",
+             lambda x: kf355.prepare_group_norm(x, torch.empty_like(x), gn["num_groups"], gw, gb, gn["eps"])),
+            ("softmax", sm_x, False, "kf_stream_copy of its input",
+             lambda x: kf355.prepare_softmax(x, torch.empty_like(x), -1)))
+        for op, src, reader, kind, prep in cases:
+            nb = src.numel() * src.element_size()
+            n = sets_for(nb * (1 if reader else 2))
+            ops = [prep(src.clone()) for _ in range(n)]
+            op_us = time_graph(torch, ops, steps, st)
+            del ops
+            fl_us = time_graph(torch, floor_fns(nb, reader, n), steps, st)
+            torch.cuda.empty_cache()
+            row[op] = {"kind": kind, "bytes_moved": nb if reader else 2 * nb, "floor_us": round(fl_us, 3),
+                       "op_us": round(op_us, 3), "op_over_floor": round(op_us / fl_us, 3), "buffer_sets": n}
+    torch.cuda.synchronize()
+    return row
+
+
 def time_launches(torch, fns, steps, warmup):
     """Mean µs per call over `steps` back-to-back launches (cycling through
     fns), between two HIP events on the current stream."""
@@ -664,6 +711,7 @@ def main():
                                                           sets_for)
 
     calib = copy_calibration(torch, dev, nbytes["softmax"])
+    floors = floors_row(torch, dev, kf355, w, args.steps, sets_for)
     sm = per_op["softmax"]
     traffic = measured_traffic()
     roofline = {"bound": "hbm", "achieved": sm["gbps"], "peak": PEAK_HBM_GBS, "unit": "GB/s",
@@ -686,7 +734,7 @@ def main():
         "config": {"workload": WORKLOAD, "step_algorithmic_bytes": step_bytes},
         "per_op": per_op, "roofline": roofline, "cpu_baseline": base, "cpu_baseline_parallel": base_mt,
         "torch_eager": eager, "inputs_sha256": input_hashes,
-        "calibration": calib, "next_rows": next_rows,
+        "calibration": calib, "floors": floors, "next_rows": next_rows,
     }
     print(json.dumps(out), flush=True)
 

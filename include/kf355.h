@@ -290,6 +290,22 @@ kf_status kf_max_pool2d_output_size(int64_t h, int64_t w, const int64_t* window,
  */
 kf_status kf_stream_copy(const void* src, void* dst, int64_t bytes, void* stream);
 
+/*
+ * kf_stream_read -- measurement aid, not an operator: reads `bytes` from src
+ * with kf_stream_copy's load pattern and writes, for every 4 KiB block of src
+ * (the last one possibly shorter), the bitwise XOR of its 16-byte words: the
+ * HBM read alone, the floor of an operator that reads much and writes
+ * little (such as adaptive_avgpool2d to 1x1).
+ *
+ *  src     device pointer, 16-byte aligned; the caller owns it.
+ *  bytes   a multiple of 16 (0 is a no-op), else KF_ERR_BAD_SHAPE.
+ *  dst     device pointer, 16-byte aligned, ceil(bytes / 4096) * 16 bytes,
+ *          not overlapping src (else KF_ERR_BAD_ARG); word b is the XOR of
+ *          src's 16-byte words 256 * b .. 256 * b + 255.
+ *  Asynchronous on stream.
+ */
+kf_status kf_stream_read(const void* src, int64_t bytes, void* dst, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -455,6 +455,17 @@ kf_status kf_stream_copy(const void* src, void* dst, int64_t bytes, void* stream
     return done(stream_copy_launch(src, dst, bytes, static_cast<hipStream_t>(stream)), "stream_copy");
 }
 
+kf_status kf_stream_read(const void* src, int64_t bytes, void* dst, void* stream) {
+    begin();
+    if (bytes < 0 || bytes % 16) return fail(KF_ERR_BAD_SHAPE, "bytes must be a non-negative multiple of 16");
+    if (bytes == 0) return done(KF_OK, "noop");
+    if (!src || !dst) return fail(KF_ERR_NULL_POINTER, "src or dst is NULL");
+    if ((uintptr_t)src % 16 || (uintptr_t)dst % 16) return fail(KF_ERR_BAD_ARG, "src and dst must be 16-byte aligned");
+    const int64_t out_bytes = (bytes + 4095) / 4096 * 16;
+    if (overlaps(src, bytes, dst, out_bytes)) return fail(KF_ERR_BAD_ARG, "src and dst overlap");
+    return done(stream_read_launch(src, bytes, dst, static_cast<hipStream_t>(stream)), "stream_read");
+}
+
 kf_status kf_max_pool2d(const void* x, kf_dtype dtype, void* y, int64_t* indices, int32_t ndim, const int64_t* shape,
                         const int64_t* x_strides, const int64_t* y_strides, const int64_t* window, int32_t ceil_mode,
                         void* stream) {

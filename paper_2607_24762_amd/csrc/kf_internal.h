@@ -97,6 +97,7 @@ kf_status max_pool2d_launch(const MaxPoolArgs& a, hipStream_t s, const char** va
 // Calibration copy of `bytes` (a multiple of 16) between 16-byte aligned,
 // non-overlapping device buffers.
 kf_status stream_copy_launch(const void* src, void* dst, int64_t bytes, hipStream_t s);
+kf_status stream_read_launch(const void* src, int64_t bytes, void* dst, hipStream_t s);
 
 // Records the detail text of the current failure (thread-local).
 void set_error(const char* fmt, ...);

@@ -55,6 +55,7 @@ _SIGNATURES = {
     "kf_adaptive_avgpool2d": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p, ctypes.c_int32, _i64p,
                                              _i64p, _i64p, ctypes.c_int64, ctypes.c_int64, ctypes.c_void_p]),
     "kf_stream_copy": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p]),
+    "kf_stream_read": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p]),
 }
 
 _lib = None
@@ -406,6 +407,20 @@ def stream_copy(src: torch.Tensor, dst: torch.Tensor) -> torch.Tensor:
         raise KfError(2, "stream_copy needs contiguous tensors of equal byte size")
     with _on(src):
         _check(lib().kf_stream_copy(src.data_ptr(), dst.data_ptr(), nbytes, _stream(src)))
+    return dst
+
+
+def stream_read(src: torch.Tensor, dst: torch.Tensor) -> torch.Tensor:
+    """Calibration read through kf_stream_read (a measurement aid, no
+    operator): dst receives the XOR of every 4 KiB block of the contiguous
+    GPU tensor src, one 16-byte word per block."""
+    _need_cuda(src, dst)
+    nbytes = src.numel() * src.element_size()
+    need = -(-nbytes // 4096) * 16
+    if not (src.is_contiguous() and dst.is_contiguous()) or dst.numel() * dst.element_size() < need:
+        raise KfError(2, f"stream_read needs contiguous tensors and {need} bytes of output")
+    with _on(src):
+        _check(lib().kf_stream_read(src.data_ptr(), nbytes, dst.data_ptr(), _stream(src)))
     return dst
 
 

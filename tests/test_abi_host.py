@@ -310,3 +310,15 @@ def test_stream_copy_rejections(lib):
     assert lib.kf_stream_copy(None, FAKE, 64, None) == NULLP
     assert lib.kf_stream_copy(FAKE + 4, FAKE + (1 << 30), 64, None) == ARG    # misaligned
     assert lib.kf_stream_copy(FAKE, FAKE + 32, 64, None) == ARG               # overlap
+
+
+def test_stream_read_rejections(lib):
+    # The calibration read checks its arguments on the host like the operators.
+    assert lib.kf_stream_read(FAKE, 0, FAKE + (1 << 30), None) == OK          # no-op
+    assert lib.kf_stream_read(FAKE, 24, FAKE + (1 << 30), None) == SHAPE      # not a multiple of 16
+    assert lib.kf_stream_read(FAKE, -16, FAKE + (1 << 30), None) == SHAPE
+    assert lib.kf_stream_read(None, 64, FAKE, None) == NULLP
+    assert lib.kf_stream_read(FAKE, 64, None, None) == NULLP
+    assert lib.kf_stream_read(FAKE, 64, FAKE + (1 << 30) + 8, None) == ARG    # misaligned
+    assert lib.kf_stream_read(FAKE, 8192, FAKE + 4096, None) == ARG           # output inside the input
+    assert lib.kf_stream_read(FAKE, 4096, FAKE + 4080, None) == ARG           # output (16 B) on the last input word
