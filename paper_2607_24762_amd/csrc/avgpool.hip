@@ -43,8 +43,9 @@ constexpr int slots() {
 
 // Stage elements [base, base + span) of x in LDS as fp32 (span <= kSpanMax).
 // Every load is issued before the first LDS store, so a thread has all its
-// requests in flight at once; only the last workgroup can have a remainder
-// that is not whole vectors (VECTOR needs x + base 16-byte aligned).  A lane
+// requests in flight at once (non-temporal: the span is read once); only
+// the last workgroup can have a remainder that is not whole vectors (VECTOR
+// needs x + base 16-byte aligned).  A lane
 // writes its four fp32 values with one 16-byte LDS store: as 4-byte stores,
 // lanes 16 apart would hit the same bank.  Ends with a barrier.
 template <class T, bool VECTOR>
@@ -58,7 +59,7 @@ __device__ __forceinline__ void stage_span(const void* __restrict__ x, int64_t b
     for (int k = 0; k < NV; ++k) {
         const int32_t e = (k * kNT + (int)threadIdx.x) * VEC;
         if (e < whole) {
-            if constexpr (VECTOR) load_vec<T>(x, base + e, v[k]);
+            if constexpr (VECTOR) load_vec<T, true>(x, base + e, v[k]);
             else v[k][0] = load1<T>(x, base + e);
         }
     }

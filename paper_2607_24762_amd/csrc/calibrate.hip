@@ -3,9 +3,10 @@
 // for a copy, the figure the operators' achieved bandwidth is read against.
 //
 //   stream_copy  each wave copies 64 * kCopyVecs consecutive 16-byte vectors
-//                (4 KiB): all loads issued, then non-temporal stores, the
-//                pattern that measured fastest among grid-strided and
-//                wave-contiguous copies with 1-16 vectors per lane.
+//                (4 KiB): all non-temporal loads issued, then non-temporal
+//                stores, the pattern that measured fastest among grid-strided
+//                and wave-contiguous copies with 1-16 vectors per lane and
+//                among the cache-policy bits of loads and stores.
 //   stream_read  the same loads; each wave writes only the XOR of its 4 KiB
 //                (one 16-byte word), so the bytes moved are the read: the
 //                floor of an operator that reads much and writes little.
@@ -29,7 +30,7 @@ __global__ __launch_bounds__(kCopyNT) void stream_copy(const u32x4* __restrict__
 #pragma unroll
     for (int k = 0; k < kCopyVecs; ++k) {
         const int64_t i = base + k * kWave + lane;
-        v[k] = x[i < n16 ? i : 0];
+        v[k] = __builtin_nontemporal_load(x + (i < n16 ? i : 0));
     }
 #pragma unroll
     for (int k = 0; k < kCopyVecs; ++k) {
@@ -47,7 +48,7 @@ __global__ __launch_bounds__(kCopyNT) void stream_read(const u32x4* __restrict__
 #pragma unroll
     for (int k = 0; k < kCopyVecs; ++k) {
         const int64_t i = base + k * kWave + lane;
-        v[k] = x[i < n16 ? i : 0];
+        v[k] = __builtin_nontemporal_load(x + (i < n16 ? i : 0));
     }
     u32x4 acc = {0u, 0u, 0u, 0u};
 #pragma unroll

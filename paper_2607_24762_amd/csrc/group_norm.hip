@@ -111,13 +111,15 @@ struct Chunk {
     }
     // All slots load unconditionally so the loads issue back to back; a slot
     // past the group's end re-reads the group's first element and is never
-    // used afterwards.
+    // used afterwards.  NT: non-temporal loads, for the read that is the
+    // chunk's last.
+    template <bool NT = false>
     __device__ __forceinline__ void load(const GNParams& p, int64_t ng, int part) {
 #pragma unroll
         for (int k = 0; k < NV; ++k) {
             const int64_t o = off(part, k);
             const int64_t e = at(p, ng, o < p.group_elems ? o : 0);
-            if constexpr (VECTOR) load_vec<T>(p.x, e, v[k]);
+            if constexpr (VECTOR) load_vec<T, NT>(p.x, e, v[k]);
             else v[k][0] = load1<T>(p.x, e);
         }
     }
@@ -324,7 +326,10 @@ __global__ __launch_bounds__(kNT) void gn_fused(GNParams p) {
     const int g = (int)(ng % p.groups);
 
     C c;
-    c.load(p, ng, part);
+    // Non-temporal for NCHW, where each chunk is read once; channels last
+    // keeps the lines in L2, where the workgroups of the neighbouring groups
+    // that share them read them too.
+    c.template load<!NHWC>(p, ng, part);
     c.template load_affine<A>(p, part, g);
     const Moments m = moments_block<kNT / kWave>(c.moments(p, part), lds);
     if (p.ex.parts > 1 && threadIdx.x == 0) ex_publish(p.ex, ng, part, encode(m));

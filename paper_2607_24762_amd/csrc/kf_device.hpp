@@ -51,27 +51,28 @@ __device__ __forceinline__ uint32_t pack2(F16, float a, float b) {
     return __builtin_bit_cast(uint32_t, v);
 }
 
+// One 16-byte load.  With NT the load is non-temporal (the line is not kept
+// for reuse), which is what an input read exactly once wants: measured on
+// MI355X, a 256 MiB copy takes 84.9 us with non-temporal loads and stores
+// against 87.4 us with non-temporal stores alone.
+template <bool NT>
+__device__ __forceinline__ u32x4 load16(const void* p) {
+    if constexpr (NT) return __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+    else return *reinterpret_cast<const u32x4*>(p);
+}
+
 // 16-byte vector load of T::vec elements at element offset `e` (e must be a
-// multiple of T::vec and the address 16-byte aligned).
-template <class T>
-__device__ __forceinline__ void load_vec(const void* base, int64_t e, float* out);
-template <>
-__device__ __forceinline__ void load_vec<F32>(const void* base, int64_t e, float* out) {
-    u32x4 v = *reinterpret_cast<const u32x4*>(static_cast<const float*>(base) + e);
+// multiple of T::vec and the address 16-byte aligned), widened to float.
+template <class T, bool NT = false>
+__device__ __forceinline__ void load_vec(const void* base, int64_t e, float* out) {
+    const u32x4 v = load16<NT>(static_cast<const char*>(base) + e * T::bytes);
+    if constexpr (T::vec == 4) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) out[i] = __uint_as_float(v[i]);
-}
-template <>
-__device__ __forceinline__ void load_vec<BF16>(const void* base, int64_t e, float* out) {
-    u32x4 v = *reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(base) + e);
+        for (int i = 0; i < 4; ++i) out[i] = __uint_as_float(v[i]);
+    } else {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) unpack2(BF16{}, v[i], out[2 * i], out[2 * i + 1]);
-}
-template <>
-__device__ __forceinline__ void load_vec<F16>(const void* base, int64_t e, float* out) {
-    u32x4 v = *reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(base) + e);
-#pragma unroll
-    for (int i = 0; i < 4; ++i) unpack2(F16{}, v[i], out[2 * i], out[2 * i + 1]);
+        for (int i = 0; i < 4; ++i) unpack2(T{}, v[i], out[2 * i], out[2 * i + 1]);
+    }
 }
 
 // 16-byte vector store of T::vec elements, rounded to nearest-even.  With

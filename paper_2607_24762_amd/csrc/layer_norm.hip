@@ -139,7 +139,7 @@ __global__ __launch_bounds__(256) void ln_wave(LNArgsDev p) {
         e0[k] = (lr + k * LPR) * VEC;
         ok[k] = row_ok && e0[k] < p.d;
         const int64_t at = base + (ok[k] ? e0[k] : 0);
-        if constexpr (VECTOR) load_vec<T>(p.x, at, v[k]);
+        if constexpr (VECTOR) load_vec<T, true>(p.x, at, v[k]);
         else v[k][0] = load1<T>(p.x, at);
     }
     const Moments m = moments_group<LPR>(slot_moments<NV, VEC>(v, ok));
@@ -164,7 +164,7 @@ __global__ __launch_bounds__(NT) void ln_block(LNArgsDev p) {
         e0[k] = (seg + k * kWave) * VEC;
         ok[k] = e0[k] < p.d;
         const int64_t at = base + (ok[k] ? e0[k] : 0);
-        if constexpr (VECTOR) load_vec<T>(p.x, at, v[k]);
+        if constexpr (VECTOR) load_vec<T, true>(p.x, at, v[k]);
         else v[k][0] = load1<T>(p.x, at);
     }
     const Moments m = moments_block<NW>(slot_moments<NV, VEC>(v, ok), lds);

@@ -109,7 +109,7 @@ __global__ __launch_bounds__(256) void sm_wave(const void* __restrict__ x, void*
     for (int k = 0; k < NV; ++k) {
         const int e0 = (lr + k * LPR) * VEC;
         const int64_t at = (row_ok && e0 < len) ? base + e0 : 0;
-        if constexpr (VECTOR) load_vec<TI>(x, at, v[k]);
+        if constexpr (VECTOR) load_vec<TI, true>(x, at, v[k]);
         else v[k][0] = load1<TI>(x, at);
     }
     if (!__all(full)) mask_slots<NV, VEC, LPR>(v, lr, row_ok, len);
@@ -178,7 +178,7 @@ __global__ __launch_bounds__(NT) void sm_block(const void* __restrict__ x, void*
     for (int k = 0; k < NV; ++k) {
         const int e0 = (seg + k * kWave) * VEC;
         const int64_t at = base + (e0 < len ? e0 : 0);
-        if constexpr (VECTOR) load_vec<TI>(x, at, v[k]);
+        if constexpr (VECTOR) load_vec<TI, true>(x, at, v[k]);
         else v[k][0] = load1<TI>(x, at);
     }
     if (NT * NV * VEC != len) mask_slots<NV, VEC, kWave>(v, seg, true, len);
@@ -242,7 +242,7 @@ __device__ __forceinline__ void edge_load(const void* x, int64_t a0, int s0, int
     for (int k = 0; k < NV; ++k) {
         const int32_t e = (s0 + k * STRIDE) * VEC;
         const bool use = row_ok && e < hi && e <= room - VEC;
-        load_vec<TI>(xa, use ? e : 0, v[k]);
+        load_vec<TI>(xa, use ? e : 0, v[k]);  // not non-temporal: neighbouring rows share the end vectors
     }
 #pragma unroll
     for (int k = 0; k < NV; ++k) {
@@ -388,7 +388,7 @@ __global__ __launch_bounds__(256) void sm_span(const void* __restrict__ x, void*
 #pragma unroll
     for (int k = 0; k < NL; ++k) {
         const int32_t e = (k * 256 + (int)threadIdx.x) * VI;
-        if (e < whole_in) load_vec<TI>(x, base + e, v[k]);
+        if (e < whole_in) load_vec<TI, true>(x, base + e, v[k]);
     }
 #pragma unroll
     for (int k = 0; k < NL; ++k) {
@@ -474,7 +474,7 @@ __global__ __launch_bounds__(NT) void sm_causal(const void* __restrict__ x, void
         for (int kk = 0; kk < NV; ++kk) {
             const int e0 = (seg + kk * kWave) * VEC;
             const int64_t at = base + (e0 < live ? e0 : 0);
-            if constexpr (VECTOR) load_vec<TI>(x, at, v[kk]);
+            if constexpr (VECTOR) load_vec<TI, true>(x, at, v[kk]);
             else v[kk][0] = load1<TI>(x, at);
         }
 #pragma unroll
@@ -751,7 +751,7 @@ struct SplitPart {
         for (int k = 0; k < NV; ++k) {
             const int64_t e = at(r0, part, k);
             const bool use = e < r1 && e + VEC > r0 && e + VEC <= p.total;
-            load_vec<TI>(p.x, use ? e : safe, v[k]);
+            load_vec<TI, true>(p.x, use ? e : safe, v[k]);
             edge = edge || e < r0 || e + VEC > r1;
         }
         if (__any(edge)) {
