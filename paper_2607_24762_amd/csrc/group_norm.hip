@@ -78,6 +78,32 @@ __device__ __forceinline__ void block_chunk(const GNParams& p, int64_t b, int64_
     }
 }
 
+// What an absent weight (element 0) or bias (element 1) reads, in each
+// affine storage type.  The affine loads read these instead of branching on
+// the pointers: inside a branch, the conversion of the loaded values made
+// the compiler wait for every outstanding load (the chunk's too) before the
+// branch could end, so each workgroup paid an extra load round trip before
+// it could publish its moments.  Plain (not const) device globals, so the
+// pointer chosen between them and a kernel argument stays in the global
+// address space and the loads remain global loads.  Never written.
+__device__ float kIdentityF32[2] = {1.f, 0.f};
+__device__ uint16_t kIdentityBF16[2] = {0x3F80u, 0u};
+__device__ uint16_t kIdentityF16[2] = {0x3C00u, 0u};
+template <class A>
+__device__ __forceinline__ const void* affine_identity();
+template <>
+__device__ __forceinline__ const void* affine_identity<F32>() {
+    return kIdentityF32;
+}
+template <>
+__device__ __forceinline__ const void* affine_identity<BF16>() {
+    return kIdentityBF16;
+}
+template <>
+__device__ __forceinline__ const void* affine_identity<F16>() {
+    return kIdentityF16;
+}
+
 // Elements held by part p of a group.
 __device__ __forceinline__ float part_count(const GNParams& p, int64_t chunk, int part) {
     const int64_t left = p.group_elems - (int64_t)part * chunk;
@@ -179,19 +205,15 @@ struct Chunk {
             else
                 c[k] = (int64_t)g * p.cpg + (int64_t)(oc / (uint32_t)p.spatial);
         }
-        if (p.w) {
+        // No branch: nothing here waits, so the loads stay in flight until
+        // normalise_store uses them.
+        const bool hw = p.w != nullptr, hb = p.b != nullptr;
+        const void* ws = hw ? p.w : affine_identity<A>();
+        const void* bs = hb ? p.b : affine_identity<A>();
 #pragma unroll
-            for (int k = 0; k < NV; ++k) wv[k] = load1<A>(p.w, c[k]);
-        } else {
-#pragma unroll
-            for (int k = 0; k < NV; ++k) wv[k] = 1.f;
-        }
-        if (p.b) {
-#pragma unroll
-            for (int k = 0; k < NV; ++k) bv[k] = load1<A>(p.b, c[k]);
-        } else {
-#pragma unroll
-            for (int k = 0; k < NV; ++k) bv[k] = 0.f;
+        for (int k = 0; k < NV; ++k) {
+            wv[k] = load1<A>(ws, hw ? c[k] : 0);
+            bv[k] = load1<A>(bs, hb ? c[k] : 1);
         }
     }
     // y = (x - mean) * (rstd * w[c]) + b[c], non-temporal stores.
