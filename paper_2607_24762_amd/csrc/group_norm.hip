@@ -457,6 +457,16 @@ uint32_t gn_wait_ticks() {
     return ticks;
 }
 
+// The exchange of a launch with `parts` parts per group.  Whatever its slots
+// need, every path keeps the error word where callers find it: at the start
+// of the last 256 bytes of the size kf_group_norm_workspace_bytes reports
+// (the largest any path needs, so the word never overlaps slots or counters).
+Exchange gn_exchange(const GroupNormArgs& a, int64_t parts) {
+    ExchangeLayout l = exchange_layout(a.n * a.groups, parts);
+    l.error_off = group_norm_workspace_bytes(a.n, a.c, a.spatial, a.groups, a.xt) - 256;
+    return exchange_view(a.workspace, l, parts, gn_wait_ticks());
+}
+
 template <class T, class A, bool VECTOR, bool NHWC>
 kf_status run(const GroupNormArgs& a, hipStream_t s, const char** variant) {
     const Layout l = layout(a.n, a.c, a.spatial, a.groups, a.xt, VECTOR);
@@ -465,7 +475,7 @@ kf_status run(const GroupNormArgs& a, hipStream_t s, const char** variant) {
     p.y = a.y;
     p.w = a.weight;
     p.b = a.bias;
-    p.ex = exchange_view(a.workspace, l.ex, l.parts, gn_wait_ticks());
+    p.ex = gn_exchange(a, l.parts);
     p.group_elems = (a.c / a.groups) * a.spatial;
     p.spatial = a.spatial;
     p.channels = a.c;

@@ -224,6 +224,10 @@ def test_group_norm_zero_elements_and_workspace_query(lib):
     # 32 groups x 16 chunks of 16384 elements: 8-byte (mean, M2) partials,
     # then one 256-byte counter line per group, then the 256-byte error block.
     assert st == OK and n == 32 * 16 * 8 + 32 * 256 + 256
+    # 12-channel groups: 3 chunks of 16384 elements per group, partials
+    # padded to 256 bytes.
+    st, n = gn_ws(lib, (1, 24, 64, 64), 2)
+    assert st == OK and n == 256 + 2 * 256 + 256
     st, _ = gn_ws(lib, (1, 6, 4), 4)
     assert st == ARG
     assert lib.kf_group_norm_workspace_bytes(F32, 2, arr((2, 4)), 2, None) == NULLP

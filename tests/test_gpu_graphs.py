@@ -25,8 +25,8 @@ def gpu():
     kf355.lib()
 
 
-NAMES = ["softmax", "softmax_causal", "softmax_split", "group_norm", "layer_norm", "adaptive_avgpool2d",
-         "max_pool2d"]
+NAMES = ["softmax", "softmax_causal", "softmax_split", "group_norm", "group_norm_nhwc", "layer_norm",
+         "adaptive_avgpool2d", "max_pool2d"]
 
 
 def case(name):
@@ -48,7 +48,7 @@ def case(name):
         return ((1, 8, 1, 32768), "bf16",
                 lambda x, y, ws: kf355.kf_softmax_split(x, -1, out_dtype=torch.float32, out=y, workspace=ws),
                 lambda x: torch.empty(x.shape, dtype=torch.float32, device="cuda"), ws_split)
-    if name == "group_norm":
+    if name in ("group_norm", "group_norm_nhwc"):      # the nhwc input is made channels last below
         w = torch.full((512,), 1.25, device="cuda", dtype=torch.bfloat16)
         b = torch.full((512,), -0.5, device="cuda", dtype=torch.bfloat16)
         return ((1, 512, 128, 128), "bf16",
@@ -69,6 +69,8 @@ def test_capture_and_replay(name):
     shape, dt, call, make_out, make_ws = case(name)
     note(f"graph {name} {shape} {dt}")
     x = randn_device(shape, dt, seed=41)
+    if name.endswith("_nhwc"):
+        x = x.contiguous(memory_format=torch.channels_last)
     y = make_out(x)
     ws = make_ws(x) if make_ws else None
     call(x, y, ws)                                   # warm up outside the capture
@@ -84,11 +86,12 @@ def test_capture_and_replay(name):
         torch.cuda.synchronize()
         g.replay()
         torch.cuda.synchronize()
-        got = y.clone()
+        got = y.contiguous().clone()                 # dense copy: byte views need a unit last stride
         call(x, ref_out, ws)                         # the same call outside the graph
         torch.cuda.synchronize()
+        ref = ref_out.contiguous()
         assert torch.equal(got.view(torch.uint8) if got.dtype != torch.float32 else got.view(torch.int32),
-                           ref_out.view(torch.uint8) if ref_out.dtype != torch.float32 else ref_out.view(torch.int32)), \
+                           ref.view(torch.uint8) if ref.dtype != torch.float32 else ref.view(torch.int32)), \
             (name, i)
         if ws is not None:
             assert int(ws.count_nonzero().item()) == 0, (name, i)

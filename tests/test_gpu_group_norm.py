@@ -199,7 +199,10 @@ CHANNELS_LAST = [
     ((1, 24, 64, 64), 2),        # 12-channel groups: scalar layout, 3 chunks
     ((3, 256, 10, 5), 1),        # one group of every channel
     ((2, 32, 60, 50), 2),        # 16-channel groups, 3 chunks
+    ((2, 64, 48, 45), 8),        # 8-channel groups, 2 chunks per group, the last one ragged
+    ((2, 128, 36, 23), 4),       # 32-channel groups, 2 chunks per group, the last one ragged
 ]
+
 
 
 @pytest.mark.parametrize("dt", ["bf16", "f32", "f16"])
