@@ -89,6 +89,17 @@ def test_affine_variants(affine):
     run((2, 64, 32, 32), 16, "bf16", affine=affine)
 
 
+@pytest.mark.parametrize("dt", ["bf16", "f16", "f32"])
+@pytest.mark.parametrize("affine", ["same", "f32", "w", "b", "none"])
+def test_affine_variants_multi_chunk(affine, dt):
+    # 4 chunks per group: the fused kernel with the cross-workgroup exchange,
+    # where an absent weight or bias reads the identity element of the
+    # affine dtype instead of branching.
+    note(f"group_norm multi-chunk affine={affine} {dt}")
+    _, variant = run((1, 64, 64, 64), 4, dt, affine=affine)
+    assert variant == "gn_fused_vec", variant
+
+
 def test_two_kernel_path_for_grids_that_cannot_be_resident():
     # 8 samples x 32 groups x 16 chunks = 4096 workgroups.
     note("group_norm two-pass (8,128,256,256)")
