@@ -22,8 +22,14 @@ ARCH = "gfx950"
 
 # Packed-fp32 VALU ops are disabled for all device code (-packed-fp32-ops);
 # the host pass warns that it does not know the feature, which is harmless.
+# The atomic optimizer is off: every atomic here is issued by one lane (the
+# cross-workgroup exchange's departure count), and the optimizer's wave-wide
+# form broadcasts the returned value with readfirstlane, which makes the
+# wave wait for the atomic's round trip right away instead of after the
+# stores placed between the atomic and the use of its result.
 FLAGS = ["-std=c++17", "-O3", "-fPIC", f"--offload-arch={ARCH}",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+         "-mllvm", "-amdgpu-atomic-optimizer-strategy=None",
          "-Wall", "-Wno-unused-function", f"-I{INCLUDE}", f"-I{CSRC}"]
 
 
