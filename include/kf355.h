@@ -112,14 +112,16 @@ kf_status kf_softmax(const void* x, kf_dtype x_dtype, void* y, kf_dtype y_dtype,
  *  workspace, workspace_bytes
  *              device memory of at least kf_softmax_split_workspace_bytes()
  *              bytes, 256-byte aligned, owned by the caller, ZERO-FILLED before
- *              its first use; every call returns it to all-zero, so it can be
- *              reused by later calls in stream order.  Calls that may run
- *              concurrently need separate workspaces.  May be NULL when the
- *              required size is 0.  Too small: KF_ERR_WORKSPACE.  The last 256
- *              bytes of the required size start with a 32-bit word the kernel
- *              sets to 1 when a workgroup gave up waiting for the rest of its
- *              row and recomputed the row's state itself (results are the same
- *              either way; informational).
+ *              its first use.  Layout as for kf_group_norm: a 256-byte status
+ *              block at offset 0 whose first 32-bit word counts workgroups
+ *              that gave up waiting for the rest of their row and recomputed
+ *              the row's state themselves (results are the same either way;
+ *              informational, cumulative, reset only by the caller), then the
+ *              exchange, which every completed call returns to zero.  One
+ *              workspace may serve kf_softmax_split and kf_group_norm calls of
+ *              any shapes in stream order; calls that may run concurrently
+ *              need separate workspaces.  May be NULL when the required size is
+ *              0.  Too small: KF_ERR_WORKSPACE.
  */
 kf_status kf_softmax_split(const void* x, kf_dtype x_dtype, void* y, kf_dtype y_dtype, int32_t ndim,
                            const int64_t* shape, const int64_t* x_strides, const int64_t* y_strides, int64_t dim,
@@ -172,14 +174,19 @@ kf_status kf_softmax_causal(const void* x, kf_dtype x_dtype, void* y, kf_dtype y
  *  eps           >= 0 (used as fp32).
  *  workspace     device buffer of at least kf_group_norm_workspace_bytes()
  *                bytes, 256-byte aligned, ZERO-FILLED before its first use
- *                and left alone by the caller between calls: it carries the
- *                cross-workgroup exchange, which every completed call returns
- *                to zero.  Its last 256 bytes start with a 32-bit word that a
- *                call sets to 1 when a workgroup stopped waiting for the rest
- *                of its group (e.g. because other kernels held the compute
- *                units) and recomputed the group's statistics itself; the
- *                results are identical either way, the word is informational.
- *                Calls that may run concurrently must not share a workspace.
+ *                and otherwise left alone by the caller between calls.  Bytes
+ *                0-255 are a status block: its first 32-bit word counts the
+ *                workgroups that stopped waiting for the rest of their group
+ *                (e.g. because other kernels held the compute units) and
+ *                recomputed the group's statistics themselves; the results
+ *                are identical either way, so the count is informational.  It
+ *                is cumulative and sits at offset 0 for every shape and path;
+ *                the caller may read it or reset it to 0 between calls.  The
+ *                bytes after it carry the cross-workgroup exchange, which
+ *                every completed call returns to zero, so one workspace serves
+ *                later calls of any shape (kf_softmax_split's too) in stream
+ *                order.  Calls that may run concurrently must not share a
+ *                workspace.
  *  y may equal x (in place); any other overlap is KF_ERR_BAD_ARG.
  */
 kf_status kf_group_norm(const void* x, kf_dtype x_dtype, void* y, int32_t ndim, const int64_t* shape,

@@ -321,7 +321,7 @@ __device__ __forceinline__ void settle(const GNParams& p, C& c, int64_t ng, int 
             if (threadIdx.x == 0) {
                 stats[0] = acc.mean;
                 stats[1] = 1.f / sqrtf(acc.m2 / (float)p.group_elems + p.eps);
-                ex_flag_timeout(p.ex);
+                ex_count_give_up(p.ex);
             }
         }
         c.load(p, ng, part);
@@ -457,14 +457,10 @@ uint32_t gn_wait_ticks() {
     return ticks;
 }
 
-// The exchange of a launch with `parts` parts per group.  Whatever its slots
-// need, every path keeps the error word where callers find it: at the start
-// of the last 256 bytes of the size kf_group_norm_workspace_bytes reports
-// (the largest any path needs, so the word never overlaps slots or counters).
+// The exchange of a launch with `parts` parts per group (the give-up count
+// at offset 0 of the workspace on every path).
 Exchange gn_exchange(const GroupNormArgs& a, int64_t parts) {
-    ExchangeLayout l = exchange_layout(a.n * a.groups, parts);
-    l.error_off = group_norm_workspace_bytes(a.n, a.c, a.spatial, a.groups, a.xt) - 256;
-    return exchange_view(a.workspace, l, parts, gn_wait_ticks());
+    return exchange_view(a.workspace, exchange_layout(a.n * a.groups, parts), parts, gn_wait_ticks());
 }
 
 template <class T, class A, bool VECTOR, bool NHWC>

@@ -11,10 +11,14 @@
 // sees the data, so no fences and no cache write-back / invalidation are
 // needed; polls are relaxed agent-scope loads.  The last workgroup of a unit
 // to depart (a per-unit counter) clears the unit's slots and the counter, so
-// every launch leaves the workspace as it found it: all zero.  Waits are
-// bounded by the 100 MHz real-time clock; a workgroup that gives up must
-// recompute the missing partials itself (the kernels do, bit-identically)
-// and records that in the error word, which is informational only.
+// every launch leaves its slots and counters as it found them: all zero.
+// Waits are bounded by the 100 MHz real-time clock; a workgroup that gives up
+// must recompute the missing partials itself (the kernels do,
+// bit-identically) and adds one to the give-up count.  That count is the
+// first word of a 256-byte status block at offset 0 of every workspace,
+// whatever the shape, so a count left by one call can never be taken for a
+// published partial or a departure count by a later call of another shape
+// sharing the workspace; it is informational and only the caller resets it.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -28,7 +32,7 @@ constexpr size_t kCounterStride = 256;  // bytes between two units' counters
 struct Exchange {
     uint64_t* slot;       // [units * parts] published partials, 0 = empty
     unsigned* depart;     // one counter per unit, kCounterStride bytes apart
-    unsigned* error;      // set to 1 when a wait gave up
+    unsigned* give_ups;   // workgroups that stopped waiting (cumulative)
     int32_t parts;        // workgroups per unit
     uint32_t wait_ticks;  // give up waiting after this many 100 MHz ticks
 };
@@ -79,25 +83,27 @@ __device__ __forceinline__ void ex_leave(const Exchange& ex, int64_t unit, unsig
 
 __device__ __forceinline__ void ex_release(const Exchange& ex, int64_t unit) { ex_leave(ex, unit, ex_depart(ex, unit)); }
 
-__device__ __forceinline__ void ex_flag_timeout(const Exchange& ex) {
-    __hip_atomic_store(ex.error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+__device__ __forceinline__ void ex_count_give_up(const Exchange& ex) {
+    __hip_atomic_fetch_add(ex.give_ups, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // ---------------------------------------------------------------------------
-// Host side: workspace layout.  Slots first, then one 256-byte line per unit
-// for its counter (so different units never share a line), then a 256-byte
-// error block whose first word is the give-up flag.
+// Host side: workspace layout.  The 256-byte status block first (its first
+// 32-bit word the give-up count; the rest unused), then the slots, then one
+// 256-byte line per unit for its counter (so different units never share a
+// line).
+constexpr size_t kStatusBytes = 256;
+
 struct ExchangeLayout {
-    size_t slot_off, depart_off, error_off, total;
+    size_t slot_off, depart_off, total;
 };
 
 inline ExchangeLayout exchange_layout(int64_t units, int64_t parts) {
     auto up = [](size_t v) { return (v + 255) & ~(size_t)255; };
     ExchangeLayout l;
-    l.slot_off = 0;
-    l.depart_off = up((size_t)(units * parts) * sizeof(uint64_t));
-    l.error_off = l.depart_off + (size_t)units * kCounterStride;
-    l.total = l.error_off + 256;
+    l.slot_off = kStatusBytes;
+    l.depart_off = l.slot_off + up((size_t)(units * parts) * sizeof(uint64_t));
+    l.total = l.depart_off + (size_t)units * kCounterStride;
     return l;
 }
 
@@ -106,7 +112,7 @@ inline Exchange exchange_view(void* workspace, const ExchangeLayout& l, int64_t 
     Exchange ex;
     ex.slot = reinterpret_cast<uint64_t*>(ws + l.slot_off);
     ex.depart = reinterpret_cast<unsigned*>(ws + l.depart_off);
-    ex.error = reinterpret_cast<unsigned*>(ws + l.error_off);
+    ex.give_ups = reinterpret_cast<unsigned*>(ws);
     ex.parts = (int32_t)parts;
     ex.wait_ticks = wait_ticks;
     return ex;

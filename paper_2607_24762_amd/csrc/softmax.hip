@@ -864,7 +864,7 @@ __global__ __launch_bounds__(kSplitNT) void sm_split(SplitParams p) {
             if (threadIdx.x == 0) {
                 stat[0] = acc.m;
                 stat[1] = 1.f / acc.s;
-                ex_flag_timeout(p.ex);
+                ex_count_give_up(p.ex);
             }
         }
         c.load(p, r0, part);

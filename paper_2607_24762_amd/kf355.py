@@ -226,6 +226,21 @@ def _query_bytes(key, query) -> int:
     return n
 
 
+def workspace_give_ups(ws: torch.Tensor) -> int:
+    """The give-up count of an exchange workspace (kf_group_norm,
+    kf_softmax_split): the first 32-bit word of its status block, the number
+    of workgroups that stopped waiting for the rest of their group or row and
+    recomputed its statistics themselves since the count was last reset.
+    Reads the device word (synchronises with the workspace's device)."""
+    return int(ws[:4].cpu().view(torch.int32).item())
+
+
+def reset_workspace_give_ups(ws: torch.Tensor) -> None:
+    """Sets the give-up count of an exchange workspace back to 0 (on the
+    current stream, in order with the calls that use it)."""
+    ws[:4].zero_()
+
+
 def group_norm_workspace(x: torch.Tensor, num_groups: int) -> torch.Tensor:
     """The cached zero-filled workspace, large enough for kf_group_norm on x."""
     shape, _s = _arr(x.shape)

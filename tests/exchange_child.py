@@ -1,13 +1,14 @@
-"""Child process for the exchange-fallback tests: runs one workload of a
-kernel that exchanges partials between workgroups (GroupNorm's fused path,
-the split-row softmax) once, with the environment it was started with
-(KF355_GN_WAIT_TICKS=0 or KF355_SM_WAIT_TICKS=0 makes every waiting
-workgroup give up at once and recompute the partials itself), and saves the
-output bits, the workspace's give-up word and the count of other non-zero
-workspace bytes.
+"""Child process for the exchange-fallback tests: runs one or more workloads
+of the kernels that exchange partials between workgroups (GroupNorm's fused
+path, the split-row softmax) in order, on ONE shared zero-filled workspace,
+with the environment it was started with (KF355_GN_WAIT_TICKS=0 or
+KF355_SM_WAIT_TICKS=0 makes every waiting workgroup of that operator give up
+at once and recompute the partials itself), and saves each output's bits and
+variant, the workspace's give-up count (the first word of its status block)
+and the count of non-zero bytes after the status block.
 
-usage: exchange_child.py group_norm|group_norm_nhwc|softmax_split OUT.npz"""
-import ctypes
+usage: exchange_child.py OUT.npz OP [OP ...]
+OP: group_norm | group_norm_nhwc | group_norm_small | softmax_split"""
 import os
 import sys
 
@@ -18,31 +19,63 @@ sys.path.insert(0, os.path.dirname(os.path.dirname(os.path.abspath(__file__))))
 from paper_2607_24762_amd import kf355  # noqa: E402
 from paper_2607_24762_amd import workloads as W  # noqa: E402
 
-op, out_path = sys.argv[1], sys.argv[2]
-print(f"[child] op={op} KF355_GN_WAIT_TICKS={os.environ.get('KF355_GN_WAIT_TICKS')} "
-      f"KF355_SM_WAIT_TICKS={os.environ.get('KF355_SM_WAIT_TICKS')}", flush=True)
-ws = torch.zeros(1 << 20, dtype=torch.uint8, device="cuda")
-nb = ctypes.c_size_t(0)
-if op in ("group_norm", "group_norm_nhwc"):
-    w = W.groupnorm_vae_bf16()
-    x = w["x"].cuda()
+
+def inputs(op: str) -> dict:
+    """The inputs of each op, on the host (the parent draws the same ones)."""
+    if op in ("group_norm", "group_norm_nhwc"):
+        w = W.groupnorm_vae_bf16()
+        return {"x": w["x"], "groups": 32, "weight": w["weight"], "bias": w["bias"], "eps": w["eps"]}
+    if op == "group_norm_small":
+        # 24 channels per group over 32 x 32: two parts per group, eight groups.
+        return {"x": W.randn((2, 96, 32, 32), "bf16", seed=31, mean=-0.2, std=2.0), "groups": 4,
+                "weight": W.randn((96,), "bf16", seed=32, mean=1.0, std=0.1),
+                "bias": W.randn((96,), "bf16", seed=33, std=0.1), "eps": 1e-5}
+    if op == "softmax_split":
+        return {"x": W.attn_decode_bf16()["x"]}
+    raise SystemExit(f"unknown op {op}")
+
+
+def run(op: str, ws: torch.Tensor) -> torch.Tensor:
+    a = inputs(op)
+    x = a["x"].cuda()
+    if op == "softmax_split":
+        return kf355.kf_softmax_split(x, -1, out_dtype=torch.float32, workspace=ws)
     if op == "group_norm_nhwc":
         x = x.contiguous(memory_format=torch.channels_last)
-    y = kf355.kf_group_norm(x, 32, w["weight"].cuda(), w["bias"].cuda(), w["eps"], workspace=ws)
-    shape = (ctypes.c_int64 * 4)(1, 512, 128, 128)
-    kf355.lib().kf_group_norm_workspace_bytes(1, 4, shape, 32, ctypes.byref(nb))
-elif op == "softmax_split":
-    w = W.attn_decode_bf16()
-    x = w["x"].cuda()
-    y = kf355.kf_softmax_split(x, -1, out_dtype=torch.float32, workspace=ws)
-    shape = (ctypes.c_int64 * 4)(*x.shape)
-    kf355.lib().kf_softmax_split_workspace_bytes(1, 0, 4, shape, -1, ctypes.byref(nb))
-else:
-    raise SystemExit(f"unknown op {op}")
-torch.cuda.synchronize()
-variant = kf355.last_variant()
-flag = int(ws[nb.value - 256:nb.value - 252].cpu().view(torch.int32).item())
-rest = int(ws[: nb.value - 256].count_nonzero().item())
-bits = y.contiguous().view(torch.int16 if y.element_size() == 2 else torch.int32).cpu().numpy()
-np.savez(out_path, bits=bits, flag=flag, rest=rest, variant=variant)
-print(f"[child] variant={variant} flag={flag} nonzero_before_flag={rest}", flush=True)
+    return kf355.kf_group_norm(x, a["groups"], a["weight"].cuda(), a["bias"].cuda(), a["eps"], workspace=ws)
+
+
+def spawn(tmp_path, ops, **env) -> dict:
+    """Runs this file in a child process with `env` added to the environment
+    (the wait bounds are read once per process) and returns what it saved."""
+    import subprocess
+    out = str(tmp_path / ("child_" + "_".join(ops) + ".npz"))
+    r = subprocess.run([sys.executable, "-u", os.path.abspath(__file__), out, *ops],
+                       env=dict(os.environ, **env), timeout=300, capture_output=True, text=True)
+    print(r.stdout, r.stderr[-2000:])
+    assert r.returncode == 0, r.returncode
+    got = np.load(out)
+    return {k: got[k] for k in got.files}
+
+
+def main():
+    out_path, ops = sys.argv[1], sys.argv[2:]
+    print(f"[child] ops={ops} KF355_GN_WAIT_TICKS={os.environ.get('KF355_GN_WAIT_TICKS')} "
+          f"KF355_SM_WAIT_TICKS={os.environ.get('KF355_SM_WAIT_TICKS')}", flush=True)
+    ws = torch.zeros(1 << 20, dtype=torch.uint8, device="cuda")
+    saved = {}
+    for i, op in enumerate(ops):
+        y = run(op, ws)
+        torch.cuda.synchronize()
+        saved[f"variant{i}"] = kf355.last_variant()
+        y = y.contiguous()
+        saved[f"bits{i}"] = y.view(torch.int16 if y.element_size() == 2 else torch.int32).cpu().numpy()
+        print(f"[child] {op}: variant={saved[f'variant{i}']} give_ups={kf355.workspace_give_ups(ws)}", flush=True)
+    saved["give_ups"] = kf355.workspace_give_ups(ws)
+    saved["rest"] = int(ws[256:].count_nonzero().item())
+    np.savez(out_path, **saved)
+    print(f"[child] give_ups={saved['give_ups']} nonzero_after_status={saved['rest']}", flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -126,18 +126,18 @@ def test_softmax_split_rejections(lib):
 
 def test_softmax_split_workspace_query(lib):
     # 8 rows of 32768 bf16 -> fp32 (192 KiB of traffic each): the smallest
-    # parts that leave at most 16 per row, 16 parts of 2048 elements; 8-byte
-    # (m, s) partials (1024 bytes, a whole number of 256-byte lines), one
-    # 256-byte counter line per row, the 256-byte error block.
-    assert split_ws(lib, (1, 8, 1, 32768)) == (OK, 1024 + 8 * 256 + 256)
+    # parts that leave at most 16 per row, 16 parts of 2048 elements: the
+    # 256-byte status block, 8-byte (m, s) partials (1024 bytes, a whole
+    # number of 256-byte lines), one 256-byte counter line per row.
+    assert split_ws(lib, (1, 8, 1, 32768)) == (OK, 256 + 1024 + 8 * 256)
     # The same rows with bf16 output move 128 KiB each: not split.
     assert split_ws(lib, (1, 8, 1, 32768), yt=BF16) == (OK, 0)
     # A row that does not start on a 16-byte boundary spans one more vector:
     # 40001 elements take 10 parts of 4096.
-    assert split_ws(lib, (3, 40001)) == (OK, 256 + 3 * 256 + 256)
+    assert split_ws(lib, (3, 40001)) == (OK, 256 + 256 + 3 * 256)
     # Rows of partial vectors beyond 16384 elements are split at any size
     # (the per-row path would stream them twice): 16385 -> 9 parts of 2048.
-    assert split_ws(lib, (2, 16385), yt=BF16) == (OK, 256 + 2 * 256 + 256)
+    assert split_ws(lib, (2, 16385), yt=BF16) == (OK, 256 + 256 + 2 * 256)
     assert split_ws(lib, (2, 16384), yt=BF16) == (OK, 0)
     # 127 rows of 70000: 9 parts of 8192 (the first size with at most 16 per
     # row) would make 1143 workgroups, so parts of 16384 (5 per row).
@@ -221,13 +221,13 @@ def test_group_norm_zero_elements_and_workspace_query(lib):
     st, n = gn_ws(lib, (0, 8, 4), 2)
     assert st == OK and n == 0
     st, n = gn_ws(lib, (1, 512, 128, 128), 32)
-    # 32 groups x 16 chunks of 16384 elements: 8-byte (mean, M2) partials,
-    # then one 256-byte counter line per group, then the 256-byte error block.
-    assert st == OK and n == 32 * 16 * 8 + 32 * 256 + 256
+    # 32 groups x 16 chunks of 16384 elements: the 256-byte status block,
+    # 8-byte (mean, M2) partials, then one 256-byte counter line per group.
+    assert st == OK and n == 256 + 32 * 16 * 8 + 32 * 256
     # 12-channel groups: 3 chunks of 16384 elements per group, partials
     # padded to 256 bytes.
     st, n = gn_ws(lib, (1, 24, 64, 64), 2)
-    assert st == OK and n == 256 + 2 * 256 + 256
+    assert st == OK and n == 256 + 256 + 2 * 256
     st, _ = gn_ws(lib, (1, 6, 4), 4)
     assert st == ARG
     assert lib.kf_group_norm_workspace_bytes(F32, 2, arr((2, 4)), 2, None) == NULLP

@@ -15,6 +15,7 @@ import pytest
 import torch
 
 from compare import assert_close, note
+from exchange_child import inputs, spawn
 from oracle import oracle
 from paper_2607_24762_amd import kf355
 from paper_2607_24762_amd import workloads as W
@@ -101,10 +102,14 @@ def test_affine_variants_multi_chunk(affine, dt):
 
 
 def test_two_kernel_path_for_grids_that_cannot_be_resident():
-    # 8 samples x 32 groups x 16 chunks = 4096 workgroups.
+    # 8 samples x 32 groups x 16 chunks = 4096 workgroups of 4 waves: a CU
+    # holds at most 32 waves, so no device of 256 CUs can hold more than 2048
+    # of them at once, and the fused kernel's own register use allows fewer.
     note("group_norm two-pass (8,128,256,256)")
+    props = torch.cuda.get_device_properties(0)
+    assert 4096 > props.multi_processor_count * 32 // 4
     _, variant = run((8, 128, 256, 256), 32, "bf16", seed=4)
-    assert variant.startswith("gn_two_pass") or variant.startswith("gn_fused"), variant
+    assert variant == "gn_two_pass_vec", variant
 
 
 def test_in_place():
@@ -149,26 +154,48 @@ def test_wait_timeout_recompute_is_bitwise_identical(tmp_path):
     # A child process with KF355_GN_WAIT_TICKS=0 makes every workgroup that
     # does not find its whole group published on the first poll recompute the
     # group's statistics itself; the output must equal the normal path's bit
-    # for bit, the give-up word must be set and everything else left zero.
-    import subprocess
-    import sys
-    import os
+    # for bit, the give-up count must be non-zero and everything after the
+    # status block left zero.
     note("group_norm forced-timeout recompute")
     w = W.groupnorm_vae_bf16()
     y = kf355.kf_group_norm(w["x"].cuda(), 32, w["weight"].cuda(), w["bias"].cuda(), w["eps"])
     torch.cuda.synchronize()
-    child = os.path.join(os.path.dirname(os.path.abspath(__file__)), "exchange_child.py")
-    out = str(tmp_path / "child.npz")
-    env = dict(os.environ, KF355_GN_WAIT_TICKS="0")
-    r = subprocess.run([sys.executable, "-u", child, "group_norm", out], env=env, timeout=300,
-                       capture_output=True, text=True)
-    print(r.stdout, r.stderr[-2000:])
-    assert r.returncode == 0
-    got = np.load(out)
-    assert str(got["variant"]) == "gn_fused_vec"
-    assert int(got["flag"]) == 1
+    got = spawn(tmp_path, ["group_norm"], KF355_GN_WAIT_TICKS="0")
+    assert str(got["variant0"]) == "gn_fused_vec"
+    assert int(got["give_ups"]) >= 1
     assert int(got["rest"]) == 0
-    assert np.array_equal(got["bits"], y.view(torch.int16).cpu().numpy())
+    assert np.array_equal(got["bits0"], y.view(torch.int16).cpu().numpy())
+
+
+def _oracle_of(op):
+    a = inputs(op)
+    if op == "softmax_split":
+        return oracle.softmax(a["x"], -1), "f32"
+    return oracle.group_norm(a["x"], a["groups"], a["weight"], a["bias"], a["eps"]), "bf16"
+
+
+def _as_tensor(bits):
+    t = torch.from_numpy(bits)
+    return t.view(torch.bfloat16) if t.dtype == torch.int16 else t.view(torch.float32)
+
+
+@pytest.mark.parametrize("env,ops", [
+    ({"KF355_SM_WAIT_TICKS": "0"}, ["softmax_split", "group_norm", "group_norm_small"]),
+    ({"KF355_GN_WAIT_TICKS": "0"}, ["group_norm_small", "softmax_split", "group_norm"]),
+    ({"KF355_GN_WAIT_TICKS": "0"}, ["group_norm", "group_norm_small", "group_norm"]),
+], ids=["split-gave-up", "small-gave-up", "large-gave-up"])
+def test_give_up_count_never_corrupts_later_calls(tmp_path, env, ops):
+    # A call whose workgroups gave up leaves a non-zero give-up count in the
+    # workspace; later calls of other shapes and of the other operator on the
+    # same workspace must still match the oracle, and leave every byte after
+    # the status block zero.
+    note(f"exchange workspace reuse after give-ups {env} {ops}")
+    got = spawn(tmp_path, ops, **env)
+    assert int(got["give_ups"]) >= 1
+    assert int(got["rest"]) == 0
+    for i, op in enumerate(ops):
+        ref, fmt = _oracle_of(op)
+        assert_close(_as_tensor(got[f"bits{i}"]), ref, fmt, **({"floor": FLOOR} if fmt == "bf16" else {}))
 
 
 def test_concurrent_calls_on_two_streams():
@@ -253,22 +280,12 @@ def test_channels_last_matches_nchw_statistics():
 
 
 def test_channels_last_gave_up_waiting_recomputes_bit_identically(tmp_path):
-    import os
-    import subprocess
-    import sys
     note("group_norm channels last forced recompute (child process)")
     w = W.groupnorm_vae_bf16()
     x = w["x"].cuda().contiguous(memory_format=torch.channels_last)
     y = kf355.kf_group_norm(x, 32, w["weight"].cuda(), w["bias"].cuda(), w["eps"])
     torch.cuda.synchronize()
-    child = os.path.join(os.path.dirname(os.path.abspath(__file__)), "exchange_child.py")
-    out = str(tmp_path / "child.npz")
-    env = dict(os.environ, KF355_GN_WAIT_TICKS="0")
-    r = subprocess.run([sys.executable, "-u", child, "group_norm_nhwc", out], env=env, timeout=300,
-                       capture_output=True, text=True)
-    print(r.stdout, r.stderr[-2000:])
-    assert r.returncode == 0
-    got = np.load(out)
-    assert str(got["variant"]) == "gn_nhwc_fused_vec"
-    assert int(got["flag"]) == 1 and int(got["rest"]) == 0
-    assert np.array_equal(got["bits"], y.contiguous().view(torch.int16).cpu().numpy())
+    got = spawn(tmp_path, ["group_norm_nhwc"], KF355_GN_WAIT_TICKS="0")
+    assert str(got["variant0"]) == "gn_nhwc_fused_vec"
+    assert int(got["give_ups"]) >= 1 and int(got["rest"]) == 0
+    assert np.array_equal(got["bits0"], y.contiguous().view(torch.int16).cpu().numpy())

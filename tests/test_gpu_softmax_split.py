@@ -8,15 +8,13 @@ base, many rows), determinism, workspace hygiene, concurrent streams and the
 recompute fallback when a workgroup gives up waiting.  Tolerances as for
 kf_softmax: fp32 outputs max abs error <= 1e-6; bf16 / fp16 outputs within
 1 unit in the last place of the oracle rounded once to the format."""
-import os
-import subprocess
-import sys
 
 import numpy as np
 import pytest
 import torch
 
 from compare import assert_close, note
+from exchange_child import spawn
 from oracle import oracle
 from paper_2607_24762_amd import kf355
 from paper_2607_24762_amd import workloads as W
@@ -175,15 +173,8 @@ def test_gave_up_waiting_recomputes_bit_identically(tmp_path):
     x = W.attn_decode_bf16()["x"].cuda()
     y = kf355.kf_softmax_split(x, -1, out_dtype=torch.float32)
     torch.cuda.synchronize()
-    child = os.path.join(os.path.dirname(os.path.abspath(__file__)), "exchange_child.py")
-    out = str(tmp_path / "child.npz")
-    env = dict(os.environ, KF355_SM_WAIT_TICKS="0")
-    r = subprocess.run([sys.executable, "-u", child, "softmax_split", out], env=env, timeout=300,
-                       capture_output=True, text=True)
-    print(r.stdout, r.stderr[-2000:])
-    assert r.returncode == 0
-    got = np.load(out)
-    assert str(got["variant"]).startswith("sm_split")
-    assert int(got["flag"]) == 1
+    got = spawn(tmp_path, ["softmax_split"], KF355_SM_WAIT_TICKS="0")
+    assert str(got["variant0"]).startswith("sm_split")
+    assert int(got["give_ups"]) >= 1
     assert int(got["rest"]) == 0
-    assert np.array_equal(got["bits"], y.view(torch.int32).cpu().numpy())
+    assert np.array_equal(got["bits0"], y.view(torch.int32).cpu().numpy())
