@@ -30,6 +30,7 @@
 
 #include <cstdlib>
 #include <cstring>
+#include <type_traits>
 
 #include "kf_device.hpp"
 #include "kf_exchange.hpp"
@@ -216,13 +217,24 @@ struct Chunk {
             bv[k] = load1<A>(bs, hb ? c[k] : 1);
         }
     }
-    // y = (x - mean) * (rstd * w[c]) + b[c], non-temporal stores.
+    // y = (x - mean) * (rstd * w[c]) + b[c] with rstd = 1 / sqrt(M2/n + eps),
+    // non-temporal stores.  16-bit outputs evaluate it in fp32.  fp32
+    // outputs evaluate it in double and round once: x - mean is exact there
+    // and rstd * w[c] carries no fp32 rounding, so the output's error is one
+    // fp32 rounding plus what the fp32 statistics carry (in fp32 the three
+    // extra roundings reached 1e-6 at |y| ~ 5).
+    static constexpr bool kF64Apply = std::is_same_v<T, F32>;
+    using Acc = std::conditional_t<kF64Apply, double, float>;
     __device__ __forceinline__ void normalise_store(const GNParams& p, int64_t ng, int part, float mean,
-                                                    float rstd) {
-        float ai[VEC];
+                                                    float m2) {
+        Acc rstd;
+        if constexpr (kF64Apply) rstd = 1.0 / sqrt((double)m2 / (double)p.group_elems + (double)p.eps);
+        else rstd = 1.f / sqrtf(m2 / (float)p.group_elems + p.eps);
+        const Acc mu = (Acc)mean;
+        Acc ai[VEC];
         if constexpr (kFixedChannels) {
 #pragma unroll
-            for (int i = 0; i < VEC; ++i) ai[i] = rstd * wv[i];
+            for (int i = 0; i < VEC; ++i) ai[i] = rstd * (Acc)wv[i];
         }
 #pragma unroll
         for (int k = 0; k < NV; ++k) {
@@ -231,11 +243,11 @@ struct Chunk {
                 float out[VEC];
                 if constexpr (kFixedChannels) {
 #pragma unroll
-                    for (int i = 0; i < VEC; ++i) out[i] = fmaf(v[k][i] - mean, ai[i], bv[i]);
+                    for (int i = 0; i < VEC; ++i) out[i] = (float)fma((Acc)v[k][i] - mu, ai[i], (Acc)bv[i]);
                 } else {
-                    const float a = rstd * wv[k];
+                    const Acc a = rstd * (Acc)wv[k];
 #pragma unroll
-                    for (int i = 0; i < VEC; ++i) out[i] = fmaf(v[k][i] - mean, a, bv[k]);
+                    for (int i = 0; i < VEC; ++i) out[i] = (float)fma((Acc)v[k][i] - mu, a, (Acc)bv[k]);
                 }
                 // Non-temporal stores for NCHW (each workgroup writes whole
                 // lines).  Channels last, a group's 16-byte runs share their
@@ -296,7 +308,7 @@ __device__ __forceinline__ void settle(const GNParams& p, C& c, int64_t ng, int 
         if (threadIdx.x == 0) {
             *gathered = ok;
             stats[0] = m.mean;
-            stats[1] = 1.f / sqrtf(m.m2 / (float)p.group_elems + p.eps);
+            stats[1] = m.m2;
         }
     }
     __syncthreads();
@@ -320,7 +332,7 @@ __device__ __forceinline__ void settle(const GNParams& p, C& c, int64_t ng, int 
             acc = moments_wave(acc);
             if (threadIdx.x == 0) {
                 stats[0] = acc.mean;
-                stats[1] = 1.f / sqrtf(acc.m2 / (float)p.group_elems + p.eps);
+                stats[1] = acc.m2;
                 ex_count_give_up(p.ex);
             }
         }
@@ -390,7 +402,7 @@ __global__ __launch_bounds__(kNT) void gn_apply(GNParams p) {
         if (threadIdx.x == 0) ex_release(p.ex, ng);
         if (threadIdx.x == 0) {
             stats[0] = m.mean;
-            stats[1] = 1.f / sqrtf(m.m2 / (float)p.group_elems + p.eps);
+            stats[1] = m.m2;
         }
     }
     __syncthreads();

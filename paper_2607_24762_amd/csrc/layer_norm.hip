@@ -80,18 +80,27 @@ __device__ __forceinline__ Moments slot_moments(const float (&v)[NV][VEC], const
     return Moments{cnt, K + d1, fmaxf(fmaf(-s1, d1, s2), 0.f)};
 }
 
-// y = (x - mean) * rstd * w[j] + b[j] for the valid slots, stored
-// non-temporally.  Slot k starts at element e0[k] of the row.
+// y = (x - mean) * rstd * w[j] + b[j] for the valid slots, with
+// rstd = 1 / sqrt(M2/d + eps), stored non-temporally.  Slot k starts at
+// element e0[k] of the row.  16-bit outputs evaluate it in fp32; fp32
+// outputs in double, rounded once (x - mean is exact there and rstd * w[j]
+// carries no fp32 rounding: the output's error is one fp32 rounding plus
+// what the fp32 statistics carry).
 template <class T, class A, int NV, int VEC, bool VECTOR>
 __device__ __forceinline__ void normalise_slots(const LNArgsDev& p, int64_t base, const int (&e0)[NV],
                                                 const bool (&ok)[NV], float (&v)[NV][VEC], float mean,
-                                                float rstd) {
+                                                float m2) {
+    using Acc = std::conditional_t<std::is_same_v<T, F32>, double, float>;
+    Acc rstd;
+    if constexpr (std::is_same_v<Acc, double>) rstd = 1.0 / sqrt((double)m2 / (double)p.d + (double)p.eps);
+    else rstd = 1.f / sqrtf(m2 / (float)p.d + p.eps);
+    const Acc mu = (Acc)mean;
     if constexpr (std::is_same_v<A, NoAffine>) {
 #pragma unroll
         for (int k = 0; k < NV; ++k) {
             if (ok[k]) {
 #pragma unroll
-                for (int i = 0; i < VEC; ++i) v[k][i] = (v[k][i] - mean) * rstd;
+                for (int i = 0; i < VEC; ++i) v[k][i] = (float)(((Acc)v[k][i] - mu) * rstd);
                 if constexpr (VECTOR) store_vec<T, true>(p.y, base + e0[k], v[k]);
                 else store1<T>(p.y, base + e0[k], v[k][0]);
             }
@@ -111,8 +120,8 @@ __device__ __forceinline__ void normalise_slots(const LNArgsDev& p, int64_t base
             if (ok[k]) {
 #pragma unroll
                 for (int i = 0; i < VEC; ++i) {
-                    const float a = p.w ? rstd * wv[k][i] : rstd;
-                    v[k][i] = fmaf(v[k][i] - mean, a, p.b ? bv[k][i] : 0.f);
+                    const Acc a = p.w ? rstd * (Acc)wv[k][i] : rstd;
+                    v[k][i] = (float)fma((Acc)v[k][i] - mu, a, p.b ? (Acc)bv[k][i] : (Acc)0);
                 }
                 if constexpr (VECTOR) store_vec<T, true>(p.y, base + e0[k], v[k]);
                 else store1<T>(p.y, base + e0[k], v[k][0]);
@@ -143,8 +152,7 @@ __global__ __launch_bounds__(256) void ln_wave(LNArgsDev p) {
         else v[k][0] = load1<T>(p.x, at);
     }
     const Moments m = moments_group<LPR>(slot_moments<NV, VEC>(v, ok));
-    const float rstd = 1.f / sqrtf(m.m2 / (float)p.d + p.eps);
-    normalise_slots<T, A, NV, VEC, VECTOR>(p, base, e0, ok, v, m.mean, rstd);
+    normalise_slots<T, A, NV, VEC, VECTOR>(p, base, e0, ok, v, m.mean, m.m2);
 }
 
 template <class T, class A, int NT, int NV, bool VECTOR>
@@ -168,8 +176,7 @@ __global__ __launch_bounds__(NT) void ln_block(LNArgsDev p) {
         else v[k][0] = load1<T>(p.x, at);
     }
     const Moments m = moments_block<NW>(slot_moments<NV, VEC>(v, ok), lds);
-    const float rstd = 1.f / sqrtf(m.m2 / (float)p.d + p.eps);
-    normalise_slots<T, A, NV, VEC, VECTOR>(p, base, e0, ok, v, m.mean, rstd);
+    normalise_slots<T, A, NV, VEC, VECTOR>(p, base, e0, ok, v, m.mean, m.m2);
 }
 
 template <class T, class A, int NT, bool VECTOR>
@@ -195,7 +202,6 @@ __global__ __launch_bounds__(NT) void ln_stream(LNArgsDev p) {
         acc = chan(acc, slot_moments<DEPTH, VEC>(v, ok));
     }
     const Moments m = moments_block<NW>(acc, lds);
-    const float rstd = 1.f / sqrtf(m.m2 / (float)p.d + p.eps);
     // Pass 2: normalise.
     for (int64_t e = (int64_t)threadIdx.x * VEC; e < p.d; e += (int64_t)DEPTH * NT * VEC) {
         float v[DEPTH][VEC];
@@ -210,7 +216,7 @@ __global__ __launch_bounds__(NT) void ln_stream(LNArgsDev p) {
             if constexpr (VECTOR) load_vec<T>(p.x, at, v[k]);
             else v[k][0] = load1<T>(p.x, at);
         }
-        normalise_slots<T, A, DEPTH, VEC, VECTOR>(p, base, e0, ok, v, m.mean, rstd);
+        normalise_slots<T, A, DEPTH, VEC, VECTOR>(p, base, e0, ok, v, m.mean, m.m2);
     }
 }
 
