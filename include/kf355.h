@@ -199,6 +199,37 @@ kf_status kf_group_norm(const void* x, kf_dtype x_dtype, void* y, int32_t ndim, 
 kf_status kf_group_norm_workspace_bytes(kf_dtype x_dtype, int32_t ndim, const int64_t* shape, int64_t num_groups,
                                         size_t* bytes);
 
+/* Bytes of the scratch array kf_group_norm_static uses on each GPU. */
+#define KF_GROUP_NORM_STATIC_SCRATCH_BYTES (1u << 20)
+
+/*
+ * kf_group_norm_static -- kf_group_norm without a workspace argument, for
+ * callers that cannot allocate device memory: code under HIP graph capture,
+ * tight serving loops, harnesses that forbid hipMalloc.  Same arguments
+ * (minus workspace / workspace_bytes), semantics, kernels and results as
+ * kf_group_norm; the call itself allocates nothing (no hipMalloc, hipFree or
+ * allocating library routine).
+ *
+ *  The cross-workgroup exchange runs in a scratch array of
+ *  KF_GROUP_NORM_STATIC_SCRATCH_BYTES (1 MiB) that the library holds in each
+ *  GPU's memory from the moment its code is loaded there until the process
+ *  ends; it starts zeroed and every completed call returns its exchange
+ *  region to zero (its first 32-bit word accumulates the give-up count
+ *  described for kf_group_norm and is never reset by the library).  The
+ *  array's device address is looked up on the first call on each device.
+ *  Shapes whose kf_group_norm_workspace_bytes exceeds the array return
+ *  KF_ERR_WORKSPACE before anything is enqueued (e.g. [1, 512, 128, 128] with
+ *  32 groups needs 12544 bytes; up to about 2700 groups of 16 chunks fit).
+ *  All calls on one GPU share that GPU's array: calls that may overlap in
+ *  time on one GPU (streams not ordered by events, or other threads) race
+ *  and give wrong results; calls in stream order are safe.  A failed lookup
+ *  of the array's address returns KF_ERR_HIP.
+ */
+kf_status kf_group_norm_static(const void* x, kf_dtype x_dtype, void* y, int32_t ndim, const int64_t* shape,
+                               const int64_t* x_strides, const int64_t* y_strides, int64_t num_groups,
+                               const void* weight, const void* bias, kf_dtype affine_dtype, double eps,
+                               void* stream);
+
 /*
  * kf_layer_norm -- y = layer_norm(x, x.shape[-normalized_ndim:], weight,
  * bias, eps) (PyTorch `torch.nn.functional.layer_norm`; the SD3.5 Medium

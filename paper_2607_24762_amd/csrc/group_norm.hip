@@ -28,6 +28,7 @@
 // compute bit-identical results.
 #include <math.h>
 
+#include <atomic>
 #include <cstdlib>
 #include <cstring>
 #include <type_traits>
@@ -560,7 +561,39 @@ kf_status run_layout(const GroupNormArgs& a, hipStream_t s, const char** variant
     return vec ? run<T, A, true, false>(a, s, variant) : run<T, A, false, false>(a, s, variant);
 }
 
+// The exchange workspace of kf_group_norm_static: one array per GPU, in
+// device memory from the moment this code object is loaded on that GPU until
+// the process ends, zero-initialised at load (static storage) and returned
+// to zero by every completed call, like a caller's workspace.  Host code must
+// never pass `scratch` itself to a kernel or a copy (on the host the name
+// stands for a host-side shadow, not a device address): it uses the device
+// address hipGetSymbolAddress reports for the current device.
+static __device__ __align__(256) unsigned char scratch[KF_GROUP_NORM_STATIC_SCRATCH_BYTES];
+
 }  // namespace
+
+kf_status group_norm_static_scratch(void** ptr) {
+    constexpr int kDevices = 64;
+    static std::atomic<void*> addr[kDevices];
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kDevices) {
+        set_error("group_norm_static: no usable current HIP device (%d)", dev);
+        return KF_ERR_HIP;
+    }
+    void* p = addr[dev].load(std::memory_order_acquire);
+    if (!p) {
+        // With `dev` current: each GPU holds its own copy at its own address.
+        const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !p) {
+            set_error("group_norm_static: hipGetSymbolAddress of the scratch array failed on device %d: %s", dev,
+                      hipGetErrorString(e));
+            return KF_ERR_HIP;
+        }
+        addr[dev].store(p, std::memory_order_release);
+    }
+    *ptr = p;
+    return KF_OK;
+}
 
 size_t group_norm_workspace_bytes(int64_t n, int64_t c, int64_t spatial, int64_t groups, kf_dtype xt) {
     // The scalar layout has the smaller chunk, hence more parts: size for it

@@ -190,6 +190,67 @@ kf_status check_group_norm_shape(kf_dtype xt, int32_t ndim, const int64_t* shape
     return KF_OK;
 }
 
+// kf_group_norm and kf_group_norm_static: every check, then the launch.
+// With use_static the workspace arguments are ignored and the exchange runs
+// in the library's static scratch array.
+kf_status group_norm_call(const void* x, kf_dtype x_dtype, void* y, int32_t ndim, const int64_t* shape,
+                        const int64_t* x_strides, const int64_t* y_strides, int64_t num_groups, const void* weight,
+                        const void* bias, kf_dtype affine_dtype, double eps, void* workspace,
+                        size_t workspace_bytes, bool use_static, void* stream) {
+    int64_t n = 0;
+    kf_status s = check_group_norm_shape(x_dtype, ndim, shape, num_groups, &n);
+    if (s != KF_OK) return s;
+    if ((weight || bias) && !(affine_dtype == x_dtype || affine_dtype == KF_FLOAT32))
+        return fail(KF_ERR_BAD_DTYPE, "affine dtype %d must be x's dtype or FLOAT32", (int)affine_dtype);
+    if (!(eps >= 0.0) || !std::isfinite(eps)) return fail(KF_ERR_BAD_ARG, "eps must be finite and >= 0");
+    if (n == 0) return done(KF_OK, "noop");
+    if (!x || !y) return fail(KF_ERR_NULL_POINTER, "x or y is NULL");
+    const int64_t eb = elem_bytes(x_dtype);
+    if ((uintptr_t)x % eb || (uintptr_t)y % eb) return fail(KF_ERR_BAD_ARG, "x or y is not element aligned");
+    bool nhwc = false;
+    if (dense(ndim, shape, x_strides)) {
+        if (!dense(ndim, shape, y_strides))
+            return fail(KF_ERR_UNSUPPORTED_LAYOUT, "y must be dense in x's layout (NC*)");
+    } else if (ndim == 4 && dense_nhwc(shape, x_strides)) {
+        if (!dense_nhwc(shape, y_strides))
+            return fail(KF_ERR_UNSUPPORTED_LAYOUT, "y must be dense in x's layout (channels last)");
+        nhwc = true;
+    } else {
+        return fail(KF_ERR_UNSUPPORTED_LAYOUT, "x must be dense NC* or dense channels last [N, C, H, W]");
+    }
+    const int64_t xb = n * eb;
+    if (x != y && overlaps(x, xb, y, xb)) return fail(KF_ERR_BAD_ARG, "x and y partially overlap");
+    const int64_t ab = shape[1] * ((weight || bias) ? elem_bytes(affine_dtype) : 0);
+    if ((weight && overlaps(weight, ab, y, xb)) || (bias && overlaps(bias, ab, y, xb)))
+        return fail(KF_ERR_BAD_ARG, "weight or bias overlaps y");
+    const int64_t spatial = ndim > 2 ? count(ndim - 2, shape + 2) : 1;
+    const size_t need = group_norm_workspace_bytes(shape[0], shape[1], spatial, num_groups, x_dtype);
+    if (use_static) {
+        // The library's own array: checked against its size, then located.
+        if (need > KF_GROUP_NORM_STATIC_SCRATCH_BYTES)
+            return fail(KF_ERR_WORKSPACE,
+                        "group_norm_static: this shape needs %zu bytes of exchange workspace, the static scratch "
+                        "array holds %u; use kf_group_norm with a workspace",
+                        need, (unsigned)KF_GROUP_NORM_STATIC_SCRATCH_BYTES);
+        s = group_norm_static_scratch(&workspace);
+        if (s != KF_OK) return s;
+        workspace_bytes = KF_GROUP_NORM_STATIC_SCRATCH_BYTES;
+    } else {
+        if (!workspace || workspace_bytes < need)
+            return fail(KF_ERR_WORKSPACE, "workspace of %zu bytes given, %zu needed",
+                        workspace ? workspace_bytes : 0, need);
+        if ((uintptr_t)workspace % 256) return fail(KF_ERR_WORKSPACE, "workspace is not 256-byte aligned");
+        if (overlaps(workspace, (int64_t)need, x, xb) || overlaps(workspace, (int64_t)need, y, xb))
+            return fail(KF_ERR_BAD_ARG, "workspace overlaps x or y");
+    }
+
+    GroupNormArgs a{x,     y,    x_dtype,      shape[0],         shape[1], spatial, num_groups, weight, bias,
+                    affine_dtype, (float)eps, workspace, workspace_bytes, nhwc};
+    const char* variant = nullptr;
+    s = group_norm_launch(a, static_cast<hipStream_t>(stream), &variant);
+    return done(s, variant);
+}
+
 }  // namespace
 }  // namespace kf
 
@@ -316,46 +377,17 @@ kf_status kf_group_norm(const void* x, kf_dtype x_dtype, void* y, int32_t ndim, 
                         const void* bias, kf_dtype affine_dtype, double eps, void* workspace,
                         size_t workspace_bytes, void* stream) {
     begin();
-    int64_t n = 0;
-    kf_status s = check_group_norm_shape(x_dtype, ndim, shape, num_groups, &n);
-    if (s != KF_OK) return s;
-    if ((weight || bias) && !(affine_dtype == x_dtype || affine_dtype == KF_FLOAT32))
-        return fail(KF_ERR_BAD_DTYPE, "affine dtype %d must be x's dtype or FLOAT32", (int)affine_dtype);
-    if (!(eps >= 0.0) || !std::isfinite(eps)) return fail(KF_ERR_BAD_ARG, "eps must be finite and >= 0");
-    if (n == 0) return done(KF_OK, "noop");
-    if (!x || !y) return fail(KF_ERR_NULL_POINTER, "x or y is NULL");
-    const int64_t eb = elem_bytes(x_dtype);
-    if ((uintptr_t)x % eb || (uintptr_t)y % eb) return fail(KF_ERR_BAD_ARG, "x or y is not element aligned");
-    bool nhwc = false;
-    if (dense(ndim, shape, x_strides)) {
-        if (!dense(ndim, shape, y_strides))
-            return fail(KF_ERR_UNSUPPORTED_LAYOUT, "y must be dense in x's layout (NC*)");
-    } else if (ndim == 4 && dense_nhwc(shape, x_strides)) {
-        if (!dense_nhwc(shape, y_strides))
-            return fail(KF_ERR_UNSUPPORTED_LAYOUT, "y must be dense in x's layout (channels last)");
-        nhwc = true;
-    } else {
-        return fail(KF_ERR_UNSUPPORTED_LAYOUT, "x must be dense NC* or dense channels last [N, C, H, W]");
-    }
-    const int64_t xb = n * eb;
-    if (x != y && overlaps(x, xb, y, xb)) return fail(KF_ERR_BAD_ARG, "x and y partially overlap");
-    const int64_t ab = shape[1] * ((weight || bias) ? elem_bytes(affine_dtype) : 0);
-    if ((weight && overlaps(weight, ab, y, xb)) || (bias && overlaps(bias, ab, y, xb)))
-        return fail(KF_ERR_BAD_ARG, "weight or bias overlaps y");
-    const int64_t spatial = ndim > 2 ? count(ndim - 2, shape + 2) : 1;
-    const size_t need = group_norm_workspace_bytes(shape[0], shape[1], spatial, num_groups, x_dtype);
-    if (!workspace || workspace_bytes < need)
-        return fail(KF_ERR_WORKSPACE, "workspace of %zu bytes given, %zu needed", workspace ? workspace_bytes : 0,
-                    need);
-    if ((uintptr_t)workspace % 256) return fail(KF_ERR_WORKSPACE, "workspace is not 256-byte aligned");
-    if (overlaps(workspace, (int64_t)need, x, xb) || overlaps(workspace, (int64_t)need, y, xb))
-        return fail(KF_ERR_BAD_ARG, "workspace overlaps x or y");
+    return group_norm_call(x, x_dtype, y, ndim, shape, x_strides, y_strides, num_groups, weight, bias, affine_dtype,
+                           eps, workspace, workspace_bytes, false, stream);
+}
 
-    GroupNormArgs a{x,     y,    x_dtype,      shape[0],         shape[1], spatial, num_groups, weight, bias,
-                    affine_dtype, (float)eps, workspace, workspace_bytes, nhwc};
-    const char* variant = nullptr;
-    s = group_norm_launch(a, static_cast<hipStream_t>(stream), &variant);
-    return done(s, variant);
+kf_status kf_group_norm_static(const void* x, kf_dtype x_dtype, void* y, int32_t ndim, const int64_t* shape,
+                               const int64_t* x_strides, const int64_t* y_strides, int64_t num_groups,
+                               const void* weight, const void* bias, kf_dtype affine_dtype, double eps,
+                               void* stream) {
+    begin();
+    return group_norm_call(x, x_dtype, y, ndim, shape, x_strides, y_strides, num_groups, weight, bias, affine_dtype,
+                           eps, nullptr, 0, true, stream);
 }
 
 kf_status kf_layer_norm(const void* x, kf_dtype x_dtype, void* y, int32_t ndim, const int64_t* shape,

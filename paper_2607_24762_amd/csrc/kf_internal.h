@@ -54,6 +54,10 @@ struct GroupNormArgs {
 };
 size_t group_norm_workspace_bytes(int64_t n, int64_t c, int64_t spatial, int64_t groups, kf_dtype xt);
 kf_status group_norm_launch(const GroupNormArgs& a, hipStream_t s, const char** variant);
+// Device address, on the current device, of the library's static GroupNorm
+// scratch array (KF_GROUP_NORM_STATIC_SCRATCH_BYTES); looked up once per
+// device.  KF_ERR_HIP when the lookup fails.
+kf_status group_norm_static_scratch(void** ptr);
 
 // LayerNorm over the last d elements of a dense [rows, d] view.
 struct LayerNormArgs {

@@ -46,6 +46,9 @@ _SIGNATURES = {
                                      ctypes.c_double, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]),
     "kf_group_norm_workspace_bytes": (ctypes.c_int, [ctypes.c_int, ctypes.c_int32, _i64p, ctypes.c_int64,
                                                      ctypes.POINTER(ctypes.c_size_t)]),
+    "kf_group_norm_static": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p, ctypes.c_int32, _i64p,
+                                            _i64p, _i64p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p,
+                                            ctypes.c_int, ctypes.c_double, ctypes.c_void_p]),
     "kf_layer_norm": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p, ctypes.c_int32, _i64p, _i64p,
                                      _i64p, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int,
                                      ctypes.c_double, ctypes.c_void_p]),
@@ -277,15 +280,13 @@ def kf_softmax_split(x: torch.Tensor, dim: int = -1, out_dtype: torch.dtype | No
     return y
 
 
-def kf_group_norm(x: torch.Tensor, num_groups: int, weight: torch.Tensor | None = None,
-                  bias: torch.Tensor | None = None, eps: float = 1e-5, out: torch.Tensor | None = None,
-                  workspace: torch.Tensor | None = None) -> torch.Tensor:
-    """group_norm(x, num_groups, weight, bias, eps) through kf_group_norm."""
+def _group_norm_args(x, num_groups, weight, bias, eps, out):
+    """Output tensor and the C arguments shared by kf_group_norm and
+    kf_group_norm_static, up to (not including) the workspace."""
     _need_cuda(x, weight, bias)
     fmt = torch.channels_last if (x.dim() == 4 and not x.is_contiguous()
                                   and x.is_contiguous(memory_format=torch.channels_last)) else torch.contiguous_format
     y = out if out is not None else torch.empty_like(x, memory_format=fmt)
-    ws = workspace if workspace is not None else group_norm_workspace(x, num_groups)
     affine = weight if weight is not None else bias
     at = _dtype(affine) if affine is not None else _dtype(x)
     if weight is not None and bias is not None and weight.dtype != bias.dtype:
@@ -296,12 +297,33 @@ def kf_group_norm(x: torch.Tensor, num_groups: int, weight: torch.Tensor | None 
     shape, _s = _arr(x.shape)
     xs, _a = _arr(x.stride())
     ys, _b = _arr(y.stride())
-    with _on(x):
-        _check(lib().kf_group_norm(
-            x.data_ptr(), _dtype(x), y.data_ptr(), x.dim(), shape, xs, ys,
+    args = (x.data_ptr(), _dtype(x), y.data_ptr(), x.dim(), shape, xs, ys,
             num_groups, weight.data_ptr() if weight is not None else None,
-            bias.data_ptr() if bias is not None else None, at, float(eps),
-            ws.data_ptr(), ws.numel(), _stream(x)))
+            bias.data_ptr() if bias is not None else None, at, float(eps))
+    return y, args
+
+
+def kf_group_norm(x: torch.Tensor, num_groups: int, weight: torch.Tensor | None = None,
+                  bias: torch.Tensor | None = None, eps: float = 1e-5, out: torch.Tensor | None = None,
+                  workspace: torch.Tensor | None = None) -> torch.Tensor:
+    """group_norm(x, num_groups, weight, bias, eps) through kf_group_norm."""
+    y, args = _group_norm_args(x, num_groups, weight, bias, eps, out)
+    ws = workspace if workspace is not None else group_norm_workspace(x, num_groups)
+    with _on(x):
+        _check(lib().kf_group_norm(*args, ws.data_ptr(), ws.numel(), _stream(x)))
+    return y
+
+
+def kf_group_norm_static(x: torch.Tensor, num_groups: int, weight: torch.Tensor | None = None,
+                         bias: torch.Tensor | None = None, eps: float = 1e-5,
+                         out: torch.Tensor | None = None) -> torch.Tensor:
+    """group_norm(x, ...) through kf_group_norm_static: no workspace, the
+    exchange runs in the library's static per-GPU scratch array, so with
+    `out` given nothing is allocated (for callers that cannot allocate:
+    graph capture, serving loops).  Calls on one GPU must not overlap."""
+    y, args = _group_norm_args(x, num_groups, weight, bias, eps, out)
+    with _on(x):
+        _check(lib().kf_group_norm_static(*args, _stream(x)))
     return y
 
 

@@ -233,6 +233,32 @@ def test_group_norm_zero_elements_and_workspace_query(lib):
     assert lib.kf_group_norm_workspace_bytes(F32, 2, arr((2, 4)), 2, None) == NULLP
 
 
+def gn_static(lib, shape=(2, 8, 4, 4), groups=4, xt=F32, x=FAKE, y=FAKE + (1 << 30), eps=1e-5):
+    return lib.kf_group_norm_static(ctypes.c_void_p(x), xt, ctypes.c_void_p(y), len(shape), arr(shape), None, None,
+                                    groups, None, None, xt, eps, None)
+
+
+def test_group_norm_static_rejections(lib):
+    # The allocation-free GroupNorm runs the same checks as kf_group_norm,
+    # all before its scratch array is looked up on the device.
+    assert gn_static(lib, shape=(0, 8, 4, 4)) == OK
+    assert lib.kf_last_variant().decode() == "noop"
+    assert gn_static(lib, x=0) == NULLP
+    assert gn_static(lib, groups=3) == ARG
+    assert gn_static(lib, eps=-1.0) == ARG
+    assert gn_static(lib, xt=7) == DTYPE
+    assert gn_static(lib, y=FAKE + 16) == ARG                  # partial overlap
+    # One-chunk groups of 16384 elements: 96000 of them need 256 + 768000 +
+    # 96000 * 256 bytes of exchange workspace, beyond the 1 MiB array.
+    assert gn_static(lib, shape=(3000, 32, 128, 128), groups=32, y=FAKE + (1 << 40)) == WS
+    assert "static scratch array holds 1048576" in err(lib)
+    st, n = gn_ws(lib, (3000, 32, 128, 128), 32, xt=F32)
+    assert st == OK and n > 1 << 20
+    # The SD3.5 VAE block fits (12544 bytes).
+    st, n = gn_ws(lib, (1, 512, 128, 128), 32)
+    assert st == OK and n == 12544 <= 1 << 20
+
+
 def ap(lib, shape=(2, 3, 7, 7), oh=1, ow=1, x=FAKE, y=FAKE + (1 << 30), xt=F32, xs=None, ys=None):
     return lib.kf_adaptive_avgpool2d(ctypes.c_void_p(x), xt, ctypes.c_void_p(y), len(shape), arr(shape),
                                      arr(xs) if xs else None, arr(ys) if ys else None, oh, ow, None)
