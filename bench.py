@@ -77,18 +77,57 @@ def cpu_baseline(w, bytes_per_op, min_seconds: float = 10.0, max_reps: int = 8) 
 
     ap, gn, sm = w["avgpool"], w["group_norm"], w["softmax"]["x"]
     reps = 0
+    refs = {}
     t0 = time.perf_counter()
     while reps < max_reps and (reps == 0 or time.perf_counter() - t0 < min_seconds):
-        oracle.round_to(oracle.adaptive_avg_pool2d(ap["x"], ap["output_size"]), "f32")
-        oracle.round_to(oracle.group_norm(gn["x"], gn["num_groups"], gn["weight"], gn["bias"], gn["eps"]), "bf16")
-        oracle.round_to(oracle.softmax(sm, -1), "bf16")
+        r_ap = oracle.adaptive_avg_pool2d(ap["x"], ap["output_size"])
+        oracle.round_to(r_ap, "f32")
+        r_gn = oracle.group_norm(gn["x"], gn["num_groups"], gn["weight"], gn["bias"], gn["eps"])
+        oracle.round_to(r_gn, "bf16")
+        r_sm = oracle.softmax(sm, -1)
+        oracle.round_to(r_sm, "bf16")
+        if reps == 0:
+            refs = {"adaptive_avgpool2d": r_ap, "group_norm": r_gn, "softmax": r_sm}
+        del r_ap, r_gn, r_sm
         reps += 1
     dt = time.perf_counter() - t0
     sample_bytes = reps * sum(bytes_per_op.values())
     return {"value": round(sample_bytes / dt / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
             "sample": f"{reps} whole step(s) of the same workload ({sample_bytes} algorithmic bytes) in "
                       f"{dt:.1f} s, single-threaded C in float64 plus marshalling and rounding",
-            "host": host_cpu()}
+            "host": host_cpu()}, refs
+
+
+# Parity bars (the oracle's float64 result is the reference): fp32 outputs
+# max abs error <= 1e-6; bf16 outputs within 1 ulp of the oracle rounded once,
+# GroupNorm also accepting |error| <= 2^-22 where |oracle| < 2^-19.
+GN_FLOOR = (2.0 ** -19, 2.0 ** -22)
+
+
+def parity_row(outputs, refs, w):
+    """The oracle side of the measurement's parity check, run inside the CPU
+    baseline leg: each timed kf355 output (and torch eager's output on the
+    same input, as information) against the oracle.  `outputs` maps a
+    configuration to (input, fmt, kf355 output, eager output) on the host;
+    `refs` holds the oracle results the baseline already computed for the
+    step's operators; the fp32 softmax configurations are evaluated here."""
+    sys.path.insert(0, os.path.join(ROOT, "tests"))
+    from compare import compare
+    from oracle import oracle
+
+    row = {"bar": "fp32 max abs error <= 1e-6; bf16 <= 1 ulp of the oracle rounded once (GroupNorm: or "
+                  "|error| <= 2^-22 where |oracle| < 2^-19, counted as floor_hits)"}
+    for name, (x, fmt, got, eager) in outputs.items():
+        ref = refs.get(name)
+        if ref is None:
+            ref = oracle.softmax(x, -1)
+        kw = {"floor": GN_FLOOR} if name == "group_norm" else {}
+        row[name] = {"kf355": compare(got, ref, fmt, **kw)}
+        if eager is not None:
+            row[name]["torch_eager"] = compare(eager, ref, fmt, **kw)
+        del ref
+    row["all_ok"] = all(v["kf355"]["ok"] for k, v in row.items() if isinstance(v, dict))
+    return row
 
 
 def cpu_baseline_parallel(w, bytes_per_op, threads: int, min_seconds: float = 10.0, max_reps: int = 8) -> dict:
@@ -132,6 +171,16 @@ def torch_chunks(t, n: int) -> list:
     """t split along its first axis into at most n contiguous pieces."""
     step = -(-t.shape[0] // n)
     return [t[i:i + step] for i in range(0, t.shape[0], step)]
+
+
+def child_processes() -> int:
+    """Processes this run started that are still alive (0 expected: the
+    benchmark starts none of its own)."""
+    try:
+        import psutil
+        return len(psutil.Process().children(recursive=True))
+    except Exception:
+        return -1
 
 
 def host_cpu() -> dict:
@@ -302,7 +351,8 @@ def decode_row(torch, dev, kf355, W, steps, warmup, sets_for):
             "timing": "HIP graph of back-to-back calls (graph_us); launched_us = launched from Python",
             "split": out["split"], "plain": out["plain"], "torch_eager": out["eager"],
             "vs_plain": round(out["plain"]["graph_us"] / g_us, 3),
-            "vs_torch_eager": round(out["eager"]["graph_us"] / g_us, 3), "graph_output_matches": same}
+            "vs_torch_eager": round(out["eager"]["graph_us"] / g_us, 3), "graph_output_matches": same,
+            "give_ups": kf355.workspace_give_ups(ws)}
 
 
 def maxpool_row(torch, F, dev, kf355, W, steps, warmup, sets_for):
@@ -447,10 +497,12 @@ def resnet_fp16_row(torch, F, dev, kf355, W, steps, warmup, sets_for):
     return row
 
 
-def small_softmax_row(torch, dev, kf355, W, steps, warmup, sets_for):
+def small_softmax_row(torch, dev, kf355, W, steps, warmup, sets_for, outputs):
     """The fp32 softmax configurations reported beside the large one: a
     square [1024, 1024] and the MoE router logits [16384, 256] and [16384,
-    257] (rows not whole 16-byte vectors), libkf355 against torch eager."""
+    257] (rows not whole 16-byte vectors), libkf355 against torch eager.
+    The first buffer set's timed output and eager's output on the same input
+    go to `outputs` for the parity check."""
     row = {}
     for name in ("softmax_f32_1024x1024", "router_softmax_f32_16384x256", "router_softmax_f32_16384x257"):
         wl = W.WORKLOADS[name]()
@@ -462,6 +514,7 @@ def small_softmax_row(torch, dev, kf355, W, steps, warmup, sets_for):
         variant = kf355.last_variant()
         us = time_launches(torch, fns, steps, warmup)
         eager_us = time_launches(torch, [lambda x=x: torch.softmax(x, -1) for x in xs], min(steps, 50), warmup)
+        outputs[name] = (wl["x"], "f32", fns[0]._keep[1].cpu(), torch.softmax(xs[0], -1).cpu())
         gbs = nb / (us * 1e-6) / 1e9
         row[name] = {"workload": f"fp32 {list(src.shape)} softmax over the last dim", "variant": variant,
                      "algorithmic_bytes": nb, "us_per_call": round(us, 3), "gbps": round(gbs, 1),
@@ -605,6 +658,13 @@ def main():
                                  "gbps": round(nbytes[name] / (warm_us * 1e-6) / 1e9, 1),
                                  "note": "one buffer set reused: cache-resident, not HBM"}}
 
+    # The timed outputs of the step (each buffer set holds the same input
+    # and, after the timed calls, the same output), for the parity check.
+    step_fmt = {"adaptive_avgpool2d": "f32", "group_norm": "bf16", "softmax": "bf16"}
+    step_in = {"adaptive_avgpool2d": w["avgpool"]["x"], "group_norm": gn["x"], "softmax": w["softmax"]["x"]}
+    outputs = {name: [step_in[name], step_fmt[name], calls[name][0]._keep[1].cpu(), None] for name in order}
+    gn_ws = calls["group_norm"][0]._keep[4]
+
     eager = None
     if not args.no_eager:
         # torch eager on the same MI355X, same rotating input sets.
@@ -628,6 +688,7 @@ def main():
             torch.cuda.synchronize()
             us = e0.elapsed_time(e1) * 1e3 / n
             eager[name] = {"us_per_call": round(us, 3), "kf355_speedup": round(us / per_op[name]["us_per_call"], 3)}
+            outputs[name][3] = op(inputs[0]).cpu()
 
     next_rows = None
     if not args.no_next:
@@ -702,13 +763,22 @@ def main():
         next_rows["resnet50_fp16"] = resnet_fp16_row(torch, F, dev, kf355, W, args.steps, args.warmup, sets_for)
         next_rows["softmax_unaligned_rows"] = unaligned_softmax_row(torch, dev, kf355, W, args.steps, args.warmup,
                                                                     sets_for)
-        next_rows["softmax_fp32_configs"] = small_softmax_row(torch, dev, kf355, W, args.steps, args.warmup, sets_for)
         next_rows["avgpool_general_sizes"] = avgpool_general_row(torch, F, dev, kf355, W, args.steps, args.warmup,
                                                                   sets_for)
         next_rows["avgpool_channels_last"] = avgpool_cl_row(torch, F, dev, kf355, W, args.steps, args.warmup,
                                                             sets_for)
         next_rows["group_norm_channels_last"] = gn_cl_row(torch, F, dev, kf355, W, args.steps, args.warmup,
                                                           sets_for)
+
+    # The fp32 softmax configurations (the square rows and the router logits).
+    softmax_fp32 = small_softmax_row(torch, dev, kf355, W, args.steps, args.warmup, sets_for, outputs)
+    # Workgroups of the exchange kernels that stopped waiting and recomputed
+    # their statistics (0 unless something else held the GPU): every cached
+    # workspace's count, plus the decode row's own.
+    give_ups = {"group_norm_step_workspace": kf355.workspace_give_ups(gn_ws),
+                "all_cached_workspaces": sum(kf355.workspace_give_ups(t) for t in kf355._ws_cache.values())}
+    if next_rows is not None:
+        give_ups["softmax_decode_split"] = next_rows["softmax_decode_split"].pop("give_ups")
 
     calib = copy_calibration(torch, dev, nbytes["softmax"])
     floors = floors_row(torch, dev, kf355, w, args.steps, sets_for)
@@ -719,9 +789,12 @@ def main():
                 "timing": "HIP events around back-to-back launches on the launch stream, rotating buffer sets",
                 "algorithmic_bytes_per_launch": nbytes["softmax"]}
 
-    base = base_mt = None
+    base = base_mt = parity = None
     if not args.no_cpu_baseline:
-        base = cpu_baseline(w, nbytes)
+        base, refs = cpu_baseline(w, nbytes)
+        outputs = {k: tuple(v) for k, v in outputs.items()}
+        parity = parity_row(outputs, refs, w)
+        del refs, outputs
         usable = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else (os.cpu_count() or 1)
         base_mt = cpu_baseline_parallel(w, nbytes, threads=max(1, min(usable, 16)))
 
@@ -733,8 +806,10 @@ def main():
         "data": "synthetic (seeded, shapes and distributions of the paper's workloads)",
         "config": {"workload": WORKLOAD, "step_algorithmic_bytes": step_bytes},
         "per_op": per_op, "roofline": roofline, "cpu_baseline": base, "cpu_baseline_parallel": base_mt,
-        "torch_eager": eager, "inputs_sha256": input_hashes,
+        "torch_eager": eager, "inputs_sha256": input_hashes, "parity": parity,
+        "exchange_give_ups": give_ups, "softmax_fp32_configs": softmax_fp32,
         "calibration": calib, "floors": floors, "next_rows": next_rows,
+        "child_processes_at_exit": child_processes(),
     }
     print(json.dumps(out), flush=True)
 
