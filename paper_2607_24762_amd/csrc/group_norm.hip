@@ -411,6 +411,382 @@ __global__ __launch_bounds__(kNT) void gn_apply(GNParams p) {
 }
 
 // --------------------------------------------------------------------------
+// gn_pipe: the fused kernel for dense NCHW 16-bit tensors whose spatial
+// size is a multiple of 2048.  A workgroup is four data waves and one
+// exchange wave and carries R chunks of 2048 * NV elements, one per round;
+// round r holds whole groups only (groups r * per_round ...), so a round's
+// exchange never waits on a later round.  The data waves issue the loads of
+// every round at once and hold the chunks in registers as raw 16-bit pairs.
+// The exchange wave does all the cross-workgroup work (publish, poll, merge,
+// affine, departure): loads return in issue order per wave, so a poll issued
+// by a wave that still has chunk loads outstanding would wait for them; this
+// wave has none.  Against gn_fused on the SD3.5 VAE block (12.1 us per call)
+// this form runs 8.3 us: its per-element work is four VALU operations
+// instead of about ten, and its merges have no divergent branches.
+//
+// Moments of a data wave: raw sums S1 = sum x and S2 = sum x^2, each pair of
+// 16-bit values folded by one v_dot2 (their products are exact in fp32),
+// reduced over the wave's lanes; S1 in double from the lanes' fp32 sums on,
+// and the means merged in double.  The mean enters every output as an
+// absolute error (x - mean) * a: one fp32 rounding of a mean near 0.3 is
+// already 1.5e-8, 1 to 3 bf16 units in the last place of outputs just above
+// 2^-19, whereas the lanes' rounding errors average out and the double sums
+// keep the group mean within about 1e-10.  The output is then
+// (x - hi) * a + (b - lo * a) with the mean split as hi + lo in fp32.  M2 = S2 - S1^2/n
+// cancels when the mean is large against the spread, so it is used only when
+// 64 * M2 >= S2 (mean^2 <= 63 var over the wave's values), where its
+// relative error stays below 2^-12 (a shift of at most 2^-13 of the output
+// before rounding to 16 bits); otherwise the wave recomputes M2 exactly:
+// per-lane squared deviations from the lane's mean, merged over lanes.  All
+// merges are of equal counts, where the Chan et al. update is
+// M2 = Ma + Mb + (mb - ma)^2 * n / 2 for n values per side; operands are
+// ordered by lane (or wave, or part), so both lanes of a butterfly pair get
+// identical bits and the result depends on that order alone.
+constexpr int kPipeDataWaves = 4;
+constexpr int kPipeNT = (kPipeDataWaves + 1) * kWave;
+
+struct PipeParams {
+    const void* x;
+    void* y;
+    const void* w;
+    const void* b;
+    Exchange ex;                 // one unit per (sample, group), ex.parts chunks each
+    int64_t group_elems;         // (c/G) * spatial
+    int64_t spatial;             // a multiple of 2048: every 16-byte slot row lies in one channel
+    int32_t cpg;                 // channels per group
+    int32_t groups;              // G
+    int32_t groups_total;        // n * G
+    int32_t per_round;           // groups per round
+    int32_t xcd_map;             // 1: all parts of a group on one XCD (per_round % 8 == 0)
+    float eps;
+};
+
+// Moments of a set of values: the mean in double, M2 in float.
+struct PipeMoments {
+    double mean;
+    float m2;
+};
+
+// a.x * b.x + a.y * b.y + c on two packed 16-bit values.
+__device__ __forceinline__ float dot2(BF16, uint32_t a, uint32_t b, float c) {
+    return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, a), __builtin_bit_cast(bf16x2, b), c, false);
+}
+__device__ __forceinline__ float dot2(F16, uint32_t a, uint32_t b, float c) {
+    return __builtin_amdgcn_fdot2(__builtin_bit_cast(f16x2, a), __builtin_bit_cast(f16x2, b), c, false);
+}
+__device__ __forceinline__ uint32_t ones2(BF16) { return 0x3F803F80u; }
+__device__ __forceinline__ uint32_t ones2(F16) { return 0x3C003C00u; }
+
+// Butterfly partner of a double (both halves moved by the same DPP /
+// permlane pattern).
+template <int S>
+__device__ __forceinline__ double partner_f64(double v) {
+    const uint64_t u = __builtin_bit_cast(uint64_t, v);
+    const float lo = partner<S>(__uint_as_float((uint32_t)u));
+    const float hi = partner<S>(__uint_as_float((uint32_t)(u >> 32)));
+    return __builtin_bit_cast(double, (uint64_t)__float_as_uint(lo) | ((uint64_t)__float_as_uint(hi) << 32));
+}
+
+// Equal-count merge of a and b (a first), n values each.
+__device__ __forceinline__ PipeMoments merge_equal(PipeMoments a, PipeMoments b, float n) {
+#pragma clang fp contract(off)
+    PipeMoments m;
+    m.mean = (a.mean + b.mean) * 0.5;
+    const float d = (float)(b.mean - a.mean);
+    m.m2 = fmaf(d * d, 0.5f * n, a.m2 + b.m2);
+    return m;
+}
+
+// Butterfly step S over moments, the lower lane of each pair first.
+template <int S>
+__device__ __forceinline__ PipeMoments pipe_step(PipeMoments m, float n) {
+    const PipeMoments o{partner_f64<S>(m.mean), partner<S>(m.m2)};
+    const bool lower = (__lane_id() & (1 << S)) == 0;
+    return merge_equal(lower ? m : o, lower ? o : m, n);
+}
+
+// Moments of one wave's values: lane l holds NV 16-byte words of 16-bit
+// values.  Uniform across the wave.
+template <class T, int NV>
+__device__ __forceinline__ PipeMoments wave_moments(const u32x4 (&v)[NV]) {
+#pragma clang fp contract(off)
+    constexpr float kLane = (float)(NV * 8);
+    constexpr double kWaveN = (double)kLane * kWave;
+    float s1a = 0.f, s1b = 0.f, s2a = 0.f, s2b = 0.f;
+#pragma unroll
+    for (int j = 0; j < NV; ++j) {
+#pragma unroll
+        for (int i = 0; i < 4; i += 2) {
+            s1a = dot2(T{}, v[j][i], ones2(T{}), s1a);
+            s2a = dot2(T{}, v[j][i], v[j][i], s2a);
+            s1b = dot2(T{}, v[j][i + 1], ones2(T{}), s1b);
+            s2b = dot2(T{}, v[j][i + 1], v[j][i + 1], s2b);
+        }
+    }
+    const float lane_s1 = s1a + s1b;
+    // The wave's sum in double (the addition is commutative, so both lanes
+    // of a pair get the same bits).
+    double s1 = (double)lane_s1;
+    s1 += partner_f64<0>(s1);
+    s1 += partner_f64<1>(s1);
+    s1 += partner_f64<2>(s1);
+    s1 += partner_f64<3>(s1);
+    s1 += partner_f64<4>(s1);
+    s1 += partner_f64<5>(s1);
+    const float s2 = group_reduce<kWave>(s2a + s2b, OpSum{});
+    PipeMoments m;
+    m.mean = s1 * (1.0 / kWaveN);
+    m.m2 = s2 - (float)(s1 * m.mean);
+    if (__builtin_expect(m.m2 * 64.f >= s2, 1)) return m;
+    // Exact M2: per-lane squared deviations from the lane's mean (values
+    // widened again here, so no register copy of them is held), merged over
+    // the lanes; the wave's mean stays.
+    const float mt = lane_s1 * (1.f / kLane);
+    float mt2 = 0.f;
+#pragma unroll
+    for (int j = 0; j < NV; ++j)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            float lo, hi;
+            unpack2(T{}, v[j][i], lo, hi);
+            const float dl = lo - mt, dh = hi - mt;
+            mt2 = fmaf(dl, dl, mt2);
+            mt2 = fmaf(dh, dh, mt2);
+        }
+    PipeMoments t{(double)mt, mt2};
+    t = pipe_step<0>(t, kLane);
+    t = pipe_step<1>(t, 2.f * kLane);
+    t = pipe_step<2>(t, 4.f * kLane);
+    t = pipe_step<3>(t, 8.f * kLane);
+    t = pipe_step<4>(t, 16.f * kLane);
+    t = pipe_step<5>(t, 32.f * kLane);
+    m.m2 = t.m2;
+    return m;
+}
+
+// Stores of a chunk's output, non-temporal and device-scope (write-through):
+// the output lines go on to HBM as they are written instead of waiting in L2
+// for the end-of-kernel write-back.  A 16 MiB output fits in the L2s, and
+// with plain non-temporal stores the write-back of all of it ran after the
+// last workgroup had finished (SD3.5 VAE block 8.59 -> 8.26 us per call).
+// Written as raw buffer stores, whose cache-policy operand takes these bits,
+// over a descriptor that spans exactly the chunk (stores outside a buffer's
+// range are dropped, never performed); the compiler sees them as stores and
+// keeps the wait states a 16-byte store needs before its data registers are
+// reused.
+constexpr int kCpolNtSc1 = 2 | 16;           // nt | sc1
+constexpr int kRawBufferWord3 = 0x00020000;  // 32-bit data format, raw access
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t chunk_buffer(char* base, int64_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(base, 0, (int)bytes, kRawBufferWord3);
+}
+__device__ __forceinline__ void store16_through(__amdgpu_buffer_rsrc_t r, int offset, u32x4 v) {
+    __builtin_amdgcn_raw_buffer_store_b128(v, r, offset, 0, kCpolNtSc1);
+}
+
+// Loads of chunk (ng, part) for virtual thread t (0..255): slot j holds the
+// 16 bytes at element (j * 256 + t) * 8 of the chunk.
+template <int NV>
+__device__ __forceinline__ void pipe_load(const PipeParams& p, int64_t ng, int part, int t, u32x4 (&v)[NV]) {
+    constexpr int64_t CH = (int64_t)kPipeDataWaves * kWave * NV * 8;
+    const char* base = static_cast<const char*>(p.x) + (ng * p.group_elems + part * CH) * 2;
+#pragma unroll
+    for (int j = 0; j < NV; ++j) v[j] = load16<true>(base + ((int64_t)j * 256 + t) * 16);
+}
+
+// Moments of a whole chunk from its four wave partials, in a fixed tree.
+template <int NV>
+__device__ __forceinline__ PipeMoments chunk_moments(const PipeMoments (&w)[kPipeDataWaves]) {
+    constexpr float kWaveN = (float)(NV * 8 * kWave);
+    return merge_equal(merge_equal(w[0], w[1], kWaveN), merge_equal(w[2], w[3], kWaveN), 2.f * kWaveN);
+}
+
+// A part's moments as one published word, never 0 (the value of an empty
+// slot), written with one single-copy-atomic store: the part's mean rounded
+// to fp32 in the low half, M2 in the high half with its sign bit (M2 >= 0)
+// forced on.  M2 keeps full fp32 precision: near y = 0 the output is the
+// difference of (x - mean) * a and -b, so a relative error e of the rstd
+// inside a shows as an absolute error |b| * e there (a 15-bit M2 measured
+// 1e-6 of it).  The mean loses at most half an fp32 unit per part; the
+// group mean is the double average of the P part means.
+__device__ __forceinline__ uint64_t pipe_encode(PipeMoments m) {
+    return (uint64_t)__float_as_uint((float)m.mean) |
+           ((uint64_t)(__float_as_uint(fmaxf(m.m2, 0.f)) | 0x80000000u) << 32);
+}
+__device__ __forceinline__ PipeMoments pipe_decode(uint64_t w) {
+    return PipeMoments{(double)__uint_as_float((uint32_t)w), __uint_as_float((uint32_t)(w >> 32) & 0x7fffffffu)};
+}
+
+// The group's statistics for the exchange wave: every part's published
+// word (lane q polls part q's), merged in
+// part order (P a power of two <= 64).  Without all parts published in time,
+// the wave recomputes every part's moments with the data waves' loads, lane
+// mapping and arithmetic, so the result is bit-identical either way.
+template <class T, int NV>
+__device__ __forceinline__ PipeMoments pipe_gather(const PipeParams& p, int64_t ng) {
+    constexpr float kChunkN = (float)(NV * 8 * kWave * kPipeDataWaves);
+    const int lane = threadIdx.x & (kWave - 1);
+    const int P = p.ex.parts;
+    const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
+    PipeMoments m{0.0, 0.f};
+    bool ok = true;
+    if (lane < P) {
+        uint64_t* at = p.ex.slot + ng * P + lane;
+        uint64_t w = __hip_atomic_load(at, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        while (w == 0) {
+            if (__builtin_amdgcn_s_memrealtime() - t0 > p.ex.wait_ticks) break;
+            w = __hip_atomic_load(at, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+        ok = w != 0;
+        m = pipe_decode(w);
+    }
+    if (!__all(ok)) {
+        for (int q = 0; q < P; ++q) {
+            PipeMoments w[kPipeDataWaves];
+#pragma unroll
+            for (int k = 0; k < kPipeDataWaves; ++k) {
+                u32x4 v[NV];
+                pipe_load<NV>(p, ng, q, k * kWave + lane, v);
+                w[k] = wave_moments<T, NV>(v);
+            }
+            // Through the same encoding a published word takes, so the
+            // statistics match the normal path bit for bit.
+            const PipeMoments c = pipe_decode(pipe_encode(chunk_moments<NV>(w)));
+            if (lane == q) m = c;
+        }
+        if (lane == 0) ex_count_give_up(p.ex);
+    }
+    // Merge over P lanes (P = 2^k): the first k butterfly steps.
+    float n = kChunkN;
+#define KF_STEP(S)                    \
+    if ((2 << S) <= P) {              \
+        m = pipe_step<S>(m, n);       \
+        n *= 2.f;                     \
+    }
+    KF_STEP(0) KF_STEP(1) KF_STEP(2) KF_STEP(3) KF_STEP(4) KF_STEP(5)
+#undef KF_STEP
+    const uint64_t u = __builtin_bit_cast(uint64_t, m.mean);
+    const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)u), hi = __builtin_amdgcn_readfirstlane((uint32_t)(u >> 32));
+    return PipeMoments{__builtin_bit_cast(double, (uint64_t)lo | ((uint64_t)hi << 32)), uniform0(m.m2)};
+}
+
+// The (group, part) chunk workgroup b handles in round r.  With xcd_map
+// (groups per round a multiple of 8) all parts of a group run on XCD
+// ng % 8 (workgroups are handed to the 8 XCDs in turn), so the group's
+// exchange stays inside one XCD; otherwise the plain order.
+__device__ __forceinline__ void pipe_chunk(const PipeParams& p, int b, int r, int64_t* ng, int* part) {
+    const int P = p.ex.parts;
+    if (p.xcd_map) {
+        const int s = b >> 3;
+        *ng = (int64_t)r * p.per_round + (b & 7) + 8 * (s / P);
+        *part = s - (s / P) * P;
+    } else {
+        *ng = (int64_t)r * p.per_round + b / P;
+        *part = b - (b / P) * P;
+    }
+}
+
+template <class T, class A, int NV, int R>
+__global__ __launch_bounds__(kPipeNT) void gn_pipe(PipeParams p) {
+    constexpr int64_t CH = (int64_t)kPipeDataWaves * kWave * NV * 8;
+    __shared__ PipeMoments part_lds[R][kPipeDataWaves];
+    __shared__ float stats_lds[R][NV][2];  // per slot: a = rstd * w[c], c = b[c] - lo * a
+    __shared__ float mean_lds[R];          // hi of the group mean
+    const int wave = threadIdx.x / kWave;
+    const int lane = threadIdx.x & (kWave - 1);
+
+    if (wave < kPipeDataWaves) {
+        u32x4 v[R][NV];
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            int64_t ng;
+            int part;
+            pipe_chunk(p, blockIdx.x, r, &ng, &part);
+            pipe_load<NV>(p, ng < p.groups_total ? ng : p.groups_total - 1, part, threadIdx.x, v[r]);
+        }
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            int64_t ng;
+            int part;
+            pipe_chunk(p, blockIdx.x, r, &ng, &part);
+            const bool live = ng < p.groups_total;
+            if (live) {
+                const PipeMoments m = wave_moments<T, NV>(v[r]);
+                if (lane == 0) part_lds[r][wave] = m;
+            }
+            __syncthreads();  // partials of round r in LDS
+            __syncthreads();  // statistics of round r in LDS
+            if (live) {
+                // y = (x - hi) * a + (b - lo * a): x - hi is exact wherever
+                // the output is near zero (x within a factor 2 of hi).
+                const __amdgpu_buffer_rsrc_t out =
+                    chunk_buffer(static_cast<char*>(p.y) + (ng * p.group_elems + part * CH) * 2, CH * 2);
+                const float mu = mean_lds[r];
+#pragma unroll
+                for (int j = 0; j < NV; ++j) {
+                    const float a = stats_lds[r][j][0], c = stats_lds[r][j][1];
+                    u32x4 o;
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        float lo, hi;
+                        unpack2(T{}, v[r][j][i], lo, hi);
+                        o[i] = pack2(T{}, fmaf(lo - mu, a, c), fmaf(hi - mu, a, c));
+                    }
+                    store16_through(out, (j * 256 + (int)threadIdx.x) * 16, o);
+                }
+            }
+        }
+    } else {
+        // Affine of each round's slot channels (lane j: slot j), loaded
+        // first: nothing waits on them until the statistics are known.
+        const bool hw = p.w != nullptr, hb = p.b != nullptr;
+        const void* ws = hw ? p.w : affine_identity<A>();
+        const void* bs = hb ? p.b : affine_identity<A>();
+        float wv[R], bv[R];
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            int64_t ng;
+            int part;
+            pipe_chunk(p, blockIdx.x, r, &ng, &part);
+            if (ng >= p.groups_total) ng = p.groups_total - 1;
+            const int j = lane < NV ? lane : 0;
+            const int64_t c = (ng % p.groups) * p.cpg + (part * CH + (int64_t)j * 2048) / p.spatial;
+            wv[r] = load1<A>(ws, hw ? c : 0);
+            bv[r] = load1<A>(bs, hb ? c : 1);
+        }
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            int64_t ng;
+            int part;
+            pipe_chunk(p, blockIdx.x, r, &ng, &part);
+            const bool live = ng < p.groups_total;
+            __syncthreads();  // partials of round r in LDS
+            unsigned before = 0;
+            if (live) {
+                PipeMoments w[kPipeDataWaves];
+#pragma unroll
+                for (int k = 0; k < kPipeDataWaves; ++k) w[k] = part_lds[r][k];
+                const PipeMoments mine = chunk_moments<NV>(w);
+                if (lane == 0) ex_publish(p.ex, ng, part, pipe_encode(mine));
+                const PipeMoments g = pipe_gather<T, NV>(p, ng);
+                // Done reading the group's slots: count this workgroup out
+                // now, so the atomic's round trip overlaps the rest.
+                if (lane == 0) before = ex_depart(p.ex, ng);
+                const float rstd = 1.f / sqrtf(g.m2 / (float)p.group_elems + p.eps);
+                const float hi = (float)g.mean, lo = (float)(g.mean - (double)hi);
+                if (lane < NV) {
+                    const float a = rstd * wv[r];
+                    stats_lds[r][lane][0] = a;
+                    stats_lds[r][lane][1] = bv[r] - lo * a;
+                }
+                if (lane == 0) mean_lds[r] = hi;
+            }
+            __syncthreads();  // statistics of round r in LDS
+            if (live && lane == 0) ex_leave(p.ex, ng, before);
+        }
+    }
+}
+
+// --------------------------------------------------------------------------
 // Host side.
 
 // Elements per workgroup chunk for a dtype / vectorisation choice.
@@ -446,19 +822,36 @@ Layout layout(int64_t n, int64_t c, int64_t spatial, int64_t groups, kf_dtype xt
     return l;
 }
 
-// KF355_GN_MODE selects the multi-chunk path: unset or "auto" (fused when
-// resident, else two kernels), "coop" (fused only under a cooperative
-// launch), "two_pass" (always two kernels).  Read once per process.
-constexpr int kModeAuto = 0, kModeCoop = 1, kModeTwoPass = 2;
+// KF355_GN_MODE selects the multi-chunk path: unset or "auto" (gn_pipe where
+// it applies, else fused when resident, else two kernels), "fused" (as auto
+// without gn_pipe), "coop" (fused only under a cooperative launch),
+// "two_pass" (always two kernels).  Read once per process.
+constexpr int kModeAuto = 0, kModeCoop = 1, kModeTwoPass = 2, kModeFused = 3;
 int gn_mode() {
     static const int mode = [] {
         const char* e = std::getenv("KF355_GN_MODE");
         if (!e) return kModeAuto;
         if (!std::strcmp(e, "coop")) return kModeCoop;
         if (!std::strcmp(e, "two_pass")) return kModeTwoPass;
+        if (!std::strcmp(e, "fused")) return kModeFused;
         return kModeAuto;
     }();
     return mode;
+}
+
+// KF355_GN_PARTS (tests only): gn_pipe with exactly this many workgroups per
+// group where a chunk size gives it, including 1 (0 or unset: the default
+// plan).  Read once per process.
+uint32_t gn_parts_override() {
+    static const uint32_t parts = env_u32("KF355_GN_PARTS", 0u);
+    return parts;
+}
+
+// KF355_GN_ROUNDS (tests only): the fewest rounds gn_pipe may use (1 or 2;
+// unset: 1).  Read once per process.
+uint32_t gn_min_rounds() {
+    static const uint32_t rounds = env_u32("KF355_GN_ROUNDS", 1u);
+    return rounds;
 }
 
 // How long (100 MHz ticks of s_memrealtime) a fused workgroup waits for the
@@ -554,8 +947,112 @@ kf_status run(const GroupNormArgs& a, hipStream_t s, const char** variant) {
     return KF_OK;
 }
 
+// gn_pipe for dense NCHW 16-bit tensors, not in place, on 16-byte aligned
+// bases, whose spatial size is a multiple of 2048 (every slot row of a
+// chunk lies inside one channel) and whose groups split into 2 to 64 chunks,
+// a power of two (the gather's lane butterfly).  Chunks of 16384 elements
+// (8 slots per thread), else 32768 (16); one round when the grid of
+// (groups x parts) workgroups is resident, else two.  Returns false, having
+// launched nothing, when the shape is outside this.
+template <class T, class A, int NV, int R>
+const void* pipe_kernel() {
+    return reinterpret_cast<const void*>(gn_pipe<T, A, NV, R>);
+}
+
+template <class T, class A>
+bool run_pipe(const GroupNormArgs& a, hipStream_t s, const char** variant, kf_status* status) {
+    const int mode = gn_mode();
+    if (mode == kModeTwoPass || mode == kModeFused || mode == kModeCoop) return false;
+    if (a.nhwc || a.x == a.y || !vector_ok(a) || a.spatial % 2048 != 0) return false;
+    const int64_t ge = (a.c / a.groups) * a.spatial;
+    const int64_t gt = a.n * a.groups;
+    const int64_t forced = gn_parts_override();
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess) return false;
+    static ResidencyCache cap[4][2];
+    static const int nvs[4] = {8, 16, 4, 2};
+    static const void* kernels[4][2] = {{pipe_kernel<T, A, 8, 1>(), pipe_kernel<T, A, 8, 2>()},
+                                        {pipe_kernel<T, A, 16, 1>(), pipe_kernel<T, A, 16, 2>()},
+                                        {pipe_kernel<T, A, 4, 1>(), pipe_kernel<T, A, 4, 2>()},
+                                        {pipe_kernel<T, A, 2, 1>(), pipe_kernel<T, A, 2, 2>()}};
+    static const char* names[4][2] = {{"gn_pipe_nv8_r1", "gn_pipe_nv8_r2"},
+                                      {"gn_pipe_nv16_r1", "gn_pipe_nv16_r2"},
+                                      {"gn_pipe_nv4_r1", "gn_pipe_nv4_r2"},
+                                      {"gn_pipe_nv2_r1", "gn_pipe_nv2_r2"}};
+    // The default plan tries 16384- then 32768-element chunks; an override
+    // may also use 8192 and 4096.
+    const int tries = forced ? 4 : 2;
+    for (int k = 0; k < tries; ++k) {
+        const int64_t ch = 2048 * (int64_t)nvs[k];
+        if (ge % ch != 0) continue;
+        const int64_t parts = ge / ch;
+        if (forced ? parts != forced : parts < 2) continue;
+        if (parts > 64 || (parts & (parts - 1)) != 0) continue;
+        // The default chunks never need more exchange workspace than
+        // kf_group_norm_workspace_bytes reports; a forced smaller chunk must
+        // fit the caller's workspace, which must then not reach x or y.
+        const size_t ws_need = exchange_layout(gt, parts).total;
+        if (ws_need > a.workspace_bytes) continue;
+        if (forced) {
+            const uintptr_t w0 = (uintptr_t)a.workspace, w1 = w0 + ws_need;
+            const uintptr_t bytes = (uintptr_t)(a.n * a.c * a.spatial * 2);
+            const uintptr_t x0 = (uintptr_t)a.x, y0 = (uintptr_t)a.y;
+            if ((w0 < x0 + bytes && x0 < w1) || (w0 < y0 + bytes && y0 < w1)) continue;
+        }
+        for (int r = gn_min_rounds() >= 2 ? 1 : 0; r < 2; ++r) {
+            const int64_t rounds = r + 1;
+            int64_t per_round = (gt + rounds - 1) / rounds;
+            const bool xcd = gt % 8 == 0;
+            if (xcd) per_round = (per_round + 7) / 8 * 8;
+            if ((gt + per_round - 1) / per_round > rounds) continue;
+            const int64_t grid = per_round * parts;
+            if (grid > INT32_MAX || (int64_t)resident_capacity(cap[k][r], dev, kernels[k][r], kPipeNT) < grid)
+                continue;
+            PipeParams p;
+            p.x = a.x;
+            p.y = a.y;
+            p.w = a.weight;
+            p.b = a.bias;
+            p.ex = gn_exchange(a, parts);
+            p.group_elems = ge;
+            p.spatial = a.spatial;
+            p.cpg = (int32_t)(a.c / a.groups);
+            p.groups = (int32_t)a.groups;
+            p.groups_total = (int32_t)gt;
+            p.per_round = (int32_t)per_round;
+            p.xcd_map = xcd && per_round % 8 == 0 ? 1 : 0;
+            p.eps = a.eps;
+            const dim3 g((unsigned)grid), b(kPipeNT);
+            switch (k * 2 + r) {
+                case 0: hipLaunchKernelGGL((gn_pipe<T, A, 8, 1>), g, b, 0, s, p); break;
+                case 1: hipLaunchKernelGGL((gn_pipe<T, A, 8, 2>), g, b, 0, s, p); break;
+                case 2: hipLaunchKernelGGL((gn_pipe<T, A, 16, 1>), g, b, 0, s, p); break;
+                case 3: hipLaunchKernelGGL((gn_pipe<T, A, 16, 2>), g, b, 0, s, p); break;
+                case 4: hipLaunchKernelGGL((gn_pipe<T, A, 4, 1>), g, b, 0, s, p); break;
+                case 5: hipLaunchKernelGGL((gn_pipe<T, A, 4, 2>), g, b, 0, s, p); break;
+                case 6: hipLaunchKernelGGL((gn_pipe<T, A, 2, 1>), g, b, 0, s, p); break;
+                default: hipLaunchKernelGGL((gn_pipe<T, A, 2, 2>), g, b, 0, s, p); break;
+            }
+            const hipError_t err = hipGetLastError();
+            *variant = names[k][r];
+            if (err != hipSuccess) {
+                set_error("group_norm launch failed: %s", hipGetErrorString(err));
+                *status = KF_ERR_HIP;
+            } else {
+                *status = KF_OK;
+            }
+            return true;
+        }
+    }
+    return false;
+}
+
 template <class T, class A>
 kf_status run_layout(const GroupNormArgs& a, hipStream_t s, const char** variant) {
+    if constexpr (!std::is_same_v<T, F32>) {
+        kf_status st;
+        if (run_pipe<T, A>(a, s, variant, &st)) return st;
+    }
     const bool vec = vector_ok(a);
     if (a.nhwc) return vec ? run<T, A, true, true>(a, s, variant) : run<T, A, false, true>(a, s, variant);
     return vec ? run<T, A, true, false>(a, s, variant) : run<T, A, false, false>(a, s, variant);
@@ -596,8 +1093,9 @@ kf_status group_norm_static_scratch(void** ptr) {
 }
 
 size_t group_norm_workspace_bytes(int64_t n, int64_t c, int64_t spatial, int64_t groups, kf_dtype xt) {
-    // The scalar layout has the smaller chunk, hence more parts: size for it
-    // so one workspace serves either path.
+    // The scalar layout has the smallest chunk gn_fused uses, hence the most
+    // parts, and gn_pipe's default chunks are no smaller: size for it so one
+    // workspace serves every path.
     return layout(n, c, spatial, groups, xt, false).ex.total;
 }
 

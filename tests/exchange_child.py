@@ -8,7 +8,10 @@ variant, the workspace's give-up count (the first word of its status block)
 and the count of non-zero bytes after the status block.
 
 usage: exchange_child.py OUT.npz OP [OP ...]
-OP: group_norm | group_norm_nhwc | group_norm_small | softmax_split"""
+OP: group_norm | group_norm_nhwc | group_norm_small | group_norm_parts | softmax_split
+
+Further environment knobs the tests use: KF355_GN_MODE=fused (GroupNorm
+without gn_pipe) and KF355_GN_PARTS=k (gn_pipe with k workgroups per group)."""
 import os
 import sys
 
@@ -30,6 +33,12 @@ def inputs(op: str) -> dict:
         return {"x": W.randn((2, 96, 32, 32), "bf16", seed=31, mean=-0.2, std=2.0), "groups": 4,
                 "weight": W.randn((96,), "bf16", seed=32, mean=1.0, std=0.1),
                 "bias": W.randn((96,), "bf16", seed=33, std=0.1), "eps": 1e-5}
+    if op == "group_norm_parts":
+        # 4 channels of 64 x 64 per group: 16384 elements, one 16384-element
+        # chunk, two of 8192 or four of 4096.
+        return {"x": W.randn((2, 32, 64, 64), "bf16", seed=41, mean=0.5, std=1.2), "groups": 8,
+                "weight": W.randn((32,), "bf16", seed=42, mean=1.0, std=0.1),
+                "bias": W.randn((32,), "bf16", seed=43, std=0.1), "eps": 1e-6}
     if op == "softmax_split":
         return {"x": W.attn_decode_bf16()["x"]}
     raise SystemExit(f"unknown op {op}")
@@ -60,8 +69,8 @@ def spawn(tmp_path, ops, **env) -> dict:
 
 def main():
     out_path, ops = sys.argv[1], sys.argv[2:]
-    print(f"[child] ops={ops} KF355_GN_WAIT_TICKS={os.environ.get('KF355_GN_WAIT_TICKS')} "
-          f"KF355_SM_WAIT_TICKS={os.environ.get('KF355_SM_WAIT_TICKS')}", flush=True)
+    knobs = ("KF355_GN_WAIT_TICKS", "KF355_SM_WAIT_TICKS", "KF355_GN_MODE", "KF355_GN_PARTS")
+    print(f"[child] ops={ops} " + " ".join(f"{k}={os.environ.get(k)}" for k in knobs), flush=True)
     ws = torch.zeros(1 << 20, dtype=torch.uint8, device="cuda")
     saved = {}
     for i, op in enumerate(ops):

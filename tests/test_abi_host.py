@@ -222,7 +222,8 @@ def test_group_norm_zero_elements_and_workspace_query(lib):
     assert st == OK and n == 0
     st, n = gn_ws(lib, (1, 512, 128, 128), 32)
     # 32 groups x 16 chunks of 16384 elements: the 256-byte status block,
-    # 8-byte (mean, M2) partials, then one 256-byte counter line per group.
+    # one 8-byte published word per chunk, then one 256-byte counter line
+    # per group.
     assert st == OK and n == 256 + 32 * 16 * 8 + 32 * 256
     # 12-channel groups: 3 chunks of 16384 elements per group, partials
     # padded to 256 bytes.

@@ -89,12 +89,42 @@ def test_affine_variants(affine):
 @pytest.mark.parametrize("dt", ["bf16", "f16", "f32"])
 @pytest.mark.parametrize("affine", ["same", "f32", "w", "b", "none"])
 def test_affine_variants_multi_chunk(affine, dt):
-    # 4 chunks per group: the fused kernel with the cross-workgroup exchange,
-    # where an absent weight or bias reads the identity element of the
-    # affine dtype instead of branching.
+    # 4 chunks per group with the cross-workgroup exchange, where an absent
+    # weight or bias reads the identity element of the affine dtype instead
+    # of branching: gn_pipe for 16-bit tensors, the fused kernel for fp32.
     note(f"group_norm multi-chunk affine={affine} {dt}")
     _, variant = run((1, 64, 64, 64), 4, dt, affine=affine)
-    assert variant == "gn_fused_vec", variant
+    assert variant == ("gn_fused_vec" if dt == "f32" else "gn_pipe_nv8_r1"), variant
+
+
+@pytest.mark.parametrize("shape,groups", [
+    ((1, 512, 128, 128), 32),    # the SD3.5 VAE block: 16 parts per group
+    ((1, 64, 128, 128), 8),      # 8 parts per group, 8 groups
+    ((3, 32, 64, 64), 4),        # 12 groups of 2 parts: no per-XCD placement
+    ((1, 32, 512, 512), 32),     # one 256K-element channel per group, 16 parts
+    ((2, 512, 128, 128), 32),    # 64 groups of 16 parts: one round if resident, else two
+], ids=lambda v: str(v))
+@pytest.mark.parametrize("dt", ["bf16", "f16"])
+def test_pipe_plans(shape, groups, dt):
+    note(f"group_norm gn_pipe {shape} G={groups} {dt}")
+    _, variant = run(shape, groups, dt, seed=5)
+    assert variant in ("gn_pipe_nv8_r1", "gn_pipe_nv8_r2"), variant
+
+
+def test_pipe_exact_moments_fallback():
+    # Channels whose mean is large against their spread (mean^2 > 63 var over
+    # a wave's 4096 values) make the raw-sum moments cancel; those waves
+    # recompute them exactly.  Mixed with ordinary channels in one group.
+    note("group_norm gn_pipe exact-moment fallback")
+    x = randn((1, 64, 64, 64), "bf16", seed=9, mean=0.3, std=1.5)
+    x[:, 8:12] = randn((1, 4, 64, 64), "bf16", seed=10, mean=40.0, std=0.25)
+    x[:, 40:48] = randn((1, 8, 64, 64), "bf16", seed=11, mean=-300.0, std=2.0)
+    w = randn((64,), "bf16", seed=12, mean=1.0, std=0.1)
+    b = randn((64,), "bf16", seed=13, std=0.1)
+    y = kf355.kf_group_norm(x.cuda(), 4, w.cuda(), b.cuda(), 1e-6)
+    torch.cuda.synchronize()
+    assert kf355.last_variant() == "gn_pipe_nv8_r1"
+    check(y, oracle.group_norm(x, 4, w, b, 1e-6), "bf16")
 
 
 def test_two_kernel_path_for_grids_that_cannot_be_resident():
@@ -157,10 +187,61 @@ def test_wait_timeout_recompute_is_bitwise_identical(tmp_path):
     y = kf355.kf_group_norm(w["x"].cuda(), 32, w["weight"].cuda(), w["bias"].cuda(), w["eps"])
     torch.cuda.synchronize()
     got = spawn(tmp_path, ["group_norm"], KF355_GN_WAIT_TICKS="0")
-    assert str(got["variant0"]) == "gn_fused_vec"
+    assert str(got["variant0"]) == "gn_pipe_nv8_r1"
     assert int(got["give_ups"]) >= 1
     assert int(got["rest"]) == 0
     assert np.array_equal(got["bits0"], y.view(torch.int16).cpu().numpy())
+
+
+def test_fused_kernel_wait_timeout_recompute_is_bitwise_identical(tmp_path):
+    # The same for the fused kernel gn_pipe replaced on 16-bit NCHW tensors
+    # (still used for fp32, channels last and shapes outside gn_pipe):
+    # KF355_GN_MODE=fused selects it, once with the normal wait and once with
+    # every wait given up at once.
+    note("group_norm fused-kernel forced-timeout recompute")
+    a = spawn(tmp_path, ["group_norm"], KF355_GN_MODE="fused")
+    b = spawn(tmp_path, ["group_norm"], KF355_GN_MODE="fused", KF355_GN_WAIT_TICKS="0")
+    assert str(a["variant0"]) == "gn_fused_vec" and str(b["variant0"]) == "gn_fused_vec"
+    assert int(a["give_ups"]) == 0 and int(b["give_ups"]) >= 1
+    assert int(a["rest"]) == 0 and int(b["rest"]) == 0
+    assert np.array_equal(a["bits0"], b["bits0"])
+    w = W.groupnorm_vae_bf16()
+    ref = oracle.group_norm(w["x"], 32, w["weight"], w["bias"], w["eps"])
+    check(_as_tensor(a["bits0"]), ref, "bf16")
+
+
+@pytest.mark.parametrize("parts,want", [(1, "gn_pipe_nv8_r1"), (2, "gn_pipe_nv4_r1"), (4, "gn_pipe_nv2_r1")])
+def test_forced_parts_per_group_deterministic(tmp_path, parts, want):
+    # KF355_GN_PARTS forces the number of workgroups per group (1, 2 and the
+    # most the smallest chunk gives for this shape): each setting matches the
+    # oracle, two calls give identical bits, no wait gives up and the
+    # workspace is left zero.
+    note(f"group_norm forced parts per group = {parts}")
+    got = spawn(tmp_path, ["group_norm_parts", "group_norm_parts"], KF355_GN_PARTS=str(parts))
+    assert str(got["variant0"]) == want and str(got["variant1"]) == want
+    assert int(got["give_ups"]) == 0 and int(got["rest"]) == 0
+    assert np.array_equal(got["bits0"], got["bits1"])
+    a = inputs("group_norm_parts")
+    ref = oracle.group_norm(a["x"], a["groups"], a["weight"], a["bias"], a["eps"])
+    check(_as_tensor(got["bits0"]), ref, "bf16")
+
+
+@pytest.mark.parametrize("env,want", [
+    ({"KF355_GN_PARTS": "64"}, ("gn_pipe_nv2_r1", "gn_pipe_nv2_r2")),  # 4096-element chunks, the most parts
+    ({"KF355_GN_PARTS": "8"}, ("gn_pipe_nv16_r1",)),                  # 32768-element chunks: two channels each
+    ({"KF355_GN_ROUNDS": "2"}, ("gn_pipe_nv8_r2",)),                  # two rounds of 16 groups
+], ids=["parts64", "parts8", "rounds2"])
+def test_pipe_forced_plans_on_the_vae_block(tmp_path, env, want):
+    # The SD3.5 VAE block under plans the default does not pick: each matches
+    # the oracle, repeats bit for bit, gives up no wait and leaves the
+    # workspace zero.
+    note(f"group_norm gn_pipe forced plan {env}")
+    got = spawn(tmp_path, ["group_norm", "group_norm"], **env)
+    assert str(got["variant0"]) in want, got["variant0"]
+    assert int(got["give_ups"]) == 0 and int(got["rest"]) == 0
+    assert np.array_equal(got["bits0"], got["bits1"])
+    a = inputs("group_norm")
+    check(_as_tensor(got["bits0"]), oracle.group_norm(a["x"], a["groups"], a["weight"], a["bias"], a["eps"]), "bf16")
 
 
 def _oracle_of(op):
