@@ -235,7 +235,7 @@ def copy_calibration(torch, dev, nbytes: int, reps: int = 48, pairs: int = 3) ->
 def floors_row(torch, dev, kf355, w, steps, sets_for):
     """What this box does for the same bytes with no operator arithmetic and
     no exchange: the library's plain read of the pooling input
-    (kf_stream_read, 16 bytes out per 4 KiB in) and its plain copy of the
+    (kf_stream_read, 8 bytes out per 2 KiB in) and its plain copy of the
     GroupNorm and softmax inputs (kf_stream_copy), each over rotating buffers
     like the operator, and a one-wave read (the cost of a launch by itself).
     Floors and operators are both timed as replayed HIP graphs of
@@ -251,13 +251,13 @@ def floors_row(torch, dev, kf355, w, steps, sets_for):
         def floor_fns(src_bytes, reader, n):
             srcs = [torch.empty(src_bytes, dtype=torch.uint8, device=dev) for _ in range(n)]
             if reader:
-                dsts = [torch.empty(-(-src_bytes // 4096) * 16, dtype=torch.uint8, device=dev) for _ in srcs]
+                dsts = [torch.empty(-(-src_bytes // 2048) * 8, dtype=torch.uint8, device=dev) for _ in srcs]
                 return [lambda s=s, d=d: kf355.stream_read(s, d) for s, d in zip(srcs, dsts)]
             dsts = [torch.empty_like(s) for s in srcs]
             return [lambda s=s, d=d: kf355.stream_copy(s, d) for s, d in zip(srcs, dsts)]
 
-        row["launch_us"] = round(time_graph(torch, floor_fns(4096, True, 1), steps, st), 3)
-        row["launch_kind"] = "kf_stream_read of 4 KiB (one wave)"
+        row["launch_us"] = round(time_graph(torch, floor_fns(2048, True, 1), steps, st), 3)
+        row["launch_kind"] = "kf_stream_read of 2 KiB (one wave)"
         cases = (
             ("adaptive_avgpool2d", ap_x, True, "kf_stream_read of its input",
              lambda x: kf355.prepare_adaptive_avgpool2d(x, torch.empty(x.shape[0], x.shape[1], 1, 1, device=dev))),
@@ -515,11 +515,29 @@ def small_softmax_row(torch, dev, kf355, W, steps, warmup, sets_for, outputs):
         us = time_launches(torch, fns, steps, warmup)
         eager_us = time_launches(torch, [lambda x=x: torch.softmax(x, -1) for x in xs], min(steps, 50), warmup)
         outputs[name] = (wl["x"], "f32", fns[0]._keep[1].cpu(), torch.softmax(xs[0], -1).cpu())
+        # Device time without host launch cost: the same calls, torch eager's
+        # and the library's plain copy of the same bytes, as replayed HIP graphs.
+        st = torch.cuda.Stream()
+        st.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(st):
+            gfns = [kf355.prepare_softmax(x, torch.empty_like(x), -1) for x in xs]
+            graph_us = time_graph(torch, gfns, steps, st)
+            eager_graph_us = time_graph(torch, [lambda x=x: torch.softmax(x, -1) for x in xs], steps, st)
+            srcs = [torch.empty(nb // 2, dtype=torch.uint8, device=dev) for _ in xs]
+            dsts = [torch.empty_like(s) for s in srcs]
+            floor_us = time_graph(torch, [lambda s=s, d=d: kf355.stream_copy(s, d) for s, d in zip(srcs, dsts)],
+                                  steps, st)
+            del gfns, srcs, dsts
+        torch.cuda.synchronize()
         gbs = nb / (us * 1e-6) / 1e9
         row[name] = {"workload": f"fp32 {list(src.shape)} softmax over the last dim", "variant": variant,
                      "algorithmic_bytes": nb, "us_per_call": round(us, 3), "gbps": round(gbs, 1),
                      "frac_of_peak": round(gbs / PEAK_HBM_GBS, 4), "torch_eager_us": round(eager_us, 3),
                      "kf355_speedup": round(eager_us / us, 3), "buffer_sets": len(xs),
+                     "graph": {"us_per_call": round(graph_us, 3), "torch_eager_us": round(eager_graph_us, 3),
+                               "floor_us": round(floor_us, 3), "floor_kind": "kf_stream_copy of its input",
+                               "op_over_floor": round(graph_us / floor_us, 3),
+                               "frac_of_peak": round(nb / (graph_us * 1e-6) / 1e9 / PEAK_HBM_GBS, 4)},
                      "input_sha256": W.sha256(wl["x"])}
         if "outliers" in wl:
             row[name]["outliers"] = wl["outliers"]

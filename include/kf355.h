@@ -316,10 +316,11 @@ kf_status kf_max_pool2d_output_size(int64_t h, int64_t w, const int64_t* window,
 
 /*
  * kf_stream_copy -- measurement aid, not an operator: copies `bytes` from src
- * to dst with the library's own streaming kernel (each wave moves 4 KiB of
- * consecutive 16-byte vectors, non-temporal stores), so a benchmark can state
- * what the HBM of this GPU sustains for a plain copy beside the operators'
- * achieved bandwidth.
+ * to dst with the library's own streaming kernel (each wave moves 1 KiB of
+ * consecutive 16-byte vectors for copies of at most 8 MiB, 4 KiB above;
+ * non-temporal loads and stores), so a benchmark can state what the HBM of
+ * this GPU sustains for a plain copy beside the operators' achieved
+ * bandwidth.
  *
  *  src, dst  device pointers, 16-byte aligned, not overlapping; the caller
  *            owns both.
@@ -330,16 +331,18 @@ kf_status kf_stream_copy(const void* src, void* dst, int64_t bytes, void* stream
 
 /*
  * kf_stream_read -- measurement aid, not an operator: reads `bytes` from src
- * with kf_stream_copy's load pattern and writes, for every 4 KiB block of src
- * (the last one possibly shorter), the bitwise XOR of its 16-byte words: the
- * HBM read alone, the floor of an operator that reads much and writes
- * little (such as adaptive_avgpool2d to 1x1).
+ * (each wave 2 KiB of consecutive 16-byte vectors, non-temporal loads) and
+ * writes, for every 2 KiB block of src (the last one possibly shorter), one
+ * 64-bit word of parities: the HBM read alone, the floor of an operator that
+ * reads much and writes little (such as adaptive_avgpool2d to 1x1).
  *
  *  src     device pointer, 16-byte aligned; the caller owns it.
  *  bytes   a multiple of 16 (0 is a no-op), else KF_ERR_BAD_SHAPE.
- *  dst     device pointer, 16-byte aligned, ceil(bytes / 4096) * 16 bytes,
- *          not overlapping src (else KF_ERR_BAD_ARG); word b is the XOR of
- *          src's 16-byte words 256 * b .. 256 * b + 255.
+ *  dst     device pointer, 8-byte aligned, ceil(bytes / 2048) * 8 bytes,
+ *          not overlapping src (else KF_ERR_BAD_ARG); bit L (0..63) of
+ *          64-bit word b is the parity of the number of set bits in src's
+ *          16-byte vectors 128 * b + L and 128 * b + 64 + L (a vector past
+ *          the end counts as zero).
  *  Asynchronous on stream.
  */
 kf_status kf_stream_read(const void* src, int64_t bytes, void* dst, void* stream);

@@ -492,8 +492,8 @@ kf_status kf_stream_read(const void* src, int64_t bytes, void* dst, void* stream
     if (bytes < 0 || bytes % 16) return fail(KF_ERR_BAD_SHAPE, "bytes must be a non-negative multiple of 16");
     if (bytes == 0) return done(KF_OK, "noop");
     if (!src || !dst) return fail(KF_ERR_NULL_POINTER, "src or dst is NULL");
-    if ((uintptr_t)src % 16 || (uintptr_t)dst % 16) return fail(KF_ERR_BAD_ARG, "src and dst must be 16-byte aligned");
-    const int64_t out_bytes = (bytes + 4095) / 4096 * 16;
+    if ((uintptr_t)src % 16 || (uintptr_t)dst % 8) return fail(KF_ERR_BAD_ARG, "src must be 16-byte and dst 8-byte aligned");
+    const int64_t out_bytes = (bytes + 2047) / 2048 * 8;
     if (overlaps(src, bytes, dst, out_bytes)) return fail(KF_ERR_BAD_ARG, "src and dst overlap");
     return done(stream_read_launch(src, bytes, dst, static_cast<hipStream_t>(stream)), "stream_read");
 }

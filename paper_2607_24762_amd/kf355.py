@@ -449,11 +449,12 @@ def stream_copy(src: torch.Tensor, dst: torch.Tensor) -> torch.Tensor:
 
 def stream_read(src: torch.Tensor, dst: torch.Tensor) -> torch.Tensor:
     """Calibration read through kf_stream_read (a measurement aid, no
-    operator): dst receives the XOR of every 4 KiB block of the contiguous
-    GPU tensor src, one 16-byte word per block."""
+    operator): for every 2 KiB block of the contiguous GPU tensor src, dst
+    receives one 64-bit word whose bit L is the parity of the set bits in
+    the block's 16-byte vectors L and 64 + L."""
     _need_cuda(src, dst)
     nbytes = src.numel() * src.element_size()
-    need = -(-nbytes // 4096) * 16
+    need = -(-nbytes // 2048) * 8
     if not (src.is_contiguous() and dst.is_contiguous()) or dst.numel() * dst.element_size() < need:
         raise KfError(2, f"stream_read needs contiguous tensors and {need} bytes of output")
     with _on(src):

@@ -350,6 +350,7 @@ def test_stream_read_rejections(lib):
     assert lib.kf_stream_read(FAKE, -16, FAKE + (1 << 30), None) == SHAPE
     assert lib.kf_stream_read(None, 64, FAKE, None) == NULLP
     assert lib.kf_stream_read(FAKE, 64, None, None) == NULLP
-    assert lib.kf_stream_read(FAKE, 64, FAKE + (1 << 30) + 8, None) == ARG    # misaligned
+    assert lib.kf_stream_read(FAKE, 64, FAKE + (1 << 30) + 4, None) == ARG    # dst not 8-byte aligned
+    assert lib.kf_stream_read(FAKE + 8, 64, FAKE + (1 << 30), None) == ARG    # src not 16-byte aligned
     assert lib.kf_stream_read(FAKE, 8192, FAKE + 4096, None) == ARG           # output inside the input
-    assert lib.kf_stream_read(FAKE, 4096, FAKE + 4080, None) == ARG           # output (16 B) on the last input word
+    assert lib.kf_stream_read(FAKE, 4096, FAKE + 4080, None) == ARG           # output (two 8-byte words) on the input's end
