@@ -145,10 +145,12 @@ kf_status kf_softmax_split_workspace_bytes(kf_dtype x_dtype, kf_dtype y_dtype, i
  *  included) and the masked triangle is not read from memory; masked
  *  outputs are +0.  A row with no visible key (q > k) is NaN, as the masked
  *  softmax gives.  Arguments are as for kf_softmax, with ndim >= 2 and
- *  `scale` any finite value.  Rows longer than 65536 (16-bit) / 32768 (fp32)
- *  elements, rows that are not whole 16-byte vectors longer than 40960 /
- *  36864, and rows longer than 8192 on bases that are not 16-byte aligned
- *  return KF_ERR_UNSUPPORTED_LAYOUT.  y may equal x (in place).
+ *  `scale` any finite value.  Rows of any length up to INT32_MAX keys and
+ *  up to INT32_MAX rows: rows beyond the register-resident kernels (65536
+ *  16-bit / 32768 fp32 elements; 40960 / 36864 when rows are not whole
+ *  16-byte vectors; 8192 on bases that are not 16-byte aligned) are read
+ *  twice, once for the statistics and once for the output.  y may equal x
+ *  (in place).
  */
 kf_status kf_softmax_causal(const void* x, kf_dtype x_dtype, void* y, kf_dtype y_dtype, int32_t ndim,
                             const int64_t* shape, const int64_t* x_strides, const int64_t* y_strides, double scale,

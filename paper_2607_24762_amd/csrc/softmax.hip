@@ -20,6 +20,10 @@
 //             on aligned bases: the aligned 16-byte vectors covering the row,
 //             neighbouring rows' elements masked, the two end vectors
 //             written element by element.
+//   sm_causal / sm_causal_edge / sm_causal_stream  the scaled causal
+//             softmax of eager attention: the resident kernels' layouts,
+//             and for longer rows the two-pass stream, each reading only
+//             the visible prefix of a row.
 //   sm_cols   softmax over a non-innermost axis: one thread per column,
 //             online pass then write pass, coalesced across the inner axis.
 #include <math.h>
@@ -671,6 +675,78 @@ __global__ __launch_bounds__(NT) void sm_stream(const void* __restrict__ x, void
 }
 
 // --------------------------------------------------------------------------
+// sm_causal for rows of any length: one workgroup per row, the online
+// (max, sum) pass of sm_stream over the visible prefix [0, live) only (the
+// masked triangle is not read), then a write pass over the whole row that
+// reads the prefix again.  In-place safe: every element is read and written
+// by the same thread, the write pass after the barrier that ends the first.
+template <class TI, class TO, int NT, bool VECTOR>
+__global__ __launch_bounds__(NT) void sm_causal_stream(const void* __restrict__ x, void* __restrict__ y, int64_t q,
+                                                       int64_t k, float scale) {
+    constexpr int VEC = VECTOR ? TI::vec : 1;
+    constexpr int NW = NT / kWave;
+    constexpr int DEPTH = 4;
+    constexpr int64_t STEP = (int64_t)DEPTH * NT * VEC;
+    __shared__ float red_m[NW], red_s[NW];
+    const int64_t row = blockIdx.x;
+    const int64_t i = row % q;
+    const int64_t live = i + (k - q) + 1 < 0 ? 0 : (i + (k - q) + 1 > k ? k : i + (k - q) + 1);
+    const int64_t base = row * k;
+
+    MS st{-INFINITY, 0.f};
+    for (int64_t e0 = (int64_t)threadIdx.x * VEC; e0 < live; e0 += STEP) {
+        float v[DEPTH * VEC];
+#pragma unroll
+        for (int d = 0; d < DEPTH; ++d) {
+            const int64_t e = e0 + (int64_t)d * NT * VEC;
+            if (e < live) {
+                if constexpr (VECTOR) load_vec<TI>(x, base + e, v + d * VEC);
+                else v[d] = load1<TI>(x, base + e);
+            }
+#pragma unroll
+            for (int ii = 0; ii < VEC; ++ii)
+                v[d * VEC + ii] = (e + ii < live) ? v[d * VEC + ii] * scale : -INFINITY;
+        }
+        st = ms_add<TO, DEPTH * VEC>(st, v);
+    }
+    st = ms_wave(st);
+    const int w = threadIdx.x / kWave;
+    if ((threadIdx.x & (kWave - 1)) == 0) {
+        red_m[w] = st.m;
+        red_s[w] = st.s;
+    }
+    __syncthreads();
+    MS tot{red_m[0], red_s[0]};
+#pragma unroll
+    for (int j = 1; j < NW; ++j) tot = ms_merge(tot, MS{red_m[j], red_s[j]});
+    // No visible key: m = -inf and every output is exp(-inf - -inf) = NaN.
+    const float inv = 1.f / tot.s;
+
+    for (int64_t e0 = (int64_t)threadIdx.x * VEC; e0 < k; e0 += STEP) {
+        float v[DEPTH][VEC];
+#pragma unroll
+        for (int d = 0; d < DEPTH; ++d) {
+            const int64_t e = e0 + (int64_t)d * NT * VEC;
+            if (e < live) {
+                if constexpr (VECTOR) load_vec<TI>(x, base + e, v[d]);
+                else v[d][0] = load1<TI>(x, base + e);
+            }
+        }
+#pragma unroll
+        for (int d = 0; d < DEPTH; ++d) {
+            const int64_t e = e0 + (int64_t)d * NT * VEC;
+            if (e < k) {
+#pragma unroll
+                for (int ii = 0; ii < VEC; ++ii)
+                    v[d][ii] = exp_out<TO>((e + ii < live) ? v[d][ii] * scale : -INFINITY, tot.m) * inv;
+                if constexpr (VECTOR) store_span<TO, VEC>(y, base + e, v[d]);
+                else store1<TO>(y, base + e, v[d][0]);
+            }
+        }
+    }
+}
+
+// --------------------------------------------------------------------------
 // Softmax over a non-innermost axis of [outer, len, inner]: thread per
 // (outer, inner) column; neighbouring threads read neighbouring addresses.
 template <class TI, class TO>
@@ -1205,8 +1281,17 @@ kf_status run_causal(const CausalSoftmaxArgs& a, hipStream_t s, const char** var
     KF_CAUSAL(1024, 8)
 #undef KF_CAUSAL
     if (!done) {
-        set_error("softmax_causal: rows of %lld elements exceed the register-resident kernels", (long long)a.k);
-        return KF_ERR_UNSUPPORTED_LAYOUT;
+        // Beyond the register-resident tables: stream the row twice, with
+        // 16-byte vectors when the rows are whole aligned vectors.
+        if (vec) {
+            hipLaunchKernelGGL((sm_causal_stream<TI, TO, 1024, true>), dim3((unsigned)(a.batch * a.q)), dim3(1024), 0,
+                               s, a.x, a.y, a.q, a.k, a.scale);
+            *variant = "sm_causal_stream_vec";
+        } else {
+            hipLaunchKernelGGL((sm_causal_stream<TI, TO, 1024, false>), dim3((unsigned)(a.batch * a.q)), dim3(1024),
+                               0, s, a.x, a.y, a.q, a.k, a.scale);
+            *variant = "sm_causal_stream_scalar";
+        }
     }
     const hipError_t err = hipGetLastError();
     if (err != hipSuccess) {

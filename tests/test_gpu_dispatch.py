@@ -1,16 +1,19 @@
 """Guarded dispatch on the GPU: with the PyTorch entry points routed through
 a dispatcher, a small network (GroupNorm -> avgpool head, LayerNorm ->
-attention softmax) gives the eager outputs within the dispatch tolerance,
-every variant gets an audit label, the VAE-sized GroupNorm variant is
-measured faster and routed to libkf355, an unsupported layout stays on eager
-with its reason, autograd inputs bypass the dispatcher, and a saved package
-is reused without re-measuring."""
+attention softmax) gives the eager outputs within the dispatch tolerance and
+the oracle's within the parity tolerances, every variant gets an audit
+label, the VAE-sized GroupNorm variant is measured faster and routed to
+libkf355, an unsupported layout stays on eager with its reason, autograd
+inputs bypass the dispatcher, and a saved package is reused without
+re-measuring."""
 import os
 
 import pytest
 import torch
 import torch.nn.functional as F
 
+from compare import assert_close, gpu_bits
+from oracle import oracle
 from paper_2607_24762_amd import dispatch, kf355
 from paper_2607_24762_amd.workloads import randn
 
@@ -37,7 +40,7 @@ def net(x, t, gw, gb):
     q = s.softmax(-1)
     r = F.softmax(s.bfloat16(), dim=-1, dtype=torch.float32)
     m, mi = F.max_pool2d(x, 3, 2, 1, return_indices=True)
-    return h, pooled, u, p, q, r, m, mi
+    return h, pooled, u, p, q, r, m, mi, s
 
 
 def inputs():
@@ -71,6 +74,31 @@ def test_network_matches_eager_and_labels_every_variant(measure):
         assert not r["reason"].startswith(("invalid", "unsupported")), r
         if not measure:
             assert r["backend"] == "kf355" and r["kernel"], r
+
+
+GN_FLOOR = (2.0 ** -19, 2.0 ** -22)
+
+
+def test_routed_outputs_match_the_oracle():
+    """Every op of the network routed to libkf355 (validated, not timed),
+    each output against the oracle on the input that op saw: 1 bf16 ulp for
+    the norms (absolute 2^-22 where |y| < 2^-19) and the pool, max abs 1e-6
+    for the fp32 softmaxes, bit-exact values and indices for max pooling."""
+    x, t, gw, gb = inputs()
+    with dispatch.installed(dispatch.GuardedDispatcher(measure=False)) as d:
+        h, pooled, u, p, q, r, m, mi, s = net(x, t, gw, gb)
+    assert all(e["backend"] == "kf355" for e in d.report()), d.report()
+    torch.cuda.synchronize()
+    assert_close(h, oracle.group_norm(x.cpu(), 8, gw.cpu(), gb.cpu(), 1e-6), "bf16", floor=GN_FLOOR)
+    assert_close(pooled, oracle.adaptive_avg_pool2d(h.cpu(), (1, 1)), "bf16")
+    assert_close(u, oracle.layer_norm(t.cpu(), 1, None, None, 1e-6), "bf16", floor=GN_FLOOR)
+    s_cpu = s.cpu()
+    for y in (p, q):
+        assert_close(y, oracle.softmax(s_cpu, -1), "f32")
+    assert_close(r, oracle.softmax(s_cpu.bfloat16(), -1), "f32")
+    ref, ref_idx = oracle.max_pool2d(x.cpu(), 3, 2, 1)
+    assert (gpu_bits(m) == oracle.round_bits(ref, "bf16")).all()
+    assert (mi.cpu().numpy() == ref_idx).all()
 
 
 def test_vae_group_norm_is_routed_to_kf355():

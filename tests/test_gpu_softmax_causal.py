@@ -63,12 +63,13 @@ def test_attention_workload_matches_oracle_and_unfused_path():
                                 (300, 4096), (64, 8192), (2, 16384), (1, 65536)])
 def test_lengths_and_dtypes(pair, qk):
     q, k = qk
-    if pair[0] == "f32" and k > 32768:
-        pytest.skip("fp32 rows above 32768 are outside the register-resident table")
     note(f"softmax_causal {pair} q={q} k={k}")
     x = randn((2, q, k), pair[0], seed=q + k, std=3.0)
     _, variant = run(x, 0.125, pair[1])
-    assert variant.startswith("sm_causal_"), variant
+    # fp32 rows above 32768 keys leave the register-resident table for the
+    # two-pass stream.
+    expect = "sm_causal_stream_vec" if pair[0] == "f32" and k > 32768 else "sm_causal_"
+    assert variant.startswith(expect), variant
 
 
 @pytest.mark.parametrize("scale", [1.0, 0.0625, 0.37, -0.5])
@@ -99,12 +100,13 @@ def test_rows_that_are_not_whole_vectors(pair, qk):
     covering each row (q < k puts the visible boundary mid-row; two batches
     so rows share end vectors across the batch boundary too)."""
     q, k = qk
-    if pair[0] == "f32" and k > 36864:
-        pytest.skip("fp32 rows that are not whole vectors above 36864 are outside the table")
     note(f"softmax_causal masked-vector rows {pair} q={q} k={k}")
     x = randn((2, q, k), pair[0], seed=q * k, std=3.0)
     _, variant = run(x, 0.37, pair[1])
-    assert variant.startswith("sm_causal_edge"), variant
+    # fp32 rows above 36864 keys leave the masked-vector table for the
+    # element-wise two-pass stream.
+    expect = "sm_causal_stream_scalar" if pair[0] == "f32" and k > 36864 else "sm_causal_edge"
+    assert variant.startswith(expect), variant
 
 
 def test_rows_that_are_not_whole_vectors_ignore_the_masked_triangle_in_place():
@@ -122,13 +124,40 @@ def test_rows_that_are_not_whole_vectors_ignore_the_masked_triangle_in_place():
     assert_close(b, oracle.softmax_causal(x, 0.25), "bf16")
 
 
-@pytest.mark.parametrize("dt,k", [("bf16", 40961), ("f32", 36865)])
-def test_rows_beyond_the_masked_vector_table_are_refused(dt, k):
-    note(f"softmax_causal {dt} k={k} refused")
-    x = torch.zeros((1, k), dtype=TORCH[dt], device="cuda")
-    with pytest.raises(kf355.KfError) as e:
-        kf355.kf_softmax_causal(x, 1.0)
-    assert e.value.status == 5  # KF_ERR_UNSUPPORTED_LAYOUT
+@pytest.mark.parametrize("dt,qk,variant", [
+    ("bf16", (3, 40961), "sm_causal_stream_scalar"),   # just past the masked-vector table
+    ("f32", (3, 36865), "sm_causal_stream_scalar"),
+    ("bf16", (2, 65544), "sm_causal_stream_vec"),      # whole vectors past the resident table
+    ("f16", (3, 131072), "sm_causal_stream_vec"),
+    ("f32", (5, 100000), "sm_causal_stream_vec"),      # several STEP-sized passes, ragged last one
+    ("f32", (4, 3), "sm_causal_scalar_nt64_nv1"),      # (a resident case beside them)
+])
+def test_rows_beyond_the_tables_stream(dt, qk, variant):
+    """Rows too long for the register-resident and masked-vector kernels are
+    read twice by sm_causal_stream: against the oracle, with q > 1 so the
+    visible prefix ends mid-row and the masked tail is never read."""
+    q, k = qk
+    note(f"softmax_causal stream {dt} q={q} k={k}")
+    x = randn((2, q, k), dt, seed=k % 1009, std=3.0)
+    _, got = run(x, 0.37, dt)
+    assert got == variant, got
+
+
+def test_stream_in_place_ignores_the_masked_triangle():
+    note("softmax_causal stream: NaN in the masked triangle, in place, unaligned base")
+    q, k = 3, 40001
+    big = randn((q * k + 1,), "bf16", seed=21, std=2.0)
+    x = big[1:].view(1, q, k)
+    poisoned = big.clone()
+    poisoned[1:].view(1, q, k)[0, torch.ones(q, k, dtype=torch.bool).triu(k - q + 1)] = float("nan")
+    a = kf355.kf_softmax_causal(big.cuda()[1:].view(1, q, k), 0.25)
+    assert kf355.last_variant() == "sm_causal_stream_scalar"
+    pd = poisoned.cuda()[1:].view(1, q, k)            # 2 bytes past an aligned base
+    b = kf355.kf_softmax_causal(pd, 0.25, out=pd)
+    torch.cuda.synchronize()
+    assert kf355.last_variant() == "sm_causal_stream_scalar"
+    assert torch.equal(a.view(torch.int16), b.view(torch.int16))
+    assert_close(b, oracle.softmax_causal(x, 0.25), "bf16")
 
 
 def test_masked_triangle_is_never_used():
