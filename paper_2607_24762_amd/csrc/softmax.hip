@@ -27,6 +27,9 @@
 //   sm_cols   softmax over a non-innermost axis: one thread per column,
 //             online pass then write pass, coalesced across the inner axis.
 #include <math.h>
+#include <stdio.h>
+
+#include <array>
 
 #include <type_traits>
 
@@ -369,11 +372,12 @@ __global__ __launch_bounds__(NT) void sm_block_edge(const void* __restrict__ x, 
 
 // --------------------------------------------------------------------------
 // Rows of `len` elements that are not whole 16-byte vectors, R rows per
-// workgroup (R * len <= kSpanFloats, R a multiple of what makes r0 * len a
+// workgroup (R * len <= TILE floats, R a multiple of what makes r0 * len a
 // whole number of input and output vectors, so every span starts aligned).
-constexpr int kSpanFloats = 4096;  // 16 KiB of fp32 staging per workgroup
+constexpr int kSpanFloats = 4096;      // staging that decides whether spans apply: 16 KiB of fp32
+constexpr int kSpanFloatsWide = 8192;  // the 16-row plan's staging, up to 32 KiB
 
-template <class TI, class TO, int LPR, int NPL>
+template <class TI, class TO, int LPR, int NPL, int TILE>
 __global__ __launch_bounds__(256) void sm_span(const void* __restrict__ x, void* __restrict__ y, int64_t rows,
                                                int32_t len, int32_t R) {
     extern __shared__ float4 tile4[];  // R * len floats
@@ -386,7 +390,7 @@ __global__ __launch_bounds__(256) void sm_span(const void* __restrict__ x, void*
     // Stage: whole input vectors first (all loads before the LDS stores),
     // then the span's last partial vector element by element.
     constexpr int VI = TI::vec;
-    constexpr int NL = (kSpanFloats + 256 * VI - 1) / (256 * VI);
+    constexpr int NL = (TILE + 256 * VI - 1) / (256 * VI);
     const int32_t whole_in = span - span % VI;
     float v[NL][VI];
 #pragma unroll
@@ -406,11 +410,12 @@ __global__ __launch_bounds__(256) void sm_span(const void* __restrict__ x, void*
     for (int32_t e = whole_in + threadIdx.x; e < span; e += 256) tile[e] = load1<TI>(x, base + e);
     __syncthreads();
 
-    // Row q: elements lr, lr + LPR, ... (at most NPL of them) of the LPR
-    // lanes that own it, read from LDS into registers in one batch (slots
-    // past the row are -inf), reduced and normalised there, written back
-    // once.  Lanes of rows past nr take part in the reductions and write
-    // nothing.
+    // Row q: elements lr, lr + LPR, ... (at most NPL of them; the planner
+    // picks NPL at most 3 above ceil(len / LPR), since every slot costs an
+    // LDS read and an exponential) of the LPR lanes that own it, read from
+    // LDS into registers in one batch (slots past the row are -inf), reduced
+    // and normalised there, written back once.  Lanes of rows past nr take
+    // part in the reductions and write nothing.
     const int q = threadIdx.x / LPR, lr = threadIdx.x % LPR;
     const bool row_ok = q < nr;
     float* row = tile + (row_ok ? q : 0) * len;
@@ -1078,8 +1083,17 @@ Choice pick_edge(int64_t len) {
 }
 
 // sm_span for rows of `len` elements that are not whole vectors, when both
-// bases are 16-byte aligned and at least the aligning row count fits the
-// staging tile.  Returns false (nothing launched) otherwise.
+// bases are 16-byte aligned and at least the aligning row count fits
+// kSpanFloats.  Returns false (nothing launched) otherwise.
+//
+// Rows of 129-512 elements: 16 rows per workgroup, 16 lanes per row (four
+// rows per wave, the shape of the vector-row kernel on [16384, 256]), in up
+// to 32 KiB of LDS.  Measured on [16384, L] fp32 against the plan below:
+// L = 257 7.03 -> 6.43 us, 258 6.96 -> 6.30, 385 10.34 -> 8.52,
+// 511 13.92 -> 10.57, 129 4.67 -> 4.22, 150 4.87 -> 4.47.  Other lengths:
+// as many rows as fit 4096 floats, fewer while a lane would hold more than
+// 16 of a row's elements (on [16384, 257] fp32: 12 rows and 17 per lane
+// 8.27 us, 8 rows and 9 per lane 7.23 us, 4 rows and 5 per lane 8.88 us).
 template <class TI, class TO>
 bool run_span(const SoftmaxArgs& a, hipStream_t s, const char** variant) {
     if ((uintptr_t)a.x % 16 || (uintptr_t)a.y % 16 || a.len < 1 || a.len > kSpanFloats) return false;
@@ -1090,20 +1104,25 @@ bool run_span(const SoftmaxArgs& a, hipStream_t s, const char** variant) {
     };
     const int64_t ra = rows_for(TI::vec), rb = rows_for(TO::vec);
     const int64_t align = ra > rb ? ra : rb;  // both are powers of two, so the larger is their lcm
-    // Rows per workgroup: as many as fit the staging tile, fewer while a lane
-    // would hold more than 16 of a row's elements (on [16384, 257] fp32:
-    // 12 rows and 17 per lane 8.27 us, 8 rows and 9 per lane 7.23 us, 4 rows
-    // and 5 per lane 8.88 us).
-    int64_t R = kSpanFloats / a.len;
-    R = R > 256 ? 256 : R;
-    R -= R % align;
-    if (R < align) return false;
+    if (align * a.len > kSpanFloats) return false;
     auto lanes_for = [](int64_t rows) {  // the largest power of two <= 256 / rows, at most 64
         int l = 1;
         while (l < 64 && 2 * l * rows <= 256) l *= 2;
         return l;
     };
-    while (R - align >= align && (a.len + lanes_for(R) - 1) / lanes_for(R) > 16) R -= align;
+    int64_t R;
+    if (a.len > 128 && a.len <= 512) {
+        R = 16;  // align is at most 8, so 16 rows always start aligned
+    } else {
+        R = kSpanFloats / a.len;
+        R = R > 256 ? 256 : R;
+        R -= R % align;
+        while (R - align >= align && (a.len + lanes_for(R) - 1) / lanes_for(R) > 16) R -= align;
+    }
+    const int lpr = lanes_for(R);
+    const int64_t npl = (a.len + lpr - 1) / lpr;
+    if (npl > 32) return false;
+    const bool wide = R * a.len > kSpanFloats;  // only on the 16-row plan, where lpr = 16
     const int64_t blocks = (a.outer + R - 1) / R;
     if (blocks > INT32_MAX) return false;
     const size_t lds = (size_t)(R * a.len) * sizeof(float);
@@ -1111,38 +1130,49 @@ bool run_span(const SoftmaxArgs& a, hipStream_t s, const char** variant) {
         hipLaunchKernelGGL(kernel, dim3((unsigned)blocks), dim3(256), lds, s, a.x, a.y, a.outer, (int32_t)a.len,
                            (int32_t)R);
     };
-    // Lanes per row, then elements per lane: R * len <= 4096 and LPR > 128 / R
-    // give at most 32.
-    const int lpr = lanes_for(R);
-    const int64_t per_lane = (a.len + lpr - 1) / lpr;
-    const int npl = per_lane <= 8 ? 8 : per_lane <= 16 ? 16 : 32;
-    if (per_lane > 32) return false;
+    // Slots per lane: 8, 16 or 32, and on the 16-lane rows the next multiple
+    // of 4 (on [16384, 257] fp32, 17 elements per lane: 20 slots 6.49 us,
+    // exactly 17 slots 6.43).
+    int nplt = npl <= 8 ? 8 : npl <= 16 ? 16 : 32;
+    if (lpr == 16) nplt = npl <= 8 ? 8 : (int)((npl + 3) / 4 * 4);
     auto with_npl = [&](auto lpr_tag) {
         constexpr int L = decltype(lpr_tag)::value;
-        if (npl == 8) go(sm_span<TI, TO, L, 8>);
-        else if (npl == 16) go(sm_span<TI, TO, L, 16>);
-        else go(sm_span<TI, TO, L, 32>);
+        if (nplt == 8) go(sm_span<TI, TO, L, 8, kSpanFloats>);
+        else if (nplt == 16) go(sm_span<TI, TO, L, 16, kSpanFloats>);
+        else go(sm_span<TI, TO, L, 32, kSpanFloats>);
     };
     switch (lpr) {
         case 64: with_npl(std::integral_constant<int, 64>{}); break;
         case 32: with_npl(std::integral_constant<int, 32>{}); break;
-        case 16: with_npl(std::integral_constant<int, 16>{}); break;
+        case 16:
+            switch (nplt) {
+                case 8: go(sm_span<TI, TO, 16, 8, kSpanFloats>); break;
+                case 12: go(sm_span<TI, TO, 16, 12, kSpanFloats>); break;
+                case 16: go(sm_span<TI, TO, 16, 16, kSpanFloats>); break;
+                case 20: go(sm_span<TI, TO, 16, 20, kSpanFloatsWide>); break;
+                case 24: go(sm_span<TI, TO, 16, 24, kSpanFloatsWide>); break;
+                case 28: go(sm_span<TI, TO, 16, 28, kSpanFloatsWide>); break;
+                default:
+                    if (wide) go(sm_span<TI, TO, 16, 32, kSpanFloatsWide>);
+                    else go(sm_span<TI, TO, 16, 32, kSpanFloats>);
+                    break;
+            }
+            break;
         case 8: with_npl(std::integral_constant<int, 8>{}); break;
         case 4: with_npl(std::integral_constant<int, 4>{}); break;
         case 2: with_npl(std::integral_constant<int, 2>{}); break;
         default: with_npl(std::integral_constant<int, 1>{}); break;
     }
-    static const char* names[7][3] = {
-        {"sm_span_lpr1_npl8", "sm_span_lpr1_npl16", "sm_span_lpr1_npl32"},
-        {"sm_span_lpr2_npl8", "sm_span_lpr2_npl16", "sm_span_lpr2_npl32"},
-        {"sm_span_lpr4_npl8", "sm_span_lpr4_npl16", "sm_span_lpr4_npl32"},
-        {"sm_span_lpr8_npl8", "sm_span_lpr8_npl16", "sm_span_lpr8_npl32"},
-        {"sm_span_lpr16_npl8", "sm_span_lpr16_npl16", "sm_span_lpr16_npl32"},
-        {"sm_span_lpr32_npl8", "sm_span_lpr32_npl16", "sm_span_lpr32_npl32"},
-        {"sm_span_lpr64_npl8", "sm_span_lpr64_npl16", "sm_span_lpr64_npl32"}};
+    // "sm_span_lpr<L>_npl<slots>" for L = 1..64 and slots = 1..32.
+    static const auto names = [] {
+        std::array<std::array<std::array<char, 24>, 33>, 7> t{};
+        for (int li = 0; li < 7; ++li)
+            for (int n = 1; n <= 32; ++n) snprintf(t[li][n].data(), t[li][n].size(), "sm_span_lpr%d_npl%d", 1 << li, n);
+        return t;
+    }();
     int li = 0;
     while ((1 << li) < lpr) ++li;
-    *variant = names[li][npl == 8 ? 0 : npl == 16 ? 1 : 2];
+    *variant = names[li][nplt].data();
     return true;
 }
 
