@@ -32,6 +32,7 @@
 #include <array>
 
 #include <type_traits>
+#include <utility>
 
 #include "kf_device.hpp"
 #include "kf_exchange.hpp"
@@ -1082,6 +1083,14 @@ Choice pick_edge(int64_t len) {
     return Choice{nullptr, nullptr};
 }
 
+// Launches sm_span with 16 lanes per row and exactly `slots` (9..32) slots
+// per lane; more than 16 slots only arise from rows of more than 256
+// elements, whose 16 rows need the wide tile.
+template <class TI, class TO, class Go, int... I>
+void span_lanes16(int slots, Go& go, std::integer_sequence<int, I...>) {
+    ((slots == I + 9 ? (go(sm_span<TI, TO, 16, I + 9, (I + 9 <= 16 ? kSpanFloats : kSpanFloatsWide)>), 0) : 0), ...);
+}
+
 // sm_span for rows of `len` elements that are not whole vectors, when both
 // bases are 16-byte aligned and at least the aligning row count fits
 // kSpanFloats.  Returns false (nothing launched) otherwise.
@@ -1122,7 +1131,6 @@ bool run_span(const SoftmaxArgs& a, hipStream_t s, const char** variant) {
     const int lpr = lanes_for(R);
     const int64_t npl = (a.len + lpr - 1) / lpr;
     if (npl > 32) return false;
-    const bool wide = R * a.len > kSpanFloats;  // only on the 16-row plan, where lpr = 16
     const int64_t blocks = (a.outer + R - 1) / R;
     if (blocks > INT32_MAX) return false;
     const size_t lds = (size_t)(R * a.len) * sizeof(float);
@@ -1130,11 +1138,11 @@ bool run_span(const SoftmaxArgs& a, hipStream_t s, const char** variant) {
         hipLaunchKernelGGL(kernel, dim3((unsigned)blocks), dim3(256), lds, s, a.x, a.y, a.outer, (int32_t)a.len,
                            (int32_t)R);
     };
-    // Slots per lane: 8, 16 or 32, and on the 16-lane rows the next multiple
-    // of 4 (on [16384, 257] fp32, 17 elements per lane: 20 slots 6.49 us,
-    // exactly 17 slots 6.43).
+    // Slots per lane: 8, 16 or 32, and on the 16-lane rows exactly
+    // ceil(len / 16) from 9 up (on [16384, 257] fp32, 17 elements per lane:
+    // 17 slots 6.35 us, 20 slots 6.49).
     int nplt = npl <= 8 ? 8 : npl <= 16 ? 16 : 32;
-    if (lpr == 16) nplt = npl <= 8 ? 8 : (int)((npl + 3) / 4 * 4);
+    if (lpr == 16 && npl > 8) nplt = (int)npl;
     auto with_npl = [&](auto lpr_tag) {
         constexpr int L = decltype(lpr_tag)::value;
         if (nplt == 8) go(sm_span<TI, TO, L, 8, kSpanFloats>);
@@ -1145,18 +1153,8 @@ bool run_span(const SoftmaxArgs& a, hipStream_t s, const char** variant) {
         case 64: with_npl(std::integral_constant<int, 64>{}); break;
         case 32: with_npl(std::integral_constant<int, 32>{}); break;
         case 16:
-            switch (nplt) {
-                case 8: go(sm_span<TI, TO, 16, 8, kSpanFloats>); break;
-                case 12: go(sm_span<TI, TO, 16, 12, kSpanFloats>); break;
-                case 16: go(sm_span<TI, TO, 16, 16, kSpanFloats>); break;
-                case 20: go(sm_span<TI, TO, 16, 20, kSpanFloatsWide>); break;
-                case 24: go(sm_span<TI, TO, 16, 24, kSpanFloatsWide>); break;
-                case 28: go(sm_span<TI, TO, 16, 28, kSpanFloatsWide>); break;
-                default:
-                    if (wide) go(sm_span<TI, TO, 16, 32, kSpanFloatsWide>);
-                    else go(sm_span<TI, TO, 16, 32, kSpanFloats>);
-                    break;
-            }
+            if (nplt == 8) go(sm_span<TI, TO, 16, 8, kSpanFloats>);
+            else span_lanes16<TI, TO>(nplt, go, std::make_integer_sequence<int, 24>{});
             break;
         case 8: with_npl(std::integral_constant<int, 8>{}); break;
         case 4: with_npl(std::integral_constant<int, 4>{}); break;

@@ -131,8 +131,8 @@ def span_rows(length, pair):
 @pytest.mark.parametrize("length", [1, 3, 5, 127, 129, 257, 385, 511, 513, 1023, 1025, 4095])
 def test_ragged_rows_take_staged_spans(pair, length):
     """Rows of 129-512 elements take the 16-row plan (16 lanes per row,
-    ceil(L / 16) elements per lane in slots rounded up to a multiple of 4,
-    up to 32 KiB of staging); the rest as many rows as fit 4096 floats."""
+    ceil(L / 16) elements per lane, up to 32 KiB of staging); the rest as
+    many rows as fit 4096 floats."""
     rows = 1000                                   # not a multiple of any span's rows: a partial last workgroup
     note(f"softmax staged spans {pair} len={length}")
     x = randn((rows, length), pair[0], seed=length + 7, std=3.0)
@@ -140,7 +140,7 @@ def test_ragged_rows_take_staged_spans(pair, length):
     assert variant.startswith("sm_span") == (span_rows(length, pair) > 0), variant
     if variant.startswith("sm_span") and 128 < length <= 512:
         per_lane = -(-length // 16)
-        assert variant == f"sm_span_lpr16_npl{8 if per_lane <= 8 else -(-per_lane // 4) * 4}", variant
+        assert variant == f"sm_span_lpr16_npl{max(per_lane, 8)}", variant
 
 
 # Rows that are not whole 16-byte vectors, too long for staged spans: the
