@@ -11,6 +11,13 @@
 // contiguous bytes either way.  Each group is cut into `parts` chunks of
 // CH = 256 threads * NV * VEC elements and one workgroup owns one chunk.
 //
+//   gn_pipe   (one launch, one HBM read + one write; dense NCHW 16-bit
+//             tensors whose spatial size is a multiple of 2048)  Four data
+//             waves hold the chunk as raw 16-bit pairs and fold its moments
+//             with v_dot2; a fifth wave, which has no loads of the tensor
+//             outstanding, does the whole exchange (publish, poll, merge,
+//             affine, departure), so its polls never wait behind chunk
+//             loads.  Described at the kernel below.
 //   gn_fused  (one launch, one HBM read + one write)  Each workgroup keeps its
 //             chunk in registers, computes its (count, mean, M2) moments,
 //             publishes them as one 64-bit word in its workspace slot, polls
