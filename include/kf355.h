@@ -221,7 +221,8 @@ kf_status kf_group_norm_workspace_bytes(kf_dtype x_dtype, int32_t ndim, const in
  *  array's device address is looked up on the first call on each device.
  *  Shapes whose kf_group_norm_workspace_bytes exceeds the array return
  *  KF_ERR_WORKSPACE before anything is enqueued (e.g. [1, 512, 128, 128] with
- *  32 groups needs 12544 bytes; up to about 2700 groups of 16 chunks fit).
+ *  32 groups needs 24832 bytes, sized for its channels-last form; up to
+ *  about 2700 groups of 16 chunks fit, about 1360 of 64).
  *  All calls on one GPU share that GPU's array: calls that may overlap in
  *  time on one GPU (streams not ordered by events, or other threads) race
  *  and give wrong results; calls in stream order are safe.  A failed lookup

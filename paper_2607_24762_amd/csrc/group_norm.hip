@@ -794,6 +794,336 @@ __global__ __launch_bounds__(kPipeNT) void gn_pipe(PipeParams p) {
 }
 
 // --------------------------------------------------------------------------
+// gn_pipe_cl: gn_pipe for dense channels-last 16-bit tensors [n, hw, c]
+// with c a multiple of 64 and cpg in {8, 16, 32, 64}.  A tile is 64 adjacent
+// channels (one 128-byte line per pixel, Q = 64 / cpg whole groups) of 256
+// consecutive pixels of one sample; a workgroup owns one tile, so every
+// line it reads or writes is a whole line of its own, and a group splits
+// into hw / 256 parts (a power of two, at most 64).  Lane l of a data wave
+// holds, in slot j, the 16 bytes of tile channels 8 * (l % 8) .. + 7 at
+// pixel j * 32 + wave * 8 + l / 8: each load reads eight whole lines, the
+// eight lanes of one line consecutive (with the lanes of a line 8 apart
+// instead, the same access pattern as a plain copy took 8.1 against 7.6 us
+// on 16 MiB).  A group's lanes are a block of cpg / 8 lanes in each of the
+// eight 8-lane rows, so its moments reduce over the block (xor 1, 2, 4) and
+// then over the rows (xor 8 by ds_swizzle, 16 and 32 by permlane swaps).
+// Workgroups are numbered tile-column-major: the first 64-channel column's
+// parts go out first, so its groups finish and store while later columns
+// still load (with each column's parts on one XCD, all columns ran side by
+// side and none could store before the last loads: 14.6 against 12.6 us on
+// the SD3.5 VAE block).  The exchange wave publishes, gathers and merges
+// the tile's Q groups together (lane q polls part q of each).  Otherwise as
+// gn_pipe: raw 16-bit pairs in registers, v_dot2 sums, double means,
+// bit-identical recompute when a wait gives up, write-through stores.
+constexpr int kClNV = 8;                                // slots per lane
+constexpr int kClPixels = kPipeDataWaves * 8 * kClNV;  // pixels per tile: 256
+
+struct PipeClParams {
+    const void* x;
+    void* y;
+    const void* w;
+    const void* b;
+    Exchange ex;          // one unit per (sample, group), ex.parts tiles each
+    int64_t hw;           // pixels per sample
+    int32_t c;            // channels, a multiple of 64
+    int32_t groups;       // G
+    int32_t tiles_total;  // n * c / 64
+    float eps;
+};
+
+// Partner of a float across lanes X apart (X a power of two): xor 1 and 2
+// are quad permutations; 4 is the half-row mirror, a butterfly partner only
+// after the xor-1 and xor-2 steps (as every use here is); 8 is a ds_swizzle
+// bitmask xor; 16 and 32 the permlane swaps.
+template <int X>
+__device__ __forceinline__ float xor_partner(float v) {
+    if constexpr (X == 1) return partner<0>(v);
+    else if constexpr (X == 2) return partner<1>(v);
+    else if constexpr (X == 4) return partner<2>(v);
+    else if constexpr (X == 8)
+        return __builtin_bit_cast(float, __builtin_amdgcn_ds_swizzle(__builtin_bit_cast(int, v), 0x201F));
+    else if constexpr (X == 16) return partner<4>(v);
+    else return partner<5>(v);
+}
+template <int X>
+__device__ __forceinline__ double xor_partner_f64(double v) {
+    const uint64_t u = __builtin_bit_cast(uint64_t, v);
+    const float lo = xor_partner<X>(__uint_as_float((uint32_t)u));
+    const float hi = xor_partner<X>(__uint_as_float((uint32_t)(u >> 32)));
+    return __builtin_bit_cast(double, (uint64_t)__float_as_uint(lo) | ((uint64_t)__float_as_uint(hi) << 32));
+}
+template <int X>
+__device__ __forceinline__ PipeMoments xor_step(PipeMoments m, float n) {
+    const PipeMoments o{xor_partner_f64<X>(m.mean), xor_partner<X>(m.m2)};
+    const bool lower = (__lane_id() & X) == 0;
+    return merge_equal(lower ? m : o, lower ? o : m, n);
+}
+
+// The lane distances a group's lanes are reduced over, in order: its block
+// of CPG / 8 lanes, then the eight rows.
+template <int CPG, class F>
+__device__ __forceinline__ void cl_steps(F&& step) {
+    if constexpr (CPG >= 16) step(std::integral_constant<int, 1>{});
+    if constexpr (CPG >= 32) step(std::integral_constant<int, 2>{});
+    if constexpr (CPG >= 64) step(std::integral_constant<int, 4>{});
+    step(std::integral_constant<int, 8>{});
+    step(std::integral_constant<int, 16>{});
+    step(std::integral_constant<int, 32>{});
+}
+
+// Moments of each group's values in one wave (lane l holds kClNV 16-byte
+// words of its group's values); every lane gets its group's moments.
+template <class T, int CPG>
+__device__ __forceinline__ PipeMoments lanes_moments(const u32x4 (&v)[kClNV]) {
+#pragma clang fp contract(off)
+    constexpr float kLane = (float)(kClNV * 8);
+    constexpr double kGroupN = (double)kLane * CPG;  // CPG lanes per group
+    float s1a = 0.f, s1b = 0.f, s2a = 0.f, s2b = 0.f;
+#pragma unroll
+    for (int j = 0; j < kClNV; ++j) {
+#pragma unroll
+        for (int i = 0; i < 4; i += 2) {
+            s1a = dot2(T{}, v[j][i], ones2(T{}), s1a);
+            s2a = dot2(T{}, v[j][i], v[j][i], s2a);
+            s1b = dot2(T{}, v[j][i + 1], ones2(T{}), s1b);
+            s2b = dot2(T{}, v[j][i + 1], v[j][i + 1], s2b);
+        }
+    }
+    const float lane_s1 = s1a + s1b;
+    double s1 = (double)lane_s1;
+    float s2 = s2a + s2b;
+    cl_steps<CPG>([&](auto X) {
+        s1 += xor_partner_f64<decltype(X)::value>(s1);
+        s2 += xor_partner<decltype(X)::value>(s2);
+    });
+    PipeMoments m;
+    m.mean = s1 * (1.0 / kGroupN);
+    m.m2 = s2 - (float)(s1 * m.mean);
+    const bool fast = m.m2 * 64.f >= s2;
+    if (__builtin_expect(__all(fast), 1)) return m;
+    // Exact M2 for the groups that need it, as in wave_moments (computed by
+    // the whole wave, whose exchanges need every lane).
+    const float mt = lane_s1 * (1.f / kLane);
+    float mt2 = 0.f;
+#pragma unroll
+    for (int j = 0; j < kClNV; ++j)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            float lo, hi;
+            unpack2(T{}, v[j][i], lo, hi);
+            const float dl = lo - mt, dh = hi - mt;
+            mt2 = fmaf(dl, dl, mt2);
+            mt2 = fmaf(dh, dh, mt2);
+        }
+    PipeMoments t{(double)mt, mt2};
+    float n = kLane;
+    cl_steps<CPG>([&](auto X) {
+        t = xor_step<decltype(X)::value>(t, n);
+        n *= 2.f;
+    });
+    if (!fast) m.m2 = t.m2;
+    return m;
+}
+
+// The (tile, part) that workgroup b handles: tile-column-major.
+__device__ __forceinline__ void cl_tile(const PipeClParams& p, int b, int64_t* tile, int* part) {
+    const int P = p.ex.parts;
+    *tile = b / P;
+    *part = b - (b / P) * P;
+}
+
+// Element index of the first element of part `part` of tile `tile`.
+__device__ __forceinline__ int64_t cl_first(const PipeClParams& p, int64_t tile, int part) {
+    const int cols = p.c / 64;
+    const int64_t n = tile / cols;
+    const int col = (int)(tile - n * cols);
+    return (n * p.hw + (int64_t)part * kClPixels) * p.c + col * 64;
+}
+
+// Loads of a tile part for virtual thread t (0..255).
+__device__ __forceinline__ void cl_load(const PipeClParams& p, int64_t first, int t, u32x4 (&v)[kClNV]) {
+    const char* base = static_cast<const char*>(p.x) + first * 2;
+    const int wave = t / kWave, lane = t & (kWave - 1);
+#pragma unroll
+    for (int j = 0; j < kClNV; ++j) {
+        const int64_t px = j * 32 + wave * 8 + (lane >> 3);
+        v[j] = load16<true>(base + (px * p.c + (lane & 7) * 8) * 2);
+    }
+}
+
+// A tile part's moments of group k (0..Q-1) from the four waves' partials.
+template <int CPG>
+__device__ __forceinline__ PipeMoments cl_part_moments(const PipeMoments (&w)[kPipeDataWaves]) {
+    constexpr float kWaveN = (float)(CPG * kClNV * 8);
+    return merge_equal(merge_equal(w[0], w[1], kWaveN), merge_equal(w[2], w[3], kWaveN), 2.f * kWaveN);
+}
+
+template <class T, class A, int CPG>
+__global__ __launch_bounds__(kPipeNT) void gn_pipe_cl(PipeClParams p) {
+    constexpr int Q = 64 / CPG;  // groups per tile
+    __shared__ PipeMoments part_lds[kPipeDataWaves][Q];
+    __shared__ float gstat[Q][3];  // per group: hi and lo of the mean, rstd
+    const int wave = threadIdx.x / kWave;
+    const int lane = threadIdx.x & (kWave - 1);
+    int64_t tile;
+    int part;
+    cl_tile(p, blockIdx.x, &tile, &part);
+    const int64_t first = cl_first(p, tile, part);
+    const int cols = p.c / 64;
+    const int64_t n = tile / cols;
+    const int col = (int)(tile - n * cols);
+
+    if (wave < kPipeDataWaves) {
+        u32x4 v[kClNV];
+        cl_load(p, first, threadIdx.x, v);
+        // The affine of this lane's eight channels, after the tile's loads
+        // (nothing waits on it until the statistics are known).
+        const bool hw = p.w != nullptr, hb = p.b != nullptr;
+        const void* ws = hw ? p.w : affine_identity<A>();
+        const void* bs = hb ? p.b : affine_identity<A>();
+        const int64_t ch = (int64_t)col * 64 + (lane & 7) * 8;
+        float wv[8], bv[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            wv[i] = load1<A>(ws, hw ? ch + i : 0);
+            bv[i] = load1<A>(bs, hb ? ch + i : 1);
+        }
+        constexpr int B = CPG / 8;  // lanes of a group in each 8-lane row
+        const PipeMoments m = lanes_moments<T, CPG>(v);
+        if (lane < 8 && (lane % B) == 0) part_lds[wave][lane / B] = m;
+        __syncthreads();  // partials in LDS
+        __syncthreads();  // statistics in LDS
+        const int k = (lane & 7) / B;
+        const float mu = gstat[k][0], lo = gstat[k][1], rstd = gstat[k][2];
+        float a[8], c[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            a[i] = rstd * wv[i];
+            c[i] = bv[i] - lo * a[i];
+        }
+        const int64_t span = ((int64_t)(kClPixels - 1) * p.c + 64) * 2;
+        const __amdgpu_buffer_rsrc_t out = chunk_buffer(static_cast<char*>(p.y) + first * 2, span);
+#pragma unroll
+        for (int j = 0; j < kClNV; ++j) {
+            const int64_t px = j * 32 + wave * 8 + (lane >> 3);
+            u32x4 o;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                float x0, x1;
+                unpack2(T{}, v[j][i], x0, x1);
+                o[i] = pack2(T{}, fmaf(x0 - mu, a[2 * i], c[2 * i]), fmaf(x1 - mu, a[2 * i + 1], c[2 * i + 1]));
+            }
+            store16_through(out, (int)((px * p.c + (lane & 7) * 8) * 2), o);
+        }
+    } else {
+        const int64_t ng0 = n * p.groups + (int64_t)col * Q;  // the tile's first group
+        const int P = p.ex.parts;
+        __syncthreads();  // partials in LDS
+        if (lane < Q) {
+            PipeMoments w[kPipeDataWaves];
+#pragma unroll
+            for (int k = 0; k < kPipeDataWaves; ++k) w[k] = part_lds[k][lane];
+            ex_publish(p.ex, ng0 + lane, part, pipe_encode(cl_part_moments<CPG>(w)));
+        }
+        // Lane q polls part q of every group of the tile, all Q words per
+        // pass.
+        uint64_t word[Q];
+#pragma unroll
+        for (int k = 0; k < Q; ++k) word[k] = 0;
+        bool ok = true;
+        if (lane < P) {
+            const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
+            for (;;) {
+                bool all = true;
+#pragma unroll
+                for (int k = 0; k < Q; ++k) {
+                    word[k] = __hip_atomic_load(p.ex.slot + (ng0 + k) * P + lane, __ATOMIC_RELAXED,
+                                                __HIP_MEMORY_SCOPE_AGENT);
+                    all = all && word[k] != 0;
+                }
+                if (all) break;
+                if (__builtin_amdgcn_s_memrealtime() - t0 > p.ex.wait_ticks) {
+                    ok = false;
+                    break;
+                }
+            }
+        }
+        PipeMoments m[Q];
+#pragma unroll
+        for (int k = 0; k < Q; ++k) m[k] = pipe_decode(word[k]);
+        if (!__all(ok)) {
+            // Recompute every part of the tile column with the data waves'
+            // loads, lane mapping and arithmetic, through the published
+            // encoding, so the statistics match the normal path bit for bit.
+            const int64_t first0 = cl_first(p, tile, 0);
+            for (int q = 0; q < P; ++q) {
+                PipeMoments w[kPipeDataWaves][Q];
+#pragma unroll
+                for (int kk = 0; kk < kPipeDataWaves; ++kk) {
+                    u32x4 v[kClNV];
+                    cl_load(p, first0 + (int64_t)q * kClPixels * p.c, kk * kWave + lane, v);
+                    const PipeMoments wm = lanes_moments<T, CPG>(v);
+                    const uint64_t mb = __builtin_bit_cast(uint64_t, wm.mean);
+#pragma unroll
+                    for (int k = 0; k < Q; ++k) {
+                        const int src = k * (CPG / 8);  // the group's lane in row 0
+                        const uint32_t lo = __builtin_amdgcn_readlane((uint32_t)mb, src);
+                        const uint32_t hi = __builtin_amdgcn_readlane((uint32_t)(mb >> 32), src);
+                        w[kk][k].mean = __builtin_bit_cast(double, (uint64_t)lo | ((uint64_t)hi << 32));
+                        w[kk][k].m2 = __builtin_bit_cast(
+                            float, __builtin_amdgcn_readlane(__builtin_bit_cast(uint32_t, wm.m2), src));
+                    }
+                }
+#pragma unroll
+                for (int k = 0; k < Q; ++k) {
+                    PipeMoments wk[kPipeDataWaves];
+#pragma unroll
+                    for (int kk = 0; kk < kPipeDataWaves; ++kk) wk[kk] = w[kk][k];
+                    const PipeMoments cq = pipe_decode(pipe_encode(cl_part_moments<CPG>(wk)));
+                    if (lane == q) m[k] = cq;
+                }
+            }
+            if (lane == 0) ex_count_give_up(p.ex);
+        }
+        // Merge each group over P lanes (P = 2^k): the first k butterfly
+        // steps, in part order.
+        float nn = (float)(kPipeDataWaves * CPG * kClNV * 8);
+#define KF_STEP(S)                                                   \
+    if ((2 << S) <= P) {                                             \
+        _Pragma("unroll") for (int k = 0; k < Q; ++k) m[k] = pipe_step<S>(m[k], nn); \
+        nn *= 2.f;                                                   \
+    }
+        KF_STEP(0) KF_STEP(1) KF_STEP(2) KF_STEP(3) KF_STEP(4) KF_STEP(5)
+#undef KF_STEP
+        // Lane 0's merge (lanes past P merged empty slots).
+#pragma unroll
+        for (int k = 0; k < Q; ++k) {
+            const uint64_t u = __builtin_bit_cast(uint64_t, m[k].mean);
+            const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)u);
+            const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(u >> 32));
+            m[k] = PipeMoments{__builtin_bit_cast(double, (uint64_t)lo | ((uint64_t)hi << 32)), uniform0(m[k].m2)};
+        }
+        // Done reading the slots: count this workgroup out of every group
+        // of the tile now, so the atomics' round trips overlap the rest.
+        unsigned before = 0;
+        if (lane < Q) before = ex_depart(p.ex, ng0 + lane);
+        const float group_n = (float)(p.hw * CPG);
+#pragma unroll
+        for (int k = 0; k < Q; ++k) {
+            if (lane == k) {
+                const float rstd = 1.f / sqrtf(m[k].m2 / group_n + p.eps);
+                const float hi = (float)m[k].mean, lo = (float)(m[k].mean - (double)hi);
+                gstat[k][0] = hi;
+                gstat[k][1] = lo;
+                gstat[k][2] = rstd;
+            }
+        }
+        __syncthreads();  // statistics in LDS
+        if (lane < Q) ex_leave(p.ex, ng0 + lane, before);
+    }
+}
+
+// --------------------------------------------------------------------------
 // Host side.
 
 // Elements per workgroup chunk for a dtype / vectorisation choice.
@@ -1054,11 +1384,84 @@ bool run_pipe(const GroupNormArgs& a, hipStream_t s, const char** variant, kf_st
     return false;
 }
 
+// Parts per group of gn_pipe_cl for a channels-last shape (the tile columns
+// split each sample's pixels into hw / 256 parts), or 0 where it does not
+// apply by shape: c a multiple of 64, cpg in {8, 16, 32, 64}, hw a multiple
+// of 256 giving 2 to 64 parts, a power of two (the gather's butterfly).
+int64_t cl_parts(int64_t c, int64_t spatial, int64_t groups) {
+    const int64_t cpg = c / groups;
+    if (c % 64 != 0 || (cpg != 8 && cpg != 16 && cpg != 32 && cpg != 64)) return 0;
+    if (spatial % kClPixels != 0) return 0;
+    const int64_t parts = spatial / kClPixels;
+    if (parts < 2 || parts > 64 || (parts & (parts - 1)) != 0) return 0;
+    return parts;
+}
+
+// gn_pipe_cl for dense channels-last 16-bit tensors, not in place, on
+// 16-byte aligned bases, whose shape cl_parts admits and whose grid of
+// (n * c / 64) * parts workgroups is resident.  Returns false, having
+// launched nothing, otherwise.
+template <class T, class A, int CPG>
+const void* cl_kernel() {
+    return reinterpret_cast<const void*>(gn_pipe_cl<T, A, CPG>);
+}
+
+template <class T, class A>
+bool run_pipe_cl(const GroupNormArgs& a, hipStream_t s, const char** variant, kf_status* status) {
+    const int mode = gn_mode();
+    if (mode == kModeTwoPass || mode == kModeFused || mode == kModeCoop) return false;
+    if (!a.nhwc || a.x == a.y || !vector_ok(a) || gn_parts_override()) return false;
+    const int64_t parts = cl_parts(a.c, a.spatial, a.groups);
+    if (!parts) return false;
+    const int64_t gt = a.n * a.groups;
+    if (exchange_layout(gt, parts).total > a.workspace_bytes) return false;
+    const int64_t tiles = a.n * (a.c / 64);
+    const int64_t grid = tiles * parts;
+    if (grid > INT32_MAX || a.n * a.spatial > INT32_MAX) return false;
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess) return false;
+    const int cpg = (int)(a.c / a.groups);
+    const int ci = cpg == 8 ? 0 : cpg == 16 ? 1 : cpg == 32 ? 2 : 3;
+    static ResidencyCache cap[4];
+    static const void* kernels[4] = {cl_kernel<T, A, 8>(), cl_kernel<T, A, 16>(), cl_kernel<T, A, 32>(),
+                                     cl_kernel<T, A, 64>()};
+    static const char* names[4] = {"gn_pipe_cl_cpg8", "gn_pipe_cl_cpg16", "gn_pipe_cl_cpg32", "gn_pipe_cl_cpg64"};
+    if ((int64_t)resident_capacity(cap[ci], dev, kernels[ci], kPipeNT) < grid) return false;
+    PipeClParams p;
+    p.x = a.x;
+    p.y = a.y;
+    p.w = a.weight;
+    p.b = a.bias;
+    p.ex = gn_exchange(a, parts);
+    p.hw = a.spatial;
+    p.c = (int32_t)a.c;
+    p.groups = (int32_t)a.groups;
+    p.tiles_total = (int32_t)tiles;
+    p.eps = a.eps;
+    const dim3 g((unsigned)grid), b(kPipeNT);
+    switch (ci) {
+        case 0: hipLaunchKernelGGL((gn_pipe_cl<T, A, 8>), g, b, 0, s, p); break;
+        case 1: hipLaunchKernelGGL((gn_pipe_cl<T, A, 16>), g, b, 0, s, p); break;
+        case 2: hipLaunchKernelGGL((gn_pipe_cl<T, A, 32>), g, b, 0, s, p); break;
+        default: hipLaunchKernelGGL((gn_pipe_cl<T, A, 64>), g, b, 0, s, p); break;
+    }
+    const hipError_t err = hipGetLastError();
+    *variant = names[ci];
+    if (err != hipSuccess) {
+        set_error("group_norm launch failed: %s", hipGetErrorString(err));
+        *status = KF_ERR_HIP;
+    } else {
+        *status = KF_OK;
+    }
+    return true;
+}
+
 template <class T, class A>
 kf_status run_layout(const GroupNormArgs& a, hipStream_t s, const char** variant) {
     if constexpr (!std::is_same_v<T, F32>) {
         kf_status st;
         if (run_pipe<T, A>(a, s, variant, &st)) return st;
+        if (run_pipe_cl<T, A>(a, s, variant, &st)) return st;
     }
     const bool vec = vector_ok(a);
     if (a.nhwc) return vec ? run<T, A, true, true>(a, s, variant) : run<T, A, false, true>(a, s, variant);
@@ -1101,9 +1504,13 @@ kf_status group_norm_static_scratch(void** ptr) {
 
 size_t group_norm_workspace_bytes(int64_t n, int64_t c, int64_t spatial, int64_t groups, kf_dtype xt) {
     // The scalar layout has the smallest chunk gn_fused uses, hence the most
-    // parts, and gn_pipe's default chunks are no smaller: size for it so one
-    // workspace serves every path.
-    return layout(n, c, spatial, groups, xt, false).ex.total;
+    // parts, and gn_pipe's default chunks are no smaller; gn_pipe_cl may split
+    // a group into more parts (channels-last 16-bit tensors; the query does
+    // not see the layout, so it covers both).  One workspace serves every path.
+    const size_t fused = layout(n, c, spatial, groups, xt, false).ex.total;
+    const int64_t cl = xt == KF_FLOAT32 ? 0 : cl_parts(c, spatial, groups);
+    const size_t tiles = cl ? exchange_layout(n * groups, cl).total : 0;
+    return fused > tiles ? fused : tiles;
 }
 
 kf_status group_norm_launch(const GroupNormArgs& a, hipStream_t s, const char** variant) {

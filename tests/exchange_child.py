@@ -8,7 +8,8 @@ variant, the workspace's give-up count (the first word of its status block)
 and the count of non-zero bytes after the status block.
 
 usage: exchange_child.py OUT.npz OP [OP ...]
-OP: group_norm | group_norm_nhwc | group_norm_small | group_norm_parts | softmax_split
+OP: group_norm | group_norm_nhwc | group_norm_small | group_norm_parts | group_norm_tiles_small |
+    softmax_split
 
 Further environment knobs the tests use: KF355_GN_MODE=fused (GroupNorm
 without gn_pipe) and KF355_GN_PARTS=k (gn_pipe with k workgroups per group)."""
@@ -39,6 +40,12 @@ def inputs(op: str) -> dict:
         return {"x": W.randn((2, 32, 64, 64), "bf16", seed=41, mean=0.5, std=1.2), "groups": 8,
                 "weight": W.randn((32,), "bf16", seed=42, mean=1.0, std=0.1),
                 "bias": W.randn((32,), "bf16", seed=43, std=0.1), "eps": 1e-6}
+    if op == "group_norm_tiles_small":
+        # Channels last, 64-channel tiles: 192 channels, 64 per group, 1024
+        # pixels: 4 parts per group.
+        return {"x": W.randn((1, 192, 32, 32), "bf16", seed=54, mean=-0.4, std=1.1), "groups": 3,
+                "weight": W.randn((192,), "bf16", seed=55, mean=1.0, std=0.1),
+                "bias": W.randn((192,), "bf16", seed=56, std=0.1), "eps": 1e-6}
     if op == "softmax_split":
         return {"x": W.attn_decode_bf16()["x"]}
     raise SystemExit(f"unknown op {op}")
@@ -49,7 +56,7 @@ def run(op: str, ws: torch.Tensor) -> torch.Tensor:
     x = a["x"].cuda()
     if op == "softmax_split":
         return kf355.kf_softmax_split(x, -1, out_dtype=torch.float32, workspace=ws)
-    if op == "group_norm_nhwc":
+    if op in ("group_norm_nhwc", "group_norm_tiles_small"):
         x = x.contiguous(memory_format=torch.channels_last)
     return kf355.kf_group_norm(x, a["groups"], a["weight"].cuda(), a["bias"].cuda(), a["eps"], workspace=ws)
 

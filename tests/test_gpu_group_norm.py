@@ -325,11 +325,65 @@ CHANNELS_LAST = [
 def test_channels_last(shape, groups, dt):
     note(f"group_norm channels last {shape} G={groups} {dt}")
     y, variant = run(shape, groups, dt, channels_last=True)
-    assert variant.startswith("gn_nhwc_"), variant
     assert y.is_contiguous(memory_format=torch.channels_last)
-    vec = 4 if dt == "f32" else 8
     cpg = shape[1] // groups
+    if dt != "f32" and cl_parts(shape, groups):
+        assert variant == f"gn_pipe_cl_cpg{cpg}", variant
+        return
+    assert variant.startswith("gn_nhwc_"), variant
+    vec = 4 if dt == "f32" else 8
     assert ("_vec" in variant) == (cpg % vec == 0 and (256 * vec) % cpg == 0), variant
+
+
+def cl_parts(shape, groups):
+    """Parts per group of the channels-last tile kernel (16-bit tensors):
+    tiles of 64 channels x 256 pixels, c a multiple of 64, 8 to 64 channels
+    per group, 2 to 64 parts (a power of two); 0 where it does not apply."""
+    c, hw = shape[1], int(np.prod(shape[2:]))
+    cpg = c // groups
+    if c % 64 or cpg not in (8, 16, 32, 64) or hw % 256:
+        return 0
+    parts = hw // 256
+    return parts if 2 <= parts <= 64 and parts & (parts - 1) == 0 else 0
+
+
+CL_TILES = [
+    ((1, 512, 128, 128), 32),    # the SD3.5 VAE block: 16 channels per group, 64 parts, 8 tile columns
+    ((2, 128, 16, 32), 4),       # 32 channels per group, 2 parts, two samples
+    ((3, 256, 32, 64), 16),      # 16 channels per group, 8 parts, 12 tile columns
+    ((1, 256, 64, 64), 32),      # 8 channels per group, 16 parts
+    ((2, 512, 32, 32), 8),       # 64 channels per group, 4 parts, 16 tile columns
+    ((1, 128, 128, 128), 4),     # 32 channels per group, 64 parts
+    ((1, 512, 64, 128), 64),     # 8 channels per group, 64 groups, 32 parts
+    ((2, 64, 32, 32), 8),        # 64 channels: 8 per group, 4 parts, one tile column per sample
+    ((1, 192, 64, 64), 3),       # 64 channels per group, 16 parts, 3 tile columns (not a multiple of 8)
+    ((1, 1024, 32, 32), 32),     # 32 channels per group, 4 parts, 16 tile columns (two per XCD)
+    ((2, 384, 16, 32), 12),      # 32 channels per group, 2 parts, 12 tile columns
+    ((1, 640, 32, 32), 80),      # 8 channels per group, 4 parts, 10 tile columns
+    ((1, 64, 128, 128), 4),      # 16 channels per group, 64 parts, one tile column
+]
+
+
+@pytest.mark.parametrize("dt", ["bf16", "f16"])
+@pytest.mark.parametrize("affine", ["same", "f32", "none"])
+@pytest.mark.parametrize("shape,groups", CL_TILES, ids=lambda v: str(v))
+def test_channels_last_tiles(shape, groups, affine, dt):
+    """The channels-last tile kernel at every group width, 2 to 64 parts
+    and 1 to 16 tile columns, against the oracle; two calls give identical
+    bits."""
+    assert cl_parts(shape, groups)
+    note(f"group_norm channels last tiles {shape} G={groups} affine={affine} {dt}")
+    y, variant = run(shape, groups, dt, affine=affine, channels_last=True, seed=len(shape) + groups)
+    assert variant == f"gn_pipe_cl_cpg{shape[1] // groups}", variant
+    y2, _ = run(shape, groups, dt, affine=affine, channels_last=True, seed=len(shape) + groups)
+    assert torch.equal(y.view(torch.int16), y2.view(torch.int16))
+
+
+@pytest.mark.parametrize("shape,groups", [((1, 256, 32, 64), 16), ((1, 192, 32, 32), 3)], ids=["cpg16", "cpg64"])
+def test_channels_last_large_mean(shape, groups):
+    # A mean large against the spread takes the exact M2 path of the moments.
+    note(f"group_norm channels last {shape}, mean 40 std 0.05")
+    run(shape, groups, "bf16", channels_last=True, mean=40.0, std=0.05)
 
 
 @pytest.mark.parametrize("affine", ["none", "w", "b", "f32"])
@@ -356,13 +410,22 @@ def test_channels_last_matches_nchw_statistics():
     check(b, ref, "bf16")
 
 
-def test_channels_last_gave_up_waiting_recomputes_bit_identically(tmp_path):
-    note("group_norm channels last forced recompute (child process)")
-    w = W.groupnorm_vae_bf16()
-    x = w["x"].cuda().contiguous(memory_format=torch.channels_last)
-    y = kf355.kf_group_norm(x, 32, w["weight"].cuda(), w["bias"].cuda(), w["eps"])
+@pytest.mark.parametrize("op,variant", [("group_norm_nhwc", "gn_pipe_cl_cpg16"),
+                                        ("group_norm_tiles_small", "gn_pipe_cl_cpg64")])
+def test_channels_last_gave_up_waiting_recomputes_bit_identically(tmp_path, op, variant):
+    # With no wait at all every workgroup recomputes the parts it lacks
+    # from the tensor; the output must not change by a bit and the exchange
+    # must be left zero.
+    note(f"group_norm channels last forced recompute {op} (child process)")
+    a = inputs(op)
+    x = a["x"].cuda().contiguous(memory_format=torch.channels_last)
+    y = kf355.kf_group_norm(x, a["groups"], a["weight"].cuda(), a["bias"].cuda(), a["eps"])
     torch.cuda.synchronize()
-    got = spawn(tmp_path, ["group_norm_nhwc"], KF355_GN_WAIT_TICKS="0")
-    assert str(got["variant0"]) == "gn_nhwc_fused_vec"
+    assert kf355.last_variant() == variant
+    got = spawn(tmp_path, [op, op], KF355_GN_WAIT_TICKS="0")
+    assert str(got["variant0"]) == variant and str(got["variant1"]) == variant
     assert int(got["give_ups"]) >= 1 and int(got["rest"]) == 0
-    assert np.array_equal(got["bits0"], y.contiguous().view(torch.int16).cpu().numpy())
+    bits = y.contiguous().view(torch.int16).cpu().numpy()
+    assert np.array_equal(got["bits0"], bits) and np.array_equal(got["bits1"], bits)
+    ref = oracle.group_norm(a["x"], a["groups"], a["weight"], a["bias"], a["eps"])
+    check(y, ref, "bf16")
