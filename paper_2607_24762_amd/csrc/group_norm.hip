@@ -464,7 +464,6 @@ struct PipeParams {
     int32_t groups;              // G
     int32_t groups_total;        // n * G
     int32_t per_round;           // groups per round
-    int32_t xcd_map;             // 1: all parts of a group on one XCD (per_round % 8 == 0)
     float eps;
 };
 
@@ -676,20 +675,15 @@ __device__ __forceinline__ PipeMoments pipe_gather(const PipeParams& p, int64_t 
     return PipeMoments{__builtin_bit_cast(double, (uint64_t)lo | ((uint64_t)hi << 32)), uniform0(m.m2)};
 }
 
-// The (group, part) chunk workgroup b handles in round r.  With xcd_map
-// (groups per round a multiple of 8) all parts of a group run on XCD
-// ng % 8 (workgroups are handed to the 8 XCDs in turn), so the group's
-// exchange stays inside one XCD; otherwise the plain order.
+// The (group, part) chunk workgroup b handles in round r: group-major, a
+// group's parts on consecutive workgroups (so spread over the XCDs, which
+// take workgroups in turn), the earliest groups dispatched first.  Placing
+// all parts of a group on one XCD measured 8.41 against 8.29 us on the
+// SD3.5 VAE block.
 __device__ __forceinline__ void pipe_chunk(const PipeParams& p, int b, int r, int64_t* ng, int* part) {
     const int P = p.ex.parts;
-    if (p.xcd_map) {
-        const int s = b >> 3;
-        *ng = (int64_t)r * p.per_round + (b & 7) + 8 * (s / P);
-        *part = s - (s / P) * P;
-    } else {
-        *ng = (int64_t)r * p.per_round + b / P;
-        *part = b - (b / P) * P;
-    }
+    *ng = (int64_t)r * p.per_round + b / P;
+    *part = b - (b / P) * P;
 }
 
 template <class T, class A, int NV, int R>
@@ -1338,10 +1332,7 @@ bool run_pipe(const GroupNormArgs& a, hipStream_t s, const char** variant, kf_st
         }
         for (int r = gn_min_rounds() >= 2 ? 1 : 0; r < 2; ++r) {
             const int64_t rounds = r + 1;
-            int64_t per_round = (gt + rounds - 1) / rounds;
-            const bool xcd = gt % 8 == 0;
-            if (xcd) per_round = (per_round + 7) / 8 * 8;
-            if ((gt + per_round - 1) / per_round > rounds) continue;
+            const int64_t per_round = (gt + rounds - 1) / rounds;
             const int64_t grid = per_round * parts;
             if (grid > INT32_MAX || (int64_t)resident_capacity(cap[k][r], dev, kernels[k][r], kPipeNT) < grid)
                 continue;
@@ -1357,7 +1348,6 @@ bool run_pipe(const GroupNormArgs& a, hipStream_t s, const char** variant, kf_st
             p.groups = (int32_t)a.groups;
             p.groups_total = (int32_t)gt;
             p.per_round = (int32_t)per_round;
-            p.xcd_map = xcd && per_round % 8 == 0 ? 1 : 0;
             p.eps = a.eps;
             const dim3 g((unsigned)grid), b(kPipeNT);
             switch (k * 2 + r) {
