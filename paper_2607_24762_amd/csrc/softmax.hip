@@ -376,7 +376,6 @@ __global__ __launch_bounds__(NT) void sm_block_edge(const void* __restrict__ x, 
 // workgroup (R * len <= TILE floats, R a multiple of what makes r0 * len a
 // whole number of input and output vectors, so every span starts aligned).
 constexpr int kSpanFloats = 4096;      // staging that decides whether spans apply: 16 KiB of fp32
-constexpr int kSpanFloatsWide = 8192;  // the 16-row plan's staging, up to 32 KiB
 
 template <class TI, class TO, int LPR, int NPL, int TILE>
 __global__ __launch_bounds__(256) void sm_span(const void* __restrict__ x, void* __restrict__ y, int64_t rows,
@@ -1084,11 +1083,15 @@ Choice pick_edge(int64_t len) {
 }
 
 // Launches sm_span with 16 lanes per row and exactly `slots` (9..32) slots
-// per lane; more than 16 slots only arise from rows of more than 256
-// elements, whose 16 rows need the wide tile.
+// per lane.  More than 16 slots only arise from rows of more than 256
+// elements, whose 16 rows need a wider tile: at most 16 * 16 * slots floats,
+// rounded up to whole 1024-float load rounds (so no load slot is issued that
+// no element can fill: 5120 floats for 17 slots, where the full 8192 cost
+// 1.2% on [16384, 257] fp32).
+constexpr int span16_tile(int slots) { return slots <= 16 ? kSpanFloats : (slots + 3) / 4 * 1024; }
 template <class TI, class TO, class Go, int... I>
 void span_lanes16(int slots, Go& go, std::integer_sequence<int, I...>) {
-    ((slots == I + 9 ? (go(sm_span<TI, TO, 16, I + 9, (I + 9 <= 16 ? kSpanFloats : kSpanFloatsWide)>), 0) : 0), ...);
+    ((slots == I + 9 ? (go(sm_span<TI, TO, 16, I + 9, span16_tile(I + 9)>), 0) : 0), ...);
 }
 
 // sm_span for rows of `len` elements that are not whole vectors, when both
@@ -1098,7 +1101,7 @@ void span_lanes16(int slots, Go& go, std::integer_sequence<int, I...>) {
 // Rows of 129-512 elements: 16 rows per workgroup, 16 lanes per row (four
 // rows per wave, the shape of the vector-row kernel on [16384, 256]), in up
 // to 32 KiB of LDS.  Measured on [16384, L] fp32 against the plan below:
-// L = 257 7.03 -> 6.43 us, 258 6.96 -> 6.30, 385 10.34 -> 8.52,
+// L = 257 7.03 -> 6.33 us, 258 6.96 -> 6.30, 385 10.34 -> 8.52,
 // 511 13.92 -> 10.57, 129 4.67 -> 4.22, 150 4.87 -> 4.47.  Other lengths:
 // as many rows as fit 4096 floats, fewer while a lane would hold more than
 // 16 of a row's elements (on [16384, 257] fp32: 12 rows and 17 per lane
