@@ -464,6 +464,8 @@ struct PipeParams {
     int32_t groups;              // G
     int32_t groups_total;        // n * G
     int32_t per_round;           // groups per round
+    int32_t stagger_from;        // first workgroup whose loads wait stagger_ticks (INT32_MAX: none)
+    uint32_t stagger_ticks;      // 100 MHz ticks of s_memrealtime
     float eps;
 };
 
@@ -696,6 +698,14 @@ __global__ __launch_bounds__(kPipeNT) void gn_pipe(PipeParams p) {
     const int lane = threadIdx.x & (kWave - 1);
 
     if (wave < kPipeDataWaves) {
+        // Staggered issue: the second half of a grid with two or more
+        // workgroups per CU issues its loads a fixed time after it starts.
+        // The first half's groups then complete sooner and store while the
+        // second half still loads, as a copy overlaps its reads and writes.
+        if ((int)blockIdx.x >= p.stagger_from) {
+            const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
+            while (__builtin_amdgcn_s_memrealtime() - t0 < p.stagger_ticks) __builtin_amdgcn_s_sleep(1);
+        }
         u32x4 v[R][NV];
 #pragma unroll
         for (int r = 0; r < R; ++r) {
@@ -1185,6 +1195,22 @@ uint32_t gn_min_rounds() {
     return rounds;
 }
 
+// How long (100 MHz ticks of s_memrealtime) the second half of a one-round
+// gn_pipe grid with at least two workgroups per CU waits before issuing its
+// loads: 0.75 us by default; KF355_GN_STAGGER_TICKS overrides it (0: no
+// wait).  On the SD3.5 VAE block (512 workgroups on 256 CUs, graph replays,
+// three runs each): no wait 8.31-8.35 us; 0.6, 0.75 and 0.9 us 7.91-7.97;
+// 1.25 us 8.25, 1.5 us 8.40, 2 us 8.94.  Waiting for one probe load of its
+// own chunk instead of a fixed time gave 8.05-8.28 (two chained probe loads
+// 8.56), delaying the last 5/8 or 3/8 of the grid instead of the half 8.30
+// and 8.06, and a wait growing with the group index 8.19 at best.  The same
+// wait on gn_pipe_cl (whose strided tiles bound it) gained 1%, so it stays
+// on gn_pipe.  Read once per process.
+uint32_t gn_stagger_ticks() {
+    static const uint32_t ticks = env_u32("KF355_GN_STAGGER_TICKS", 75u);
+    return ticks;
+}
+
 // How long (100 MHz ticks of s_memrealtime) a fused workgroup waits for the
 // rest of its group before recomputing the statistics itself: 100 us by
 // default; KF355_GN_WAIT_TICKS overrides it (tests set 0 to force the
@@ -1348,6 +1374,9 @@ bool run_pipe(const GroupNormArgs& a, hipStream_t s, const char** variant, kf_st
             p.groups = (int32_t)a.groups;
             p.groups_total = (int32_t)gt;
             p.per_round = (int32_t)per_round;
+            const bool stagger = rounds == 1 && grid >= 2 * (int64_t)device_multiprocessors(dev) && gn_stagger_ticks() > 0;
+            p.stagger_from = stagger ? (int32_t)(grid / 2) : INT32_MAX;
+            p.stagger_ticks = gn_stagger_ticks();
             p.eps = a.eps;
             const dim3 g((unsigned)grid), b(kPipeNT);
             switch (k * 2 + r) {

@@ -12,7 +12,8 @@ OP: group_norm | group_norm_nhwc | group_norm_small | group_norm_parts | group_n
     softmax_split
 
 Further environment knobs the tests use: KF355_GN_MODE=fused (GroupNorm
-without gn_pipe) and KF355_GN_PARTS=k (gn_pipe with k workgroups per group)."""
+without gn_pipe), KF355_GN_PARTS=k (gn_pipe with k workgroups per group) and
+KF355_GN_STAGGER_TICKS=0 (gn_pipe without its staggered issue)."""
 import os
 import sys
 
@@ -76,7 +77,7 @@ def spawn(tmp_path, ops, **env) -> dict:
 
 def main():
     out_path, ops = sys.argv[1], sys.argv[2:]
-    knobs = ("KF355_GN_WAIT_TICKS", "KF355_SM_WAIT_TICKS", "KF355_GN_MODE", "KF355_GN_PARTS")
+    knobs = ("KF355_GN_WAIT_TICKS", "KF355_SM_WAIT_TICKS", "KF355_GN_MODE", "KF355_GN_PARTS", "KF355_GN_STAGGER_TICKS")
     print(f"[child] ops={ops} " + " ".join(f"{k}={os.environ.get(k)}" for k in knobs), flush=True)
     ws = torch.zeros(1 << 20, dtype=torch.uint8, device="cuda")
     saved = {}

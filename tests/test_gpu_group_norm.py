@@ -244,6 +244,19 @@ def test_pipe_forced_plans_on_the_vae_block(tmp_path, env, want):
     check(_as_tensor(got["bits0"]), oracle.group_norm(a["x"], a["groups"], a["weight"], a["bias"], a["eps"]), "bf16")
 
 
+def test_staggered_issue_changes_no_bit(tmp_path):
+    # On the SD3.5 VAE block (512 workgroups, two per CU) the second half of
+    # gn_pipe's grid issues its loads later; with that wait off every output
+    # bit is the same, and neither run gives up a wait.
+    note("group_norm gn_pipe with and without the staggered issue")
+    a = spawn(tmp_path, ["group_norm"])
+    b = spawn(tmp_path, ["group_norm"], KF355_GN_STAGGER_TICKS="0")
+    assert str(a["variant0"]) == str(b["variant0"]) == "gn_pipe_nv8_r1"
+    assert int(a["give_ups"]) == 0 and int(b["give_ups"]) == 0
+    assert int(a["rest"]) == 0 and int(b["rest"]) == 0
+    assert np.array_equal(a["bits0"], b["bits0"])
+
+
 def _oracle_of(op):
     a = inputs(op)
     if op == "softmax_split":
