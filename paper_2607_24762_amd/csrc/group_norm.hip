@@ -25,9 +25,14 @@
 //             them in part order (so the result does not depend on arrival
 //             order), and normalises straight from registers.  Needs every
 //             workgroup of the grid resident at once.
-//   gn_stats + gn_apply  (two launches)  The same chunking without the wait:
-//             the first kernel publishes the partials, the second merges them
-//             and re-reads x.  Used when the grid cannot be co-resident.
+//   gn_split  (two launches; dense NCHW 16-bit tensors gn_pipe cannot take)
+//             gn_pipe's chunks and arithmetic without any wait: the first
+//             launch publishes each chunk's moments and the group's last
+//             arrival merges them; the second re-reads x and normalises.
+//   gn_stats + gn_apply  (two launches)  gn_fused's chunking without the
+//             wait: the first kernel publishes the partials, the second
+//             merges them and re-reads x.  Used for the other grids that
+//             cannot be co-resident.
 //
 // Moments: each thread computes its own mean and M2 by two passes over its
 // registers, then partials are combined with the Chan et al. parallel
@@ -466,6 +471,7 @@ struct PipeParams {
     int32_t per_round;           // groups per round
     int32_t stagger_from;        // first workgroup whose loads wait stagger_ticks (INT32_MAX: none)
     uint32_t stagger_ticks;      // 100 MHz ticks of s_memrealtime
+    int32_t force_recompute;     // gn_split only, tests: recompute the parts as if a wait had run out
     float eps;
 };
 
@@ -794,6 +800,206 @@ __global__ __launch_bounds__(kPipeNT) void gn_pipe(PipeParams p) {
             __syncthreads();  // statistics of round r in LDS
             if (live && lane == 0) ex_leave(p.ex, ng, before);
         }
+    }
+}
+
+// --------------------------------------------------------------------------
+// gn_split: GroupNorm in two launches for dense NCHW 16-bit tensors whose
+// one-launch grid cannot be resident (the SD3.5 VAE decoder's full-size
+// blocks, e.g. [1, 128, 1024, 1024]: 256 MiB, no register file holds it), in
+// gn_pipe's arithmetic.  gn_split_stats reads each 16384-element chunk once,
+// folds its moments with v_dot2 and publishes them; the last workgroup of a
+// group to arrive (a per-group counter) merges the group's parts in part
+// order and writes the group's mean (double) and M2 over slots 0 and 1.
+// gn_split_apply re-reads each chunk and normalises it with those
+// statistics; its last workgroup of a group returns the group's slots and
+// counter to zero.  One read more than gn_pipe, but both passes stream: on
+// [1, 128, 1024, 1024] the moments pass of the general two-kernel form
+// (about ten VALU operations per element) ran 71 us, a read at 3.8 TB/s.
+
+// a + b for moments of na and nb values (a first).
+__device__ __forceinline__ PipeMoments merge_counts(PipeMoments a, PipeMoments b, float na, float nb) {
+#pragma clang fp contract(off)
+    const float nt = na + nb;
+    PipeMoments m;
+    m.mean = a.mean + (b.mean - a.mean) * ((double)nb / (double)nt);
+    const float d = (float)(b.mean - a.mean);
+    m.m2 = fmaf(d * d, na * (nb / nt), a.m2 + b.m2);
+    return m;
+}
+
+// The P parts of group ng merged in part order by one wave: lane l folds
+// parts l, l + 64, l + 128, ... in that order, then the lane butterfly over
+// min(P, 64) lanes (P a power of two).  Every part has been published (the
+// caller is the group's last arrival), so the bounded wait only guards the
+// memory model; if a part is still unseen after it, the wave recomputes
+// every part from x with its owner's loads and arithmetic, bit for bit.
+template <class T, int NV>
+__device__ PipeMoments split_gather(const PipeParams& p, int64_t ng) {
+    constexpr float kChunkN = (float)(NV * 8 * kWave * kPipeDataWaves);
+    constexpr int kBatch = 4;  // slot loads in flight per lane
+    const int lane = threadIdx.x & (kWave - 1);
+    const int P = p.ex.parts;
+    const int per = P > kWave ? P / kWave : 1;
+    const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
+    const uint64_t* slots = p.ex.slot + ng * P;
+    PipeMoments acc{0.0, 0.f};
+    bool ok = true;
+    for (int i0 = 0; i0 < per; i0 += kBatch) {
+        uint64_t w[kBatch];
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) {
+            const int q = lane + (i0 + u) * kWave;
+            w[u] = (i0 + u < per && q < P) ? __hip_atomic_load(slots + q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 1;
+        }
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) {
+            const int i = i0 + u;
+            const int q = lane + i * kWave;
+            if (i < per && q < P) {
+                if (w[u] == 0) w[u] = ex_poll(p.ex, ng, q, t0, true);
+                ok = ok && w[u] != 0;
+                const PipeMoments mi = pipe_decode(w[u]);
+                acc = i == 0 ? mi : merge_counts(acc, mi, (float)i * kChunkN, kChunkN);
+            }
+        }
+    }
+    if (!__all(ok) || p.force_recompute) {
+        acc = PipeMoments{0.0, 0.f};
+        for (int q = 0; q < P; ++q) {
+            PipeMoments w[kPipeDataWaves];
+#pragma unroll
+            for (int k = 0; k < kPipeDataWaves; ++k) {
+                u32x4 v[NV];
+                pipe_load<NV>(p, ng, q, k * kWave + lane, v);
+                w[k] = wave_moments<T, NV>(v);
+            }
+            const PipeMoments c = pipe_decode(pipe_encode(chunk_moments<NV>(w)));
+            const int i = q / kWave;
+            if ((q & (kWave - 1)) == lane) acc = i == 0 ? c : merge_counts(acc, c, (float)i * kChunkN, kChunkN);
+        }
+        if (lane == 0) ex_count_give_up(p.ex);
+    }
+    float n = (float)per * kChunkN;
+    const int lanes = P < kWave ? P : kWave;
+#define KF_STEP(S)                    \
+    if ((2 << S) <= lanes) {          \
+        acc = pipe_step<S>(acc, n);   \
+        n *= 2.f;                     \
+    }
+    KF_STEP(0) KF_STEP(1) KF_STEP(2) KF_STEP(3) KF_STEP(4) KF_STEP(5)
+#undef KF_STEP
+    const uint64_t u = __builtin_bit_cast(uint64_t, acc.mean);
+    const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)u), hi = __builtin_amdgcn_readfirstlane((uint32_t)(u >> 32));
+    return PipeMoments{__builtin_bit_cast(double, (uint64_t)lo | ((uint64_t)hi << 32)), uniform0(acc.m2)};
+}
+
+__device__ __forceinline__ void split_chunk(const PipeParams& p, int b, int64_t* ng, int* part) {
+    const int P = p.ex.parts;
+    *ng = b / P;
+    *part = b - (b / P) * P;
+}
+
+template <class T, int NV>
+__global__ __launch_bounds__(kPipeDataWaves * kWave) void gn_split_stats(PipeParams p) {
+    __shared__ PipeMoments part_lds[kPipeDataWaves];
+    __shared__ unsigned before_lds;
+    const int wave = threadIdx.x / kWave;
+    const int lane = threadIdx.x & (kWave - 1);
+    int64_t ng;
+    int part;
+    split_chunk(p, blockIdx.x, &ng, &part);
+    u32x4 v[NV];
+    pipe_load<NV>(p, ng, part, threadIdx.x, v);
+    const PipeMoments m = wave_moments<T, NV>(v);
+    if (lane == 0) part_lds[wave] = m;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        PipeMoments w[kPipeDataWaves];
+#pragma unroll
+        for (int k = 0; k < kPipeDataWaves; ++k) w[k] = part_lds[k];
+        ex_publish(p.ex, ng, part, pipe_encode(chunk_moments<NV>(w)));
+        // Relaxed, like every exchange access here: an agent-scope release
+        // or acquire writes back or invalidates the L2, which thousands of
+        // workgroups cannot afford.  The last arrival may see the count
+        // before some published word; it polls for the words (self-flagged).
+        before_lds = ex_depart(p.ex, ng);
+    }
+    __syncthreads();
+    if (wave != 0 || before_lds != (unsigned)p.ex.parts - 1) return;
+    // The group's last arrival: every part is published.
+    const PipeMoments g = split_gather<T, NV>(p, ng);
+    if (lane == 0) {
+        uint64_t* r = p.ex.slot + ng * p.ex.parts;
+        __hip_atomic_store(r, __builtin_bit_cast(uint64_t, g.mean), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(r + 1, (uint64_t)__float_as_uint(g.m2), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(ex_counter(p.ex, ng), 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+}
+
+template <class T, class A, int NV>
+__global__ __launch_bounds__(kPipeDataWaves * kWave) void gn_split_apply(PipeParams p) {
+    constexpr int64_t CH = (int64_t)kPipeDataWaves * kWave * NV * 8;
+    __shared__ float stats_lds[NV][2];  // per slot: a = rstd * w[c], c = b[c] - lo * a
+    __shared__ float mean_lds;          // hi of the group mean
+    const int lane = threadIdx.x & (kWave - 1);
+    int64_t ng;
+    int part;
+    split_chunk(p, blockIdx.x, &ng, &part);
+    u32x4 v[NV];
+    pipe_load<NV>(p, ng, part, threadIdx.x, v);
+    if (threadIdx.x < kWave) {
+        // Lane j: the affine of slot j's channel, and the group statistics
+        // gn_split_stats left in slots 0 and 1 (visible: an earlier launch
+        // on the same stream wrote them).
+        const bool hw = p.w != nullptr, hb = p.b != nullptr;
+        const void* ws = hw ? p.w : affine_identity<A>();
+        const void* bs = hb ? p.b : affine_identity<A>();
+        const int j = lane < NV ? lane : 0;
+        const int64_t c = (ng % p.groups) * p.cpg + (part * CH + (int64_t)j * 2048) / p.spatial;
+        const float wv = load1<A>(ws, hw ? c : 0);
+        const float bv = load1<A>(bs, hb ? c : 1);
+        uint64_t* r = p.ex.slot + ng * p.ex.parts;
+        const uint64_t mw = __hip_atomic_load(r, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        const uint64_t vw = __hip_atomic_load(r + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        const double mean = __builtin_bit_cast(double, mw);
+        const float m2 = __uint_as_float((uint32_t)vw);
+        const float rstd = 1.f / sqrtf(m2 / (float)p.group_elems + p.eps);
+        const float hi = (float)mean, lo = (float)(mean - (double)hi);
+        if (lane < NV) {
+            const float a = rstd * wv;
+            stats_lds[lane][0] = a;
+            stats_lds[lane][1] = bv - lo * a;
+        }
+        if (lane == 0) mean_lds = hi;
+        // Done reading the group's statistics: rstd consumes both loads, so
+        // they have returned before the departure count (relaxed; the empty
+        // asm keeps the count after them).  The last workgroup of the group
+        // empties its slots and counter.
+        __asm__ volatile("" : : "v"(rstd), "v"(lo) : "memory");
+        unsigned before = 0;
+        if (lane == 0) before = ex_depart(p.ex, ng);
+        before = __builtin_amdgcn_readfirstlane(before);
+        if (before == (unsigned)p.ex.parts - 1) {
+            for (int q = lane; q < p.ex.parts; q += kWave)
+                __hip_atomic_store(r + q, (uint64_t)0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            if (lane == 0) __hip_atomic_store(ex_counter(p.ex, ng), 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+    }
+    __syncthreads();
+    const __amdgpu_buffer_rsrc_t out = chunk_buffer(static_cast<char*>(p.y) + (ng * p.group_elems + part * CH) * 2, CH * 2);
+    const float mu = mean_lds;
+#pragma unroll
+    for (int j = 0; j < NV; ++j) {
+        const float a = stats_lds[j][0], c = stats_lds[j][1];
+        u32x4 o;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            float x0, x1;
+            unpack2(T{}, v[j][i], x0, x1);
+            o[i] = pack2(T{}, fmaf(x0 - mu, a, c), fmaf(x1 - mu, a, c));
+        }
+        store16_through(out, (j * 256 + (int)threadIdx.x) * 16, o);
     }
 }
 
@@ -1211,6 +1417,14 @@ uint32_t gn_stagger_ticks() {
     return ticks;
 }
 
+// KF355_GN_SPLIT_RECOMPUTE=1 (tests only): gn_split's last arrival of each
+// group recomputes every part from x as it does when a published part stays
+// unseen, and counts a give-up.  Read once per process.
+bool gn_split_recompute() {
+    static const bool on = env_u32("KF355_GN_SPLIT_RECOMPUTE", 0u) != 0;
+    return on;
+}
+
 // How long (100 MHz ticks of s_memrealtime) a fused workgroup waits for the
 // rest of its group before recomputing the statistics itself: 100 us by
 // default; KF355_GN_WAIT_TICKS overrides it (tests set 0 to force the
@@ -1377,6 +1591,7 @@ bool run_pipe(const GroupNormArgs& a, hipStream_t s, const char** variant, kf_st
             const bool stagger = rounds == 1 && grid >= 2 * (int64_t)device_multiprocessors(dev) && gn_stagger_ticks() > 0;
             p.stagger_from = stagger ? (int32_t)(grid / 2) : INT32_MAX;
             p.stagger_ticks = gn_stagger_ticks();
+            p.force_recompute = 0;
             p.eps = a.eps;
             const dim3 g((unsigned)grid), b(kPipeNT);
             switch (k * 2 + r) {
@@ -1475,12 +1690,70 @@ bool run_pipe_cl(const GroupNormArgs& a, hipStream_t s, const char** variant, kf
     return true;
 }
 
+// gn_split for dense NCHW 16-bit tensors that gn_pipe cannot take: 16384-
+// element chunks (a multiple of 2048 spatial, so every slot row lies in one
+// channel), a power-of-two number of 2 to 4096 parts per group, any grid
+// size (nothing waits on another workgroup's progress), in place or not.
+template <class T, class A>
+bool run_split(const GroupNormArgs& a, hipStream_t s, const char** variant, kf_status* status) {
+    constexpr int NV = 8;
+    constexpr int64_t CH = (int64_t)kPipeDataWaves * kWave * NV * 8;
+    const int mode = gn_mode();
+    if (mode == kModeTwoPass || mode == kModeFused || mode == kModeCoop || gn_parts_override() != 0) return false;
+    if (a.nhwc || !vector_ok(a) || a.spatial % 2048 != 0) return false;
+    if (a.x != a.y) {  // exact aliasing is fine (each chunk is read before it is written); no partial overlap
+        const uintptr_t bytes = (uintptr_t)(a.n * a.c * a.spatial * 2);
+        const uintptr_t x0 = (uintptr_t)a.x, y0 = (uintptr_t)a.y;
+        if (x0 < y0 + bytes && y0 < x0 + bytes) return false;
+    }
+    const int64_t ge = (a.c / a.groups) * a.spatial;
+    if (ge % CH != 0) return false;
+    const int64_t parts = ge / CH;
+    if (parts < 2 || parts > 4096 || (parts & (parts - 1)) != 0) return false;
+    const int64_t gt = a.n * a.groups;
+    const int64_t grid = gt * parts;
+    if (grid > INT32_MAX) return false;
+    if (exchange_layout(gt, parts).total > a.workspace_bytes) return false;
+    PipeParams p;
+    p.x = a.x;
+    p.y = a.y;
+    p.w = a.weight;
+    p.b = a.bias;
+    p.ex = gn_exchange(a, parts);
+    p.group_elems = ge;
+    p.spatial = a.spatial;
+    p.cpg = (int32_t)(a.c / a.groups);
+    p.groups = (int32_t)a.groups;
+    p.groups_total = (int32_t)gt;
+    p.per_round = (int32_t)gt;
+    p.stagger_from = INT32_MAX;
+    p.stagger_ticks = 0;
+    p.force_recompute = gn_split_recompute() ? 1 : 0;
+    p.eps = a.eps;
+    const dim3 g((unsigned)grid), b(kPipeDataWaves * kWave);
+    hipLaunchKernelGGL((gn_split_stats<T, NV>), g, b, 0, s, p);
+    hipError_t err = hipGetLastError();
+    if (err == hipSuccess) {
+        hipLaunchKernelGGL((gn_split_apply<T, A, NV>), g, b, 0, s, p);
+        err = hipGetLastError();
+    }
+    *variant = "gn_split_nv8";
+    if (err != hipSuccess) {
+        set_error("group_norm launch failed: %s", hipGetErrorString(err));
+        *status = KF_ERR_HIP;
+    } else {
+        *status = KF_OK;
+    }
+    return true;
+}
+
 template <class T, class A>
 kf_status run_layout(const GroupNormArgs& a, hipStream_t s, const char** variant) {
     if constexpr (!std::is_same_v<T, F32>) {
         kf_status st;
         if (run_pipe<T, A>(a, s, variant, &st)) return st;
         if (run_pipe_cl<T, A>(a, s, variant, &st)) return st;
+        if (run_split<T, A>(a, s, variant, &st)) return st;
     }
     const bool vec = vector_ok(a);
     if (a.nhwc) return vec ? run<T, A, true, true>(a, s, variant) : run<T, A, false, true>(a, s, variant);

@@ -9,11 +9,12 @@ and the count of non-zero bytes after the status block.
 
 usage: exchange_child.py OUT.npz OP [OP ...]
 OP: group_norm | group_norm_nhwc | group_norm_small | group_norm_parts | group_norm_tiles_small |
-    softmax_split
+    group_norm_split | softmax_split
 
 Further environment knobs the tests use: KF355_GN_MODE=fused (GroupNorm
 without gn_pipe), KF355_GN_PARTS=k (gn_pipe with k workgroups per group) and
-KF355_GN_STAGGER_TICKS=0 (gn_pipe without its staggered issue)."""
+KF355_GN_STAGGER_TICKS=0 (gn_pipe without its staggered issue) and
+KF355_GN_SPLIT_RECOMPUTE=1 (gn_split recomputing every part)."""
 import os
 import sys
 
@@ -47,6 +48,11 @@ def inputs(op: str) -> dict:
         return {"x": W.randn((1, 192, 32, 32), "bf16", seed=54, mean=-0.4, std=1.1), "groups": 3,
                 "weight": W.randn((192,), "bf16", seed=55, mean=1.0, std=0.1),
                 "bias": W.randn((192,), "bf16", seed=56, std=0.1), "eps": 1e-6}
+    if op == "group_norm_split":
+        # 16 channels of 512 x 512 per group: 256 chunks of 16384, gn_split.
+        return {"x": W.randn((1, 32, 512, 512), "bf16", seed=61, mean=0.8, std=1.3), "groups": 2,
+                "weight": W.randn((32,), "bf16", seed=62, mean=1.0, std=0.1),
+                "bias": W.randn((32,), "bf16", seed=63, std=0.1), "eps": 1e-6}
     if op == "softmax_split":
         return {"x": W.attn_decode_bf16()["x"]}
     raise SystemExit(f"unknown op {op}")
@@ -77,7 +83,8 @@ def spawn(tmp_path, ops, **env) -> dict:
 
 def main():
     out_path, ops = sys.argv[1], sys.argv[2:]
-    knobs = ("KF355_GN_WAIT_TICKS", "KF355_SM_WAIT_TICKS", "KF355_GN_MODE", "KF355_GN_PARTS", "KF355_GN_STAGGER_TICKS")
+    knobs = ("KF355_GN_WAIT_TICKS", "KF355_SM_WAIT_TICKS", "KF355_GN_MODE", "KF355_GN_PARTS", "KF355_GN_STAGGER_TICKS",
+             "KF355_GN_SPLIT_RECOMPUTE")
     print(f"[child] ops={ops} " + " ".join(f"{k}={os.environ.get(k)}" for k in knobs), flush=True)
     ws = torch.zeros(1 << 20, dtype=torch.uint8, device="cuda")
     saved = {}

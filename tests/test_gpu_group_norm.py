@@ -1,6 +1,6 @@
 """GPU parity of kf_group_norm against the float64 oracle across shapes that
 exercise every path: single-chunk groups, fused multi-chunk groups with the
-cross-workgroup exchange (and its recompute fallback), the two-kernel path
+cross-workgroup exchange (and its recompute fallback), the two-launch paths
 for grids that cannot be co-resident and for in-place calls, scalar (non-vectorisable) layouts, every dtype and
 affine combination, in-place use, determinism and workspace hygiene.
 
@@ -127,22 +127,78 @@ def test_pipe_exact_moments_fallback():
     check(y, oracle.group_norm(x, 4, w, b, 1e-6), "bf16")
 
 
-def test_two_kernel_path_for_grids_that_cannot_be_resident():
+def test_two_launch_path_for_grids_that_cannot_be_resident():
     # 8 samples x 32 groups x 16 chunks = 4096 workgroups of 4 waves: a CU
     # holds at most 32 waves, so no device of 256 CUs can hold more than 2048
-    # of them at once, and the fused kernel's own register use allows fewer.
-    note("group_norm two-pass (8,128,256,256)")
+    # of them at once (gn_pipe's workgroups have a fifth wave).  Dense NCHW
+    # 16-bit: gn_split's two launches; the general two-kernel form is pinned
+    # by the forced plans below.
+    note("group_norm split (8,128,256,256)")
     props = torch.cuda.get_device_properties(0)
     assert 4096 > props.multi_processor_count * 32 // 4
     _, variant = run((8, 128, 256, 256), 32, "bf16", seed=4)
-    assert variant == "gn_two_pass_vec", variant
+    assert variant == "gn_split_nv8", variant
+
+
+SPLIT_CASES = [
+    ((1, 64, 512, 512), 1, "bf16", "same"),    # one 16M-element group: 1024 parts, 16 per lane
+    ((1, 32, 512, 512), 2, "bf16", "f32"),     # 256 parts per group, fp32 affine
+    ((1, 32, 512, 512), 2, "f16", "none"),     # fp16, no affine
+    ((2, 16, 512, 1024), 2, "f16", "same"),    # 256 parts per group, two samples
+    ((1, 64, 256, 512), 1, "bf16", "w"),       # 512 parts, weight only
+]
+
+
+@pytest.mark.parametrize("shape,groups,dt,affine", SPLIT_CASES, ids=lambda v: str(v))
+def test_split_path_matches_the_oracle(shape, groups, dt, affine):
+    # Groups of more than 64 parts even in 32768-element chunks: gn_pipe's
+    # one-wave gather cannot take them, gn_split's two launches do (the last
+    # arrival of a group folds its parts 2 to 16 per lane, then the lane
+    # butterfly).  Parity with the oracle, bit-identical repeats, and the
+    # workspace left zero after the status block with no give-up.
+    note(f"group_norm split {shape} G={groups} {dt} affine={affine}")
+    y, variant = run(shape, groups, dt, affine=affine, seed=21, mean=-0.7, std=2.0)
+    assert variant == "gn_split_nv8", variant
+    x = randn(shape, dt, seed=21, mean=-0.7, std=2.0).cuda()
+    c = shape[1]
+    adt = dt if affine == "same" else "f32"
+    w = randn((c,), adt, seed=22, mean=1.0, std=0.1).cuda() if affine in ("same", "f32", "w") else None
+    b = randn((c,), adt, seed=23, std=0.1).cuda() if affine in ("same", "f32", "b") else None
+    ws = torch.zeros(kf355.group_norm_workspace(x, groups).numel(), dtype=torch.uint8, device="cuda")
+    y1 = kf355.kf_group_norm(x, groups, w, b, 1e-6, workspace=ws)
+    y2 = kf355.kf_group_norm(x, groups, w, b, 1e-6, workspace=ws)
+    torch.cuda.synchronize()
+    assert torch.equal(y1.view(torch.int16), y2.view(torch.int16))
+    assert torch.equal(y1.view(torch.int16), y.view(torch.int16))
+    assert kf355.workspace_give_ups(ws) == 0
+    assert int(ws[256:].count_nonzero().item()) == 0
+
+
+def test_split_recompute_is_bit_identical(tmp_path):
+    # KF355_GN_SPLIT_RECOMPUTE=1 makes each group's last arrival recompute
+    # every part from x, as it does when a published part stays unseen: the
+    # same bits, one give-up per group, the workspace zero again.
+    note("group_norm split with the recompute path forced")
+    a = spawn(tmp_path, ["group_norm_split"])
+    b = spawn(tmp_path, ["group_norm_split"], KF355_GN_SPLIT_RECOMPUTE="1")
+    assert str(a["variant0"]) == str(b["variant0"]) == "gn_split_nv8"
+    assert int(a["give_ups"]) == 0 and int(b["give_ups"]) == inputs("group_norm_split")["groups"]
+    assert int(a["rest"]) == 0 and int(b["rest"]) == 0
+    assert np.array_equal(a["bits0"], b["bits0"])
+    i = inputs("group_norm_split")
+    check(_as_tensor(b["bits0"]), oracle.group_norm(i["x"], i["groups"], i["weight"], i["bias"], i["eps"]), "bf16")
 
 
 def test_in_place():
-    # In place, chunks of a group are overwritten while others may still be
-    # read, so multi-chunk groups take the two-kernel path.
+    # In place: gn_pipe's chunks of a group would be overwritten while its
+    # recompute fallback might still read them, so multi-chunk groups take
+    # gn_split (whose second launch reads each chunk before writing it) or,
+    # where gn_split does not apply (spatial size not a multiple of 2048),
+    # the general two-kernel form.
     note("group_norm in place")
     _, variant = run((1, 512, 64, 64), 32, "bf16", in_place=True, seed=6)   # 4 chunks per group
+    assert variant == "gn_split_nv8", variant
+    _, variant = run((1, 256, 48, 48), 32, "bf16", in_place=True, seed=7)   # 2 chunks, spatial 2304
     assert variant.startswith("gn_two_pass"), variant
     _, variant = run((2, 64, 8, 8), 8, "bf16", in_place=True, seed=8)
     assert variant.startswith("gn_fused"), variant  # one chunk per group: no exchange
@@ -230,7 +286,8 @@ def test_forced_parts_per_group_deterministic(tmp_path, parts, want):
     ({"KF355_GN_PARTS": "64"}, ("gn_pipe_nv2_r1", "gn_pipe_nv2_r2")),  # 4096-element chunks, the most parts
     ({"KF355_GN_PARTS": "8"}, ("gn_pipe_nv16_r1",)),                  # 32768-element chunks: two channels each
     ({"KF355_GN_ROUNDS": "2"}, ("gn_pipe_nv8_r2",)),                  # two rounds of 16 groups
-], ids=["parts64", "parts8", "rounds2"])
+    ({"KF355_GN_MODE": "two_pass"}, ("gn_two_pass_vec",)),            # the general two-kernel form
+], ids=["parts64", "parts8", "rounds2", "two_pass"])
 def test_pipe_forced_plans_on_the_vae_block(tmp_path, env, want):
     # The SD3.5 VAE block under plans the default does not pick: each matches
     # the oracle, repeats bit for bit, gives up no wait and leaves the
