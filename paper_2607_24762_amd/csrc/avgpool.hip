@@ -18,10 +18,10 @@
 //   ap_nhwc_cell  channels last, windows of at most 4 x 4: a thread per
 //             output cell and 16-byte channel vector.
 //   ap_nhwc   channels last, any output size: a workgroup owns one output
-//             cell of one sample and 64 vectors of 16 bytes of channels;
-//             its four thread groups sum interleaved window pixels, so
-//             every load is a coalesced 1 KiB channel run, and the four
-//             partials are added in group order through LDS.
+//             cell of one sample and 32 vectors of 16 bytes of channels;
+//             its 16 thread groups sum interleaved window pixels, so every
+//             load is a coalesced 512-byte channel run, and the 16 partials
+//             are added in group order through LDS.
 #include <algorithm>
 #include <type_traits>
 
@@ -228,23 +228,47 @@ __global__ __launch_bounds__(kNT) void ap_window(const void* __restrict__ x, voi
     store1<T>(y, idx, sum / (float)((h1 - h0) * (w1 - w0)));
 }
 
-constexpr int kCB = 64;         // channel vectors per ap_nhwc workgroup
-constexpr int kPG = kNT / kCB;  // pixel groups per workgroup
+// ap_nhwc: a workgroup owns kCB consecutive 16-byte channel vectors of one
+// output cell of one sample; its kPG thread groups take the window's pixels
+// g, g + kPG, ... (kPD of them per thread per batch, every load of a batch
+// issued before the first add), and the groups' sums meet in LDS in group
+// order.  Consecutive threads read consecutive channel vectors, so each
+// pixel is a 512-byte run.  On the channels-last ResNet-50 head ([32, 2048,
+// 7, 7] fp32 -> 1x1, graph replays, one box): 5.82 us for the earlier 64 x 4
+// shape with 16 loads per thread in flight (three of them re-reading pixel 0
+// past the window's 13), 4.76 us for 64 x 4 with the loads here, 4.40 us
+// for 32 x 16 (16 x 16: 4.66, 16 x 32: 4.69, 32 x 32: 4.63, 128 x 8: 5.03),
+// against 3.78 us for a plain read of the 12.25 MiB.  Loads are non-temporal
+// where the windows tile the input (every pixel read once: 4.40 against 4.55
+// us with ordinary loads), ordinary where adaptive windows overlap.
+constexpr int kCB = 32;               // channel vectors per ap_nhwc workgroup
+constexpr int kPG = 16;               // pixel groups per workgroup
+constexpr int kPD = 4;                // window pixels per thread per batch
+constexpr int kNhwcNT = kCB * kPG;    // 512 threads
 
-template <class T, int VEC>
-__global__ __launch_bounds__(kNT) void ap_nhwc(const void* __restrict__ x, void* __restrict__ y, int32_t H,
-                                               int32_t W, int32_t C, int32_t OH, int32_t OW) {
+template <class T, int VEC, bool NT>
+__global__ __launch_bounds__(kNhwcNT) void ap_nhwc(const void* __restrict__ x, void* __restrict__ y, int32_t H,
+                                                   int32_t W, int32_t C, int32_t OH, int32_t OW) {
     __shared__ float part[kPG - 1][kCB][VEC];
     const int lc = threadIdx.x % kCB, g = threadIdx.x / kCB;
     const int cv = blockIdx.x * kCB + lc;
     const bool active = cv < C / VEC;
     const int i = blockIdx.y / OW, j = blockIdx.y - (blockIdx.y / OW) * OW;
     const int64_t n = blockIdx.z;
-    const int h0 = (int)(((int64_t)i * H) / OH), h1 = (int)((((int64_t)i + 1) * H + OH - 1) / OH);
-    const int w0 = (int)(((int64_t)j * W) / OW), w1 = (int)((((int64_t)j + 1) * W + OW - 1) / OW);
+    // Window bounds; a 1 x 1 output's window is the whole plane, with none
+    // of the 64-bit divisions (hundreds of instructions ahead of the loads).
+    int h0 = 0, h1 = H, w0 = 0, w1 = W;
+    if (OH != 1 || OW != 1) {
+        h0 = (int)(((int64_t)i * H) / OH), h1 = (int)((((int64_t)i + 1) * H + OH - 1) / OH);
+        w0 = (int)(((int64_t)j * W) / OW), w1 = (int)((((int64_t)j + 1) * W + OW - 1) / OW);
+    }
     const int ww = w1 - w0, count = (h1 - h0) * ww;
     const int64_t base = n * H * W * (int64_t)C + (int64_t)cv * VEC;
+    // Pixel q of the window, row-major; a window spanning whole rows (every
+    // 1 x 1 or one-column output) is one run of pixels, with no division.
+    const bool rows = ww == W;
     auto at = [&](int q) {
+        if (rows) return base + ((int64_t)h0 * W + q) * C;
         const int r = h0 + q / ww, c = w0 + (q - (q / ww) * ww);
         return base + ((int64_t)r * W + c) * C;
     };
@@ -252,22 +276,19 @@ __global__ __launch_bounds__(kNT) void ap_nhwc(const void* __restrict__ x, void*
 #pragma unroll
     for (int k = 0; k < VEC; ++k) acc[k] = 0.f;
     if (active) {
-        // Window pixels g, g + 4, ... in order, DEPTH loads in flight (64
-        // floats of registers: a 7x7 window's 13 pixels per group go out
-        // in one or two batches); a slot past the window re-reads the
-        // first pixel and is not added.
-        constexpr int DEPTH = 64 / VEC < 16 ? 64 / VEC : 16;
-        for (int q0 = g; q0 < count; q0 += DEPTH * kPG) {
-            float v[DEPTH][VEC];
+        // A slot past the window re-reads the window's first pixel and is
+        // not added.
+        for (int q0 = g; q0 < count; q0 += kPD * kPG) {
+            float v[kPD][VEC];
 #pragma unroll
-            for (int d = 0; d < DEPTH; ++d) {
+            for (int d = 0; d < kPD; ++d) {
                 const int q = q0 + d * kPG;
                 const int64_t e = at(q < count ? q : 0);
-                if constexpr (VEC > 1) load_vec<T>(x, e, v[d]);
+                if constexpr (VEC > 1) load_vec<T, NT>(x, e, v[d]);
                 else v[d][0] = load1<T>(x, e);
             }
 #pragma unroll
-            for (int d = 0; d < DEPTH; ++d)
+            for (int d = 0; d < kPD; ++d)
                 if (q0 + d * kPG < count) {
 #pragma unroll
                     for (int k = 0; k < VEC; ++k) acc[k] += v[d][k];
@@ -302,20 +323,34 @@ __global__ __launch_bounds__(kNT) void ap_nhwc(const void* __restrict__ x, void*
 // issued before the adds, and the pixels inside the window are added in
 // row-major order.  No LDS and no barrier: small windows leave too little
 // work per output cell to split it over thread groups as ap_nhwc does.
-template <class T, int VEC, int K>
+// I32: the thread index, the products i * H and j * W and their bounds fit
+// in 32 bits (checked on the host), so the index arithmetic divides in 32
+// bits: seven 64-bit divisions by run-time values cost about a thousand
+// VALU instructions per thread ahead of the loads.
+template <class I>
+__device__ __forceinline__ void cell_of(I idx, I CV, I OH, I OW, I H, I W, int* cv, int* i, int* j, int64_t* n,
+                                        int* h0, int* h1, int* w0, int* w1) {
+    const I cell = idx / CV, t = cell / OW;
+    *cv = (int)(idx - cell * CV);
+    *j = (int)(cell - t * OW);
+    *n = (int64_t)(t / OH);
+    *i = (int)(t - (t / OH) * OH);
+    *h0 = (int)(((I)*i * H) / OH), *h1 = (int)((((I)*i + 1) * H + OH - 1) / OH);
+    *w0 = (int)(((I)*j * W) / OW), *w1 = (int)((((I)*j + 1) * W + OW - 1) / OW);
+}
+
+template <class T, int VEC, int K, bool I32>
 __global__ __launch_bounds__(kNT) void ap_nhwc_cell(const void* __restrict__ x, void* __restrict__ y, int64_t total,
                                                     int32_t CV, int32_t H, int32_t W, int32_t C, int32_t OH,
                                                     int32_t OW) {
     const int64_t idx = (int64_t)blockIdx.x * kNT + threadIdx.x;
     if (idx >= total) return;
-    const int32_t cv = (int32_t)(idx % CV);
-    const int64_t cell = idx / CV;
-    const int32_t j = (int32_t)(cell % OW);
-    const int64_t t = cell / OW;
-    const int32_t i = (int32_t)(t % OH);
-    const int64_t n = t / OH;
-    const int h0 = (int)(((int64_t)i * H) / OH), h1 = (int)((((int64_t)i + 1) * H + OH - 1) / OH);
-    const int w0 = (int)(((int64_t)j * W) / OW), w1 = (int)((((int64_t)j + 1) * W + OW - 1) / OW);
+    int cv, i, j, h0, h1, w0, w1;
+    int64_t n;
+    if constexpr (I32)
+        cell_of<uint32_t>((uint32_t)idx, CV, OH, OW, H, W, &cv, &i, &j, &n, &h0, &h1, &w0, &w1);
+    else
+        cell_of<int64_t>(idx, CV, OH, OW, H, W, &cv, &i, &j, &n, &h0, &h1, &w0, &w1);
     const int hh = h1 - h0, ww = w1 - w0;
     const int64_t base = n * H * W * (int64_t)C + (int64_t)cv * VEC;
     float v[K][K][VEC];
@@ -400,11 +435,18 @@ kf_status run(const AvgPoolArgs& a, hipStream_t s, const char** variant) {
                 hipLaunchKernelGGL(kernel, dim3(blocks), dim3(kNT), 0, s, a.x, a.y, total, (int32_t)cvs,
                                    (int32_t)a.h, (int32_t)a.w, (int32_t)a.c, (int32_t)a.oh, (int32_t)a.ow);
             };
+            const bool i32 = total <= INT32_MAX && (a.oh + 1) * (a.h + 1) <= INT32_MAX && (a.ow + 1) * (a.w + 1) <= INT32_MAX;
             auto pick = [&](auto vec_tag) {
                 constexpr int V = decltype(vec_tag)::value;
-                if (kc == 2) go(ap_nhwc_cell<T, V, 2>);
-                else if (kc == 3) go(ap_nhwc_cell<T, V, 3>);
-                else go(ap_nhwc_cell<T, V, 4>);
+                if (i32) {
+                    if (kc == 2) go(ap_nhwc_cell<T, V, 2, true>);
+                    else if (kc == 3) go(ap_nhwc_cell<T, V, 3, true>);
+                    else go(ap_nhwc_cell<T, V, 4, true>);
+                } else {
+                    if (kc == 2) go(ap_nhwc_cell<T, V, 2, false>);
+                    else if (kc == 3) go(ap_nhwc_cell<T, V, 3, false>);
+                    else go(ap_nhwc_cell<T, V, 4, false>);
+                }
             };
             if (vec) pick(std::integral_constant<int, T::vec>{});
             else pick(std::integral_constant<int, 1>{});
@@ -419,13 +461,14 @@ kf_status run(const AvgPoolArgs& a, hipStream_t s, const char** variant) {
             }
             return KF_OK;
         }
-        const dim3 grid((unsigned)gx, (unsigned)gy, (unsigned)a.n);
-        if (vec)
-            hipLaunchKernelGGL((ap_nhwc<T, T::vec>), grid, dim3(kNT), 0, s, a.x, a.y, (int32_t)a.h, (int32_t)a.w,
-                               (int32_t)a.c, (int32_t)a.oh, (int32_t)a.ow);
-        else
-            hipLaunchKernelGGL((ap_nhwc<T, 1>), grid, dim3(kNT), 0, s, a.x, a.y, (int32_t)a.h, (int32_t)a.w,
-                               (int32_t)a.c, (int32_t)a.oh, (int32_t)a.ow);
+        const dim3 grid((unsigned)gx, (unsigned)gy, (unsigned)a.n), block(kNhwcNT);
+        const bool tiled = a.h % a.oh == 0 && a.w % a.ow == 0;  // windows tile x: every pixel read once
+        auto go = [&](auto kernel) {
+            hipLaunchKernelGGL(kernel, grid, block, 0, s, a.x, a.y, (int32_t)a.h, (int32_t)a.w, (int32_t)a.c,
+                               (int32_t)a.oh, (int32_t)a.ow);
+        };
+        if (vec) tiled ? go(ap_nhwc<T, T::vec, true>) : go(ap_nhwc<T, T::vec, false>);
+        else go(ap_nhwc<T, 1, false>);
         *variant = vec ? "ap_nhwc_vec" : "ap_nhwc_scalar";
     } else if (a.oh == 1 && a.ow == 1) {
         // Planes per workgroup: the largest power of two (<= 256) whose span

@@ -136,6 +136,9 @@ CHANNELS_LAST = [
     ((2, 256, 13, 13), 6),          # overlapping 3 x 3 windows
     ((2, 64, 8, 8), 2),             # 4 x 4 windows
     ((2, 64, 10, 10), 2),           # 5 x 5 windows: split over thread groups
+    ((2, 6, 10, 10), 1),            # large window, channels not whole vectors: scalar thread groups
+    ((2, 32, 12, 12), 1),           # 144-pixel window: three batches of 64 per workgroup
+    ((1, 40, 11, 11), 2),           # overlapping 6 x 6 windows (ordinary loads), a partial channel block
 ]
 
 
