@@ -1279,6 +1279,11 @@ kf_status run_causal(const CausalSoftmaxArgs& a, hipStream_t s, const char** var
         KF_CAUSAL_EDGE(64, 2)
         KF_CAUSAL_EDGE(128, 2)
         KF_CAUSAL_EDGE(128, 3)
+        // Three waves of three slots for the 513 masked vectors of a 4097-key
+        // bf16 row: 75.1 us against 78.4 us for 128 x 5 ([1, 8, 4097, 4097],
+        // graph replays; the same cut on the non-causal rows, 320 x 2, was
+        // slower than 256 x 3: 97.8 against 92.5 us).
+        KF_CAUSAL_EDGE(192, 3)
         KF_CAUSAL_EDGE(128, 5)
         KF_CAUSAL_EDGE(512, 2)
         KF_CAUSAL_EDGE(512, 3)

@@ -93,8 +93,8 @@ PAIRS = [("f32", "f32"), ("bf16", "bf16"), ("bf16", "f32"), ("f16", "f16"), ("f1
 
 
 @pytest.mark.parametrize("pair", PAIRS, ids=lambda p: f"{p[0]}-{p[1]}")
-@pytest.mark.parametrize("qk", [(3, 9), (9, 9), (33, 257), (40, 1001), (12, 4097), (3, 12001), (2, 30001),
-                                (1, 40001)])
+@pytest.mark.parametrize("qk", [(3, 9), (9, 9), (33, 257), (40, 1001), (8, 2001), (12, 4097), (3, 12001),
+                                (2, 30001), (1, 40001)])
 def test_rows_that_are_not_whole_vectors(pair, qk):
     """Aligned bases, k not a multiple of the 16-byte vector: masked vectors
     covering each row (q < k puts the visible boundary mid-row; two batches
