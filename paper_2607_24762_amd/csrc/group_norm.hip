@@ -810,10 +810,12 @@ __global__ __launch_bounds__(kPipeNT) void gn_pipe(PipeParams p) {
 // gn_pipe's arithmetic.  gn_split_stats reads each 16384-element chunk once,
 // folds its moments with v_dot2 and publishes them; the last workgroup of a
 // group to arrive (a per-group counter) merges the group's parts in part
-// order and writes the group's mean (double) and M2 over slots 0 and 1.
+// order and writes the group's mean (double) and M2 into two words of the
+// group's counter line (bytes 8 and 16; the counter is bytes 0-3), never
+// over a part's slot, which a publish still in flight could overwrite.
 // gn_split_apply re-reads each chunk and normalises it with those
-// statistics; its last workgroup of a group returns the group's slots and
-// counter to zero.  One read more than gn_pipe, but both passes stream: on
+// statistics; its last workgroup of a group returns the group's slots,
+// statistics words and counter to zero.  One read more than gn_pipe, but both passes stream: on
 // [1, 128, 1024, 1024] the moments pass of the general two-kernel form
 // (about ten VALU operations per element) ran 71 us, a read at 3.8 TB/s.
 
@@ -894,6 +896,12 @@ __device__ PipeMoments split_gather(const PipeParams& p, int64_t ng) {
     return PipeMoments{__builtin_bit_cast(double, (uint64_t)lo | ((uint64_t)hi << 32)), uniform0(acc.m2)};
 }
 
+// The group's statistics words: the mean (double bits) and M2 (fp32 bits),
+// in the group's 256-byte counter line after the counter.
+__device__ __forceinline__ uint64_t* split_stats(const PipeParams& p, int64_t ng) {
+    return reinterpret_cast<uint64_t*>(ex_counter(p.ex, ng)) + 1;
+}
+
 __device__ __forceinline__ void split_chunk(const PipeParams& p, int b, int64_t* ng, int* part) {
     const int P = p.ex.parts;
     *ng = b / P;
@@ -930,7 +938,7 @@ __global__ __launch_bounds__(kPipeDataWaves * kWave) void gn_split_stats(PipePar
     // The group's last arrival: every part is published.
     const PipeMoments g = split_gather<T, NV>(p, ng);
     if (lane == 0) {
-        uint64_t* r = p.ex.slot + ng * p.ex.parts;
+        uint64_t* r = split_stats(p, ng);
         __hip_atomic_store(r, __builtin_bit_cast(uint64_t, g.mean), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         __hip_atomic_store(r + 1, (uint64_t)__float_as_uint(g.m2), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         __hip_atomic_store(ex_counter(p.ex, ng), 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -950,7 +958,7 @@ __global__ __launch_bounds__(kPipeDataWaves * kWave) void gn_split_apply(PipePar
     pipe_load<NV>(p, ng, part, threadIdx.x, v);
     if (threadIdx.x < kWave) {
         // Lane j: the affine of slot j's channel, and the group statistics
-        // gn_split_stats left in slots 0 and 1 (visible: an earlier launch
+        // gn_split_stats left beside the counter (visible: an earlier launch
         // on the same stream wrote them).
         const bool hw = p.w != nullptr, hb = p.b != nullptr;
         const void* ws = hw ? p.w : affine_identity<A>();
@@ -959,7 +967,7 @@ __global__ __launch_bounds__(kPipeDataWaves * kWave) void gn_split_apply(PipePar
         const int64_t c = (ng % p.groups) * p.cpg + (part * CH + (int64_t)j * 2048) / p.spatial;
         const float wv = load1<A>(ws, hw ? c : 0);
         const float bv = load1<A>(bs, hb ? c : 1);
-        uint64_t* r = p.ex.slot + ng * p.ex.parts;
+        uint64_t* r = split_stats(p, ng);
         const uint64_t mw = __hip_atomic_load(r, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         const uint64_t vw = __hip_atomic_load(r + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         const double mean = __builtin_bit_cast(double, mw);
@@ -981,8 +989,10 @@ __global__ __launch_bounds__(kPipeDataWaves * kWave) void gn_split_apply(PipePar
         if (lane == 0) before = ex_depart(p.ex, ng);
         before = __builtin_amdgcn_readfirstlane(before);
         if (before == (unsigned)p.ex.parts - 1) {
+            uint64_t* slots = p.ex.slot + ng * p.ex.parts;
             for (int q = lane; q < p.ex.parts; q += kWave)
-                __hip_atomic_store(r + q, (uint64_t)0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                __hip_atomic_store(slots + q, (uint64_t)0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            if (lane < 2) __hip_atomic_store(r + lane, (uint64_t)0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             if (lane == 0) __hip_atomic_store(ex_counter(p.ex, ng), 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         }
     }
