@@ -567,6 +567,31 @@ def gn_cl_row(torch, F, dev, kf355, W, steps, warmup, sets_for):
             "kf355_speedup": round(eager_us / us, 3), "buffer_sets": len(xs)}
 
 
+def gn_large_row(torch, F, dev, kf355, W, steps, warmup, sets_for):
+    """The SD3.5 VAE decoder's full-resolution GroupNorm: bf16
+    [1,128,1024,1024] (256 MiB), 32 groups, bf16 affine, eps 1e-6; too large
+    for a one-launch grid, so two launches (gn_split), against torch eager
+    and (added by the caller) against the calibration copy of 256 MiB."""
+    shape = (1, 128, 1024, 1024)
+    gw = W.randn((128,), "bf16", seed=72, mean=1.0, std=0.1).to(dev)
+    gb = W.randn((128,), "bf16", seed=73, std=0.1).to(dev)
+    nb = 2 * 2 * (1 << 27) + 2 * 128 * 2
+    xs = [W.randn_device(shape, "bf16", seed=71 + 100 * i, device=dev, mean=0.3, std=1.5)
+          for i in range(sets_for(nb))]
+    ys = [torch.empty_like(x) for x in xs]
+    fns = [kf355.prepare_group_norm(x, y, 32, gw, gb, 1e-6) for x, y in zip(xs, ys)]
+    fns[0]()
+    variant = kf355.last_variant()
+    n = max(4, min(steps, 40))
+    us = time_launches(torch, fns, n, min(warmup, 4))
+    eager_us = time_launches(torch, [lambda x=x: F.group_norm(x, 32, gw, gb, 1e-6) for x in xs], min(n, 8), 2)
+    gbs = nb / (us * 1e-6) / 1e9
+    return {"workload": "bf16 [1,128,1024,1024], 32 groups, affine, eps 1e-6 (SD3.5 VAE decoder, full resolution)",
+            "variant": variant, "algorithmic_bytes": nb, "us_per_call": round(us, 3), "gbps": round(gbs, 1),
+            "frac_of_peak": round(gbs / PEAK_HBM_GBS, 4), "torch_eager_us": round(eager_us, 3),
+            "kf355_speedup": round(eager_us / us, 3), "buffer_sets": len(xs)}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -574,7 +599,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-eager", action="store_true")
-    ap.add_argument("--no-next", action="store_true", help="skip the next-row measurements (fused causal softmax, layer_norm, decode split softmax, max_pool2d, channels-last and general-size pooling, channels-last group_norm, rows that are not whole vectors)")
+    ap.add_argument("--no-next", action="store_true", help="skip the next-row measurements (fused causal softmax, layer_norm, decode split softmax, max_pool2d, channels-last and general-size pooling, channels-last group_norm, the full-resolution VAE decoder group_norm, rows that are not whole vectors)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: the operators shard by rows / groups / planes with no exchange, "
@@ -787,6 +812,8 @@ def main():
                                                             sets_for)
         next_rows["group_norm_channels_last"] = gn_cl_row(torch, F, dev, kf355, W, args.steps, args.warmup,
                                                           sets_for)
+        next_rows["group_norm_vae_decoder"] = gn_large_row(torch, F, dev, kf355, W, args.steps, args.warmup,
+                                                           sets_for)
 
     # The fp32 softmax configurations (the square rows and the router logits).
     softmax_fp32 = small_softmax_row(torch, dev, kf355, W, args.steps, args.warmup, sets_for, outputs)
@@ -799,6 +826,10 @@ def main():
         give_ups["softmax_decode_split"] = next_rows["softmax_decode_split"].pop("give_ups")
 
     calib = copy_calibration(torch, dev, nbytes["softmax"])
+    if next_rows is not None:
+        row = next_rows["group_norm_vae_decoder"]
+        row["copy_256mib_us"] = calib["own_copy"]["us_per_call"]
+        row["op_over_copy"] = round(row["us_per_call"] / row["copy_256mib_us"], 3)
     floors = floors_row(torch, dev, kf355, w, args.steps, sets_for)
     sm = per_op["softmax"]
     traffic = measured_traffic()
