@@ -219,10 +219,12 @@ kf_status kf_group_norm_workspace_bytes(kf_dtype x_dtype, int32_t ndim, const in
  *  region to zero (its first 32-bit word accumulates the give-up count
  *  described for kf_group_norm and is never reset by the library).  The
  *  array's device address is looked up on the first call on each device.
- *  Shapes whose kf_group_norm_workspace_bytes exceeds the array return
- *  KF_ERR_WORKSPACE before anything is enqueued (e.g. [1, 512, 128, 128] with
- *  32 groups needs 24832 bytes, sized for its channels-last form; up to
- *  about 2700 groups of 16 chunks fit, about 1360 of 64).
+ *  Shapes whose exchange workspace for their layout exceeds the array
+ *  return KF_ERR_WORKSPACE before anything is enqueued ([1, 512, 128, 128]
+ *  with 32 groups needs 24832 bytes in NCHW and 270592 in channels last, as
+ *  kf_group_norm_workspace_bytes reports for either layout; about 2700
+ *  groups of 16 NCHW chunks fit, about 120 groups of 64 channels-last
+ *  parts).
  *  All calls on one GPU share that GPU's array: calls that may overlap in
  *  time on one GPU (streams not ordered by events, or other threads) race
  *  and give wrong results; calls in stream order are safe.  A failed lookup

@@ -644,7 +644,7 @@ __device__ __forceinline__ PipeMoments pipe_gather(const PipeParams& p, int64_t 
     PipeMoments m{0.0, 0.f};
     bool ok = true;
     if (lane < P) {
-        uint64_t* at = p.ex.slot + ng * P + lane;
+        uint64_t* at = ex_slot(p.ex, ng, lane);
         uint64_t w = __hip_atomic_load(at, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         while (w == 0) {
             if (__builtin_amdgcn_s_memrealtime() - t0 > p.ex.wait_ticks) break;
@@ -847,7 +847,6 @@ __device__ PipeMoments split_gather(const PipeParams& p, int64_t ng) {
     const int P = p.ex.parts;
     const int per = P > kWave ? P / kWave : 1;
     const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
-    const uint64_t* slots = p.ex.slot + ng * P;
     PipeMoments acc{0.0, 0.f};
     bool ok = true;
     for (int i0 = 0; i0 < per; i0 += kBatch) {
@@ -855,7 +854,7 @@ __device__ PipeMoments split_gather(const PipeParams& p, int64_t ng) {
 #pragma unroll
         for (int u = 0; u < kBatch; ++u) {
             const int q = lane + (i0 + u) * kWave;
-            w[u] = (i0 + u < per && q < P) ? __hip_atomic_load(slots + q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 1;
+            w[u] = (i0 + u < per && q < P) ? __hip_atomic_load(ex_slot(p.ex, ng, q), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 1;
         }
 #pragma unroll
         for (int u = 0; u < kBatch; ++u) {
@@ -992,9 +991,8 @@ __global__ __launch_bounds__(kPipeDataWaves * kWave) void gn_split_apply(PipePar
         if (lane == 0) before = ex_depart(p.ex, ng);
         before = __builtin_amdgcn_readfirstlane(before);
         if (before == (unsigned)p.ex.parts - 1) {
-            uint64_t* slots = p.ex.slot + ng * p.ex.parts;
             for (int q = lane; q < p.ex.parts; q += kWave)
-                __hip_atomic_store(slots + q, (uint64_t)0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                __hip_atomic_store(ex_slot(p.ex, ng, q), (uint64_t)0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             if (lane < 2) __hip_atomic_store(r + lane, (uint64_t)0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             if (lane == 0) __hip_atomic_store(ex_counter(p.ex, ng), 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         }
@@ -1038,7 +1036,13 @@ __global__ __launch_bounds__(kPipeDataWaves * kWave) void gn_split_apply(PipePar
 // the tile's Q groups together (lane q polls part q of each).  Otherwise as
 // gn_pipe: raw 16-bit pairs in registers, v_dot2 sums, double means,
 // bit-identical recompute when a wait gives up, write-through stores.
-constexpr int kClNV = 8;                                // slots per lane
+constexpr int kClNV = 8;                               // slots per lane
+// Exchange slots of gn_pipe_cl one 128-byte line apart: its 64 parts per
+// group would otherwise publish 16 to a line (SD3.5 block in channels last,
+// two boxes: 12.65 -> 11.97 us and 12.28 -> 12.00; 2 words apart 12.16 on
+// the first; the NCHW gn_pipe, 16 parts per group, gained nothing from it
+// and keeps its packed slots).
+constexpr int kClSlotStride = 16;
 constexpr int kClPixels = kPipeDataWaves * 8 * kClNV;  // pixels per tile: 256
 
 struct PipeClParams {
@@ -1263,7 +1267,7 @@ __global__ __launch_bounds__(kPipeNT) void gn_pipe_cl(PipeClParams p) {
                 bool all = true;
 #pragma unroll
                 for (int k = 0; k < Q; ++k) {
-                    word[k] = __hip_atomic_load(p.ex.slot + (ng0 + k) * P + lane, __ATOMIC_RELAXED,
+                    word[k] = __hip_atomic_load(ex_slot(p.ex, ng0 + k, lane), __ATOMIC_RELAXED,
                                                 __HIP_MEMORY_SCOPE_AGENT);
                     all = all && word[k] != 0;
                 }
@@ -1452,8 +1456,8 @@ uint32_t gn_wait_ticks() {
 
 // The exchange of a launch with `parts` parts per group (the give-up count
 // at offset 0 of the workspace on every path).
-Exchange gn_exchange(const GroupNormArgs& a, int64_t parts) {
-    return exchange_view(a.workspace, exchange_layout(a.n * a.groups, parts), parts, gn_wait_ticks());
+Exchange gn_exchange(const GroupNormArgs& a, int64_t parts, int stride = 1) {
+    return exchange_view(a.workspace, exchange_layout(a.n * a.groups, parts, stride), parts, gn_wait_ticks(), stride);
 }
 
 template <class T, class A, bool VECTOR, bool NHWC>
@@ -1664,7 +1668,7 @@ bool run_pipe_cl(const GroupNormArgs& a, hipStream_t s, const char** variant, kf
     const int64_t parts = cl_parts(a.c, a.spatial, a.groups);
     if (!parts) return false;
     const int64_t gt = a.n * a.groups;
-    if (exchange_layout(gt, parts).total > a.workspace_bytes) return false;
+    if (exchange_layout(gt, parts, kClSlotStride).total > a.workspace_bytes) return false;
     const int64_t tiles = a.n * (a.c / 64);
     const int64_t grid = tiles * parts;
     if (grid > INT32_MAX || a.n * a.spatial > INT32_MAX) return false;
@@ -1682,7 +1686,7 @@ bool run_pipe_cl(const GroupNormArgs& a, hipStream_t s, const char** variant, kf
     p.y = a.y;
     p.w = a.weight;
     p.b = a.bias;
-    p.ex = gn_exchange(a, parts);
+    p.ex = gn_exchange(a, parts, kClSlotStride);
     p.hw = a.spatial;
     p.c = (int32_t)a.c;
     p.groups = (int32_t)a.groups;
@@ -1810,15 +1814,22 @@ kf_status group_norm_static_scratch(void** ptr) {
     return KF_OK;
 }
 
-size_t group_norm_workspace_bytes(int64_t n, int64_t c, int64_t spatial, int64_t groups, kf_dtype xt) {
+size_t group_norm_workspace_bytes_for(int64_t n, int64_t c, int64_t spatial, int64_t groups, kf_dtype xt,
+                                      bool nhwc) {
     // The scalar layout has the smallest chunk gn_fused uses, hence the most
-    // parts, and gn_pipe's default chunks are no smaller; gn_pipe_cl may split
-    // a group into more parts (channels-last 16-bit tensors; the query does
-    // not see the layout, so it covers both).  One workspace serves every path.
+    // parts, and the chunks of gn_pipe (default) and gn_split are no smaller;
+    // gn_pipe_cl (channels-last 16-bit tensors) splits a group into more
+    // parts, each slot on a line of its own.
     const size_t fused = layout(n, c, spatial, groups, xt, false).ex.total;
-    const int64_t cl = xt == KF_FLOAT32 ? 0 : cl_parts(c, spatial, groups);
-    const size_t tiles = cl ? exchange_layout(n * groups, cl).total : 0;
+    const int64_t cl = !nhwc || xt == KF_FLOAT32 ? 0 : cl_parts(c, spatial, groups);
+    const size_t tiles = cl ? exchange_layout(n * groups, cl, kClSlotStride).total : 0;
     return fused > tiles ? fused : tiles;
+}
+
+size_t group_norm_workspace_bytes(int64_t n, int64_t c, int64_t spatial, int64_t groups, kf_dtype xt) {
+    // The query does not see the layout, so it covers both: one workspace
+    // serves every path.
+    return group_norm_workspace_bytes_for(n, c, spatial, groups, xt, true);
 }
 
 kf_status group_norm_launch(const GroupNormArgs& a, hipStream_t s, const char** variant) {

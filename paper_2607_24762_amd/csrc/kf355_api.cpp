@@ -224,7 +224,8 @@ kf_status group_norm_call(const void* x, kf_dtype x_dtype, void* y, int32_t ndim
     if ((weight && overlaps(weight, ab, y, xb)) || (bias && overlaps(bias, ab, y, xb)))
         return fail(KF_ERR_BAD_ARG, "weight or bias overlaps y");
     const int64_t spatial = ndim > 2 ? count(ndim - 2, shape + 2) : 1;
-    const size_t need = group_norm_workspace_bytes(shape[0], shape[1], spatial, num_groups, x_dtype);
+    // What this call's layout needs (the size query, blind to layout, may report more).
+    const size_t need = group_norm_workspace_bytes_for(shape[0], shape[1], spatial, num_groups, x_dtype, nhwc);
     if (use_static) {
         // The library's own array: checked against its size, then located.
         if (need > KF_GROUP_NORM_STATIC_SCRATCH_BYTES)

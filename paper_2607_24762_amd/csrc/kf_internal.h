@@ -53,6 +53,10 @@ struct GroupNormArgs {
     bool nhwc;  // x, y dense [n, spatial, c] (channels last) instead of [n, c, spatial]
 };
 size_t group_norm_workspace_bytes(int64_t n, int64_t c, int64_t spatial, int64_t groups, kf_dtype xt);
+// The exchange workspace the paths of one layout need (nhwc: channels last),
+// never more than group_norm_workspace_bytes, which covers both layouts.
+size_t group_norm_workspace_bytes_for(int64_t n, int64_t c, int64_t spatial, int64_t groups, kf_dtype xt,
+                                      bool nhwc);
 kf_status group_norm_launch(const GroupNormArgs& a, hipStream_t s, const char** variant);
 // Device address, on the current device, of the library's static GroupNorm
 // scratch array (KF_GROUP_NORM_STATIC_SCRATCH_BYTES); looked up once per
