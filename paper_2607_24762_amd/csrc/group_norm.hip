@@ -818,9 +818,10 @@ __global__ __launch_bounds__(kPipeNT) void gn_pipe(PipeParams p) {
 // flight could overwrite.
 // gn_split_apply re-reads each chunk and normalises it with those
 // statistics; its last workgroup of a group returns the group's slots,
-// statistics words and counter to zero.  One read more than gn_pipe, but both passes stream: on
-// [1, 128, 1024, 1024] the moments pass of the general two-kernel form
-// (about ten VALU operations per element) ran 71 us, a read at 3.8 TB/s.
+// statistics words and counter to zero.  One read more than gn_pipe, but
+// both passes stream (45 + 90 us on [1, 128, 1024, 1024], where the moments
+// pass of the general two-kernel form, about ten VALU operations per
+// element, ran 71 us: a read at 3.8 TB/s).
 
 // a + b for moments of na and nb values (a first).
 __device__ __forceinline__ PipeMoments merge_counts(PipeMoments a, PipeMoments b, float na, float nb) {
