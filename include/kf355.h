@@ -221,7 +221,7 @@ kf_status kf_group_norm_workspace_bytes(kf_dtype x_dtype, int32_t ndim, const in
  *  array's device address is looked up on the first call on each device.
  *  Shapes whose exchange workspace for their layout exceeds the array
  *  return KF_ERR_WORKSPACE before anything is enqueued ([1, 512, 128, 128]
- *  with 32 groups needs 24832 bytes in NCHW and 270592 in channels last, as
+ *  with 32 groups needs 12544 bytes in NCHW and 270592 in channels last, as
  *  kf_group_norm_workspace_bytes reports for either layout; about 2700
  *  groups of 16 NCHW chunks fit, about 120 groups of 64 channels-last
  *  parts).

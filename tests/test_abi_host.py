@@ -261,7 +261,7 @@ def test_group_norm_static_rejections(lib):
     st, n = gn_ws(lib, (3000, 32, 128, 128), 32, xt=F32)
     assert st == OK and n > 1 << 20
     # The SD3.5 VAE block fits in either layout (the query's 270592 bytes
-    # cover channels last; NCHW needs 24832).
+    # cover channels last; NCHW needs 12544).
     st, n = gn_ws(lib, (1, 512, 128, 128), 32)
     assert st == OK and n == 270592 <= 1 << 20
 

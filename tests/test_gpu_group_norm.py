@@ -174,6 +174,26 @@ def test_split_path_matches_the_oracle(shape, groups, dt, affine):
     assert int(ws[256:].count_nonzero().item()) == 0
 
 
+def test_a_call_needs_only_its_layouts_workspace():
+    # The size query, blind to layout, covers channels last (270592 bytes for
+    # the SD3.5 block: 64 parts per group, one line each); an NCHW call needs
+    # only its own layout's 12544 bytes and accepts exactly that, one byte
+    # less is KF_ERR_WORKSPACE, and the workspace comes back zero.
+    note("group_norm NCHW workspace of its own layout")
+    a = inputs("group_norm")
+    x, w, b = a["x"].cuda(), a["weight"].cuda(), a["bias"].cuda()
+    assert kf355.group_norm_workspace(x, 32).numel() == 270592
+    ws = torch.zeros(12544, dtype=torch.uint8, device="cuda")   # 256 + 32 * 16 * 8 + 32 * 256
+    y = kf355.kf_group_norm(x, 32, w, b, a["eps"], workspace=ws)
+    torch.cuda.synchronize()
+    assert kf355.last_variant() == "gn_pipe_nv8_r1"
+    check(y.cpu(), oracle.group_norm(a["x"], 32, a["weight"], a["bias"], a["eps"]), "bf16")
+    assert int(ws[256:].count_nonzero().item()) == 0
+    with pytest.raises(kf355.KfError) as e:
+        kf355.kf_group_norm(x, 32, w, b, a["eps"], workspace=ws[:12543])
+    assert e.value.status == 6
+
+
 def test_split_recompute_is_bit_identical(tmp_path):
     # KF355_GN_SPLIT_RECOMPUTE=1 makes each group's last arrival recompute
     # every part from x, as it does when a published part stays unseen: the
