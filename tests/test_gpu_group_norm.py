@@ -218,6 +218,8 @@ def test_in_place():
     note("group_norm in place")
     _, variant = run((1, 512, 64, 64), 32, "bf16", in_place=True, seed=6)   # 4 chunks per group
     assert variant == "gn_split_nv8", variant
+    _, variant = run((1, 32, 64, 64), 4, "f16", in_place=True, seed=9)     # 2 chunks per group, the fewest
+    assert variant == "gn_split_nv8", variant
     _, variant = run((1, 256, 48, 48), 32, "bf16", in_place=True, seed=7)   # 2 chunks, spatial 2304
     assert variant.startswith("gn_two_pass"), variant
     _, variant = run((2, 64, 8, 8), 8, "bf16", in_place=True, seed=8)
