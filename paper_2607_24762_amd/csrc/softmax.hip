@@ -22,8 +22,9 @@
 //             written element by element.
 //   sm_causal / sm_causal_edge / sm_causal_stream  the scaled causal
 //             softmax of eager attention: the resident kernels' layouts,
-//             and for longer rows the two-pass stream, each reading only
-//             the visible prefix of a row.
+//             and for longer rows the two-pass stream (whole or masked
+//             16-byte vectors on aligned bases), each reading only the
+//             visible prefix of a row.
 //   sm_cols   softmax over a non-innermost axis: one thread per column,
 //             online pass then write pass, coalesced across the inner axis.
 #include <math.h>
@@ -681,14 +682,29 @@ __global__ __launch_bounds__(NT) void sm_stream(const void* __restrict__ x, void
 
 // --------------------------------------------------------------------------
 // sm_causal for rows of any length: one workgroup per row, the online
-// (max, sum) pass of sm_stream over the visible prefix [0, live) only (the
-// masked triangle is not read), then a write pass over the whole row that
-// reads the prefix again.  In-place safe: every element is read and written
-// by the same thread, the write pass after the barrier that ends the first.
-template <class TI, class TO, int NT, bool VECTOR>
+// (max, sum) pass of sm_stream over the visible prefix only (the masked
+// triangle is not read), then a write pass over the whole row that reads the
+// prefix again.  Three access modes:
+//   kStreamVec     rows of whole 16-byte vectors on aligned bases;
+//   kStreamEdge    other rows on aligned bases, covered by the aligned
+//                  vectors from the one at or below the row's start, as in
+//                  sm_causal_edge: neighbouring rows' elements in the two end
+//                  vectors are read and masked, only the row's own elements
+//                  are written (whole vectors inside the row, the end vectors
+//                  element by element), and a vector that would cross the end
+//                  of the tensor is read element by element;
+//   kStreamScalar  bases that are not 16-byte aligned: element by element.
+// In-place safe: every element of the row is read and written by the same
+// thread, the write pass after the barrier that ends the first; elements of
+// a neighbouring row that an end vector reads are only ever masked.
+constexpr int kStreamScalar = 0;
+constexpr int kStreamVec = 1;
+constexpr int kStreamEdge = 2;
+
+template <class TI, class TO, int NT, int MODE>
 __global__ __launch_bounds__(NT) void sm_causal_stream(const void* __restrict__ x, void* __restrict__ y, int64_t q,
-                                                       int64_t k, float scale) {
-    constexpr int VEC = VECTOR ? TI::vec : 1;
+                                                       int64_t k, float scale, int64_t total) {
+    constexpr int VEC = MODE == kStreamScalar ? 1 : TI::vec;
     constexpr int NW = NT / kWave;
     constexpr int DEPTH = 4;
     constexpr int64_t STEP = (int64_t)DEPTH * NT * VEC;
@@ -696,21 +712,45 @@ __global__ __launch_bounds__(NT) void sm_causal_stream(const void* __restrict__ 
     const int64_t row = blockIdx.x;
     const int64_t i = row % q;
     const int64_t live = i + (k - q) + 1 < 0 ? 0 : (i + (k - q) + 1 > k ? k : i + (k - q) + 1);
-    const int64_t base = row * k;
+    // Loop offset e is tensor element a0 + e; the row's elements are
+    // [lo, end) and its visible keys [lo, vis).
+    const int64_t r0 = row * k;
+    const int64_t a0 = MODE == kStreamEdge ? r0 / VEC * VEC : r0;
+    const int64_t lo = r0 - a0, vis = lo + live, end = lo + k;
+    const int64_t room = total - a0;  // tensor elements from a0 on
+    auto load_slot = [&](int64_t e, float* v) {
+        if constexpr (MODE == kStreamScalar) {
+            v[0] = load1<TI>(x, a0 + e);
+        } else if constexpr (MODE == kStreamVec) {
+            load_vec<TI>(x, a0 + e, v);
+        } else if (e + VEC <= room) {
+            load_vec<TI>(x, a0 + e, v);
+        } else {
+#pragma unroll
+            for (int ii = 0; ii < VEC; ++ii) v[ii] = e + ii < room ? load1<TI>(x, a0 + e + ii) : 0.f;
+        }
+    };
+
+    // Elements [from, to) of the slot at e (clamped to [0, VEC]) lie in
+    // [lo, bound): 32-bit compares per element.
+    auto span = [&](int64_t e, int64_t bound, int& from, int& to) {
+        const int64_t f = lo - e, t = bound - e;
+        from = f < 0 ? 0 : (f > VEC ? VEC : (int)f);
+        to = t < 0 ? 0 : (t > VEC ? VEC : (int)t);
+    };
 
     MS st{-INFINITY, 0.f};
-    for (int64_t e0 = (int64_t)threadIdx.x * VEC; e0 < live; e0 += STEP) {
+    for (int64_t e0 = (int64_t)threadIdx.x * VEC; e0 < vis; e0 += STEP) {
         float v[DEPTH * VEC];
 #pragma unroll
         for (int d = 0; d < DEPTH; ++d) {
             const int64_t e = e0 + (int64_t)d * NT * VEC;
-            if (e < live) {
-                if constexpr (VECTOR) load_vec<TI>(x, base + e, v + d * VEC);
-                else v[d] = load1<TI>(x, base + e);
-            }
+            if (e < vis) load_slot(e, v + d * VEC);
+            int from, to;
+            span(e, vis, from, to);
 #pragma unroll
             for (int ii = 0; ii < VEC; ++ii)
-                v[d * VEC + ii] = (e + ii < live) ? v[d * VEC + ii] * scale : -INFINITY;
+                v[d * VEC + ii] = (ii >= from && ii < to) ? v[d * VEC + ii] * scale : -INFINITY;
         }
         st = ms_add<TO, DEPTH * VEC>(st, v);
     }
@@ -727,25 +767,32 @@ __global__ __launch_bounds__(NT) void sm_causal_stream(const void* __restrict__ 
     // No visible key: m = -inf and every output is exp(-inf - -inf) = NaN.
     const float inv = 1.f / tot.s;
 
-    for (int64_t e0 = (int64_t)threadIdx.x * VEC; e0 < k; e0 += STEP) {
+    for (int64_t e0 = (int64_t)threadIdx.x * VEC; e0 < end; e0 += STEP) {
         float v[DEPTH][VEC];
 #pragma unroll
         for (int d = 0; d < DEPTH; ++d) {
             const int64_t e = e0 + (int64_t)d * NT * VEC;
-            if (e < live) {
-                if constexpr (VECTOR) load_vec<TI>(x, base + e, v[d]);
-                else v[d][0] = load1<TI>(x, base + e);
-            }
+            if (e < vis) load_slot(e, v[d]);
         }
 #pragma unroll
         for (int d = 0; d < DEPTH; ++d) {
             const int64_t e = e0 + (int64_t)d * NT * VEC;
-            if (e < k) {
+            if (e < end) {
+                int from, to;
+                span(e, vis, from, to);
 #pragma unroll
                 for (int ii = 0; ii < VEC; ++ii)
-                    v[d][ii] = exp_out<TO>((e + ii < live) ? v[d][ii] * scale : -INFINITY, tot.m) * inv;
-                if constexpr (VECTOR) store_span<TO, VEC>(y, base + e, v[d]);
-                else store1<TO>(y, base + e, v[d][0]);
+                    v[d][ii] = exp_out<TO>((ii >= from && ii < to) ? v[d][ii] * scale : -INFINITY, tot.m) * inv;
+                if constexpr (MODE == kStreamScalar) {
+                    store1<TO>(y, a0 + e, v[d][0]);
+                } else if (MODE == kStreamVec || (e >= lo && e + VEC <= end)) {
+                    store_span<TO, VEC>(y, a0 + e, v[d]);
+                } else {
+                    span(e, end, from, to);
+#pragma unroll
+                    for (int ii = 0; ii < VEC; ++ii)
+                        if (ii >= from && ii < to) store1<TO>(y, a0 + e + ii, v[d][ii]);
+                }
             }
         }
     }
@@ -1318,14 +1365,20 @@ kf_status run_causal(const CausalSoftmaxArgs& a, hipStream_t s, const char** var
 #undef KF_CAUSAL
     if (!done) {
         // Beyond the register-resident tables: stream the row twice, with
-        // 16-byte vectors when the rows are whole aligned vectors.
+        // 16-byte vectors wherever the bases are aligned.
+        const dim3 g((unsigned)(a.batch * a.q)), b(1024);
+        const int64_t total = a.batch * a.q * a.k;
         if (vec) {
-            hipLaunchKernelGGL((sm_causal_stream<TI, TO, 1024, true>), dim3((unsigned)(a.batch * a.q)), dim3(1024), 0,
-                               s, a.x, a.y, a.q, a.k, a.scale);
+            hipLaunchKernelGGL((sm_causal_stream<TI, TO, 1024, kStreamVec>), g, b, 0, s, a.x, a.y, a.q, a.k, a.scale,
+                               total);
             *variant = "sm_causal_stream_vec";
+        } else if (edge) {
+            hipLaunchKernelGGL((sm_causal_stream<TI, TO, 1024, kStreamEdge>), g, b, 0, s, a.x, a.y, a.q, a.k, a.scale,
+                               total);
+            *variant = "sm_causal_stream_edge";
         } else {
-            hipLaunchKernelGGL((sm_causal_stream<TI, TO, 1024, false>), dim3((unsigned)(a.batch * a.q)), dim3(1024),
-                               0, s, a.x, a.y, a.q, a.k, a.scale);
+            hipLaunchKernelGGL((sm_causal_stream<TI, TO, 1024, kStreamScalar>), g, b, 0, s, a.x, a.y, a.q, a.k,
+                               a.scale, total);
             *variant = "sm_causal_stream_scalar";
         }
     }

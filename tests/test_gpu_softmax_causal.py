@@ -104,8 +104,8 @@ def test_rows_that_are_not_whole_vectors(pair, qk):
     x = randn((2, q, k), pair[0], seed=q * k, std=3.0)
     _, variant = run(x, 0.37, pair[1])
     # fp32 rows above 36864 keys leave the masked-vector table for the
-    # element-wise two-pass stream.
-    expect = "sm_causal_stream_scalar" if pair[0] == "f32" and k > 36864 else "sm_causal_edge"
+    # two-pass stream over the same masked vectors.
+    expect = "sm_causal_stream_edge" if pair[0] == "f32" and k > 36864 else "sm_causal_edge"
     assert variant.startswith(expect), variant
 
 
@@ -125,8 +125,11 @@ def test_rows_that_are_not_whole_vectors_ignore_the_masked_triangle_in_place():
 
 
 @pytest.mark.parametrize("dt,qk,variant", [
-    ("bf16", (3, 40961), "sm_causal_stream_scalar"),   # just past the masked-vector table
-    ("f32", (3, 36865), "sm_causal_stream_scalar"),
+    ("bf16", (3, 40961), "sm_causal_stream_edge"),     # just past the masked-vector table
+    ("f32", (3, 36865), "sm_causal_stream_edge"),
+    ("f16", (3, 131071), "sm_causal_stream_edge"),     # four or five STEP-sized passes
+    ("bf16", (5, 65543), "sm_causal_stream_edge"),     # two whole passes and a few keys
+    ("f32", (4, 100003), "sm_causal_stream_edge"),
     ("bf16", (2, 65544), "sm_causal_stream_vec"),      # whole vectors past the resident table
     ("f16", (3, 131072), "sm_causal_stream_vec"),
     ("f32", (5, 100000), "sm_causal_stream_vec"),      # several STEP-sized passes, ragged last one
@@ -141,6 +144,37 @@ def test_rows_beyond_the_tables_stream(dt, qk, variant):
     x = randn((2, q, k), dt, seed=k % 1009, std=3.0)
     _, got = run(x, 0.37, dt)
     assert got == variant, got
+
+
+@pytest.mark.parametrize("pair", PAIRS, ids=lambda p: f"{p[0]}-{p[1]}")
+def test_masked_vector_stream_every_dtype_pair(pair):
+    """The masked-vector stream for every dtype pair: two batches of rows
+    that are not whole vectors, so rows share end vectors across the batch
+    boundary and the tensor's last vector is partial (read element by
+    element)."""
+    q, k = 3, 40961
+    note(f"softmax_causal masked-vector stream {pair} q={q} k={k}")
+    x = randn((2, q, k), pair[0], seed=77, std=3.0)
+    _, variant = run(x, 0.37, pair[1])
+    assert variant == "sm_causal_stream_edge", variant
+
+
+def test_masked_vector_stream_in_place_ignores_the_masked_triangle():
+    note("softmax_causal masked-vector stream: NaN in the masked triangle, in place, aligned base")
+    q, k = 4, 40963
+    x = randn((2, q, k), "bf16", seed=23, std=2.0)
+    poisoned = x.clone()
+    poisoned[:, torch.ones(q, k, dtype=torch.bool).triu(k - q + 1)] = float("nan")
+    a = kf355.kf_softmax_causal(x.cuda(), 0.25)
+    assert kf355.last_variant() == "sm_causal_stream_edge"
+    pd = poisoned.cuda()
+    b = kf355.kf_softmax_causal(pd, 0.25, out=pd)
+    torch.cuda.synchronize()
+    assert kf355.last_variant() == "sm_causal_stream_edge"
+    assert torch.equal(a.view(torch.int16), b.view(torch.int16))
+    assert_close(b, oracle.softmax_causal(x, 0.25), "bf16")
+    masked = b.cpu()[:, torch.ones(q, k, dtype=torch.bool).triu(k - q + 1)]
+    assert (masked.view(torch.int16) == 0).all()   # exact +0
 
 
 def test_stream_in_place_ignores_the_masked_triangle():
