@@ -244,12 +244,19 @@ def reset_workspace_give_ups(ws: torch.Tensor) -> None:
     ws[:4].zero_()
 
 
-def group_norm_workspace(x: torch.Tensor, num_groups: int) -> torch.Tensor:
-    """The cached zero-filled workspace, large enough for kf_group_norm on x."""
+def kf_group_norm_workspace_bytes(x: torch.Tensor, num_groups: int) -> int:
+    """Workspace bytes kf_group_norm needs for x's shape and dtype, in either
+    layout (the size query through the C ABI, cached per shape)."""
     shape, _s = _arr(x.shape)
-    n = _query_bytes(("gn", _dtype(x), tuple(x.shape), num_groups),
-                     lambda out: lib().kf_group_norm_workspace_bytes(_dtype(x), x.dim(), shape, num_groups, out))
-    return _workspace(x, n)
+    return _query_bytes(("gn", _dtype(x), tuple(x.shape), num_groups),
+                        lambda out: lib().kf_group_norm_workspace_bytes(_dtype(x), x.dim(), shape, num_groups, out))
+
+
+def group_norm_workspace(x: torch.Tensor, num_groups: int) -> torch.Tensor:
+    """The cached zero-filled workspace (shared by every call on the stream,
+    so possibly larger than this call needs), large enough for kf_group_norm
+    on x."""
+    return _workspace(x, kf_group_norm_workspace_bytes(x, num_groups))
 
 
 def softmax_split_workspace(x: torch.Tensor, dim: int = -1, out_dtype: torch.dtype | None = None) -> torch.Tensor:

@@ -33,7 +33,7 @@ def case(name):
     """(input shape, dtype, call(x, out, ws) -> None, output factory, workspace factory) for one operator;
     built inside the test, so collecting this module on a host without a GPU allocates nothing."""
     def ws_gn(x):
-        return torch.zeros(kf355.group_norm_workspace(x, 32).numel(), dtype=torch.uint8, device="cuda")
+        return torch.zeros(kf355.kf_group_norm_workspace_bytes(x, 32), dtype=torch.uint8, device="cuda")
 
     def ws_split(x):
         return torch.zeros(kf355.softmax_split_workspace(x, -1, torch.float32).numel(), dtype=torch.uint8,

@@ -164,7 +164,7 @@ def test_split_path_matches_the_oracle(shape, groups, dt, affine):
     adt = dt if affine == "same" else "f32"
     w = randn((c,), adt, seed=22, mean=1.0, std=0.1).cuda() if affine in ("same", "f32", "w") else None
     b = randn((c,), adt, seed=23, std=0.1).cuda() if affine in ("same", "f32", "b") else None
-    ws = torch.zeros(kf355.group_norm_workspace(x, groups).numel(), dtype=torch.uint8, device="cuda")
+    ws = torch.zeros(kf355.kf_group_norm_workspace_bytes(x, groups), dtype=torch.uint8, device="cuda")
     y1 = kf355.kf_group_norm(x, groups, w, b, 1e-6, workspace=ws)
     y2 = kf355.kf_group_norm(x, groups, w, b, 1e-6, workspace=ws)
     torch.cuda.synchronize()
@@ -182,7 +182,7 @@ def test_a_call_needs_only_its_layouts_workspace():
     note("group_norm NCHW workspace of its own layout")
     a = inputs("group_norm")
     x, w, b = a["x"].cuda(), a["weight"].cuda(), a["bias"].cuda()
-    assert kf355.group_norm_workspace(x, 32).numel() == 270592
+    assert kf355.kf_group_norm_workspace_bytes(x, 32) == 270592
     ws = torch.zeros(12544, dtype=torch.uint8, device="cuda")   # 256 + 32 * 16 * 8 + 32 * 256
     y = kf355.kf_group_norm(x, 32, w, b, a["eps"], workspace=ws)
     torch.cuda.synchronize()
