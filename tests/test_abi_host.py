@@ -266,6 +266,17 @@ def test_group_norm_static_rejections(lib):
     assert st == OK and n == 270592 <= 1 << 20
 
 
+def test_binding_workspace_query_is_the_abi_query(lib):
+    # kf355.kf_group_norm_workspace_bytes marshals the same query (shape and
+    # dtype only: a CPU tensor serves), and repeats it per shape from its cache.
+    import torch
+    x = torch.empty((1, 512, 128, 128), dtype=torch.bfloat16)
+    assert kf355.kf_group_norm_workspace_bytes(x, 32) == gn_ws(lib, (1, 512, 128, 128), 32)[1] == 270592
+    assert kf355.kf_group_norm_workspace_bytes(x, 32) == 270592
+    y = torch.empty((2, 96, 32, 32), dtype=torch.float16)
+    assert kf355.kf_group_norm_workspace_bytes(y, 4) == gn_ws(lib, (2, 96, 32, 32), 4, xt=F16)[1]
+
+
 def ap(lib, shape=(2, 3, 7, 7), oh=1, ow=1, x=FAKE, y=FAKE + (1 << 30), xt=F32, xs=None, ys=None):
     return lib.kf_adaptive_avgpool2d(ctypes.c_void_p(x), xt, ctypes.c_void_p(y), len(shape), arr(shape),
                                      arr(xs) if xs else None, arr(ys) if ys else None, oh, ow, None)
