@@ -466,6 +466,31 @@ def unaligned_softmax_row(torch, dev, kf355, W, steps, warmup, sets_for):
     return row
 
 
+def causal_long_rows_row(torch, dev, kf355, W, steps, warmup, sets_for):
+    """Causal attention scores longer than the register-resident kernels (a
+    64-query prefill chunk against a 65537-key cache: bf16 [8, 64, 65537],
+    scale 1/8, drawn on the device): rows that are not whole 16-byte vectors
+    stream the masked vectors covering each row; the same shape with 65544
+    keys (whole vectors) beside it."""
+    q, scale = 64, 0.125
+    row = {"workload": "bf16 [8,64,k] raw scores, causal, scale 1/8 (prefill chunk against a long cache)"}
+    for name, k in (("k65537", 65537), ("k65544", 65544)):
+        raw = W.randn_device((8, q, k), "bf16", seed=14, std=3.0 / 16.0)
+        visible = 8 * sum(min(k, i + (k - q) + 1) for i in range(q))
+        nb = visible * 2 + raw.numel() * 2
+        xs = [raw.clone() for _ in range(sets_for(nb))]
+        fns = [kf355.prepare_softmax_causal(x, torch.empty_like(x), scale) for x in xs]
+        fns[0]()
+        variant = kf355.last_variant()
+        us = time_launches(torch, fns, steps, warmup)
+        gbs = nb / (us * 1e-6) / 1e9
+        row[name] = {"variant": variant, "algorithmic_bytes": nb, "us_per_call": round(us, 3),
+                     "gbps": round(gbs, 1), "frac_of_peak": round(gbs / PEAK_HBM_GBS, 4), "buffer_sets": len(xs)}
+        del raw, xs, fns
+        torch.cuda.empty_cache()
+    return row
+
+
 def resnet_fp16_row(torch, F, dev, kf355, W, steps, warmup, sets_for):
     """The ResNet-50 pooling shapes in fp16 (the precision the paper's
     ResNet-50 ran in): head adaptive_avgpool2d [32,2048,7,7] -> 1x1 and stem
@@ -804,6 +829,8 @@ def main():
                                                        sets_for)
         next_rows["max_pool2d_stem"] = maxpool_row(torch, F, dev, kf355, W, args.steps, args.warmup, sets_for)
         next_rows["resnet50_fp16"] = resnet_fp16_row(torch, F, dev, kf355, W, args.steps, args.warmup, sets_for)
+        next_rows["softmax_causal_long_rows"] = causal_long_rows_row(torch, dev, kf355, W, args.steps, args.warmup,
+                                                                     sets_for)
         next_rows["softmax_unaligned_rows"] = unaligned_softmax_row(torch, dev, kf355, W, args.steps, args.warmup,
                                                                     sets_for)
         next_rows["avgpool_general_sizes"] = avgpool_general_row(torch, F, dev, kf355, W, args.steps, args.warmup,
